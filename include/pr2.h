@@ -1,0 +1,161 @@
+/*
+ * pr2.h -- C ABI of the MI355X (gfx950) Predictive Routing Replay MoE-layer hot path.
+ *
+ * One MoE layer of a Pr^2 model, in both phases of the method:
+ *   rollout:  predictive route  I_hat = TopK(Softmax(h W + h W_p), k)   (Sec. 4.1,
+ *             Eq. pr2_predict, Eq. pr2_route; Alg. 2 in Appendix D), recorded into a
+ *             caller-owned route buffer;
+ *   training: replay of the recorded ids with weights from the current router and the
+ *             predictor bypassed, o = sum_{j in I_hat} rho_j E_j(h)  (Sec. 4.1, Eq. pr2_output;
+ *             Alg. 3), experts being gated MLPs with gate, up and down projections
+ *             (Appendix E.2).
+ *
+ * Conventions shared by every entry point
+ *   - All tensor arguments are DEVICE pointers owned by the caller, row-major, 16-byte
+ *     aligned.  The library never allocates, frees or keeps them; scratch memory comes from
+ *     the caller's workspace `ws` of at least pr2_workspace_bytes(desc, op) bytes (16-byte
+ *     aligned; may be NULL when that size is 0).
+ *   - Calls are asynchronous on `stream` (NULL = the null stream of the current device) and
+ *     run on the current HIP device.  They return once the kernels are enqueued.
+ *   - Every argument is checked on the host before any HIP call.  On an error nothing is
+ *     enqueued, outputs are untouched, the status says what was wrong and pr2_last_error()
+ *     (thread-local) gives a sentence naming the argument.
+ *   - T == 0 is a no-op returning PR2_OK.
+ *   - Expert ids are 0-based.  Results are deterministic: the same inputs on the same device
+ *     give bitwise identical outputs (no floating-point atomics anywhere).
+ *   - Route contents (0 <= id < N, distinct within a row) are a precondition.  Kernels never
+ *     touch memory out of bounds for any id value: an out-of-range id is skipped and counted.
+ *     With the environment variable PR2_VALIDATE=1 each call that reads a route also
+ *     synchronises its stream and returns PR2_ERR_ROUTE if any id was out of range or
+ *     repeated within its row.
+ *   - Inputs must be finite; NaN or Inf give unspecified (but memory-safe) results.
+ */
+#ifndef PR2_H
+#define PR2_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Same type as hipStream_t. */
+typedef struct ihipStream_t* pr2_stream_t;
+
+typedef enum {
+    PR2_OK = 0,
+    PR2_ERR_NULL = 1,        /* a required pointer is NULL                                  */
+    PR2_ERR_SHAPE = 2,       /* a size is out of range (k > N, k < 1, d < 1, ldi < k, ...)     */
+    PR2_ERR_DTYPE = 3,       /* unknown act_dtype / idx_dtype code                             */
+    PR2_ERR_ALIGN = 4,       /* a pointer is not 16-byte aligned                               */
+    PR2_ERR_WORKSPACE = 5,   /* workspace smaller than pr2_workspace_bytes(desc, op)           */
+    PR2_ERR_UNSUPPORTED = 6, /* valid but not implemented (e.g. N > 1024)                      */
+    PR2_ERR_ROUTE = 7,       /* PR2_VALIDATE=1 found an out-of-range or repeated id             */
+    PR2_ERR_DEVICE = 8,      /* no usable HIP device, or the device is not gfx950              */
+    PR2_ERR_HIP = 9          /* a HIP runtime call or kernel launch failed                     */
+} pr2_status;
+
+/* act_dtype: storage type of activations (x, y, dy, dx) and expert weights.
+ * The router W_r, its bias, the predictor factors A, B, gates and logits are always fp32. */
+enum { PR2_F32 = 0, PR2_BF16 = 1 };
+/* idx_dtype: storage type of recorded expert ids. */
+enum { PR2_I32 = 0, PR2_I16 = 1 };
+/* op codes for pr2_workspace_bytes. */
+enum { PR2_OP_ROUTE = 0, PR2_OP_REPLAY_FWD = 1, PR2_OP_REPLAY_BWD = 2, PR2_OP_ROLLOUT_FWD = 3 };
+
+/*
+ * Layer descriptor.
+ *   T tokens (>= 0), d hidden size, N experts (1..1024), k experts per token (1..N),
+ *   m expert intermediate size, r predictor rank (>= 0; 0 = no predictor),
+ *   act_dtype PR2_F32 | PR2_BF16, idx_dtype PR2_I32 | PR2_I16 (PR2_I16 needs N <= 32767),
+ *   renorm: 1 = the k weights are the softmax restricted to the k ids (they sum to one);
+ *           0 = the weight of id j is rho_j of the softmax over all N experts, as Eq.
+ *               pr2_old_output and Eq. pr2_output print it.
+ */
+typedef struct {
+    int64_t T;
+    int32_t d, N, k, m, r;
+    int32_t act_dtype;
+    int32_t idx_dtype;
+    int32_t renorm;
+} pr2_moe_desc;
+
+/* Bytes of workspace an op needs for this descriptor (0 if none).  Never fails: an invalid
+ * descriptor yields 0 and the call itself then reports the error. */
+size_t pr2_workspace_bytes(const pr2_moe_desc* desc, int op);
+
+/*
+ * Route prediction during rollout (Sec. 4.1 "Route Prediction During Rollout";
+ * Eq. pr2_predict, Eq. pr2_route; Alg. 2 in Appendix D, its logits, top-k and caching steps).
+ *
+ *   p = x W_r + b_r                      router logits (the feature-cache p_old)
+ *   z = p + (x A) B                      predictive logits, W_p = A B of rank r
+ *   idx = TopK(z, k)                     ties to the lower id, stored ASCENDING by id
+ *   gate_j = softmax(z) restricted to idx (renorm = 1) or softmax over all N (renorm = 0)
+ *
+ *   x          [T, d] act_dtype
+ *   W_r        [d, N] fp32;  b_r [N] fp32 or NULL (no router bias)
+ *   A          [d, r] fp32;  B [r, N] fp32.  Both ignored when r == 0.  B may be NULL only
+ *              when r == N, meaning the identity (a full-rank predictor W_p = A).
+ *   idx_out    route record: token t's k ids go to idx_out + t*ldi (elements of idx_dtype),
+ *              ldi >= k.  Rows of other tokens and elements beyond k in a row are never
+ *              written, so a [seq, pos, k] buffer can be filled one decode step at a time
+ *              (pass idx_out = buf + pos*k, ldi = n_pos*k).
+ *   gate_out   [T, k] fp32, aligned with idx_out's order; may be NULL.
+ *   logits_out [T, N] fp32 router logits p (without the predictor term); may be NULL.
+ *   ws         unused (pr2_workspace_bytes(desc, PR2_OP_ROUTE) is 0).
+ */
+pr2_status pr2_route_predict(const pr2_moe_desc* desc, const void* x, const float* W_r,
+                             const float* b_r, const float* A, const float* B, void* idx_out,
+                             int64_t ldi, float* gate_out, float* logits_out, void* ws,
+                             size_t ws_bytes, pr2_stream_t stream);
+
+/*
+ * Replay forward during training (Sec. 4.1 "Replay During Training"; Eq. pr2_output;
+ * Alg. 3 in Appendix D, its first two steps).  No fresh top-k: the recorded ids are used as
+ * given, in any order; the weights come from the current router with the predictor bypassed:
+ *
+ *   p = x W_r + b_r,  g_{t,s} = softmax over the k recorded ids (renorm = 1) or rho of the
+ *   softmax over all N (renorm = 0),
+ *   y_t = sum_s g_{t,s} E_{idx[t,s]}(x_t),  E_j(h) = W_down_j (silu(W_gate_j h) * (W_up_j h)).
+ *
+ *   x        [T, d] act_dtype;  idx: token t's ids at idx + t*ldi (idx_dtype), ldi >= k
+ *   W_r      [d, N] fp32;  b_r [N] fp32 or NULL
+ *   W_gate   [N, m, d], W_up [N, m, d], W_down [N, d, m]   act_dtype
+ *   y        [T, d] act_dtype (overwritten)
+ *   gate_out [T, k] fp32 replay weights in idx's slot order; may be NULL.
+ *   ws       >= pr2_workspace_bytes(desc, PR2_OP_REPLAY_FWD)
+ * bf16 expert GEMMs use MFMA with fp32 accumulation; the SwiGLU activation is rounded to
+ * act_dtype before the down projection and the weighted expert outputs are rounded to
+ * act_dtype before the combine, which sums each token's k terms in slot order in fp32.
+ */
+pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const void* idx,
+                                  int64_t ldi, const float* W_r, const float* b_r,
+                                  const void* W_gate, const void* W_up, const void* W_down,
+                                  void* y, float* gate_out, void* ws, size_t ws_bytes,
+                                  pr2_stream_t stream);
+
+/* Status name ("PR2_OK", ...); never NULL. */
+const char* pr2_status_string(pr2_status s);
+/* Detail of the last error on this thread ("" if none); valid until the next call. */
+const char* pr2_last_error(void);
+/* Library version string. */
+const char* pr2_version(void);
+
+/*
+ * Measurement hooks (not part of the method).  While enabled, every kernel the library
+ * enqueues is bracketed by a pair of HIP events recorded on the same stream.
+ * pr2_profile_collect waits for the recorded events, adds each kernel's elapsed time to a
+ * per-kernel-name total and fills up to `cap` entries of names / total_ms / launches,
+ * returning the number of distinct kernel names seen since the last reset (or -1 on a HIP
+ * error).  Names are static strings.  Not thread-safe; for single-threaded benchmarking.
+ */
+void pr2_profile_enable(int on);
+void pr2_profile_reset(void);
+int pr2_profile_collect(const char** names, double* total_ms, int64_t* launches, int cap);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PR2_H */

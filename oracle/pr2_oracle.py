@@ -180,15 +180,12 @@ def rollout_forward(h, W_r, beta, A, B, k, W_gate, W_up, W_down, renorm=True):
 
 def replay_forward_rows(rows, h_rows, idx_rows, W_r, beta, W_gate, W_up, W_down,
                         renorm=True):
-    """Replay forward for selected tokens only: one token at a time, one
-    expert at a time.  ``h_rows``/``idx_rows`` are the selected tokens' rows."""
+    """Replay forward for selected tokens only (their rows of h and of the
+    recorded ids): the same masked per-expert combine restricted to them, so
+    each expert's weights are read once however many tokens are sampled."""
+    del rows
     g, _ = replay_gates(h_rows, W_r, beta, idx_rows, renorm)
-    out = np.zeros((len(rows), np.asarray(W_down).shape[1]))
-    for i in range(len(rows)):
-        for s, e in enumerate(np.asarray(idx_rows[i], dtype=np.int64)):
-            out[i] += g[i, s] * expert_ffn(_f64(h_rows[i:i + 1]), W_gate[e], W_up[e],
-                                           W_down[e])[0]
-    return out, g
+    return moe_combine(h_rows, idx_rows, g, W_gate, W_up, W_down), g
 
 
 # --------------------------------------------------------------- backward --

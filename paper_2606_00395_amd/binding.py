@@ -1,0 +1,192 @@
+"""ctypes binding of libpr2.so: argument marshalling only.
+
+Every computation runs in the library's HIP kernels; this module only reads
+shapes, dtypes, strides and device pointers off torch tensors and passes them
+through the C ABI declared in include/pr2.h.  Importing it needs no GPU; the
+library itself is loaded on first use and a missing build raises at once.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, byref, c_char_p, c_double, c_int, c_int32, c_int64, c_size_t, c_void_p
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libpr2.so")
+
+PR2_F32, PR2_BF16 = 0, 1
+PR2_I32, PR2_I16 = 0, 1
+OP_ROUTE, OP_REPLAY_FWD, OP_REPLAY_BWD, OP_ROLLOUT_FWD = 0, 1, 2, 3
+
+STATUS = ["PR2_OK", "PR2_ERR_NULL", "PR2_ERR_SHAPE", "PR2_ERR_DTYPE", "PR2_ERR_ALIGN",
+          "PR2_ERR_WORKSPACE", "PR2_ERR_UNSUPPORTED", "PR2_ERR_ROUTE", "PR2_ERR_DEVICE",
+          "PR2_ERR_HIP"]
+
+# every symbol include/pr2.h declares
+EXPORTS = ["pr2_workspace_bytes", "pr2_route_predict", "pr2_moe_replay_forward",
+           "pr2_status_string", "pr2_last_error", "pr2_version", "pr2_profile_enable",
+           "pr2_profile_reset", "pr2_profile_collect"]
+
+
+class Pr2Error(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        self.status = status
+        name = STATUS[status] if 0 <= status < len(STATUS) else str(status)
+        super().__init__(f"{name}: {detail}")
+
+
+class MoeDesc(ctypes.Structure):
+    _fields_ = [("T", c_int64), ("d", c_int32), ("N", c_int32), ("k", c_int32), ("m", c_int32),
+                ("r", c_int32), ("act_dtype", c_int32), ("idx_dtype", c_int32),
+                ("renorm", c_int32)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it first "
+                           "(python -c 'import __graft_entry__ as g; g.build()')")
+    L = ctypes.CDLL(LIB_PATH)
+    P = c_void_p
+    L.pr2_workspace_bytes.argtypes = [POINTER(MoeDesc), c_int]
+    L.pr2_workspace_bytes.restype = c_size_t
+    L.pr2_route_predict.argtypes = [POINTER(MoeDesc), P, P, P, P, P, P, c_int64, P, P, P,
+                                    c_size_t, P]
+    L.pr2_route_predict.restype = c_int
+    L.pr2_moe_replay_forward.argtypes = [POINTER(MoeDesc), P, P, c_int64, P, P, P, P, P, P, P,
+                                         P, c_size_t, P]
+    L.pr2_moe_replay_forward.restype = c_int
+    L.pr2_status_string.argtypes = [c_int]
+    L.pr2_status_string.restype = c_char_p
+    L.pr2_last_error.argtypes = []
+    L.pr2_last_error.restype = c_char_p
+    L.pr2_version.argtypes = []
+    L.pr2_version.restype = c_char_p
+    L.pr2_profile_enable.argtypes = [c_int]
+    L.pr2_profile_enable.restype = None
+    L.pr2_profile_reset.argtypes = []
+    L.pr2_profile_reset.restype = None
+    L.pr2_profile_collect.argtypes = [POINTER(c_char_p), POINTER(c_double), POINTER(c_int64), c_int]
+    L.pr2_profile_collect.restype = c_int
+    _lib = L
+    return L
+
+
+def check(status: int):
+    if status != 0:
+        raise Pr2Error(status, lib().pr2_last_error().decode())
+
+
+# ----------------------------------------------------------- torch glue ----
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t):
+    return None if t is None else c_void_p(t.data_ptr())
+
+
+def _act_code(t):
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return PR2_BF16
+    if t.dtype == torch.float32:
+        return PR2_F32
+    raise TypeError(f"activations must be bfloat16 or float32, got {t.dtype}")
+
+
+def _idx_code(t):
+    torch = _torch()
+    if t.dtype == torch.int16:
+        return PR2_I16
+    if t.dtype == torch.int32:
+        return PR2_I32
+    raise TypeError(f"expert ids must be int16 or int32, got {t.dtype}")
+
+
+def _stream(stream):
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return c_void_p(stream.cuda_stream)
+
+
+def _row_stride(idx):
+    if idx.dim() != 2 or idx.stride(1) != 1:
+        raise ValueError("ids must be a 2-D view [T, k] with unit stride along k")
+    return idx.stride(0)
+
+
+def make_desc(T, d, N, k, m=0, r=0, act=PR2_BF16, idx=PR2_I32, renorm=True) -> MoeDesc:
+    return MoeDesc(T, d, N, k, m, r, act, idx, 1 if renorm else 0)
+
+
+def workspace_bytes(desc: MoeDesc, op: int) -> int:
+    return int(lib().pr2_workspace_bytes(byref(desc), op))
+
+
+def route_predict(x, W_r, b_r, A, B, k, idx_out, gate_out=None, logits_out=None, renorm=True,
+                  stream=None):
+    """pr2_route_predict on torch tensors.  ``idx_out`` is a [T, k] view (any row stride)
+    of int16/int32; A/B may be None (no predictor); B None with A given means identity."""
+    T, d = x.shape
+    N = W_r.shape[1]
+    r = 0 if A is None else A.shape[1]
+    desc = make_desc(T, d, N, k, 0, r, _act_code(x), _idx_code(idx_out), renorm)
+    check(lib().pr2_route_predict(byref(desc), _ptr(x), _ptr(W_r), _ptr(b_r), _ptr(A), _ptr(B),
+                                  _ptr(idx_out), _row_stride(idx_out), _ptr(gate_out),
+                                  _ptr(logits_out), None, 0, _stream(stream)))
+
+
+def replay_workspace(x, idx, W_r, W_gate, renorm=True):
+    torch = _torch()
+    T, d = x.shape
+    desc = make_desc(T, d, W_r.shape[1], idx.shape[1], W_gate.shape[1], 0, _act_code(x),
+                     _idx_code(idx), renorm)
+    return torch.empty(max(1, workspace_bytes(desc, OP_REPLAY_FWD)), dtype=torch.uint8,
+                       device=x.device)
+
+
+def moe_replay_forward(x, idx, W_r, b_r, W_gate, W_up, W_down, y, gate_out=None, ws=None,
+                       renorm=True, stream=None):
+    """pr2_moe_replay_forward on torch tensors.  ``idx`` is a [T, k] view (any row stride)."""
+    T, d = x.shape
+    N = W_r.shape[1]
+    k = idx.shape[1]
+    m = W_gate.shape[1]
+    desc = make_desc(T, d, N, k, m, 0, _act_code(x), _idx_code(idx), renorm)
+    if ws is None:
+        ws = replay_workspace(x, idx, W_r, W_gate, renorm)
+    check(lib().pr2_moe_replay_forward(byref(desc), _ptr(x), _ptr(idx), _row_stride(idx),
+                                       _ptr(W_r), _ptr(b_r), _ptr(W_gate), _ptr(W_up),
+                                       _ptr(W_down), _ptr(y), _ptr(gate_out), _ptr(ws),
+                                       ws.numel(), _stream(stream)))
+
+
+# ------------------------------------------------------ measurement hooks --
+
+def profile_enable(on: bool = True):
+    lib().pr2_profile_enable(1 if on else 0)
+
+
+def profile_reset():
+    lib().pr2_profile_reset()
+
+
+def profile_collect(cap: int = 64) -> dict:
+    """{kernel name: (total ms, launches)} since the last reset."""
+    names = (c_char_p * cap)()
+    ms = (c_double * cap)()
+    n_l = (c_int64 * cap)()
+    n = lib().pr2_profile_collect(names, ms, n_l, cap)
+    if n < 0:
+        raise RuntimeError("pr2_profile_collect failed")
+    return {names[i].decode(): (ms[i], int(n_l[i])) for i in range(min(n, cap))}

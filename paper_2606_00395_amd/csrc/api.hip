@@ -1,0 +1,330 @@
+// Host side of the C ABI: argument validation (before any HIP call), workspace
+// layout, kernel sequencing and the measurement hooks.
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "common.h"
+
+namespace pr2 {
+
+// ------------------------------------------------------------- errors ----
+static thread_local std::string t_err;
+
+static pr2_status fail(pr2_status s, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    t_err = buf;
+    return s;
+}
+
+static pr2_status ok() {
+    t_err.clear();
+    return PR2_OK;
+}
+
+static bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+static size_t act_bytes(const pr2_moe_desc& d) { return d.act_dtype == PR2_BF16 ? 2 : 4; }
+
+static bool validate_env() {
+    const char* v = getenv("PR2_VALIDATE");
+    return v && v[0] == '1';
+}
+
+// ------------------------------------------------------- device check ----
+static pr2_status device_ready() {
+    static std::mutex mu;
+    static std::map<int, int> ok_dev;  // device -> 1 gfx950, 0 not
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) {
+        (void)hipGetLastError();
+        return fail(PR2_ERR_DEVICE, "no usable HIP device");
+    }
+    std::lock_guard<std::mutex> lk(mu);
+    auto it = ok_dev.find(dev);
+    if (it == ok_dev.end()) {
+        hipDeviceProp_t prop;
+        if (hipGetDeviceProperties(&prop, dev) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(PR2_ERR_DEVICE, "hipGetDeviceProperties failed on device %d", dev);
+        }
+        int good = strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+        it = ok_dev.emplace(dev, good).first;
+    }
+    if (!it->second) return fail(PR2_ERR_DEVICE, "device %d is not gfx950 (MI355X)", dev);
+    return PR2_OK;
+}
+
+static pr2_status hip_fail(hipError_t e, const char* what) {
+    return fail(PR2_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// --------------------------------------------------- descriptor checks ----
+static pr2_status check_desc(const pr2_moe_desc* d, bool need_m, bool need_idx_dtype) {
+    if (!d) return fail(PR2_ERR_NULL, "desc is NULL");
+    if (d->act_dtype != PR2_F32 && d->act_dtype != PR2_BF16)
+        return fail(PR2_ERR_DTYPE, "act_dtype %d is not PR2_F32 or PR2_BF16", d->act_dtype);
+    if (need_idx_dtype && d->idx_dtype != PR2_I32 && d->idx_dtype != PR2_I16)
+        return fail(PR2_ERR_DTYPE, "idx_dtype %d is not PR2_I32 or PR2_I16", d->idx_dtype);
+    if (d->T < 0) return fail(PR2_ERR_SHAPE, "T = %lld < 0", (long long)d->T);
+    if (d->d < 1) return fail(PR2_ERR_SHAPE, "d = %d < 1", d->d);
+    if (d->N < 1) return fail(PR2_ERR_SHAPE, "N = %d < 1", d->N);
+    if (d->k < 1 || d->k > d->N) return fail(PR2_ERR_SHAPE, "k = %d not in [1, N = %d]", d->k, d->N);
+    if (d->r < 0) return fail(PR2_ERR_SHAPE, "r = %d < 0", d->r);
+    if (need_m && d->m < 1) return fail(PR2_ERR_SHAPE, "m = %d < 1", d->m);
+    if (d->renorm != 0 && d->renorm != 1) return fail(PR2_ERR_SHAPE, "renorm = %d is not 0 or 1", d->renorm);
+    if (d->N > kMaxExperts) return fail(PR2_ERR_UNSUPPORTED, "N = %d > %d", d->N, kMaxExperts);
+    if (d->k > 256) return fail(PR2_ERR_UNSUPPORTED, "k = %d > 256", d->k);
+    if (need_idx_dtype && d->idx_dtype == PR2_I16 && d->N > 32767)
+        return fail(PR2_ERR_SHAPE, "int16 ids need N <= 32767");
+    if (d->T > 0 && d->T * (int64_t)d->k >= ((int64_t)1 << 31))
+        return fail(PR2_ERR_UNSUPPORTED, "T*k = %lld routes exceed 2^31 - 1", (long long)(d->T * d->k));
+    return PR2_OK;
+}
+
+// ----------------------------------------------------------- workspace ----
+static size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+ReplayWs replay_ws_layout(const pr2_moe_desc& d, void* base) {
+    ReplayWs w{};
+    const int64_t Tk = d.T * (int64_t)d.k;
+    const int tb = perm_tokens_per_block(d.k);
+    w.nblk = (d.T + tb - 1) / tb;
+    w.max_tiles = (Tk + kTileM - 1) / kTileM + d.N;
+    const size_t ab = act_bytes(d);
+    char* p = (char*)(((uintptr_t)base + 255) & ~(uintptr_t)255);
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        char* q = p ? p + off : nullptr;
+        off += up256(bytes);
+        return q;
+    };
+    w.gate = (float*)take(sizeof(float) * Tk);
+    w.err = (int*)take(sizeof(int) * ERR_WORDS);
+    w.bcount = (int*)take(sizeof(int) * (size_t)d.N * w.nblk);
+    w.offsets = (int*)take(sizeof(int) * (size_t)(d.N + 1));
+    w.tile_count = (int*)take(sizeof(int));
+    w.tiles = (int*)take(sizeof(int) * 3 * (size_t)w.max_tiles);
+    w.perm_src = (int*)take(sizeof(int) * Tk);
+    w.inv = (int*)take(sizeof(int) * Tk);
+    w.H = take(ab * Tk * (size_t)d.m);
+    w.O = take(ab * Tk * (size_t)d.d);
+    w.bytes = off + 256;   // slack for aligning the caller's base
+    return w;
+}
+
+// ---------------------------------------------------- measurement hooks ----
+struct ProfState {
+    bool on = false;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> pool;
+    std::vector<int> free_slots;
+    std::vector<std::pair<const char*, int>> pending;
+    std::map<std::string, std::pair<double, int64_t>> totals;
+    std::vector<std::string> order;
+    std::vector<std::string> name_store;
+};
+static ProfState g_prof;
+
+LaunchScope::LaunchScope(const char* n, hipStream_t s) : name(n), stream(s), slot(-1) {
+    if (!g_prof.on) return;
+    if (g_prof.free_slots.empty()) {
+        hipEvent_t a, b;
+        if (hipEventCreate(&a) != hipSuccess) return;
+        if (hipEventCreate(&b) != hipSuccess) { (void)hipEventDestroy(a); return; }
+        g_prof.pool.push_back({a, b});
+        g_prof.free_slots.push_back((int)g_prof.pool.size() - 1);
+    }
+    slot = g_prof.free_slots.back();
+    g_prof.free_slots.pop_back();
+    (void)hipEventRecord(g_prof.pool[slot].first, stream);
+}
+
+LaunchScope::~LaunchScope() {
+    if (slot < 0) return;
+    (void)hipEventRecord(g_prof.pool[slot].second, stream);
+    g_prof.pending.push_back({name, slot});
+}
+
+}  // namespace pr2
+
+using namespace pr2;
+
+extern "C" {
+
+const char* pr2_version(void) { return "pr2-mi355x 0.1"; }
+
+const char* pr2_status_string(pr2_status s) {
+    switch (s) {
+        case PR2_OK: return "PR2_OK";
+        case PR2_ERR_NULL: return "PR2_ERR_NULL";
+        case PR2_ERR_SHAPE: return "PR2_ERR_SHAPE";
+        case PR2_ERR_DTYPE: return "PR2_ERR_DTYPE";
+        case PR2_ERR_ALIGN: return "PR2_ERR_ALIGN";
+        case PR2_ERR_WORKSPACE: return "PR2_ERR_WORKSPACE";
+        case PR2_ERR_UNSUPPORTED: return "PR2_ERR_UNSUPPORTED";
+        case PR2_ERR_ROUTE: return "PR2_ERR_ROUTE";
+        case PR2_ERR_DEVICE: return "PR2_ERR_DEVICE";
+        case PR2_ERR_HIP: return "PR2_ERR_HIP";
+    }
+    return "PR2_ERR_UNKNOWN";
+}
+
+const char* pr2_last_error(void) { return t_err.c_str(); }
+
+size_t pr2_workspace_bytes(const pr2_moe_desc* desc, int op) {
+    if (!desc) return 0;
+    switch (op) {
+        case PR2_OP_ROUTE:
+            return 0;
+        case PR2_OP_REPLAY_FWD: {
+            std::string saved = t_err;
+            pr2_status s = check_desc(desc, true, true);
+            t_err = saved;
+            if (s != PR2_OK) return 0;
+            return replay_ws_layout(*desc, nullptr).bytes;
+        }
+        default:
+            return 0;
+    }
+}
+
+pr2_status pr2_route_predict(const pr2_moe_desc* desc, const void* x, const float* W_r,
+                             const float* b_r, const float* A, const float* B, void* idx_out,
+                             int64_t ldi, float* gate_out, float* logits_out, void* ws,
+                             size_t ws_bytes, pr2_stream_t stream) {
+    (void)ws;
+    (void)ws_bytes;
+    pr2_status s = check_desc(desc, false, true);
+    if (s != PR2_OK) return s;
+    const pr2_moe_desc& d = *desc;
+    if (d.r > 256) return fail(PR2_ERR_UNSUPPORTED, "predictor rank r = %d > 256", d.r);
+    if (ldi < d.k) return fail(PR2_ERR_SHAPE, "ldi = %lld < k = %d", (long long)ldi, d.k);
+    if (d.T == 0) return ok();
+    if (!x) return fail(PR2_ERR_NULL, "x is NULL");
+    if (!W_r) return fail(PR2_ERR_NULL, "W_r is NULL");
+    if (!idx_out) return fail(PR2_ERR_NULL, "idx_out is NULL");
+    if (d.r > 0 && !A) return fail(PR2_ERR_NULL, "A is NULL with r = %d > 0", d.r);
+    if (d.r > 0 && !B && d.r != d.N)
+        return fail(PR2_ERR_NULL, "B is NULL but r = %d != N = %d (identity needs r == N)", d.r, d.N);
+    if (!aligned(x, 16)) return fail(PR2_ERR_ALIGN, "x is not 16-byte aligned");
+    if (!aligned(W_r, 4) || (b_r && !aligned(b_r, 4)) || (A && !aligned(A, 4)) ||
+        (B && !aligned(B, 4)))
+        return fail(PR2_ERR_ALIGN, "an fp32 router/predictor tensor is not 4-byte aligned");
+    if (!aligned(idx_out, d.idx_dtype == PR2_I16 ? 2 : 4))
+        return fail(PR2_ERR_ALIGN, "idx_out is not aligned to its element size");
+    if ((gate_out && !aligned(gate_out, 4)) || (logits_out && !aligned(logits_out, 4)))
+        return fail(PR2_ERR_ALIGN, "gate_out / logits_out is not 4-byte aligned");
+    s = device_ready();
+    if (s != PR2_OK) return s;
+    hipError_t e = launch_route_predict(d, x, W_r, b_r, A, B, idx_out, ldi, gate_out, logits_out,
+                                        (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "route_predict launch");
+    return ok();
+}
+
+pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const void* idx,
+                                  int64_t ldi, const float* W_r, const float* b_r,
+                                  const void* W_gate, const void* W_up, const void* W_down,
+                                  void* y, float* gate_out, void* ws, size_t ws_bytes,
+                                  pr2_stream_t stream) {
+    pr2_status s = check_desc(desc, true, true);
+    if (s != PR2_OK) return s;
+    const pr2_moe_desc& d = *desc;
+    if (ldi < d.k) return fail(PR2_ERR_SHAPE, "ldi = %lld < k = %d", (long long)ldi, d.k);
+    if (d.T == 0) return ok();
+    if (!x) return fail(PR2_ERR_NULL, "x is NULL");
+    if (!idx) return fail(PR2_ERR_NULL, "idx is NULL");
+    if (!W_r) return fail(PR2_ERR_NULL, "W_r is NULL");
+    if (!W_gate || !W_up || !W_down) return fail(PR2_ERR_NULL, "an expert weight pointer is NULL");
+    if (!y) return fail(PR2_ERR_NULL, "y is NULL");
+    if (!aligned(x, 16) || !aligned(y, 16) || !aligned(W_gate, 16) || !aligned(W_up, 16) ||
+        !aligned(W_down, 16))
+        return fail(PR2_ERR_ALIGN, "x, y and expert weights must be 16-byte aligned");
+    if (!aligned(W_r, 4) || (b_r && !aligned(b_r, 4)) || (gate_out && !aligned(gate_out, 4)))
+        return fail(PR2_ERR_ALIGN, "an fp32 tensor is not 4-byte aligned");
+    if (!aligned(idx, d.idx_dtype == PR2_I16 ? 2 : 4))
+        return fail(PR2_ERR_ALIGN, "idx is not aligned to its element size");
+    const size_t need = replay_ws_layout(d, nullptr).bytes;
+    if (!ws) return fail(PR2_ERR_NULL, "ws is NULL (need %zu bytes)", need);
+    if (ws_bytes < need)
+        return fail(PR2_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
+    s = device_ready();
+    if (s != PR2_OK) return s;
+
+    hipStream_t st = (hipStream_t)stream;
+    ReplayWs w = replay_ws_layout(d, ws);
+    const bool validate = validate_env();
+    hipError_t e;
+    if (validate) {
+        e = hipMemsetAsync(w.err, 0, sizeof(int) * ERR_WORDS, st);
+        if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
+    }
+    float* gate = gate_out ? gate_out : w.gate;
+    e = launch_replay_gates(d, x, idx, ldi, W_r, b_r, gate, w.err, st);
+    if (e != hipSuccess) return hip_fail(e, "replay_gates launch");
+    e = launch_permute(d, idx, ldi, w, st);
+    if (e != hipSuccess) return hip_fail(e, "permute launch");
+    e = launch_expert_gemms(d, x, W_gate, W_up, W_down, gate, w, st);
+    if (e != hipSuccess) return hip_fail(e, "expert GEMM launch");
+    e = launch_combine(d, w, y, st);
+    if (e != hipSuccess) return hip_fail(e, "combine launch");
+    if (validate) {
+        int errs[ERR_WORDS];
+        e = hipMemcpyAsync(errs, w.err, sizeof(errs), hipMemcpyDeviceToHost, st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
+        if (e != hipSuccess) return hip_fail(e, "validation readback");
+        if (errs[ERR_BAD_ID] || errs[ERR_DUP_ID])
+            return fail(PR2_ERR_ROUTE, "route has %d out-of-range and %d repeated ids",
+                        errs[ERR_BAD_ID], errs[ERR_DUP_ID]);
+    }
+    return ok();
+}
+
+void pr2_profile_enable(int on) { g_prof.on = on != 0; }
+
+void pr2_profile_reset(void) {
+    for (auto& p : g_prof.pending) g_prof.free_slots.push_back(p.second);
+    g_prof.pending.clear();
+    g_prof.totals.clear();
+    g_prof.order.clear();
+}
+
+int pr2_profile_collect(const char** names, double* total_ms, int64_t* launches, int cap) {
+    for (auto& p : g_prof.pending) {
+        auto& ev = g_prof.pool[p.second];
+        if (hipEventSynchronize(ev.second) != hipSuccess) return -1;
+        float ms = 0.0f;
+        if (hipEventElapsedTime(&ms, ev.first, ev.second) != hipSuccess) return -1;
+        std::string key(p.first);
+        auto it = g_prof.totals.find(key);
+        if (it == g_prof.totals.end()) {
+            g_prof.totals[key] = {0.0, 0};
+            g_prof.order.push_back(key);
+        }
+        g_prof.totals[key].first += ms;
+        g_prof.totals[key].second += 1;
+        g_prof.free_slots.push_back(p.second);
+    }
+    g_prof.pending.clear();
+    g_prof.name_store = g_prof.order;
+    int n = (int)g_prof.order.size();
+    for (int i = 0; i < n && i < cap; ++i) {
+        const auto& t = g_prof.totals[g_prof.order[i]];
+        if (names) names[i] = g_prof.name_store[i].c_str();
+        if (total_ms) total_ms[i] = t.first;
+        if (launches) launches[i] = t.second;
+    }
+    return n;
+}
+
+}  // extern "C"

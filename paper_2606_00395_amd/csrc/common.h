@@ -1,0 +1,106 @@
+// Internal declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "../../include/pr2.h"
+
+namespace pr2 {
+
+// ---------------------------------------------------------------- bf16 ----
+typedef uint16_t bf16_t;                    // storage of one bf16 value
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t v) {
+    return __uint_as_float(((uint32_t)v) << 16);
+}
+
+// round to nearest even; NaN stays NaN
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (bf16_t)(u >> 16);
+}
+
+template <typename T> struct Act;
+template <> struct Act<float> {
+    __device__ __forceinline__ static float load(const float* p) { return *p; }
+    __device__ __forceinline__ static float to_f32(float v) { return v; }
+    __device__ __forceinline__ static float from_f32(float v) { return v; }
+};
+template <> struct Act<bf16_t> {
+    __device__ __forceinline__ static float load(const bf16_t* p) { return bf16_to_f32(*p); }
+    __device__ __forceinline__ static float to_f32(bf16_t v) { return bf16_to_f32(v); }
+    __device__ __forceinline__ static bf16_t from_f32(float v) { return f32_to_bf16(v); }
+};
+
+__device__ __forceinline__ int load_id(const void* idx, int idx_dtype, int64_t pos) {
+    return idx_dtype == PR2_I16 ? (int)((const int16_t*)idx)[pos] : ((const int32_t*)idx)[pos];
+}
+
+// ------------------------------------------------------------ limits -----
+constexpr int kMaxExperts = 1024;
+constexpr int kEntriesPerPermBlock = 512;   // (token, slot) entries per permutation block
+constexpr int kTileM = 128;                 // rows per grouped-GEMM tile (tile list granularity)
+
+inline int perm_tokens_per_block(int k) {
+    int tb = kEntriesPerPermBlock / k;
+    return tb < 1 ? 1 : tb;
+}
+
+// error-word slots in the workspace
+enum { ERR_BAD_ID = 0, ERR_DUP_ID = 1, ERR_WORDS = 4 };
+
+// ----------------------------------------------------------- workspace ----
+struct ReplayWs {
+    float* gate;        // [T*k] (used when the caller passes no gate_out)
+    int* err;           // [ERR_WORDS]
+    int* bcount;        // [nblk*N]  per-block counts, then per-block bases
+    int* offsets;       // [N+1]
+    int* tile_count;    // [1]
+    int* tiles;         // [max_tiles*3]: expert, first permuted row, rows
+    int* perm_src;      // [T*k] permuted row -> t*k + s
+    int* inv;           // [T*k] t*k + s -> permuted row (or -1)
+    void* H;            // [T*k, m] act
+    void* O;            // [T*k, d] act
+    int64_t nblk;
+    int64_t max_tiles;
+    size_t bytes;
+};
+
+ReplayWs replay_ws_layout(const pr2_moe_desc& d, void* base);
+
+// ------------------------------------------------------------ launches ----
+// Every launch goes through this so that measurement events can bracket it.
+struct LaunchScope {
+    LaunchScope(const char* name, hipStream_t s);
+    ~LaunchScope();
+    const char* name;
+    hipStream_t stream;
+    int slot;
+};
+
+// router.hip
+hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const float* W_r,
+                                const float* b_r, const float* A, const float* B, void* idx_out,
+                                int64_t ldi, float* gate_out, float* logits_out, hipStream_t s);
+hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void* idx, int64_t ldi,
+                               const float* W_r, const float* b_r, float* gate_out, int* err,
+                               hipStream_t s);
+
+// permute.hip
+hipError_t launch_permute(const pr2_moe_desc& d, const void* idx, int64_t ldi, const ReplayWs& ws,
+                          hipStream_t s);
+hipError_t launch_combine(const pr2_moe_desc& d, const ReplayWs& ws, void* y, hipStream_t s);
+
+// gemm.hip
+hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void* W_gate,
+                               const void* W_up, const void* W_down, const float* gate,
+                               const ReplayWs& ws, hipStream_t s);
+
+}  // namespace pr2

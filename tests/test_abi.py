@@ -1,0 +1,149 @@
+"""C ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, and rejects invalid arguments on the host before any HIP call
+(outputs untouched, documented status).  A valid call on a machine without a
+GPU must report PR2_ERR_DEVICE rather than crash."""
+import ctypes
+import os
+import re
+from ctypes import byref, c_void_p
+
+import pytest
+
+from paper_2606_00395_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+pytestmark = pytest.mark.skipif(not os.path.exists(B.LIB_PATH), reason="libpr2.so not built")
+
+FAKE = 0x10000   # a 64 KiB-aligned fake device address: never dereferenced by these tests
+
+
+def header_symbols():
+    with open(os.path.join(ROOT, "include", "pr2.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(pr2_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    L = B.lib()
+    syms = header_symbols()
+    assert set(syms) == set(B.EXPORTS), syms
+    for s in syms:
+        assert hasattr(L, s), s
+    assert L.pr2_version().decode().startswith("pr2")
+
+
+def test_status_strings():
+    L = B.lib()
+    for code, name in enumerate(B.STATUS):
+        assert L.pr2_status_string(code).decode() == name
+    assert L.pr2_status_string(99).decode() == "PR2_ERR_UNKNOWN"
+
+
+def desc(**kw):
+    base = dict(T=64, d=64, N=8, k=2, m=32, r=4, act=B.PR2_BF16, idx=B.PR2_I32, renorm=True)
+    base.update(kw)
+    return B.make_desc(**base)
+
+
+def route(d, x=FAKE, W=FAKE, b=None, A=FAKE, Bm=FAKE, idx=FAKE, ldi=None, gate=None, logits=None):
+    L = B.lib()
+    ldi = d.k if ldi is None else ldi
+    st = L.pr2_route_predict(byref(d), c_void_p(x), c_void_p(W), c_void_p(b), c_void_p(A),
+                             c_void_p(Bm), c_void_p(idx), ldi, c_void_p(gate), c_void_p(logits),
+                             None, 0, None)
+    return st, L.pr2_last_error().decode()
+
+
+def replay(d, x=FAKE, idx=FAKE, ldi=None, W=FAKE, b=None, Wg=FAKE, Wu=FAKE, Wd=FAKE, y=FAKE,
+           gate=None, ws=FAKE, ws_bytes=None):
+    L = B.lib()
+    ldi = d.k if ldi is None else ldi
+    if ws_bytes is None:
+        ws_bytes = B.workspace_bytes(d, B.OP_REPLAY_FWD)
+    st = L.pr2_moe_replay_forward(byref(d), c_void_p(x), c_void_p(idx), ldi, c_void_p(W),
+                                  c_void_p(b), c_void_p(Wg), c_void_p(Wu), c_void_p(Wd),
+                                  c_void_p(y), c_void_p(gate), c_void_p(ws), ws_bytes, None)
+    return st, L.pr2_last_error().decode()
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(k=0), "PR2_ERR_SHAPE"),
+    (dict(k=9), "PR2_ERR_SHAPE"),
+    (dict(d=0), "PR2_ERR_SHAPE"),
+    (dict(N=0, k=1), "PR2_ERR_SHAPE"),
+    (dict(T=-1), "PR2_ERR_SHAPE"),
+    (dict(r=-1), "PR2_ERR_SHAPE"),
+    (dict(act=7), "PR2_ERR_DTYPE"),
+    (dict(idx=5), "PR2_ERR_DTYPE"),
+    (dict(N=2048, k=8), "PR2_ERR_UNSUPPORTED"),
+    (dict(r=300), "PR2_ERR_UNSUPPORTED"),
+])
+def test_route_rejects_bad_descriptor(kw, status):
+    st, msg = route(desc(**kw))
+    assert B.STATUS[st] == status, msg
+    assert msg
+
+
+def test_route_rejects_bad_pointers_and_strides():
+    d = desc()
+    assert B.STATUS[route(d, x=0)[0]] == "PR2_ERR_NULL"
+    assert B.STATUS[route(d, W=0)[0]] == "PR2_ERR_NULL"
+    assert B.STATUS[route(d, idx=0)[0]] == "PR2_ERR_NULL"
+    assert B.STATUS[route(d, A=0)[0]] == "PR2_ERR_NULL"          # r > 0 needs A
+    assert B.STATUS[route(d, Bm=0)[0]] == "PR2_ERR_NULL"         # r != N needs B
+    assert B.STATUS[route(d, ldi=1)[0]] == "PR2_ERR_SHAPE"       # ldi < k
+    assert B.STATUS[route(d, x=FAKE + 2)[0]] == "PR2_ERR_ALIGN"
+    assert B.STATUS[route(d, W=FAKE + 2)[0]] == "PR2_ERR_ALIGN"
+    assert B.STATUS[route(d, idx=FAKE + 2)[0]] == "PR2_ERR_ALIGN"
+    d16 = desc(idx=B.PR2_I16)
+    # int16 ids only need 2-byte alignment (a decode step writes at buf + pos*k)
+    st, msg = route(d16, idx=FAKE + 2)
+    assert B.STATUS[st] in ("PR2_ERR_DEVICE", "PR2_OK"), msg
+
+
+def test_route_noop_and_device_status():
+    # T == 0 is a no-op even with null tensors
+    assert route(desc(T=0), x=0, W=0, idx=0, A=0, Bm=0)[0] == 0
+    # no predictor: A and B may be null
+    st, msg = route(desc(r=0), A=0, Bm=0)
+    assert B.STATUS[st] in ("PR2_ERR_DEVICE", "PR2_OK"), msg
+    # full-rank predictor: B = NULL means identity when r == N
+    st, msg = route(desc(r=8), Bm=0)
+    assert B.STATUS[st] in ("PR2_ERR_DEVICE", "PR2_OK"), msg
+
+
+def test_replay_rejects_bad_arguments():
+    d = desc()
+    need = B.workspace_bytes(d, B.OP_REPLAY_FWD)
+    assert need > 0
+    assert B.STATUS[replay(d, ws_bytes=need - 1)[0]] == "PR2_ERR_WORKSPACE"
+    assert B.STATUS[replay(d, ws=0)[0]] == "PR2_ERR_NULL"
+    assert B.STATUS[replay(d, y=0)[0]] == "PR2_ERR_NULL"
+    assert B.STATUS[replay(d, Wd=0)[0]] == "PR2_ERR_NULL"
+    assert B.STATUS[replay(d, idx=0)[0]] == "PR2_ERR_NULL"
+    assert B.STATUS[replay(d, y=FAKE + 8)[0]] == "PR2_ERR_ALIGN"
+    assert B.STATUS[replay(d, ldi=1)[0]] == "PR2_ERR_SHAPE"
+    assert B.STATUS[replay(desc(m=0))[0]] == "PR2_ERR_SHAPE"
+    assert replay(desc(T=0), x=0, idx=0, W=0, Wg=0, Wu=0, Wd=0, y=0, ws=0, ws_bytes=0)[0] == 0
+    assert B.workspace_bytes(desc(k=0), B.OP_REPLAY_FWD) == 0
+    assert B.workspace_bytes(None if False else desc(), B.OP_ROUTE) == 0
+
+
+def test_valid_call_without_gpu_reports_device():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    st, msg = route(desc())
+    assert B.STATUS[st] == "PR2_ERR_DEVICE", msg
+    st, msg = replay(desc())
+    assert B.STATUS[st] == "PR2_ERR_DEVICE", msg
+
+
+def test_workspace_grows_with_tokens():
+    a = B.workspace_bytes(desc(T=1000), B.OP_REPLAY_FWD)
+    b = B.workspace_bytes(desc(T=2000), B.OP_REPLAY_FWD)
+    assert b > a > 0
+    # H [T*k, m] and O [T*k, d] in bf16 dominate
+    d = desc(T=16384, d=2048, N=128, k=8, m=768)
+    assert B.workspace_bytes(d, B.OP_REPLAY_FWD) >= 16384 * 8 * (768 + 2048) * 2

@@ -1,0 +1,140 @@
+"""GPU parity of pr2_route_predict against the float64 oracle (Sec. 4.1,
+Eq. pr2_predict / pr2_route): ids bit-exact outside the 1e-6 margin rule,
+gates within 1e-5 relative, router logits (feature-cache p_old) within fp32
+rounding, on seeded inputs from tiny to the full Qwen3-30B-A3B-shaped layer."""
+import numpy as np
+import pytest
+
+from oracle import pr2_oracle as O
+import workloads as W
+from tests.parity import compare_route, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def torch_mod():
+    import torch
+    return torch
+
+
+def run_route(L, shape, k, renorm=True, idx_dtype="int32", ldi_pad=0, predictor=True,
+              full_rank=False, logits=False):
+    torch = torch_mod()
+    from paper_2606_00395_amd import binding as B
+    x = to_dev(L["x"], shape.act)
+    Wr = to_dev(L["W_r"])
+    br = to_dev(L["beta"]) if L["beta"] is not None else None
+    A = to_dev(L["A"]) if predictor else None
+    Bm = None if (full_rank or not predictor) else to_dev(L["B"])
+    T = L["x"].shape[0]
+    dt = torch.int16 if idx_dtype == "int16" else torch.int32
+    buf = torch.full((T, k + ldi_pad), -7, dtype=dt, device="cuda")
+    idx = buf[:, :k]
+    gate = torch.empty((T, k), dtype=torch.float32, device="cuda")
+    lg = torch.empty((T, L["W_r"].shape[1]), dtype=torch.float32, device="cuda") if logits else None
+    B.route_predict(x, Wr, br, A, Bm, k, idx, gate, lg, renorm=renorm)
+    torch.cuda.synchronize()
+    out = {"idx": idx.cpu().numpy(), "gate": gate.cpu().numpy(), "buf": buf.cpu().numpy()}
+    if logits:
+        out["logits"] = lg.cpu().numpy()
+    return out
+
+
+def oracle_route(L, k, renorm=True, predictor=True, full_rank=False):
+    A = L["A"] if predictor else None
+    Bm = None if (full_rank or not predictor) else L["B"]
+    return O.route_predict(L["x"], L["W_r"], L["beta"], A, Bm, k, renorm)
+
+
+def test_route_tiny_fp32():
+    s = W.WORKLOADS["tiny_fp32_T256"]
+    L = W.layer_inputs(s, 0, experts=False)
+    g = run_route(L, s, s.k, logits=True)
+    ref = oracle_route(L, s.k)
+    assert compare_route(g["idx"], g["gate"], ref, s.k, "tiny") == 0
+    np.testing.assert_allclose(g["logits"], ref["p"], rtol=0, atol=1e-6)
+
+
+CASES = [
+    # (T, d, N, k, r, act, skew, idx_dtype, ldi_pad, renorm, full_rank)
+    (1000, 256, 16, 4, 8, "bf16", "hot8", "int32", 0, True, False),
+    (777, 200, 60, 6, 5, "bf16", "zipf", "int16", 3, True, False),
+    (513, 64, 128, 8, 16, "f32", "none", "int32", 8, False, False),
+    (300, 128, 256, 16, 0, "bf16", "hot8", "int32", 0, True, False),
+    (129, 96, 1024, 8, 32, "bf16", "zipf", "int16", 0, True, False),
+    (64, 128, 32, 32, 4, "f32", "none", "int32", 0, True, False),       # k = N
+    (250, 64, 1, 1, 0, "f32", "none", "int32", 0, True, False),         # N = 1
+    (200, 64, 64, 2, 64, "bf16", "none", "int32", 0, True, True),       # full-rank W_p = A
+    (33, 1024, 128, 8, 256, "bf16", "hot8", "int32", 0, False, False),  # NC > 256, literal
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"T{c[0]}_d{c[1]}_N{c[2]}_k{c[3]}_r{c[4]}_{c[5]}"
+                                              for c in CASES])
+def test_route_shapes(case):
+    T, d, N, k, r, act, skew, idt, pad, renorm, full = case
+    s = W.LayerShape("case", T=T, d=d, N=N, k=k, m=8, r=r, act=act, skew=skew)
+    L = W.layer_inputs(s, 3, experts=False)
+    g = run_route(L, s, k, renorm=renorm, idx_dtype=idt, ldi_pad=pad, predictor=r > 0,
+                  full_rank=full, logits=True)
+    ref = oracle_route(L, k, renorm=renorm, predictor=r > 0, full_rank=full)
+    compare_route(g["idx"], g["gate"], ref, k, str(case))
+    if pad:
+        assert np.all(g["buf"][:, k:] == -7), "padding beyond k was written"
+    np.testing.assert_allclose(g["logits"], ref["p"], rtol=0, atol=2e-6 * max(1.0, np.abs(ref["p"]).max()))
+
+
+def test_route_exact_ties_go_to_lower_id():
+    """One-hot router inputs make every logit an exact small integer, so ties
+    are exact and the lower id must win (no margin exclusion)."""
+    rng = np.random.default_rng(21)
+    T, d, N, k = 512, 64, 16, 5
+    x = np.zeros((T, d), dtype=np.float32)
+    x[np.arange(T), np.arange(T) % d] = 1.0
+    Wr = rng.integers(-2, 3, size=(d, N)).astype(np.float32)
+    L = {"x": x, "W_r": Wr, "beta": None, "A": None, "B": None}
+    s = W.LayerShape("ties", T=T, d=d, N=N, k=k, m=8, r=0, act="bf16")
+    g = run_route(L, s, k, predictor=False)
+    ref = O.route_predict(x, Wr, None, None, None, k)
+    np.testing.assert_array_equal(g["idx"], ref["idx"])
+    np.testing.assert_allclose(g["gate"], ref["gate"], rtol=1e-6)
+    # signed zeros tie too
+    x2 = np.zeros((2, d), dtype=np.float32)
+    x2[:, 0] = [1.0, -1.0]
+    Wz = np.zeros((d, N), dtype=np.float32)   # logits are +0.0 and -0.0
+    L2 = {"x": x2, "W_r": Wz, "beta": None, "A": None, "B": None}
+    g2 = run_route(L2, s.with_(T=2), k, predictor=False)
+    np.testing.assert_array_equal(g2["idx"], np.tile(np.arange(k), (2, 1)))
+
+
+def test_route_zero_predictor_equals_router_only():
+    s = W.LayerShape("zp", T=700, d=256, N=64, k=6, m=8, r=8, act="bf16", skew="hot8")
+    L = W.layer_inputs(s, 5, experts=False)
+    L0 = dict(L, A=np.zeros_like(L["A"]))
+    g0 = run_route(L0, s, s.k)
+    gn = run_route(L, s.with_(r=0), s.k, predictor=False)
+    np.testing.assert_array_equal(g0["idx"], gn["idx"])
+    np.testing.assert_array_equal(g0["gate"], gn["gate"])
+
+
+def test_route_qwen3_30b_full():
+    s = W.WORKLOADS["qwen3_30b_T16384"]
+    L = W.layer_inputs(s, 0, experts=False)
+    g = run_route(L, s, s.k, logits=True)
+    ref = oracle_route(L, s.k)
+    excl = compare_route(g["idx"], g["gate"], ref, s.k, s.name)
+    print(f"\n{s.name}: {excl} of {s.T} tokens under the 1e-6 margin")
+    np.testing.assert_allclose(g["logits"], ref["p"], rtol=0, atol=4e-6)
+    # determinism: a second call is bitwise identical
+    g2 = run_route(L, s, s.k)
+    np.testing.assert_array_equal(g["idx"], g2["idx"])
+    np.testing.assert_array_equal(g["gate"], g2["gate"])
+
+
+def test_route_empty_batch():
+    torch = torch_mod()
+    from paper_2606_00395_amd import binding as B
+    x = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")
+    Wr = torch.zeros((64, 8), device="cuda")
+    idx = torch.empty((0, 2), dtype=torch.int32, device="cuda")
+    B.route_predict(x, Wr, None, None, None, 2, idx)
