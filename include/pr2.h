@@ -104,7 +104,11 @@ size_t pr2_workspace_bytes(const pr2_moe_desc* desc, int op);
  *              (pass idx_out = buf + pos*k, ldi = n_pos*k).
  *   gate_out   [T, k] fp32, aligned with idx_out's order; may be NULL.
  *   logits_out [T, N] fp32 router logits p (without the predictor term); may be NULL.
- *   ws         unused (pr2_workspace_bytes(desc, PR2_OP_ROUTE) is 0).
+ *   ws         scratch of at least pr2_workspace_bytes(desc, PR2_OP_ROUTE) bytes (the bf16
+ *              three-way split of [W_r | A] that the MFMA router reads; 0 bytes when the shape
+ *              takes the fp64 vector path).  Reused freely between calls on one stream.
+ * Logits are accumulated from exact products (fp32 weights split into three bf16 parts times
+ * bf16 x, or fp64 FMA for fp32 x) in fp32 chunks summed in fp64, then rounded once to fp32.
  */
 pr2_status pr2_route_predict(const pr2_moe_desc* desc, const void* x, const float* W_r,
                              const float* b_r, const float* A, const float* B, void* idx_out,

@@ -133,17 +133,28 @@ def workspace_bytes(desc: MoeDesc, op: int) -> int:
     return int(lib().pr2_workspace_bytes(byref(desc), op))
 
 
+def route_workspace(x, W_r, A, k, idx_dtype_code=PR2_I32):
+    torch = _torch()
+    T, d = x.shape
+    r = 0 if A is None else A.shape[1]
+    desc = make_desc(T, d, W_r.shape[1], k, 0, r, _act_code(x), idx_dtype_code)
+    n = workspace_bytes(desc, OP_ROUTE)
+    return torch.empty(max(1, n), dtype=torch.uint8, device=x.device)
+
+
 def route_predict(x, W_r, b_r, A, B, k, idx_out, gate_out=None, logits_out=None, renorm=True,
-                  stream=None):
+                  ws=None, stream=None):
     """pr2_route_predict on torch tensors.  ``idx_out`` is a [T, k] view (any row stride)
     of int16/int32; A/B may be None (no predictor); B None with A given means identity."""
     T, d = x.shape
     N = W_r.shape[1]
     r = 0 if A is None else A.shape[1]
     desc = make_desc(T, d, N, k, 0, r, _act_code(x), _idx_code(idx_out), renorm)
+    if ws is None:
+        ws = route_workspace(x, W_r, A, k, _idx_code(idx_out))
     check(lib().pr2_route_predict(byref(desc), _ptr(x), _ptr(W_r), _ptr(b_r), _ptr(A), _ptr(B),
                                   _ptr(idx_out), _row_stride(idx_out), _ptr(gate_out),
-                                  _ptr(logits_out), None, 0, _stream(stream)))
+                                  _ptr(logits_out), _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def replay_workspace(x, idx, W_r, W_gate, renorm=True):

@@ -119,8 +119,21 @@ ReplayWs replay_ws_layout(const pr2_moe_desc& d, void* base) {
     w.inv = (int*)take(sizeof(int) * Tk);
     w.H = take(ab * Tk * (size_t)d.m);
     w.O = take(ab * Tk * (size_t)d.d);
+    w.wsplit = take(router_mfma_ok(d, d.N) ? router_split_bytes(d.N, d.d) : 0);
     w.bytes = off + 256;   // slack for aligning the caller's base
     return w;
+}
+
+// The route call folds the predictor into the router weights (N columns) when the
+// caller wants no logits, and projects [W_r | A] (N + r columns) otherwise.
+static size_t route_ws_bytes(const pr2_moe_desc& d) {
+    size_t need = 0;
+    if (router_mfma_ok(d, d.N)) need = router_split_bytes(d.N, d.d);
+    if (router_mfma_ok(d, d.N + d.r)) {
+        size_t b = router_split_bytes(d.N + d.r, d.d);
+        need = b > need ? b : need;
+    }
+    return need ? need + 256 : 0;
 }
 
 // ---------------------------------------------------- measurement hooks ----
@@ -184,8 +197,13 @@ const char* pr2_last_error(void) { return t_err.c_str(); }
 size_t pr2_workspace_bytes(const pr2_moe_desc* desc, int op) {
     if (!desc) return 0;
     switch (op) {
-        case PR2_OP_ROUTE:
-            return 0;
+        case PR2_OP_ROUTE: {
+            std::string saved = t_err;
+            pr2_status s = check_desc(desc, false, true);
+            t_err = saved;
+            if (s != PR2_OK || desc->r < 0) return 0;
+            return route_ws_bytes(*desc);
+        }
         case PR2_OP_REPLAY_FWD: {
             std::string saved = t_err;
             pr2_status s = check_desc(desc, true, true);
@@ -202,8 +220,6 @@ pr2_status pr2_route_predict(const pr2_moe_desc* desc, const void* x, const floa
                              const float* b_r, const float* A, const float* B, void* idx_out,
                              int64_t ldi, float* gate_out, float* logits_out, void* ws,
                              size_t ws_bytes, pr2_stream_t stream) {
-    (void)ws;
-    (void)ws_bytes;
     pr2_status s = check_desc(desc, false, true);
     if (s != PR2_OK) return s;
     const pr2_moe_desc& d = *desc;
@@ -224,10 +240,15 @@ pr2_status pr2_route_predict(const pr2_moe_desc* desc, const void* x, const floa
         return fail(PR2_ERR_ALIGN, "idx_out is not aligned to its element size");
     if ((gate_out && !aligned(gate_out, 4)) || (logits_out && !aligned(logits_out, 4)))
         return fail(PR2_ERR_ALIGN, "gate_out / logits_out is not 4-byte aligned");
+    const size_t need = route_ws_bytes(d);
+    if (need && !ws) return fail(PR2_ERR_NULL, "ws is NULL (need %zu bytes)", need);
+    if (ws_bytes < need)
+        return fail(PR2_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
     s = device_ready();
     if (s != PR2_OK) return s;
+    void* split = need ? (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255) : nullptr;
     hipError_t e = launch_route_predict(d, x, W_r, b_r, A, B, idx_out, ldi, gate_out, logits_out,
-                                        (hipStream_t)stream);
+                                        split, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "route_predict launch");
     return ok();
 }
@@ -270,7 +291,7 @@ pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const
         if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
     }
     float* gate = gate_out ? gate_out : w.gate;
-    e = launch_replay_gates(d, x, idx, ldi, W_r, b_r, gate, w.err, st);
+    e = launch_replay_gates(d, x, idx, ldi, W_r, b_r, gate, w.err, w.wsplit, st);
     if (e != hipSuccess) return hip_fail(e, "replay_gates launch");
     e = launch_permute(d, idx, ldi, w, st);
     if (e != hipSuccess) return hip_fail(e, "permute launch");

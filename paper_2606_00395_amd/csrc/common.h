@@ -46,7 +46,7 @@ __device__ __forceinline__ int load_id(const void* idx, int idx_dtype, int64_t p
 // ------------------------------------------------------------ limits -----
 constexpr int kMaxExperts = 1024;
 constexpr int kEntriesPerPermBlock = 512;   // (token, slot) entries per permutation block
-constexpr int kTileM = 128;                 // rows per grouped-GEMM tile (tile list granularity)
+constexpr int kTileM = 256;                 // rows per grouped-GEMM tile (tile list granularity)
 
 inline int perm_tokens_per_block(int k) {
     int tb = kEntriesPerPermBlock / k;
@@ -68,6 +68,7 @@ struct ReplayWs {
     int* inv;           // [T*k] t*k + s -> permuted row (or -1)
     void* H;            // [T*k, m] act
     void* O;            // [T*k, d] act
+    void* wsplit;       // router weight split (bf16 x 3)
     int64_t nblk;
     int64_t max_tiles;
     size_t bytes;
@@ -86,12 +87,17 @@ struct LaunchScope {
 };
 
 // router.hip
+// Scratch for the bf16 three-way split of [W_r | A] used by the MFMA router
+// (0 when the shape takes the fp64 vector path).
+size_t router_split_bytes(int NC, int d);
+bool router_mfma_ok(const pr2_moe_desc& d, int NC);
 hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const float* W_r,
                                 const float* b_r, const float* A, const float* B, void* idx_out,
-                                int64_t ldi, float* gate_out, float* logits_out, hipStream_t s);
+                                int64_t ldi, float* gate_out, float* logits_out, void* split_ws,
+                                hipStream_t s);
 hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void* idx, int64_t ldi,
                                const float* W_r, const float* b_r, float* gate_out, int* err,
-                               hipStream_t s);
+                               void* split_ws, hipStream_t s);
 
 // permute.hip
 hipError_t launch_permute(const pr2_moe_desc& d, const void* idx, int64_t ldi, const ReplayWs& ws,

@@ -4,16 +4,19 @@
 //   GEMM1  H[rows_e, m] = silu(X_e W_gate_e^T) * (X_e W_up_e^T)   X_e gathered from x
 //   GEMM2  O[rows_e, d] = g * (H_e W_down_e^T)                     g = replay weight
 //
-// bf16 path (d % 256 == 0, m % 128 == 0): one workgroup computes a 128-row tile
+// bf16 path (d % 256 == 0, m % 128 == 0): one workgroup computes a 256-row tile
 // of one expert against a 256-row panel of weights (GEMM1: 128 gate rows + the
-// matching 128 up rows; GEMM2: 256 rows of W_down), K staged through LDS in
-// slices of 32 with two LDS buffers and register prefetch of the next slice.
-// Four wavefronts in a 2 x 2 arrangement each own 64 rows x 128 panel rows as
-// 2 x 4 tiles of v_mfma_f32_32x32x16_bf16 (fp32 accumulation).  GEMM1's
-// epilogue applies SwiGLU in registers (gate and up tiles of the same columns
-// live in the same lanes) and rounds H to bf16; GEMM2's epilogue scales by the
-// route weight and rounds O to bf16.  Workgroups are mapped so that each XCD
-// takes a contiguous range of the tile list (same experts, shared L2).
+// matching 128 up rows; GEMM2: 256 rows of W_down).  K advances in slices of 64
+// (one 128-byte line per row) copied straight from global memory into LDS with
+// 16-byte DMA loads (no register staging), two LDS stages deep, 16-byte chunks
+// XOR-swizzled per row so the MFMA operand reads are free of bank conflicts.
+// Eight wavefronts (two per SIMD) in a 4 x 2 arrangement each own 64 rows x 128
+// panel rows as 2 x 4 tiles of v_mfma_f32_32x32x16_bf16 (fp32 accumulation); a
+// wavefront whose rows are all past the end of a partial tile skips its MFMAs.
+// GEMM1's epilogue applies SwiGLU in registers (gate and up tiles of the same
+// columns live in the same lanes) and rounds H to bf16; GEMM2's epilogue scales
+// by the route weight and rounds O to bf16.  Workgroups are mapped so that each
+// XCD takes a contiguous range of the tile list (same experts, shared L2).
 //
 // Other shapes and the fp32 path use a plain one-thread-per-output kernel.
 #include "common.h"
@@ -22,13 +25,15 @@ namespace pr2 {
 namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int BM = kTileM;      // 128 rows per tile
+constexpr int BM = kTileM;      // 256 rows per tile
 constexpr int BP = 256;         // weight panel rows per tile
-constexpr int BK = 32;          // K slice
-constexpr int LDS_STRIDE = BK + 8;  // bf16 elements per LDS row (16 B pad: no bank conflicts)
-constexpr int kGemmThreads = 256;
+constexpr int BK = 64;          // K slice: one 128-byte line per row
+constexpr int ROWB = BK * 2;    // bytes per LDS row (unpadded; chunks are swizzled)
+constexpr int kGemmThreads = 512;   // 8 wavefronts: 4 row quarters x 2 panel halves
 constexpr int kNumXcd = 8;
+constexpr int kGroups = (BM + BP) / 8 / (kGemmThreads / 64);   // 8-row DMA groups per wavefront
 
 struct MfmaArgs {
     const bf16_t* A;        // GEMM1: x [T, d]; GEMM2: H [T*k, m]
@@ -48,10 +53,15 @@ struct MfmaArgs {
 
 __device__ __forceinline__ float silu_f(float a) { return a / (1.0f + __expf(-a)); }
 
+// 16-byte chunk c of LDS row r is stored at position c ^ swz(r): rows 16 apart
+// repeat the pattern, and any 16 (or 8) consecutive rows read at the same
+// chunk hit disjoint banks.
+__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
 template <int MODE>
 __global__ void __launch_bounds__(kGemmThreads)
 grouped_gemm_mfma(MfmaArgs g) {
-    __shared__ __attribute__((aligned(16))) bf16_t lds[2][(BM + BP) * LDS_STRIDE];
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[2][(BM + BP) * ROWB];
 
     // XCD-aware mapping: physical block b runs on XCD b % 8; give each XCD a
     // contiguous range of the (tile, panel) work list.
@@ -70,61 +80,42 @@ grouped_gemm_mfma(MfmaArgs g) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int wr = wave >> 1;     // 64-row half
+    const int wr = wave >> 1;     // 64-row quarter
     const int wc = wave & 1;      // panel half
+    // a wavefront whose 64 rows are all past the tile's end only helps copy
+    const bool active = wr * 64 < rows;
 
-    // global source rows of this thread's copy chunks (16 B = 8 bf16 each)
-    // A: 128 rows x 4 chunks = 512 chunks, 2 per thread; panel: 256 x 4 = 1024, 4 per thread
-    const bf16_t* a_src[2];
-    bool a_ok[2];
-    int a_lds[2];
+    // DMA assignments: wavefront w copies 8-row groups w*kGroups .. of the
+    // [A rows | panel rows] tile; lane l moves row 8*grp + l/8, position l%8.
+    const bf16_t* src[kGroups];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        int q = tid + kGemmThreads * i;
-        int r = q >> 2, c = q & 3;
-        a_ok[i] = r < rows;
-        int64_t arow;
-        if (MODE == 0) {
-            int src = a_ok[i] ? g.perm_src[row0 + r] : 0;
-            arow = src / g.k;
+    for (int i = 0; i < kGroups; ++i) {
+        const int grp = wave * kGroups + i;
+        const int r = grp * 8 + (lane >> 3);          // row in [0, BM + BP)
+        const int chunk = (lane & 7) ^ swz(r);
+        const bf16_t* rowp;
+        if (r < BM) {
+            // rows past the tile's end read a valid row; their results are never stored
+            const int rr = r < rows ? r : 0;
+            if (MODE == 0) rowp = g.A + (int64_t)(g.perm_src[row0 + rr] / g.k) * g.K;
+            else rowp = g.A + ((int64_t)row0 + rr) * g.K;
         } else {
-            arow = a_ok[i] ? (int64_t)row0 + r : 0;
+            const int pr = r - BM;
+            if (MODE == 0)
+                rowp = (pr < 128 ? g.W0 : g.W1) + (int64_t)expert * g.w_stride +
+                       (int64_t)(pn * 128 + (pr & 127)) * g.K;
+            else
+                rowp = g.W0 + (int64_t)expert * g.w_stride + (int64_t)(pn * BP + pr) * g.K;
         }
-        a_src[i] = g.A + arow * g.K + c * 8;
-        a_lds[i] = r * LDS_STRIDE + c * 8;
+        src[i] = rowp + chunk * 8;
     }
-    const bf16_t* b_src[4];
-    int b_lds[4];
+    auto issue = [&](int buf, int k0) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        int q = tid + kGemmThreads * i;
-        int r = q >> 2, c = q & 3;
-        const bf16_t* wbase;
-        int wrow;
-        if (MODE == 0) {
-            wbase = (r < 128 ? g.W0 : g.W1) + (int64_t)expert * g.w_stride;
-            wrow = pn * 128 + (r & 127);
-        } else {
-            wbase = g.W0 + (int64_t)expert * g.w_stride;
-            wrow = pn * BP + r;
+        for (int i = 0; i < kGroups; ++i) {
+            const int grp = wave * kGroups + i;
+            __builtin_amdgcn_global_load_lds((const void*)(src[i] + k0),
+                                             (lds_void*)&lds[buf][grp * 8 * ROWB], 16, 0, 0);
         }
-        b_src[i] = wbase + (int64_t)wrow * g.K + c * 8;
-        b_lds[i] = (BM + r) * LDS_STRIDE + c * 8;
-    }
-
-    u32x4 ra[2], rb[4];
-    auto load_global = [&](int k0) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-            ra[i] = a_ok[i] ? *(const u32x4*)(a_src[i] + k0) : u32x4{0, 0, 0, 0};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) rb[i] = *(const u32x4*)(b_src[i] + k0);
-    };
-    auto store_lds = [&](int buf) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) *(u32x4*)&lds[buf][a_lds[i]] = ra[i];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) *(u32x4*)&lds[buf][b_lds[i]] = rb[i];
     };
 
     f32x16 acc[2][4];
@@ -137,44 +128,51 @@ grouped_gemm_mfma(MfmaArgs g) {
 
     // LDS rows each lane reads for its MFMA operands
     const int lrow = lane & 31;
-    const int lk = (lane >> 5) * 8;
-    int a_rd[2], b_rd[4];
+    const int lhalf = lane >> 5;           // 8-element half of the K=16 step
+    int a_row[2], b_row[4];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) a_rd[i] = (wr * 64 + i * 32 + lrow) * LDS_STRIDE + lk;
+    for (int i = 0; i < 2; ++i) a_row[i] = wr * 64 + i * 32 + lrow;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         int prow;
         if (MODE == 0) prow = (j < 2 ? 0 : 128) + wc * 64 + (j & 1) * 32 + lrow;
         else prow = wc * 128 + j * 32 + lrow;
-        b_rd[j] = (BM + prow) * LDS_STRIDE + lk;
+        b_row[j] = BM + prow;
     }
 
     const int nk = g.K / BK;
-    load_global(0);
-    store_lds(0);
+    issue(0, 0);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
         const int cur = kt & 1;
-        if (kt + 1 < nk) load_global((kt + 1) * BK);
+        if (kt + 1 < nk) issue(cur ^ 1, (kt + 1) * BK);
+        if (active) {
+            const unsigned char* base = lds[cur];
 #pragma unroll
-        for (int ks = 0; ks < BK; ks += 16) {
-            bf16x8 fa[2], fb[4];
+            for (int ks = 0; ks < BK / 16; ++ks) {
+                const int c = 2 * ks + lhalf;
+                bf16x8 fa[2], fb[4];
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
-                fa[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)&lds[cur][a_rd[i] + ks]);
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                fb[j] = __builtin_bit_cast(bf16x8, *(const u32x4*)&lds[cur][b_rd[j] + ks]);
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
+                for (int i = 0; i < 2; ++i)
+                    fa[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + a_row[i] * ROWB +
+                                                                       ((c ^ swz(a_row[i])) << 4)));
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j],
-                                                                         0, 0, 0);
+                    fb[j] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + b_row[j] * ROWB +
+                                                                       ((c ^ swz(b_row[j])) << 4)));
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j],
+                                                                             acc[i][j], 0, 0, 0);
+            }
         }
-        if (kt + 1 < nk) store_lds(cur ^ 1);
+        __builtin_amdgcn_s_waitcnt(0);     // this wavefront's copies of the next slice landed
         __syncthreads();
     }
+    if (!active) return;
 
     // epilogue: 32x32 accumulator element v of lane l is
     // C[8*(v/4) + 4*(l/32) + v%4][l%32]
@@ -214,8 +212,8 @@ gemm1_generic(const T* x, const int* perm_src, int k, const T* Wg, const T* Wu, 
     const int tile = blockIdx.x;
     if (tile >= *tile_count) return;
     const int expert = tiles[3 * tile], row0 = tiles[3 * tile + 1], rows = tiles[3 * tile + 2];
-    const int r = threadIdx.x % BM;
-    const int col = blockIdx.y * 2 + threadIdx.x / BM;
+    const int r = threadIdx.x;
+    const int col = blockIdx.y;
     if (r >= rows || col >= m) return;
     const int64_t tok = perm_src[row0 + r] / k;
     const T* xr = x + tok * d;
@@ -237,8 +235,8 @@ gemm2_generic(const T* H, const int* perm_src, const float* gate, const T* Wd, i
     const int tile = blockIdx.x;
     if (tile >= *tile_count) return;
     const int expert = tiles[3 * tile], row0 = tiles[3 * tile + 1], rows = tiles[3 * tile + 2];
-    const int r = threadIdx.x % BM;
-    const int col = blockIdx.y * 2 + threadIdx.x / BM;
+    const int r = threadIdx.x;
+    const int col = blockIdx.y;
     if (r >= rows || col >= d) return;
     const T* h = H + (int64_t)(row0 + r) * m;
     const T* w = Wd + ((int64_t)expert * d + col) * m;
@@ -298,8 +296,9 @@ hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void*
         }
         return hipGetLastError();
     }
-    dim3 grid1((unsigned)ws.max_tiles, (unsigned)((d.m + 1) / 2));
-    dim3 grid2((unsigned)ws.max_tiles, (unsigned)((d.d + 1) / 2));
+    static_assert(BM == 256, "generic kernels map one thread per tile row");
+    dim3 grid1((unsigned)ws.max_tiles, (unsigned)d.m);
+    dim3 grid2((unsigned)ws.max_tiles, (unsigned)d.d);
     if (d.act_dtype == PR2_BF16) {
         {
             LaunchScope scope("gemm1_generic", s);

@@ -64,31 +64,44 @@ __device__ int block_exclusive_scan(int v, int* sh, int* total) {
     return incl - v;
 }
 
-// counts: [N * nblk] expert-major; rewritten in place with exclusive prefixes.
+// counts: [N * nblk] expert-major; rewritten in place with each block's first
+// output position per expert.  One wavefront per expert scans that expert's
+// block counts (coalesced, 64 blocks per step); the expert totals are then
+// scanned across experts and added back in a second coalesced pass.
 __global__ void __launch_bounds__(kScanThreads)
 perm_scan_kernel(int* counts, int64_t nblk, int N, int bm, int* offsets, int* tiles,
                  int* tile_count) {
     __shared__ int sh[kScanThreads];
     __shared__ int s_off[kMaxExperts + 1];
     const int tid = threadIdx.x;
-    const int64_t L = (int64_t)N * nblk;
-    const int64_t chunk = (L + kScanThreads - 1) / kScanThreads;
-    const int64_t lo = tid * chunk;
-    const int64_t hi = lo + chunk < L ? lo + chunk : L;
-    int sum = 0;
-    for (int64_t i = lo; i < hi; ++i) sum += counts[i];
-    int grand;
-    int run = block_exclusive_scan(sum, sh, &grand);
-    for (int64_t i = lo; i < hi; ++i) {
-        int c = counts[i];
-        counts[i] = run;
-        run += c;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    for (int e = wave; e < N; e += kScanThreads / 64) {
+        int* row = counts + (int64_t)e * nblk;
+        int carry = 0;
+        for (int64_t b0 = 0; b0 < nblk; b0 += 64) {
+            const int64_t b = b0 + lane;
+            const int c = b < nblk ? row[b] : 0;
+            int incl = c;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                int y = __shfl_up(incl, off, 64);
+                if (lane >= off) incl += y;
+            }
+            if (b < nblk) row[b] = carry + incl - c;
+            carry += __shfl(incl, 63, 64);
+        }
+        if (lane == 0) s_off[e] = carry;
     }
-    __syncthreads();     // every thread's chunk written before reading expert starts
-    __threadfence_block();
-    for (int e = tid; e < N; e += kScanThreads) s_off[e] = counts[(int64_t)e * nblk];
+    __syncthreads();
+    int grand;
+    const int tot = tid < N ? s_off[tid] : 0;
+    const int ex = block_exclusive_scan(tot, sh, &grand);
+    if (tid < N) s_off[tid] = ex;
     if (tid == 0) s_off[N] = grand;
     __syncthreads();
+    const int64_t L = (int64_t)N * nblk;
+    for (int64_t q = tid; q < L; q += kScanThreads) counts[q] += s_off[q / nblk];
     // tiles per expert, and their exclusive prefix
     int ntile = 0;
     if (tid < N) {

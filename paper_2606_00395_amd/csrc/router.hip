@@ -2,17 +2,27 @@
 // rollout top-k epilogue (Sec. 4.1, Eq. pr2_predict / pr2_route), and the same
 // projection with the replay-weight epilogue (Sec. 4.1 replay, Eq. pr2_output).
 //
-// Projection: each block owns TM tokens and computes their logits against the
-// NC = N (+ r) columns of [W_r | A] in column passes.  x and the weight panel
-// are staged through LDS in K-slices of KB; each thread accumulates a 4-token x
-// 4-column micro-tile in float64, so the logits reach the epilogue with one
-// rounding to fp32 and the top-k decision does not depend on the summation
-// order over d.
+// MFMA path (bf16 x, d % 32 == 0, at most 192 projection columns).  x is bf16,
+// so each fp32 weight is split into three bf16 parts with hi + mid + lo == w
+// exactly and every MFMA product is exact; fp32 partial sums over two K-steps
+// of 32 are added into fp64 accumulators, and the logits are rounded to fp32
+// once.  When the caller does not ask for the router logits p, the predictor is
+// folded into the weights first (W_r + A B, formed in fp64 before the split),
+// so the projection has N columns; otherwise it has N + r columns [W_r | A]
+// and the epilogue forms z = p + u B in fp64.  The split weights are stored
+// K-tiled ([K/32][3 * columns][32] bf16) so that every K-step reads one
+// contiguous block.  A workgroup of 8 wavefronts owns 64 tokens; each
+// wavefront computes 32 tokens x a quarter of the columns with
+// v_mfma_f32_16x16x32_bf16.
 //
-// Epilogue: one wavefront per token.  Lane l holds logits l, l+64, ...; the
-// top-k is k rounds of a wavefront max over packed (orderable logit, ~id) keys,
-// so equal logits resolve to the lower id; the chosen ids are written in
-// ascending id order with their gates.
+// fp64 vector path (fp32 x or other shapes): each thread accumulates a 4-token
+// x 4-column micro-tile in fp64 from LDS-staged slices.
+//
+// Epilogues run one wavefront per token.  Rollout: k rounds of a DPP wavefront
+// max over orderable 32-bit logit keys, the lowest id among equal keys taken
+// by ballot, ids written ascending with their gates.  Replay: softmax over the
+// recorded ids (or over all N for the literal weights) from the current
+// router's logits.
 #include "common.h"
 
 namespace pr2 {
@@ -27,34 +37,17 @@ __device__ __forceinline__ uint32_t orderable(float z) {
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
-        uint32_t olo = __shfl_xor(lo, off, 64), ohi = __shfl_xor(hi, off, 64);
-        uint64_t o = ((uint64_t)ohi << 32) | olo;
-        v = o > v ? o : v;
-    }
-    return v;
+__device__ __forceinline__ float from_orderable(uint32_t key) {
+    return __uint_as_float((key & 0x80000000u) ? (key & 0x7fffffffu) : ~key);
 }
 
-__device__ __forceinline__ float wave_sum_f32(float v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
-    return v;
-}
-
-__device__ __forceinline__ float wave_max_f32(float v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
-    return v;
-}
-
-__device__ __forceinline__ int wave_sum_i32(int v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
-    return v;
-}
+// DPP wavefront reductions from the device library (fixed order: deterministic)
+extern "C" __device__ __attribute__((const)) float __ockl_wfred_add_f32(float);
+extern "C" __device__ __attribute__((const)) float __ockl_wfred_max_f32(float);
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) { return __ockl_wfred_max_u32(v); }
+__device__ __forceinline__ float wave_sum_f32(float v) { return __ockl_wfred_add_f32(v); }
+__device__ __forceinline__ float wave_max_f32(float v) { return __ockl_wfred_max_f32(v); }
+__device__ __forceinline__ int wave_sum_i32(int v) { return __ockl_wfred_add_i32(v); }
 
 struct ProjArgs {
     const void* x;
@@ -84,7 +77,6 @@ __device__ void project_tile(const ProjArgs& a, int64_t t0, float* xs, float* ws
             for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
 
         for (int k0 = 0; k0 < a.d; k0 += a.KB) {
-            // stage x[t0 .. t0+TM) x [k0 .. k0+KB) as fp32 (zero outside)
             for (int q = tid; q < a.TM * a.KB; q += kThreads) {
                 int tt = q / a.KB, kk = q % a.KB;
                 int64_t t = t0 + tt;
@@ -94,7 +86,6 @@ __device__ void project_tile(const ProjArgs& a, int64_t t0, float* xs, float* ws
                     v = Act<XT>::load((const XT*)a.x + t * (int64_t)a.d + kg);
                 xs[tt * a.KB + kk] = v;
             }
-            // stage the weight panel [k0 .. k0+KB) x [c0 .. c0+cols_per_pass)
             for (int q = tid; q < a.KB * cols_per_pass; q += kThreads) {
                 int kk = q / cols_per_pass, cc = q % cols_per_pass;
                 int kg = k0 + kk, c = c0 + cc;
@@ -134,181 +125,352 @@ __device__ void project_tile(const ProjArgs& a, int64_t t0, float* xs, float* ws
     __syncthreads();
 }
 
+// ------------------------------------------------------------ epilogues --
+struct PredictOut {
+    const float* b_r;     // [N] or null
+    const float* B;       // [r, N] or null (identity when r == N)
+    int k, renorm;
+    int folded;           // 1: the row holds x (W_r + A B); 0: [x W_r | x A]
+    void* idx_out;
+    int idx_dtype;
+    int64_t ldi;
+    float* gate_out;      // [T, k] or null
+    float* logits_out;    // [T, N] or null (only when not folded)
+};
+
+// One wavefront: rollout epilogue of token t from its LDS row of logits.
+__device__ void predict_token(const float* row, int64_t t, int N, int r, const PredictOut& o) {
+    const int lane = threadIdx.x & 63;
+    const int nv = (N + 63) / 64;
+    float z[kMaxLanesVals];
+    uint32_t key[kMaxLanesVals];
+    for (int v = 0; v < nv; ++v) {
+        int j = v * 64 + lane;
+        z[v] = -INFINITY;
+        key[v] = 0;                          // below every real logit's key
+        if (j < N) {
+            // p = xW + beta and z = p + (xA) B in fp64, one final rounding
+            double p = (double)row[j] + (o.b_r ? (double)o.b_r[j] : 0.0);
+            double zz = p;
+            if (!o.folded && r > 0) {
+                const float* u = row + N;
+                if (o.B) {
+                    for (int q = 0; q < r; ++q) zz += (double)u[q] * (double)o.B[(int64_t)q * N + j];
+                } else {
+                    zz += (double)u[j];      // B = identity (full-rank predictor)
+                }
+            }
+            if (o.logits_out) o.logits_out[t * N + j] = (float)p;
+            z[v] = (float)zz;
+            key[v] = orderable(z[v]);
+        }
+    }
+    // k rounds of a wavefront arg-max; among equal logits the lower id wins
+    uint32_t taken = 0;
+    float zmax = 0.0f;
+    for (int it = 0; it < o.k; ++it) {
+        uint32_t best = 0;
+        for (int v = 0; v < nv; ++v)
+            if (!((taken >> v) & 1u) && key[v] > best) best = key[v];
+        const uint32_t wmax = wave_max_u32(best);
+        int jw = 0;
+        for (int v = 0; v < nv; ++v) {
+            const int j = v * 64 + lane;
+            uint64_t m = __ballot(j < N && !((taken >> v) & 1u) && key[v] == wmax);
+            if (m) {
+                jw = v * 64 + (__ffsll((unsigned long long)m) - 1);
+                break;
+            }
+        }
+        if (it == 0) zmax = from_orderable(wmax);
+        if ((jw & 63) == lane) taken |= 1u << (jw >> 6);
+    }
+    float e[kMaxLanesVals];
+    float s_sel = 0.0f, s_all = 0.0f;
+    for (int v = 0; v < nv; ++v) {
+        int j = v * 64 + lane;
+        e[v] = 0.0f;
+        if (j < N) {
+            e[v] = expf(z[v] - zmax);
+            s_all += e[v];
+            if ((taken >> v) & 1u) s_sel += e[v];
+        }
+    }
+    const float denom = o.renorm ? wave_sum_f32(s_sel) : wave_sum_f32(s_all);
+    // ids ascending, gates aligned
+    int before = 0;
+    for (int v = 0; v < nv; ++v) {
+        bool mine = (taken >> v) & 1u;
+        uint64_t bal = __ballot(mine);
+        if (mine) {
+            uint64_t lt = lane ? (bal & ((~0ull) >> (64 - lane))) : 0ull;
+            int rank = before + __popcll(lt);
+            int j = v * 64 + lane;
+            int64_t pos = t * o.ldi + rank;
+            if (o.idx_dtype == PR2_I16) ((int16_t*)o.idx_out)[pos] = (int16_t)j;
+            else ((int32_t*)o.idx_out)[pos] = j;
+            if (o.gate_out) o.gate_out[t * o.k + rank] = e[v] / denom;
+        }
+        before += __popcll(bal);
+    }
+}
+
+struct ReplayOut {
+    const float* b_r;
+    int k, renorm;
+    const void* idx;
+    int idx_dtype;
+    int64_t ldi;
+    float* gate_out;      // [T, k]
+    int* err;
+    int validate;
+};
+
+// One wavefront: replay weights of token t over its recorded ids from the LDS
+// row of N current-router logits (predictor bypassed).
+__device__ void replay_token(const float* row, int64_t t, int N, const ReplayOut& o) {
+    const int lane = threadIdx.x & 63;
+    auto logit = [&](int j) {
+        return (float)((double)row[j] + (o.b_r ? (double)o.b_r[j] : 0.0));
+    };
+    float ref;
+    if (o.renorm) {
+        float pmax_sel = -INFINITY;
+        for (int s = lane; s < o.k; s += 64) {
+            int id = load_id(o.idx, o.idx_dtype, t * o.ldi + s);
+            if (id >= 0 && id < N) pmax_sel = fmaxf(pmax_sel, logit(id));
+        }
+        ref = wave_max_f32(pmax_sel);
+    } else {
+        float pmax_all = -INFINITY;
+        for (int j = lane; j < N; j += 64) pmax_all = fmaxf(pmax_all, logit(j));
+        ref = wave_max_f32(pmax_all);
+    }
+    float part = 0.0f;
+    if (o.renorm) {
+        for (int s = lane; s < o.k; s += 64) {
+            int id = load_id(o.idx, o.idx_dtype, t * o.ldi + s);
+            if (id >= 0 && id < N) part += expf(logit(id) - ref);
+        }
+    } else {
+        for (int j = lane; j < N; j += 64) part += expf(logit(j) - ref);
+    }
+    const float denom = wave_sum_f32(part);
+    int bad = 0;
+    for (int s = lane; s < o.k; s += 64) {
+        int id = load_id(o.idx, o.idx_dtype, t * o.ldi + s);
+        float g = 0.0f;
+        if (id >= 0 && id < N) g = expf(logit(id) - ref) / denom;
+        else bad++;
+        o.gate_out[t * o.k + s] = g;
+    }
+    if (o.validate) {
+        int dup = 0;
+        for (int s = lane; s < o.k; s += 64) {
+            int id = load_id(o.idx, o.idx_dtype, t * o.ldi + s);
+            for (int s2 = 0; s2 < s; ++s2)
+                if (load_id(o.idx, o.idx_dtype, t * o.ldi + s2) == id) dup++;
+        }
+        dup = wave_sum_i32(dup);
+        int nbad = wave_sum_i32(bad);
+        if (lane == 0) {
+            if (nbad) atomicAdd(o.err + ERR_BAD_ID, nbad);
+            if (dup) atomicAdd(o.err + ERR_DUP_ID, dup);
+        }
+    }
+}
+
+// ------------------------------------------------- fp64 vector-ALU path ----
 template <typename XT>
 __global__ void __launch_bounds__(kThreads)
-route_predict_kernel(ProjArgs a, const float* b_r, const float* B, int k, int renorm,
-                     void* idx_out, int idx_dtype, int64_t ldi, float* gate_out,
-                     float* logits_out) {
+route_predict_kernel(ProjArgs a, PredictOut o) {
     extern __shared__ float smem[];
     float* xs = smem;                                   // TM*KB
     float* ws = xs + a.TM * a.KB;                       // KB*cols_per_pass
     const int cols_per_pass = (kThreads / (a.TM / 4)) * 4;
     float* lg = ws + a.KB * cols_per_pass;              // TM*NC
-
     const int64_t t0 = (int64_t)blockIdx.x * a.TM;
     project_tile<XT>(a, t0, xs, ws, lg);
-
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int nv = (a.N + 63) / 64;
-    for (int tt = wave; tt < a.TM; tt += kThreads / 64) {
+    for (int tt = threadIdx.x >> 6; tt < a.TM; tt += kThreads / 64) {
         const int64_t t = t0 + tt;
         if (t >= a.T) break;
-        const float* row = lg + tt * a.NC;
-        float z[kMaxLanesVals];
-        float pz[kMaxLanesVals];
-        for (int v = 0; v < nv; ++v) {
-            int j = v * 64 + lane;
-            z[v] = -INFINITY;
-            pz[v] = 0.0f;
-            if (j < a.N) {
-                // p = xW + beta, then z = p + (xA) B, accumulated in fp64
-                double p = (double)row[j] + (b_r ? (double)b_r[j] : 0.0);
-                float pf = (float)p;
-                pz[v] = pf;
-                double zz = p;
-                if (a.r > 0) {
-                    const float* u = row + a.N;
-                    if (B) {
-                        for (int q = 0; q < a.r; ++q) zz += (double)u[q] * (double)B[(int64_t)q * a.N + j];
-                    } else {
-                        zz += (double)u[j];          // B = identity (full-rank predictor)
-                    }
-                }
-                z[v] = (float)zz;
-            }
-        }
-        if (logits_out) {
-            for (int v = 0; v < nv; ++v) {
-                int j = v * 64 + lane;
-                if (j < a.N) logits_out[t * a.N + j] = pz[v];
-            }
-        }
-        // k rounds of a wavefront arg-max; ties go to the lower id
-        uint32_t taken = 0;
-        float zmax = 0.0f;
-        for (int it = 0; it < k; ++it) {
-            uint64_t best = 0;
-            for (int v = 0; v < nv; ++v) {
-                int j = v * 64 + lane;
-                if (j < a.N && !((taken >> v) & 1u)) {
-                    uint64_t key = ((uint64_t)orderable(z[v]) << 32) | (uint32_t)(0xffffffffu - (uint32_t)j);
-                    best = key > best ? key : best;
-                }
-            }
-            best = wave_max_u64(best);
-            int jw = (int)(0xffffffffu - (uint32_t)best);
-            if (it == 0) {
-                // the top-1 logit, recovered from its owner lane
-                float zw = 0.0f;
-                for (int v = 0; v < nv; ++v)
-                    if (v * 64 + lane == jw) zw = z[v];
-                zmax = __shfl(zw, jw & 63, 64);
-            }
-            if ((jw & 63) == lane) taken |= 1u << (jw >> 6);
-        }
-        // weights
-        float e[kMaxLanesVals];
-        float s_sel = 0.0f, s_all = 0.0f;
-        for (int v = 0; v < nv; ++v) {
-            int j = v * 64 + lane;
-            e[v] = 0.0f;
-            if (j < a.N) {
-                e[v] = expf(z[v] - zmax);
-                s_all += e[v];
-                if ((taken >> v) & 1u) s_sel += e[v];
-            }
-        }
-        const float denom = renorm ? wave_sum_f32(s_sel) : wave_sum_f32(s_all);
-        // write ids ascending with their gates
-        int before = 0;
-        for (int v = 0; v < nv; ++v) {
-            bool mine = (taken >> v) & 1u;
-            uint64_t bal = __ballot(mine);
-            if (mine) {
-                uint64_t lt = lane ? (bal & ((~0ull) >> (64 - lane))) : 0ull;
-                int rank = before + __popcll(lt);
-                int j = v * 64 + lane;
-                int64_t pos = t * ldi + rank;
-                if (idx_dtype == PR2_I16) ((int16_t*)idx_out)[pos] = (int16_t)j;
-                else ((int32_t*)idx_out)[pos] = j;
-                if (gate_out) gate_out[t * k + rank] = e[v] / denom;
-            }
-            before += __popcll(bal);
-        }
+        predict_token(lg + tt * a.NC, t, a.N, a.r, o);
     }
 }
 
 template <typename XT>
 __global__ void __launch_bounds__(kThreads)
-replay_gates_kernel(ProjArgs a, const float* b_r, int k, int renorm, const void* idx,
-                    int idx_dtype, int64_t ldi, float* gate_out, int* err, int validate) {
+replay_gates_kernel(ProjArgs a, ReplayOut o) {
     extern __shared__ float smem[];
     float* xs = smem;
     float* ws = xs + a.TM * a.KB;
     const int cols_per_pass = (kThreads / (a.TM / 4)) * 4;
     float* lg = ws + a.KB * cols_per_pass;
-
     const int64_t t0 = (int64_t)blockIdx.x * a.TM;
     project_tile<XT>(a, t0, xs, ws, lg);
-
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    for (int tt = wave; tt < a.TM; tt += kThreads / 64) {
+    for (int tt = threadIdx.x >> 6; tt < a.TM; tt += kThreads / 64) {
         const int64_t t = t0 + tt;
         if (t >= a.T) break;
-        const float* row = lg + tt * a.NC;
-        // current-router logits p = xW + beta (predictor bypassed)
-        float pmax_all = -INFINITY;
-        for (int j = lane; j < a.N; j += 64) {
-            float p = (float)((double)row[j] + (b_r ? (double)b_r[j] : 0.0));
-            pmax_all = fmaxf(pmax_all, p);
-        }
-        pmax_all = wave_max_f32(pmax_all);
-        float pmax_sel = -INFINITY;
-        int bad = 0;
-        for (int s = lane; s < k; s += 64) {
-            int id = load_id(idx, idx_dtype, t * ldi + s);
-            if (id >= 0 && id < a.N) {
-                float p = (float)((double)row[id] + (b_r ? (double)b_r[id] : 0.0));
-                pmax_sel = fmaxf(pmax_sel, p);
+        replay_token(lg + tt * a.NC, t, a.N, o);
+    }
+}
+
+// ---------------------------------------------------------- MFMA path -----
+constexpr int kRTM = 64;                  // tokens per workgroup
+constexpr int kRBK = 32;                  // K step
+constexpr int kRStride = kRBK + 8;        // bf16 per LDS row (16 B pad)
+constexpr int kRThreads = 512;            // 8 wavefronts: 2 token halves x 4 column quarters
+constexpr int kRMaxNTW = 3;               // 16-column tiles per wavefront (<= 192 columns)
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Ws[kt][p * NCp + c][kk] = part p of column c at K index kt*32 + kk (zero for c >= NC).
+// Columns: folded -> W_r + A B (or W_r + A when B is null); else [W_r | A].
+__global__ void __launch_bounds__(256)
+router_split_kernel(const float* W_r, const float* A, const float* B, int d, int N, int r,
+                    int folded, int NCp, bf16_t* Ws) {
+    const int NC = folded ? N : N + r;
+    const int64_t total = (int64_t)NCp * d;
+    for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < total;
+         q += (int64_t)gridDim.x * 256) {
+        const int kk = (int)(q % kRBK);
+        const int c = (int)((q / kRBK) % NCp);
+        const int kt = (int)(q / ((int64_t)kRBK * NCp));
+        const int kg = kt * kRBK + kk;
+        double w = 0.0;
+        if (c < NC) {
+            if (c < N) {
+                w = (double)W_r[(int64_t)kg * N + c];
+                if (folded && r > 0) {
+                    if (B) {
+                        for (int j = 0; j < r; ++j)
+                            w += (double)A[(int64_t)kg * r + j] * (double)B[(int64_t)j * N + c];
+                    } else {
+                        w += (double)A[(int64_t)kg * r + c];
+                    }
+                }
             } else {
-                bad++;
+                w = (double)A[(int64_t)kg * r + (c - N)];
             }
         }
-        pmax_sel = wave_max_f32(pmax_sel);
-        const float ref = renorm ? pmax_sel : pmax_all;
-        float s_sel = 0.0f, s_all = 0.0f;
-        for (int s = lane; s < k; s += 64) {
-            int id = load_id(idx, idx_dtype, t * ldi + s);
-            if (id >= 0 && id < a.N)
-                s_sel += expf((float)((double)row[id] + (b_r ? (double)b_r[id] : 0.0)) - ref);
+        // three bf16 parts; for a weight representable in fp32 they sum to it exactly
+        const bf16_t hi = f32_to_bf16((float)w);
+        const double r1 = w - (double)bf16_to_f32(hi);
+        const bf16_t mid = f32_to_bf16((float)r1);
+        const bf16_t lo = f32_to_bf16((float)(r1 - (double)bf16_to_f32(mid)));
+        const int64_t base = (int64_t)kt * 3 * NCp * kRBK;
+        Ws[base + ((int64_t)c) * kRBK + kk] = hi;
+        Ws[base + ((int64_t)NCp + c) * kRBK + kk] = mid;
+        Ws[base + ((int64_t)2 * NCp + c) * kRBK + kk] = lo;
+    }
+}
+
+template <int NTW, int MODE>   // MODE 0: rollout, 1: replay
+__global__ void __launch_bounds__(kRThreads)
+router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, int r, int NC,
+                   PredictOut po, ReplayOut ro) {
+    constexpr int NCp = 64 * NTW;
+    constexpr int WROWS = 3 * NCp;
+    constexpr int WCH = (WROWS * 4 + kRThreads - 1) / kRThreads;
+    __shared__ __attribute__((aligned(16))) bf16_t xs[2][kRTM * kRStride];
+    __shared__ __attribute__((aligned(16))) bf16_t wsb[2][WROWS * kRStride];
+    static_assert(sizeof(bf16_t) * 2 * WROWS * kRStride >= sizeof(float) * kRTM * NCp,
+                  "logit tile must fit over the weight buffers");
+    const int64_t t0 = (int64_t)blockIdx.x * kRTM;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wr = wave >> 2, wc = wave & 3;
+
+    // copies: x 64 rows x 4 chunks (threads 0..255); weights WROWS x 4 chunks, contiguous
+    const int xr = (tid & 255) >> 2, xc = tid & 3;
+    const bool x_thread = tid < 256;
+    const bool x_ok = x_thread && t0 + xr < T;
+    const bf16_t* xsrc = x + (x_ok ? (t0 + xr) : 0) * (int64_t)d + xc * 8;
+    u32x4 rx, rw[WCH];
+    auto load_global = [&](int kt) {
+        rx = x_ok ? *(const u32x4*)(xsrc + kt * kRBK) : u32x4{0, 0, 0, 0};
+        const bf16_t* wk = Ws + (int64_t)kt * WROWS * kRBK;
+#pragma unroll
+        for (int i = 0; i < WCH; ++i) {
+            int q = tid + kRThreads * i;
+            if (q < WROWS * 4) rw[i] = *(const u32x4*)(wk + q * 8);
         }
-        if (!renorm)
-            for (int j = lane; j < a.N; j += 64)
-                s_all += expf((float)((double)row[j] + (b_r ? (double)b_r[j] : 0.0)) - ref);
-        const float denom = renorm ? wave_sum_f32(s_sel) : wave_sum_f32(s_all);
-        for (int s = lane; s < k; s += 64) {
-            int id = load_id(idx, idx_dtype, t * ldi + s);
-            float g = 0.0f;
-            if (id >= 0 && id < a.N)
-                g = expf((float)((double)row[id] + (b_r ? (double)b_r[id] : 0.0)) - ref) / denom;
-            gate_out[t * k + s] = g;
+    };
+    auto store_lds = [&](int b) {
+        if (x_thread) *(u32x4*)&xs[b][xr * kRStride + xc * 8] = rx;
+#pragma unroll
+        for (int i = 0; i < WCH; ++i) {
+            int q = tid + kRThreads * i;
+            if (q < WROWS * 4) *(u32x4*)&wsb[b][(q >> 2) * kRStride + (q & 3) * 8] = rw[i];
         }
-        if (validate) {
-            int dup = 0;
-            for (int s = lane; s < k; s += 64) {
-                int id = load_id(idx, idx_dtype, t * ldi + s);
-                for (int s2 = 0; s2 < s; ++s2)
-                    if (load_id(idx, idx_dtype, t * ldi + s2) == id) dup++;
+    };
+
+    f32x4 acc[2][NTW];
+    double acc64[2][NTW][4];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int t = 0; t < NTW; ++t)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) { acc[i][t][v] = 0.0f; acc64[i][t][v] = 0.0; }
+
+    const int lrow = lane & 15;
+    const int lk = (lane >> 4) * 8;
+    const int nk = d / kRBK;
+    load_global(0);
+    store_lds(0);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+        const int cur = kt & 1;
+        if (kt + 1 < nk) load_global(kt + 1);
+        bf16x8 fa[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+            fa[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)&xs[cur][(wr * 32 + i * 16 + lrow) * kRStride + lk]);
+#pragma unroll
+        for (int t = 0; t < NTW; ++t) {
+#pragma unroll
+            for (int p = 0; p < 3; ++p) {
+                const int wrow = p * NCp + (wc * NTW + t) * 16 + lrow;
+                bf16x8 fb = __builtin_bit_cast(bf16x8, *(const u32x4*)&wsb[cur][wrow * kRStride + lk]);
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+                    acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb, acc[i][t], 0, 0, 0);
             }
-            dup = wave_sum_i32(dup);
-            int nbad = wave_sum_i32(bad);
-            if (lane == 0) {
-                if (nbad) atomicAdd(err + ERR_BAD_ID, nbad);
-                if (dup) atomicAdd(err + ERR_DUP_ID, dup);
-            }
         }
+        if ((kt & 1) || kt + 1 == nk) {
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int t = 0; t < NTW; ++t)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        acc64[i][t][v] += (double)acc[i][t][v];
+                        acc[i][t][v] = 0.0f;
+                    }
+        }
+        if (kt + 1 < nk) store_lds(cur ^ 1);
+        __syncthreads();
+    }
+    // logits -> LDS [kRTM][NC]; 16x16 accumulator element v of lane l is C[4*(l/16)+v][l%16]
+    float* lg = (float*)&wsb[0][0];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int t = 0; t < NTW; ++t)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int tok = wr * 32 + i * 16 + 4 * (lane >> 4) + v;
+                const int col = (wc * NTW + t) * 16 + (lane & 15);
+                if (col < NC) lg[tok * NC + col] = (float)acc64[i][t][v];
+            }
+    __syncthreads();
+    for (int tt = wave; tt < kRTM; tt += kRThreads / 64) {
+        const int64_t t = t0 + tt;
+        if (t >= T) break;
+        if (MODE == 0) predict_token(lg + tt * NC, t, N, r, po);
+        else replay_token(lg + tt * NC, t, N, ro);
     }
 }
 
@@ -325,11 +487,66 @@ size_t router_smem(const ProjArgs& a) {
                             (size_t)a.TM * a.NC);
 }
 
+int ncp_of(int NC) { return ((NC + 63) / 64) * 64; }
+
+template <int MODE>
+hipError_t launch_router_mfma(const pr2_moe_desc& d, int NC, int r, const void* x,
+                              const bf16_t* Ws, const PredictOut& po, const ReplayOut& ro,
+                              hipStream_t s) {
+    const int NTW = ncp_of(NC) / 64;
+    dim3 grid((unsigned)((d.T + kRTM - 1) / kRTM));
+    const bf16_t* xb = (const bf16_t*)x;
+    switch (NTW) {
+#define PR2_CASE(n) case n: hipLaunchKernelGGL((router_mfma_kernel<n, MODE>), grid, dim3(kRThreads), 0, s, xb, Ws, d.T, d.d, d.N, r, NC, po, ro); break;
+        PR2_CASE(1) PR2_CASE(2) PR2_CASE(3)
+#undef PR2_CASE
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_split(const float* W_r, const float* A, const float* B, const pr2_moe_desc& d,
+                        int r, int folded, bf16_t* Ws, hipStream_t s) {
+    const int NC = folded ? d.N : d.N + r;
+    const int NCp = ncp_of(NC);
+    int64_t total = (int64_t)NCp * d.d;
+    int64_t blocks = (total + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    LaunchScope scope("router_split", s);
+    hipLaunchKernelGGL(router_split_kernel, dim3((unsigned)blocks), dim3(256), 0, s, W_r, A, B,
+                       d.d, d.N, r, folded, NCp, Ws);
+    return hipGetLastError();
+}
+
 }  // namespace
+
+size_t router_split_bytes(int NC, int d) { return (size_t)3 * ncp_of(NC) * d * sizeof(bf16_t); }
+
+bool router_mfma_ok(const pr2_moe_desc& d, int NC) {
+    return d.act_dtype == PR2_BF16 && d.d % kRBK == 0 && ncp_of(NC) <= 64 * kRMaxNTW;
+}
 
 hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const float* W_r,
                                 const float* b_r, const float* A, const float* B, void* idx_out,
-                                int64_t ldi, float* gate_out, float* logits_out, hipStream_t s) {
+                                int64_t ldi, float* gate_out, float* logits_out, void* split_ws,
+                                hipStream_t s) {
+    const float* Bn = d.r > 0 ? B : nullptr;
+    if (logits_out == nullptr && router_mfma_ok(d, d.N)) {
+        // the router logits are not wanted: fold the predictor into the weights
+        PredictOut o{b_r, Bn, d.k, d.renorm, 1, idx_out, d.idx_dtype, ldi, gate_out, nullptr};
+        hipError_t e = launch_split(W_r, A, Bn, d, d.r, 1, (bf16_t*)split_ws, s);
+        if (e != hipSuccess) return e;
+        LaunchScope scope("route_predict", s);
+        return launch_router_mfma<0>(d, d.N, d.r, x, (const bf16_t*)split_ws, o, ReplayOut{}, s);
+    }
+    PredictOut o{b_r, Bn, d.k, d.renorm, 0, idx_out, d.idx_dtype, ldi, gate_out, logits_out};
+    const int NC = d.N + d.r;
+    if (router_mfma_ok(d, NC)) {
+        hipError_t e = launch_split(W_r, A, Bn, d, d.r, 0, (bf16_t*)split_ws, s);
+        if (e != hipSuccess) return e;
+        LaunchScope scope("route_predict", s);
+        return launch_router_mfma<0>(d, NC, d.r, x, (const bf16_t*)split_ws, o, ReplayOut{}, s);
+    }
     ProjArgs a;
     a.x = x;
     a.W_r = W_r;
@@ -338,25 +555,30 @@ hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const floa
     a.d = d.d;
     a.N = d.N;
     a.r = d.r;
-    a.NC = d.N + d.r;
+    a.NC = NC;
     pick_tile(a);
     dim3 grid((unsigned)((d.T + a.TM - 1) / a.TM));
     size_t smem = router_smem(a);
     LaunchScope scope("route_predict", s);
     if (d.act_dtype == PR2_BF16)
-        hipLaunchKernelGGL(route_predict_kernel<bf16_t>, grid, dim3(kThreads), smem, s, a, b_r,
-                           d.r > 0 ? B : nullptr, d.k, d.renorm, idx_out, d.idx_dtype, ldi,
-                           gate_out, logits_out);
+        hipLaunchKernelGGL(route_predict_kernel<bf16_t>, grid, dim3(kThreads), smem, s, a, o);
     else
-        hipLaunchKernelGGL(route_predict_kernel<float>, grid, dim3(kThreads), smem, s, a, b_r,
-                           d.r > 0 ? B : nullptr, d.k, d.renorm, idx_out, d.idx_dtype, ldi,
-                           gate_out, logits_out);
+        hipLaunchKernelGGL(route_predict_kernel<float>, grid, dim3(kThreads), smem, s, a, o);
     return hipGetLastError();
 }
 
 hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void* idx, int64_t ldi,
                                const float* W_r, const float* b_r, float* gate_out, int* err,
-                               hipStream_t s) {
+                               void* split_ws, hipStream_t s) {
+    const char* v = getenv("PR2_VALIDATE");
+    ReplayOut o{b_r, d.k, d.renorm, idx, d.idx_dtype, ldi, gate_out, err,
+                (v && v[0] == '1') ? 1 : 0};
+    if (router_mfma_ok(d, d.N)) {
+        hipError_t e = launch_split(W_r, nullptr, nullptr, d, 0, 0, (bf16_t*)split_ws, s);
+        if (e != hipSuccess) return e;
+        LaunchScope scope("replay_gates", s);
+        return launch_router_mfma<1>(d, d.N, 0, x, (const bf16_t*)split_ws, PredictOut{}, o, s);
+    }
     ProjArgs a;
     a.x = x;
     a.W_r = W_r;
@@ -369,15 +591,11 @@ hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void*
     pick_tile(a);
     dim3 grid((unsigned)((d.T + a.TM - 1) / a.TM));
     size_t smem = router_smem(a);
-    const char* v = getenv("PR2_VALIDATE");
-    int validate = (v && v[0] == '1') ? 1 : 0;
     LaunchScope scope("replay_gates", s);
     if (d.act_dtype == PR2_BF16)
-        hipLaunchKernelGGL(replay_gates_kernel<bf16_t>, grid, dim3(kThreads), smem, s, a, b_r,
-                           d.k, d.renorm, idx, d.idx_dtype, ldi, gate_out, err, validate);
+        hipLaunchKernelGGL(replay_gates_kernel<bf16_t>, grid, dim3(kThreads), smem, s, a, o);
     else
-        hipLaunchKernelGGL(replay_gates_kernel<float>, grid, dim3(kThreads), smem, s, a, b_r,
-                           d.k, d.renorm, idx, d.idx_dtype, ldi, gate_out, err, validate);
+        hipLaunchKernelGGL(replay_gates_kernel<float>, grid, dim3(kThreads), smem, s, a, o);
     return hipGetLastError();
 }
 

@@ -46,12 +46,15 @@ def desc(**kw):
     return B.make_desc(**base)
 
 
-def route(d, x=FAKE, W=FAKE, b=None, A=FAKE, Bm=FAKE, idx=FAKE, ldi=None, gate=None, logits=None):
+def route(d, x=FAKE, W=FAKE, b=None, A=FAKE, Bm=FAKE, idx=FAKE, ldi=None, gate=None, logits=None,
+          ws=FAKE, ws_bytes=None):
     L = B.lib()
     ldi = d.k if ldi is None else ldi
+    if ws_bytes is None:
+        ws_bytes = B.workspace_bytes(d, B.OP_ROUTE)
     st = L.pr2_route_predict(byref(d), c_void_p(x), c_void_p(W), c_void_p(b), c_void_p(A),
                              c_void_p(Bm), c_void_p(idx), ldi, c_void_p(gate), c_void_p(logits),
-                             None, 0, None)
+                             c_void_p(ws), ws_bytes, None)
     return st, L.pr2_last_error().decode()
 
 
@@ -102,6 +105,19 @@ def test_route_rejects_bad_pointers_and_strides():
     assert B.STATUS[st] in ("PR2_ERR_DEVICE", "PR2_OK"), msg
 
 
+def test_route_workspace():
+    d = desc()
+    need = B.workspace_bytes(d, B.OP_ROUTE)
+    # bf16 x with d % 32 == 0 and N + r <= 160 takes the MFMA router: 3 bf16 parts of [W_r | A]
+    assert need >= 3 * 32 * 64 * 2
+    assert B.STATUS[route(d, ws_bytes=need - 1)[0]] == "PR2_ERR_WORKSPACE"
+    assert B.STATUS[route(d, ws=0)[0]] == "PR2_ERR_NULL"
+    # fp32 x takes the fp64 vector path: no workspace
+    assert B.workspace_bytes(desc(act=B.PR2_F32), B.OP_ROUTE) == 0
+    st, msg = route(desc(act=B.PR2_F32), ws=0, ws_bytes=0)
+    assert B.STATUS[st] in ("PR2_ERR_DEVICE", "PR2_OK"), msg
+
+
 def test_route_noop_and_device_status():
     # T == 0 is a no-op even with null tensors
     assert route(desc(T=0), x=0, W=0, idx=0, A=0, Bm=0)[0] == 0
@@ -127,7 +143,7 @@ def test_replay_rejects_bad_arguments():
     assert B.STATUS[replay(desc(m=0))[0]] == "PR2_ERR_SHAPE"
     assert replay(desc(T=0), x=0, idx=0, W=0, Wg=0, Wu=0, Wd=0, y=0, ws=0, ws_bytes=0)[0] == 0
     assert B.workspace_bytes(desc(k=0), B.OP_REPLAY_FWD) == 0
-    assert B.workspace_bytes(None if False else desc(), B.OP_ROUTE) == 0
+    assert B.workspace_bytes(desc(k=0), B.OP_ROUTE) == 0
 
 
 def test_valid_call_without_gpu_reports_device():

@@ -75,13 +75,18 @@ def test_route_shapes(case):
     T, d, N, k, r, act, skew, idt, pad, renorm, full = case
     s = W.LayerShape("case", T=T, d=d, N=N, k=k, m=8, r=r, act=act, skew=skew)
     L = W.layer_inputs(s, 3, experts=False)
-    g = run_route(L, s, k, renorm=renorm, idx_dtype=idt, ldi_pad=pad, predictor=r > 0,
-                  full_rank=full, logits=True)
     ref = oracle_route(L, k, renorm=renorm, predictor=r > 0, full_rank=full)
-    compare_route(g["idx"], g["gate"], ref, k, str(case))
-    if pad:
-        assert np.all(g["buf"][:, k:] == -7), "padding beyond k was written"
-    np.testing.assert_allclose(g["logits"], ref["p"], rtol=0, atol=2e-6 * max(1.0, np.abs(ref["p"]).max()))
+    # with router logits requested the projection is [W_r | A]; without, the predictor is
+    # folded into the router weights first: both must meet the same bar
+    for want_logits in (True, False):
+        g = run_route(L, s, k, renorm=renorm, idx_dtype=idt, ldi_pad=pad, predictor=r > 0,
+                      full_rank=full, logits=want_logits)
+        compare_route(g["idx"], g["gate"], ref, k, f"{case} logits={want_logits}")
+        if pad:
+            assert np.all(g["buf"][:, k:] == -7), "padding beyond k was written"
+        if want_logits:
+            np.testing.assert_allclose(g["logits"], ref["p"], rtol=0,
+                                       atol=2e-6 * max(1.0, np.abs(ref["p"]).max()))
 
 
 def test_route_exact_ties_go_to_lower_id():
@@ -120,15 +125,17 @@ def test_route_zero_predictor_equals_router_only():
 def test_route_qwen3_30b_full():
     s = W.WORKLOADS["qwen3_30b_T16384"]
     L = W.layer_inputs(s, 0, experts=False)
-    g = run_route(L, s, s.k, logits=True)
     ref = oracle_route(L, s.k)
-    excl = compare_route(g["idx"], g["gate"], ref, s.k, s.name)
+    g = run_route(L, s, s.k, logits=True)
+    excl = compare_route(g["idx"], g["gate"], ref, s.k, s.name + " with logits")
     print(f"\n{s.name}: {excl} of {s.T} tokens under the 1e-6 margin")
     np.testing.assert_allclose(g["logits"], ref["p"], rtol=0, atol=4e-6)
-    # determinism: a second call is bitwise identical
+    # the folded projection (no logits requested), twice: parity and bitwise determinism
+    g1 = run_route(L, s, s.k)
+    compare_route(g1["idx"], g1["gate"], ref, s.k, s.name + " folded")
     g2 = run_route(L, s, s.k)
-    np.testing.assert_array_equal(g["idx"], g2["idx"])
-    np.testing.assert_array_equal(g["gate"], g2["gate"])
+    np.testing.assert_array_equal(g1["idx"], g2["idx"])
+    np.testing.assert_array_equal(g1["gate"], g2["gate"])
 
 
 def test_route_empty_batch():
