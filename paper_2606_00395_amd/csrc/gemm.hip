@@ -8,15 +8,21 @@
 // of one expert against a 256-row panel of weights (GEMM1: 128 gate rows + the
 // matching 128 up rows; GEMM2: 256 rows of W_down).  K advances in slices of 64
 // (one 128-byte line per row) copied straight from global memory into LDS with
-// 16-byte DMA loads (no register staging), two LDS stages deep, 16-byte chunks
-// XOR-swizzled per row so the MFMA operand reads are free of bank conflicts.
+// 16-byte DMA loads (no register staging), two LDS stages deep (the next slice
+// in flight while one is consumed), 16-byte chunks XOR-swizzled per row so the
+// MFMA operand reads are free of bank conflicts.
 // Eight wavefronts (two per SIMD) in a 4 x 2 arrangement each own 64 rows x 128
-// panel rows as 2 x 4 tiles of v_mfma_f32_32x32x16_bf16 (fp32 accumulation); a
-// wavefront whose rows are all past the end of a partial tile skips its MFMAs.
+// panel rows as 2 x 4 tiles of v_mfma_f32_32x32x16_bf16 (fp32 accumulation);
+// operand fragments are double-buffered in registers so the LDS reads of one
+// K=16 step overlap the MFMAs of the previous one; a wavefront whose rows are
+// all past the end of a partial tile skips its MFMAs.
 // GEMM1's epilogue applies SwiGLU in registers (gate and up tiles of the same
 // columns live in the same lanes) and rounds H to bf16; GEMM2's epilogue scales
-// by the route weight and rounds O to bf16.  Workgroups are mapped so that each
-// XCD takes a contiguous range of the tile list (same experts, shared L2).
+// by the route weight and rounds O to bf16.  The MFMA operands are given as
+// (weights, tokens), so each lane's accumulators hold runs of four consecutive
+// output columns of one token row and the epilogue stores 8 bytes at a time
+// straight from registers.  Workgroups are mapped so that each XCD takes a
+// contiguous range of the tile list (same experts, shared L2).
 //
 // Other shapes and the fp32 path use a plain one-thread-per-output kernel.
 #include "common.h"
@@ -29,11 +35,21 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int BM = kTileM;      // 256 rows per tile
 constexpr int BP = 256;         // weight panel rows per tile
-constexpr int BK = 64;          // K slice: one 128-byte line per row
+constexpr int BK = 64;          // K slice: 128 bytes per row
 constexpr int ROWB = BK * 2;    // bytes per LDS row (unpadded; chunks are swizzled)
-constexpr int kGemmThreads = 512;   // 8 wavefronts: 4 row quarters x 2 panel halves
+constexpr int CHUNKS = ROWB / 16;   // 16-byte chunks per row
+constexpr int NSTAGE = 2;       // LDS stages: slice kt+1 in flight during slice kt
+constexpr int WM = 64;          // token rows per wavefront
+constexpr int WN = 128;         // panel rows per wavefront
+constexpr int MI = WM / 32;     // 32x32 MFMA tiles per wavefront, token direction
+constexpr int NJ = WN / 32;     // 32x32 MFMA tiles per wavefront, panel direction
+constexpr int NWAVE = (BM / WM) * (BP / WN);
+constexpr int kGemmThreads = 64 * NWAVE;
 constexpr int kNumXcd = 8;
-constexpr int kGroups = (BM + BP) / 8 / (kGemmThreads / 64);   // 8-row DMA groups per wavefront
+constexpr int kRowsPerDma = 1024 / ROWB;                                   // 8 rows / DMA
+constexpr int kGroups = (BM + BP) / kRowsPerDma / NWAVE;                    // DMAs / wavefront
+constexpr int STAGEB = (BM + BP) * ROWB;                                    // 64 KiB
+constexpr int LDSB = NSTAGE * STAGEB;
 
 struct MfmaArgs {
     const bf16_t* A;        // GEMM1: x [T, d]; GEMM2: H [T*k, m]
@@ -51,17 +67,29 @@ struct MfmaArgs {
     bf16_t* out;
 };
 
-__device__ __forceinline__ float silu_f(float a) { return a / (1.0f + __expf(-a)); }
+// silu(a) = a / (1 + e^-a) with the hardware reciprocal (about 1 ulp; H is rounded to bf16)
+__device__ __forceinline__ float silu_f(float a) {
+    return a * __builtin_amdgcn_rcpf(1.0f + __expf(-a));
+}
 
-// 16-byte chunk c of LDS row r is stored at position c ^ swz(r): rows 16 apart
-// repeat the pattern, and any 16 (or 8) consecutive rows read at the same
-// chunk hit disjoint banks.
-__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+// 16-byte chunk c of LDS row r is stored at position c ^ swz(r): any 16 (or
+// 8) consecutive rows read at the same chunk hit disjoint banks.  swz depends
+// on r % 16 only.
+__device__ __forceinline__ int swz(int r) {
+    return CHUNKS == 8 ? (r & 7) ^ ((r >> 3) & 1) : (r >> 2) & 3;
+}
+
+// wait until at most n of this wavefront's global loads are outstanding
+template <int n>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(n >= 0 && n < 16, "vmcnt field");
+    __builtin_amdgcn_s_waitcnt(0x0f70 | n);   // expcnt and lgkmcnt left at their maxima
+}
 
 template <int MODE>
-__global__ void __launch_bounds__(kGemmThreads)
+__global__ void __launch_bounds__(kGemmThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 grouped_gemm_mfma(MfmaArgs g) {
-    __shared__ __attribute__((aligned(1024))) unsigned char lds[2][(BM + BP) * ROWB];
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[LDSB];
 
     // XCD-aware mapping: physical block b runs on XCD b % 8; give each XCD a
     // contiguous range of the (tile, panel) work list.
@@ -80,124 +108,165 @@ grouped_gemm_mfma(MfmaArgs g) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int wr = wave >> 1;     // 64-row quarter
-    const int wc = wave & 1;      // panel half
-    // a wavefront whose 64 rows are all past the tile's end only helps copy
-    const bool active = wr * 64 < rows;
+    const int wr = wave / (BP / WN);     // token-row block of WM rows
+    const int wc = wave % (BP / WN);     // panel block of WN rows
+    // a wavefront whose rows are all past the tile's end only helps copy
+    const bool active = wr * WM < rows;
+    // each lane's accumulators belong to MI token rows (one per 32-row block);
+    // GEMM2's route weights for them are fetched now, long before the epilogue
+    float gw[MI];
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+        gw[i] = 0.0f;
+        const int r = wr * WM + i * 32 + (lane & 31);
+        if (MODE == 1 && r < rows) gw[i] = g.gate[g.perm_src[row0 + r]];
+    }
 
-    // DMA assignments: wavefront w copies 8-row groups w*kGroups .. of the
-    // [A rows | panel rows] tile; lane l moves row 8*grp + l/8, position l%8.
-    const bf16_t* src[kGroups];
+    // DMA assignments: wavefront w copies row groups w*kGroups .. of the
+    // [A rows | panel rows] tile; lane l moves row grp*kRowsPerDma + l/CHUNKS,
+    // position l%CHUNKS.  A wavefront's groups all come from one tensor (the
+    // token rows, the gate or up panel, or the down panel), so it keeps one
+    // base pointer and a 32-bit element offset per group.
+    const int wrow0 = wave * kGroups * kRowsPerDma;
+    const bf16_t* sbase;
+    if (wrow0 < BM) sbase = g.A;
+    else if (MODE == 0) sbase = (wrow0 - BM < 128 ? g.W0 : g.W1) + (int64_t)expert * g.w_stride;
+    else sbase = g.W0 + (int64_t)expert * g.w_stride;
+    uint32_t soff[kGroups];
 #pragma unroll
     for (int i = 0; i < kGroups; ++i) {
-        const int grp = wave * kGroups + i;
-        const int r = grp * 8 + (lane >> 3);          // row in [0, BM + BP)
-        const int chunk = (lane & 7) ^ swz(r);
-        const bf16_t* rowp;
+        const int r = wrow0 + i * kRowsPerDma + lane / CHUNKS;  // row in [0, BM + BP)
+        const int chunk = (lane % CHUNKS) ^ swz(r);
+        int64_t off;
         if (r < BM) {
             // rows past the tile's end read a valid row; their results are never stored
             const int rr = r < rows ? r : 0;
-            if (MODE == 0) rowp = g.A + (int64_t)(g.perm_src[row0 + rr] / g.k) * g.K;
-            else rowp = g.A + ((int64_t)row0 + rr) * g.K;
+            if (MODE == 0) off = (int64_t)(g.perm_src[row0 + rr] / g.k) * g.K;
+            else off = ((int64_t)row0 + rr) * g.K;
         } else {
             const int pr = r - BM;
-            if (MODE == 0)
-                rowp = (pr < 128 ? g.W0 : g.W1) + (int64_t)expert * g.w_stride +
-                       (int64_t)(pn * 128 + (pr & 127)) * g.K;
-            else
-                rowp = g.W0 + (int64_t)expert * g.w_stride + (int64_t)(pn * BP + pr) * g.K;
+            off = MODE == 0 ? (int64_t)(pn * 128 + (pr & 127)) * g.K
+                            : (int64_t)(pn * BP + pr) * g.K;
         }
-        src[i] = rowp + chunk * 8;
+        soff[i] = (uint32_t)(off + chunk * 8);
     }
-    auto issue = [&](int buf, int k0) {
+    auto issue = [&](int stage, int k0) {
 #pragma unroll
         for (int i = 0; i < kGroups; ++i) {
             const int grp = wave * kGroups + i;
-            __builtin_amdgcn_global_load_lds((const void*)(src[i] + k0),
-                                             (lds_void*)&lds[buf][grp * 8 * ROWB], 16, 0, 0);
+            __builtin_amdgcn_global_load_lds((const void*)(sbase + (soff[i] + (uint32_t)k0)),
+                                             (lds_void*)&lds[stage * STAGEB + grp * 1024], 16,
+                                             0, 0);
         }
     };
 
-    f32x16 acc[2][4];
+    f32x16 acc[MI][NJ];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < NJ; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
-    // LDS rows each lane reads for its MFMA operands
+    // LDS reads for the MFMA operands: lane l reads row (block base + l%32) at
+    // 16-byte position (2*ks + l/32) ^ swz(l%32); block bases are multiples of
+    // 32 rows, so the swizzle is the same for every fragment of the lane.
     const int lrow = lane & 31;
-    const int lhalf = lane >> 5;           // 8-element half of the K=16 step
-    int a_row[2], b_row[4];
+    const int sw = swz(lrow);
+    int kpos[BK / 16];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) a_row[i] = wr * 64 + i * 32 + lrow;
+    for (int ks = 0; ks < BK / 16; ++ks) kpos[ks] = lrow * ROWB + (((2 * ks + (lane >> 5)) ^ sw) << 4);
+    int a_base[MI], b_base[NJ];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int i = 0; i < MI; ++i) a_base[i] = (wr * WM + i * 32) * ROWB;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
         int prow;
-        if (MODE == 0) prow = (j < 2 ? 0 : 128) + wc * 64 + (j & 1) * 32 + lrow;
-        else prow = wc * 128 + j * 32 + lrow;
-        b_row[j] = BM + prow;
+        if (MODE == 0) prow = (j < NJ / 2 ? 0 : 128) + wc * (WN / 2) + (j % (NJ / 2)) * 32;
+        else prow = wc * WN + j * 32;
+        b_base[j] = (BM + prow) * ROWB;
     }
 
     const int nk = g.K / BK;
     issue(0, 0);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
-        if (kt + 1 < nk) issue(cur ^ 1, (kt + 1) * BK);
+        // slice kt landed and every wavefront is done with slice kt-1, whose
+        // stage is refilled next
+        wait_vmcnt<0>();
+        __syncthreads();
+        if (kt + 1 < nk) issue((kt + 1) % NSTAGE, (kt + 1) * BK);
         if (active) {
-            const unsigned char* base = lds[cur];
+            // fragments double-buffered in registers: the reads for sub-step
+            // ks+1 are in flight while the MFMAs of sub-step ks run
+            const unsigned char* base = lds + (kt % NSTAGE) * STAGEB;
+            bf16x8 fa[2][MI], fb[2][NJ];
+            auto read_frags = [&](int buf, int ks) {
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+                    fa[buf][i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + a_base[i] + kpos[ks]));
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+                    fb[buf][j] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + b_base[j] + kpos[ks]));
+            };
+            read_frags(0, 0);
 #pragma unroll
             for (int ks = 0; ks < BK / 16; ++ks) {
-                const int c = 2 * ks + lhalf;
-                bf16x8 fa[2], fb[4];
+                if (ks + 1 < BK / 16) read_frags((ks + 1) & 1, ks + 1);
+                // keep the scheduler from sinking those reads below the MFMAs
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int i = 0; i < 2; ++i)
-                    fa[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + a_row[i] * ROWB +
-                                                                       ((c ^ swz(a_row[i])) << 4)));
+                for (int i = 0; i < MI; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    fb[j] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + b_row[j] * ROWB +
-                                                                       ((c ^ swz(b_row[j])) << 4)));
-#pragma unroll
-                for (int i = 0; i < 2; ++i)
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j],
-                                                                             acc[i][j], 0, 0, 0);
+                    for (int j = 0; j < NJ; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            fb[ks & 1][j], fa[ks & 1][i], acc[i][j], 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
-        __builtin_amdgcn_s_waitcnt(0);     // this wavefront's copies of the next slice landed
-        __syncthreads();
     }
     if (!active) return;
 
-    // epilogue: 32x32 accumulator element v of lane l is
-    // C[8*(v/4) + 4*(l/32) + v%4][l%32]
-    const int ccol = lane & 31;
-    const int rbase = 4 * (lane >> 5);
+    // Epilogue.  The MFMA computed the transposed tile (weights x tokens), so
+    // accumulator element v of lane l is output column 8*(v/4) + 4*(l/32) + v%4
+    // of token row l%32 of the 32-row block: four consecutive bf16 per lane,
+    // stored as one 8-byte write.
+    const int ncol0 = 4 * (lane >> 5);
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < MI; ++i) {
+        const int r = wr * WM + i * 32 + (lane & 31);
+        if (r >= rows) continue;
+        bf16_t* orow = g.out + ((int64_t)row0 + r) * g.n_out;
+        if (MODE == 0) {
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int r = wr * 64 + i * 32 + 8 * (v >> 2) + rbase + (v & 3);
-            if (r >= rows) continue;
-            const int64_t orow = (int64_t)row0 + r;
-            if (MODE == 0) {
+            for (int j = 0; j < NJ / 2; ++j) {
+                const int col = pn * 128 + wc * (WN / 2) + j * 32 + ncol0;
 #pragma unroll
-                for (int j = 0; j < 2; ++j) {
-                    const int col = pn * 128 + wc * 64 + j * 32 + ccol;
-                    const float h = silu_f(acc[i][j][v]) * acc[i][j + 2][v];
-                    g.out[orow * g.n_out + col] = f32_to_bf16(h);
+                for (int a4 = 0; a4 < 4; ++a4) {
+                    uint32_t w[2];
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const int v0 = 4 * a4 + 2 * h;
+                        const float h0 = silu_f(acc[i][j][v0]) * acc[i][j + NJ / 2][v0];
+                        const float h1 = silu_f(acc[i][j][v0 + 1]) * acc[i][j + NJ / 2][v0 + 1];
+                        w[h] = (uint32_t)f32_to_bf16(h0) | ((uint32_t)f32_to_bf16(h1) << 16);
+                    }
+                    *(uint2*)(orow + col + 8 * a4) = make_uint2(w[0], w[1]);
                 }
-            } else {
-                const float gw = g.gate[g.perm_src[orow]];
+            }
+        } else {
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int col = pn * BP + wc * 128 + j * 32 + ccol;
-                    g.out[orow * g.n_out + col] = f32_to_bf16(gw * acc[i][j][v]);
+            for (int j = 0; j < NJ; ++j) {
+                const int col = pn * BP + wc * WN + j * 32 + ncol0;
+#pragma unroll
+                for (int a4 = 0; a4 < 4; ++a4) {
+                    uint32_t w[2];
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const int v0 = 4 * a4 + 2 * h;
+                        w[h] = (uint32_t)f32_to_bf16(gw[i] * acc[i][j][v0]) |
+                               ((uint32_t)f32_to_bf16(gw[i] * acc[i][j][v0 + 1]) << 16);
+                    }
+                    *(uint2*)(orow + col + 8 * a4) = make_uint2(w[0], w[1]);
                 }
             }
         }
@@ -248,8 +317,12 @@ gemm2_generic(const T* H, const int* perm_src, const float* gate, const T* Wd, i
 }  // namespace
 
 bool mfma_shape_ok(const pr2_moe_desc& d) {
+    // copy offsets are 32-bit element offsets from the tensor (or expert) base
+    const int64_t lim = (int64_t)1 << 31;
+    const int64_t Tk = d.T * (int64_t)d.k;
     return d.act_dtype == PR2_BF16 && d.d % BP == 0 && d.m % 128 == 0 && d.d % BK == 0 &&
-           d.m % BK == 0;
+           d.m % BK == 0 && d.T * (int64_t)d.d < lim && Tk * d.m < lim &&
+           (int64_t)d.m * d.d < lim;
 }
 
 hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void* W_gate,
