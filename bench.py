@@ -10,8 +10,10 @@ synthetic tokens already resident in HBM.  Prints ONE JSON line.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -37,6 +39,24 @@ def parse():
                     help="first run a plain device copy of this many MiB (a known-size "
                          "kernel for scaling memory-traffic counters)")
     return ap.parse_args()
+
+
+def profiled_traffic(workload, kernel="grouped_gemm_mfma<0>"):
+    """HBM bytes per launch of the dominant kernel from the committed rocprofv3
+    summary (FETCH_SIZE + WRITE_SIZE, copy-calibrated), or None when there is
+    no summary for this workload or the kernel source changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"replay_and_route_kernels_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"gemm_source_sha256: ([0-9a-f]+)", text)
+    src = os.path.join(ROOT, "paper_2606_00395_amd", "csrc", "gemm.hip")
+    cur = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if not m or m.group(1) != cur:
+        return None
+    m = re.search(r"traffic_bytes_per_launch\[" + re.escape(kernel) + r"\]: fetch (\d+) write (\d+)",
+                  text)
+    return int(m.group(1)) + int(m.group(2)) if m else None
 
 
 def cpu_baseline(shape, L, n_tok, min_seconds=10.0):
@@ -171,7 +191,8 @@ def main():
                    "expert_intermediate": m, "predictor_rank": r, "router": "fp32",
                    "idx_dtype": shape.idx_dtype, "load_skew": shape.skew},
         "roofline": {"bound": "mfma", "kernel": DOMINANT, "achieved": achieved, "peak": peak,
-                     "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None},
+                     "unit": "TFLOP/s", "frac": achieved / peak,
+                     "traffic": profiled_traffic(shape.name)},
         "kernels_ms": {n: round(v, 5) for n, v in kern.items()},
         "replay_forward": {
             "ms": t_replay,

@@ -55,6 +55,7 @@ struct MfmaArgs {
     const bf16_t* A;        // GEMM1: x [T, d]; GEMM2: H [T*k, m]
     const int* perm_src;    // permuted row -> t*k + s
     int k;
+    int Tk;                 // routes (perm_src entries)
     const bf16_t* W0;       // GEMM1: W_gate; GEMM2: W_down
     const bf16_t* W1;       // GEMM1: W_up
     int K;                  // reduction length (d or m)
@@ -119,7 +120,7 @@ grouped_gemm_mfma(MfmaArgs g) {
     for (int i = 0; i < MI; ++i) {
         gw[i] = 0.0f;
         const int r = wr * WM + i * 32 + (lane & 31);
-        if (MODE == 1 && r < rows) gw[i] = g.gate[g.perm_src[row0 + r]];
+        if (MODE == 1 && r < rows) gw[i] = g.gate[min(max(g.perm_src[row0 + r], 0), g.Tk - 1)];
     }
 
     // DMA assignments: wavefront w copies row groups w*kGroups .. of the
@@ -141,7 +142,7 @@ grouped_gemm_mfma(MfmaArgs g) {
         if (r < BM) {
             // rows past the tile's end read a valid row; their results are never stored
             const int rr = r < rows ? r : 0;
-            if (MODE == 0) off = (int64_t)(g.perm_src[row0 + rr] / g.k) * g.K;
+            if (MODE == 0) off = (int64_t)(min(max(g.perm_src[row0 + rr], 0), g.Tk - 1) / g.k) * g.K;
             else off = ((int64_t)row0 + rr) * g.K;
         } else {
             const int pr = r - BM;
@@ -333,6 +334,7 @@ hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void*
         g1.A = (const bf16_t*)x;
         g1.perm_src = ws.perm_src;
         g1.k = d.k;
+        g1.Tk = (int)(d.T * d.k);
         g1.W0 = (const bf16_t*)W_gate;
         g1.W1 = (const bf16_t*)W_up;
         g1.K = d.d;

@@ -48,6 +48,18 @@ perm_count_kernel(const void* idx, int idx_dtype, int64_t ldi, int64_t T, int k,
 
 constexpr int kScanThreads = 1024;
 
+// inclusive prefix sum across the 64 lanes of a wavefront: row_shr 1, 2, 4, 8
+// within rows of 16 lanes, then row_bcast 15 and 31 carry the row totals
+__device__ __forceinline__ int wave_incl_scan(int x) {
+    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);
+    return x;
+}
+
 __device__ int block_exclusive_scan(int v, int* sh, int* total) {
     const int tid = threadIdx.x;
     sh[tid] = v;
@@ -76,32 +88,97 @@ perm_scan_kernel(int* counts, int64_t nblk, int N, int bm, int* offsets, int* ti
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    for (int e = wave; e < N; e += kScanThreads / 64) {
-        int* row = counts + (int64_t)e * nblk;
-        int carry = 0;
-        for (int64_t b0 = 0; b0 < nblk; b0 += 64) {
-            const int64_t b = b0 + lane;
-            const int c = b < nblk ? row[b] : 0;
-            int incl = c;
-#pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                int y = __shfl_up(incl, off, 64);
-                if (lane >= off) incl += y;
-            }
-            if (b < nblk) row[b] = carry + incl - c;
-            carry += __shfl(incl, 63, 64);
-        }
-        if (lane == 0) s_off[e] = carry;
-    }
-    __syncthreads();
+    constexpr int kWaves = kScanThreads / 64;
+    constexpr int kScanE = 8, kScanC = 8;
     int grand;
-    const int tot = tid < N ? s_off[tid] : 0;
-    const int ex = block_exclusive_scan(tot, sh, &grand);
-    if (tid < N) s_off[tid] = ex;
-    if (tid == 0) s_off[N] = grand;
-    __syncthreads();
-    const int64_t L = (int64_t)N * nblk;
-    for (int64_t q = tid; q < L; q += kScanThreads) counts[q] += s_off[q / nblk];
+    if (N <= kWaves * kScanE && nblk <= 64 * kScanC) {
+        // Register-resident path: wavefront w owns experts w, w+16, ...; lane l
+        // owns blocks [l*P, l*P + P) of each, so one wavefront scan per expert
+        // turns the lanes' totals into their starting offsets.
+        const int P = ((int)nblk + 63) / 64;
+        int v[kScanE][kScanC];
+        int tot[kScanE];
+#pragma unroll
+        for (int i = 0; i < kScanE; ++i) {
+            const int e = wave + kWaves * i;
+#pragma unroll
+            for (int c = 0; c < kScanC; ++c) {
+                const int b = lane * P + c;
+                const bool ok = e < N && c < P && b < (int)nblk;
+                const int val = counts[ok ? (int64_t)e * nblk + b : 0];
+                v[i][c] = ok ? val : 0;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < kScanE; ++i) {
+            int run = 0;
+#pragma unroll
+            for (int c = 0; c < kScanC; ++c) {
+                const int x = v[i][c];
+                v[i][c] = run;                          // exclusive within the lane
+                run += x;
+            }
+            const int incl = wave_incl_scan(run);
+            const int lane_start = incl - run;
+#pragma unroll
+            for (int c = 0; c < kScanC; ++c) v[i][c] += lane_start;
+            tot[i] = __shfl(incl, 63, 64);
+        }
+        if (lane == 0)
+#pragma unroll
+            for (int i = 0; i < kScanE; ++i)
+                if (wave + kWaves * i < N) s_off[wave + kWaves * i] = tot[i];
+        __syncthreads();
+        const int t = tid < N ? s_off[tid] : 0;
+        const int ex = block_exclusive_scan(t, sh, &grand);
+        if (tid < N) s_off[tid] = ex;
+        if (tid == 0) s_off[N] = grand;
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < kScanE; ++i) {
+            const int e = wave + kWaves * i;
+            if (e >= N) continue;
+            const int add = s_off[e];
+#pragma unroll
+            for (int c = 0; c < kScanC; ++c) {
+                const int b = lane * P + c;
+                if (c < P && b < (int)nblk) counts[(int64_t)e * nblk + b] = v[i][c] + add;
+            }
+        }
+    } else {
+        // general path: experts in batches, block counts in chunks, in place
+        for (int e = wave; e < N; e += kWaves) {
+            int* row = counts + (int64_t)e * nblk;
+            int carry = 0;
+            for (int b0 = 0; b0 < (int)nblk; b0 += 64) {
+                const int b = b0 + lane;
+                const int c = b < (int)nblk ? row[b] : 0;
+                int incl = c;
+#pragma unroll
+                for (int off = 1; off < 64; off <<= 1) {
+                    int y = __shfl_up(incl, off, 64);
+                    if (lane >= off) incl += y;
+                }
+                if (b < (int)nblk) row[b] = carry + incl - c;
+                carry += __shfl(incl, 63, 64);
+            }
+            if (lane == 0) s_off[e] = carry;
+        }
+        __syncthreads();
+        for (int e0 = 0; e0 < N; e0 += kScanThreads) {
+            // N <= kMaxExperts == kScanThreads: one round
+            const int t = e0 + tid < N ? s_off[e0 + tid] : 0;
+            const int ex = block_exclusive_scan(t, sh, &grand);
+            if (e0 + tid < N) s_off[e0 + tid] = ex;
+        }
+        if (tid == 0) s_off[N] = grand;
+        __syncthreads();
+        for (int e = wave; e < N; e += kWaves) {
+            int* row = counts + (int64_t)e * nblk;
+            const int add = s_off[e];
+            for (int b = lane; b < (int)nblk; b += 64) row[b] += add;
+        }
+    }
     // tiles per expert, and their exclusive prefix
     int ntile = 0;
     if (tid < N) {
@@ -161,8 +238,12 @@ perm_scatter_kernel(const void* idx, int idx_dtype, int64_t ldi, int64_t T, int 
         if (valid) {
             int base = cnt[e];
             int pos = base + __popcll(peers & lt);
-            perm_src[pos] = (int)src;
-            inv[src] = pos;
+            if (pos < T * k) {                 // always true for a consistent scan
+                perm_src[pos] = (int)src;
+                inv[src] = pos;
+            } else {
+                inv[src] = -1;
+            }
             // the highest lane of each peer group advances the expert's cursor
             if ((peers >> lane) == 1ull) cnt[e] = base + __popcll(peers);
         }
@@ -170,45 +251,66 @@ perm_scatter_kernel(const void* idx, int idx_dtype, int64_t ldi, int64_t T, int 
     }
 }
 
-template <typename T, int V>
+// bf16, d % 8 == 0: each thread owns 8 consecutive columns of TPI tokens per
+// iteration, so TPI*k independent 16-byte loads are in flight per thread
+constexpr int kCombTok = 2;
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
 __global__ void __launch_bounds__(256)
-combine_kernel(const T* O, const int* inv, int64_t ntok, int k, int d, T* y) {
-    for (int64_t t = blockIdx.x; t < ntok; t += gridDim.x) {
-        for (int c0 = threadIdx.x * V; c0 < d; c0 += 256 * V) {
-            float acc[V];
+combine_bf16_kernel(const bf16_t* O, const int* inv, int64_t ntok, int k, int d, bf16_t* y) {
+    const int64_t step = (int64_t)gridDim.x * kCombTok;
+    for (int64_t t0 = (int64_t)blockIdx.x * kCombTok; t0 < ntok; t0 += step) {
+        for (int c0 = threadIdx.x * 8; c0 < d; c0 += 256 * 8) {
+            float acc[kCombTok][8];
 #pragma unroll
-            for (int v = 0; v < V; ++v) acc[v] = 0.0f;
+            for (int u = 0; u < kCombTok; ++u)
+#pragma unroll
+                for (int v = 0; v < 8; ++v) acc[u][v] = 0.0f;
             for (int s = 0; s < k; ++s) {
-                int r = inv[t * k + s];
-                if (r < 0) continue;
-                const T* src = O + (int64_t)r * d + c0;
-                if (V == 8 && sizeof(T) == 2) {
-                    uint4 u = *(const uint4*)src;
-                    uint32_t w[4] = {u.x, u.y, u.z, u.w};
+                u32x4 raw[kCombTok];
+#pragma unroll
+                for (int u = 0; u < kCombTok; ++u) {
+                    const int64_t t = t0 + u;
+                    const int r = t < ntok ? inv[t * k + s] : -1;
+                    raw[u] = r >= 0 ? __builtin_nontemporal_load((const u32x4*)(O + (int64_t)r * d + c0))
+                                    : u32x4{0, 0, 0, 0};
+                }
+#pragma unroll
+                for (int u = 0; u < kCombTok; ++u) {
+                    const uint32_t w[4] = {raw[u][0], raw[u][1], raw[u][2], raw[u][3]};
 #pragma unroll
                     for (int v = 0; v < 4; ++v) {
-                        acc[2 * v] += __uint_as_float(w[v] << 16);
-                        acc[2 * v + 1] += __uint_as_float(w[v] & 0xffff0000u);
+                        acc[u][2 * v] += __uint_as_float(w[v] << 16);
+                        acc[u][2 * v + 1] += __uint_as_float(w[v] & 0xffff0000u);
                     }
-                } else {
-#pragma unroll
-                    for (int v = 0; v < V; ++v)
-                        if (c0 + v < d) acc[v] += Act<T>::to_f32(src[v]);
                 }
             }
-            T* dst = y + t * (int64_t)d + c0;
-            if (V == 8 && sizeof(T) == 2) {
+#pragma unroll
+            for (int u = 0; u < kCombTok; ++u) {
+                const int64_t t = t0 + u;
+                if (t >= ntok) continue;
                 uint32_t w[4];
 #pragma unroll
                 for (int v = 0; v < 4; ++v)
-                    w[v] = (uint32_t)f32_to_bf16(acc[2 * v]) |
-                           ((uint32_t)f32_to_bf16(acc[2 * v + 1]) << 16);
-                *(uint4*)dst = make_uint4(w[0], w[1], w[2], w[3]);
-            } else {
-#pragma unroll
-                for (int v = 0; v < V; ++v)
-                    if (c0 + v < d) dst[v] = Act<T>::from_f32(acc[v]);
+                    w[v] = (uint32_t)f32_to_bf16(acc[u][2 * v]) |
+                           ((uint32_t)f32_to_bf16(acc[u][2 * v + 1]) << 16);
+                *(uint4*)(y + t * (int64_t)d + c0) = make_uint4(w[0], w[1], w[2], w[3]);
             }
+        }
+    }
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+combine_kernel(const T* O, const int* inv, int64_t ntok, int k, int d, T* y) {
+    for (int64_t t = blockIdx.x; t < ntok; t += gridDim.x) {
+        for (int c = threadIdx.x; c < d; c += 256) {
+            float acc = 0.0f;
+            for (int s = 0; s < k; ++s) {
+                int r = inv[t * k + s];
+                if (r >= 0) acc += Act<T>::to_f32(O[(int64_t)r * d + c]);
+            }
+            y[t * (int64_t)d + c] = Act<T>::from_f32(acc);
         }
     }
 }
@@ -243,19 +345,20 @@ hipError_t launch_permute(const pr2_moe_desc& d, const void* idx, int64_t ldi, c
 }
 
 hipError_t launch_combine(const pr2_moe_desc& d, const ReplayWs& ws, void* y, hipStream_t s) {
-    const int64_t grid64 = d.T < 8192 ? d.T : 8192;
-    dim3 grid((unsigned)grid64);
     LaunchScope scope("combine", s);
-    if (d.act_dtype == PR2_BF16) {
-        if (d.d % 8 == 0)
-            hipLaunchKernelGGL((combine_kernel<bf16_t, 8>), grid, dim3(256), 0, s,
-                               (const bf16_t*)ws.O, ws.inv, d.T, d.k, d.d, (bf16_t*)y);
-        else
-            hipLaunchKernelGGL((combine_kernel<bf16_t, 1>), grid, dim3(256), 0, s,
-                               (const bf16_t*)ws.O, ws.inv, d.T, d.k, d.d, (bf16_t*)y);
+    if (d.act_dtype == PR2_BF16 && d.d % 8 == 0) {
+        const int64_t want = (d.T + kCombTok - 1) / kCombTok;
+        dim3 grid((unsigned)(want < 8192 ? want : 8192));
+        hipLaunchKernelGGL(combine_bf16_kernel, grid, dim3(256), 0, s, (const bf16_t*)ws.O, ws.inv,
+                           d.T, d.k, d.d, (bf16_t*)y);
     } else {
-        hipLaunchKernelGGL((combine_kernel<float, 1>), grid, dim3(256), 0, s, (const float*)ws.O,
-                           ws.inv, d.T, d.k, d.d, (float*)y);
+        dim3 grid((unsigned)(d.T < 8192 ? d.T : 8192));
+        if (d.act_dtype == PR2_BF16)
+            hipLaunchKernelGGL(combine_kernel<bf16_t>, grid, dim3(256), 0, s, (const bf16_t*)ws.O,
+                               ws.inv, d.T, d.k, d.d, (bf16_t*)y);
+        else
+            hipLaunchKernelGGL(combine_kernel<float>, grid, dim3(256), 0, s, (const float*)ws.O,
+                               ws.inv, d.T, d.k, d.d, (float*)y);
     }
     return hipGetLastError();
 }
