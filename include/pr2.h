@@ -11,16 +11,18 @@
  *             (Appendix E.2).
  *
  * Conventions shared by every entry point
- *   - All tensor arguments are DEVICE pointers owned by the caller, row-major, 16-byte
- *     aligned.  The library never allocates, frees or keeps them; scratch memory comes from
- *     the caller's workspace `ws` of at least pr2_workspace_bytes(desc, op) bytes (16-byte
- *     aligned; may be NULL when that size is 0).
+ *   - All tensor arguments are DEVICE pointers owned by the caller, row-major.  Alignment:
+ *     activations (x, y, dy, dx) and expert weights and their gradients 16 bytes; fp32
+ *     router, predictor, gate and logit tensors 4 bytes; id buffers their element size.
+ *     The library never allocates, frees or keeps them; scratch memory comes from the
+ *     caller's workspace `ws` of at least pr2_workspace_bytes(desc, op) bytes (any
+ *     alignment; may be NULL when that size is 0).
  *   - Calls are asynchronous on `stream` (NULL = the null stream of the current device) and
  *     run on the current HIP device.  They return once the kernels are enqueued.
  *   - Every argument is checked on the host before any HIP call.  On an error nothing is
  *     enqueued, outputs are untouched, the status says what was wrong and pr2_last_error()
  *     (thread-local) gives a sentence naming the argument.
- *   - T == 0 is a no-op returning PR2_OK.
+ *   - T == 0 is a no-op returning PR2_OK (the backward then zeroes its weight gradients).
  *   - Expert ids are 0-based.  Results are deterministic: the same inputs on the same device
  *     give bitwise identical outputs (no floating-point atomics anywhere).
  *   - Route contents (0 <= id < N, distinct within a row) are a precondition.  Kernels never
@@ -48,7 +50,7 @@ typedef enum {
     PR2_ERR_NULL = 1,        /* a required pointer is NULL                                  */
     PR2_ERR_SHAPE = 2,       /* a size is out of range (k > N, k < 1, d < 1, ldi < k, ...)     */
     PR2_ERR_DTYPE = 3,       /* unknown act_dtype / idx_dtype code                             */
-    PR2_ERR_ALIGN = 4,       /* a pointer is not 16-byte aligned                               */
+    PR2_ERR_ALIGN = 4,       /* a pointer is not aligned as its argument requires              */
     PR2_ERR_WORKSPACE = 5,   /* workspace smaller than pr2_workspace_bytes(desc, op)           */
     PR2_ERR_UNSUPPORTED = 6, /* valid but not implemented (e.g. N > 1024)                      */
     PR2_ERR_ROUTE = 7,       /* PR2_VALIDATE=1 found an out-of-range or repeated id             */
@@ -139,6 +141,39 @@ pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const
                                   const void* W_gate, const void* W_up, const void* W_down,
                                   void* y, float* gate_out, void* ws, size_t ws_bytes,
                                   pr2_stream_t stream);
+
+/*
+ * Replay backward (Sec. 4.1 "Replay During Training": the current experts and router are
+ * trained through the replayed routes; Alg. 3 in Appendix D, its backward step).  Gradients
+ * of L = sum_t <dy_t, y_t> for the replay forward above, with the recorded ids held fixed and
+ * the renormalised weights g = softmax over the k recorded logits (renorm must be 1):
+ *
+ *   dg_ts = <dy_t, E_j(x_t)>,  dp_ts = g_ts (dg_ts - sum_s' g_ts' dg_ts')   (j = idx[t, s])
+ *   dW_r = sum_t x_t^T dp_t,  db_r = sum_t dp_t
+ *   dW_gate_j, dW_up_j, dW_down_j = sums over the routes through expert j of the SwiGLU
+ *   expert's weight gradients, each route's output scaled by g_ts
+ *   dx_t = sum_s g_ts dE_j/dx(x_t)^T dy_t + dp_t W_r^T
+ *
+ * The predictor (A, B) is bypassed in replay and gets no gradient.  Arguments as for
+ * pr2_moe_replay_forward, plus:
+ *   dy       [T, d] act_dtype, gradient of the output y
+ *   dx       [T, d] act_dtype (out)
+ *   dW_r     [d, N] fp32 (out);  db_r [N] fp32 (out) or NULL when not wanted
+ *   dW_gate  [N, m, d], dW_up [N, m, d], dW_down [N, d, m] fp32 (out), 16-byte aligned
+ *   ws       >= pr2_workspace_bytes(desc, PR2_OP_REPLAY_BWD)
+ * Every gradient is overwritten (not accumulated); an expert no route uses gets zeros, and
+ * T = 0 writes zeros to all weight gradients (x, idx, dy, dx, ws may then be NULL).  Results
+ * are bitwise deterministic.  renorm = 0 returns PR2_ERR_UNSUPPORTED.  The pre-activations
+ * are recomputed (nothing is saved from the forward call); on the bf16 MFMA path
+ * (d % 256 == 0, m % 256 == 0) a, u, their gradients, g H and the per-route input gradients
+ * are held in bf16, with fp32 accumulation everywhere.
+ */
+pr2_status pr2_moe_replay_backward(const pr2_moe_desc* desc, const void* x, const void* idx,
+                                   int64_t ldi, const float* W_r, const float* b_r,
+                                   const void* W_gate, const void* W_up, const void* W_down,
+                                   const void* dy, void* dx, float* dW_r, float* db_r,
+                                   float* dW_gate, float* dW_up, float* dW_down, void* ws,
+                                   size_t ws_bytes, pr2_stream_t stream);
 
 /* Status name ("PR2_OK", ...); never NULL. */
 const char* pr2_status_string(pr2_status s);

@@ -24,7 +24,7 @@ STATUS = ["PR2_OK", "PR2_ERR_NULL", "PR2_ERR_SHAPE", "PR2_ERR_DTYPE", "PR2_ERR_A
 
 # every symbol include/pr2.h declares
 EXPORTS = ["pr2_workspace_bytes", "pr2_route_predict", "pr2_moe_replay_forward",
-           "pr2_status_string", "pr2_last_error", "pr2_version", "pr2_profile_enable",
+           "pr2_moe_replay_backward", "pr2_status_string", "pr2_last_error", "pr2_version", "pr2_profile_enable",
            "pr2_profile_reset", "pr2_profile_collect"]
 
 
@@ -62,6 +62,9 @@ def lib() -> ctypes.CDLL:
     L.pr2_moe_replay_forward.argtypes = [POINTER(MoeDesc), P, P, c_int64, P, P, P, P, P, P, P,
                                          P, c_size_t, P]
     L.pr2_moe_replay_forward.restype = c_int
+    L.pr2_moe_replay_backward.argtypes = [POINTER(MoeDesc), P, P, c_int64, P, P, P, P, P, P, P,
+                                          P, P, P, P, P, P, c_size_t, P]
+    L.pr2_moe_replay_backward.restype = c_int
     L.pr2_status_string.argtypes = [c_int]
     L.pr2_status_string.restype = c_char_p
     L.pr2_last_error.argtypes = []
@@ -180,6 +183,33 @@ def moe_replay_forward(x, idx, W_r, b_r, W_gate, W_up, W_down, y, gate_out=None,
                                        _ptr(W_r), _ptr(b_r), _ptr(W_gate), _ptr(W_up),
                                        _ptr(W_down), _ptr(y), _ptr(gate_out), _ptr(ws),
                                        ws.numel(), _stream(stream)))
+
+
+def backward_workspace(x, idx, W_r, W_gate, renorm=True):
+    torch = _torch()
+    T, d = x.shape
+    desc = make_desc(T, d, W_r.shape[1], idx.shape[1], W_gate.shape[1], 0, _act_code(x),
+                     _idx_code(idx), renorm)
+    return torch.empty(max(1, workspace_bytes(desc, OP_REPLAY_BWD)), dtype=torch.uint8,
+                       device=x.device)
+
+
+def moe_replay_backward(x, idx, W_r, b_r, W_gate, W_up, W_down, dy, dx, dW_r, db_r, dW_gate,
+                        dW_up, dW_down, ws=None, renorm=True, stream=None):
+    """pr2_moe_replay_backward on torch tensors; every gradient tensor is overwritten.
+    ``db_r`` may be None."""
+    T, d = x.shape
+    N = W_r.shape[1]
+    k = idx.shape[1]
+    m = W_gate.shape[1]
+    desc = make_desc(T, d, N, k, m, 0, _act_code(x), _idx_code(idx), renorm)
+    if ws is None:
+        ws = backward_workspace(x, idx, W_r, W_gate, renorm)
+    check(lib().pr2_moe_replay_backward(byref(desc), _ptr(x), _ptr(idx), _row_stride(idx),
+                                        _ptr(W_r), _ptr(b_r), _ptr(W_gate), _ptr(W_up),
+                                        _ptr(W_down), _ptr(dy), _ptr(dx), _ptr(dW_r), _ptr(db_r),
+                                        _ptr(dW_gate), _ptr(dW_up), _ptr(dW_down), _ptr(ws),
+                                        ws.numel(), _stream(stream)))
 
 
 # ------------------------------------------------------ measurement hooks --

@@ -124,6 +124,27 @@ ReplayWs replay_ws_layout(const pr2_moe_desc& d, void* base) {
     return w;
 }
 
+BwdWs bwd_ws_layout(const pr2_moe_desc& d, void* base) {
+    BwdWs b{};
+    b.fw = replay_ws_layout(d, base);
+    const int64_t Tk = d.T * (int64_t)d.k;
+    b.np = bwd_partials(d);
+    char* p = base ? (char*)(((uintptr_t)base + 255) & ~(uintptr_t)255) : nullptr;
+    size_t off = b.fw.bytes - 256;   // end of the replay segments
+    auto take = [&](size_t bytes) {
+        char* q = p ? p + off : nullptr;
+        off += up256(bytes);
+        return q;
+    };
+    b.AU = take(act_bytes(d) * Tk * 2 * (size_t)d.m);
+    b.dgp = (float*)take(sizeof(float) * Tk * (size_t)b.np);
+    b.dp_route = (float*)take(sizeof(float) * Tk);
+    b.dp_perm = (float*)take(sizeof(float) * Tk);
+    b.wrt = (float*)take(sizeof(float) * (size_t)d.N * d.d);
+    b.bytes = off + 256;
+    return b;
+}
+
 // The route call folds the predictor into the router weights (N columns) when the
 // caller wants no logits, and projects [W_r | A] (N + r columns) otherwise.
 static size_t route_ws_bytes(const pr2_moe_desc& d) {
@@ -210,6 +231,13 @@ size_t pr2_workspace_bytes(const pr2_moe_desc* desc, int op) {
             t_err = saved;
             if (s != PR2_OK) return 0;
             return replay_ws_layout(*desc, nullptr).bytes;
+        }
+        case PR2_OP_REPLAY_BWD: {
+            std::string saved = t_err;
+            pr2_status s = check_desc(desc, true, true);
+            t_err = saved;
+            if (s != PR2_OK) return 0;
+            return bwd_ws_layout(*desc, nullptr).bytes;
         }
         default:
             return 0;
@@ -302,6 +330,78 @@ pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const
     if (validate) {
         int errs[ERR_WORDS];
         e = hipMemcpyAsync(errs, w.err, sizeof(errs), hipMemcpyDeviceToHost, st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
+        if (e != hipSuccess) return hip_fail(e, "validation readback");
+        if (errs[ERR_BAD_ID] || errs[ERR_DUP_ID])
+            return fail(PR2_ERR_ROUTE, "route has %d out-of-range and %d repeated ids",
+                        errs[ERR_BAD_ID], errs[ERR_DUP_ID]);
+    }
+    return ok();
+}
+
+pr2_status pr2_moe_replay_backward(const pr2_moe_desc* desc, const void* x, const void* idx,
+                                   int64_t ldi, const float* W_r, const float* b_r,
+                                   const void* W_gate, const void* W_up, const void* W_down,
+                                   const void* dy, void* dx, float* dW_r, float* db_r,
+                                   float* dW_gate, float* dW_up, float* dW_down, void* ws,
+                                   size_t ws_bytes, pr2_stream_t stream) {
+    pr2_status s = check_desc(desc, true, true);
+    if (s != PR2_OK) return s;
+    const pr2_moe_desc& d = *desc;
+    if (d.renorm != 1)
+        return fail(PR2_ERR_UNSUPPORTED, "the backward pass needs renorm = 1 (renormalised weights)");
+    if (ldi < d.k) return fail(PR2_ERR_SHAPE, "ldi = %lld < k = %d", (long long)ldi, d.k);
+    if (!W_r) return fail(PR2_ERR_NULL, "W_r is NULL");
+    if (!W_gate || !W_up || !W_down) return fail(PR2_ERR_NULL, "an expert weight pointer is NULL");
+    if (!dW_r || !dW_gate || !dW_up || !dW_down)
+        return fail(PR2_ERR_NULL, "a weight-gradient pointer is NULL");
+    if (d.T > 0) {
+        if (!x) return fail(PR2_ERR_NULL, "x is NULL");
+        if (!idx) return fail(PR2_ERR_NULL, "idx is NULL");
+        if (!dy) return fail(PR2_ERR_NULL, "dy is NULL");
+        if (!dx) return fail(PR2_ERR_NULL, "dx is NULL");
+    }
+    if (!aligned(x, 16) || !aligned(dy, 16) || !aligned(dx, 16) || !aligned(W_gate, 16) ||
+        !aligned(W_up, 16) || !aligned(W_down, 16))
+        return fail(PR2_ERR_ALIGN, "x, dy, dx and the expert weights must be 16-byte aligned");
+    if (!aligned(dW_gate, 16) || !aligned(dW_up, 16) || !aligned(dW_down, 16))
+        return fail(PR2_ERR_ALIGN, "expert weight gradients must be 16-byte aligned");
+    if (!aligned(W_r, 4) || !aligned(dW_r, 4) || (b_r && !aligned(b_r, 4)) || (db_r && !aligned(db_r, 4)))
+        return fail(PR2_ERR_ALIGN, "router tensors must be 4-byte aligned");
+    if (d.T > 0 && !aligned(idx, d.idx_dtype == PR2_I16 ? 2 : 4))
+        return fail(PR2_ERR_ALIGN, "idx is not aligned to its element size");
+    const BwdGrads out{dx, dW_r, db_r, dW_gate, dW_up, dW_down};
+    hipStream_t st = (hipStream_t)stream;
+    if (d.T == 0) {
+        s = device_ready();
+        if (s != PR2_OK) return s;
+        hipError_t e = launch_zero_grads(d, out, st);
+        if (e != hipSuccess) return hip_fail(e, "zero-gradient launch");
+        return ok();
+    }
+    const size_t need = bwd_ws_layout(d, nullptr).bytes;
+    if (!ws) return fail(PR2_ERR_NULL, "ws is NULL (need %zu bytes)", need);
+    if (ws_bytes < need)
+        return fail(PR2_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
+    s = device_ready();
+    if (s != PR2_OK) return s;
+
+    BwdWs w = bwd_ws_layout(d, ws);
+    const bool validate = validate_env();
+    hipError_t e;
+    if (validate) {
+        e = hipMemsetAsync(w.fw.err, 0, sizeof(int) * ERR_WORDS, st);
+        if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
+    }
+    e = launch_replay_gates(d, x, idx, ldi, W_r, b_r, w.fw.gate, w.fw.err, w.fw.wsplit, st);
+    if (e != hipSuccess) return hip_fail(e, "replay_gates launch");
+    e = launch_permute(d, idx, ldi, w.fw, st);
+    if (e != hipSuccess) return hip_fail(e, "permute launch");
+    e = launch_replay_backward(d, x, idx, ldi, W_r, W_gate, W_up, W_down, dy, w.fw.gate, w, out, st);
+    if (e != hipSuccess) return hip_fail(e, "backward launch");
+    if (validate) {
+        int errs[ERR_WORDS];
+        e = hipMemcpyAsync(errs, w.fw.err, sizeof(errs), hipMemcpyDeviceToHost, st);
         if (e == hipSuccess) e = hipStreamSynchronize(st);
         if (e != hipSuccess) return hip_fail(e, "validation readback");
         if (errs[ERR_BAD_ID] || errs[ERR_DUP_ID])

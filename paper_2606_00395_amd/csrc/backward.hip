@@ -1,0 +1,785 @@
+// Replay backward: gradients of <dy, y> for the replay forward with the
+// recorded ids held fixed (Sec. 4.1, replay during training: the experts and
+// the current router receive gradients through the replayed set; the
+// predictor is bypassed and receives none).  Weights are the renormalised
+// replay weights g = softmax of the k recorded logits.
+//
+// Per route (token t, slot s, expert e, permuted row q), with X = x_t:
+//   a = X W_gate_e^T, u = X W_up_e^T, H = silu(a) * u       (recomputed)
+//   G = dy_t W_down_e                   [m]   so that   dg = <H, G> = <dy_t, E_e(X)>
+//   dH = g G,  du = dH silu(a),  da = dH u silu'(a)
+//   dx_t   += da W_gate_e + du W_up_e + sum_j dp_tj W_r[:, j]
+//   dW_down_e = sum_q dy_t^T (g H),  dW_gate_e = sum_q da^T X,  dW_up_e = sum_q du^T X
+//   dp_ts = g_ts (dg_ts - sum_s' g_ts' dg_ts'),  dW_r[:, e] = sum_q X dp,  db_r[e] = sum_q dp
+//
+// bf16 path: four grouped GEMMs on v_mfma_f32_32x32x16_bf16 with the tile
+// shape of the forward kernels (256 x 256 output tile, K slices of 64, two
+// LDS stages, eight wavefronts of 64 x 128).  An operand whose K index runs
+// along its rows in memory (the weights in the input-gradient GEMMs, both
+// operands of the token-contracted weight-gradient GEMMs) is read with 16-byte
+// loads into registers, one 8 x 8 block per thread, transposed there and
+// written to LDS as 16-byte rows of eight consecutive K values, in the same
+// swizzled layout the direct-to-LDS copies of K-contiguous operands produce.
+// Every gradient is written exactly once (no atomics): results are
+// deterministic and overwrite the outputs.
+#include "common.h"
+
+namespace pr2 {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+constexpr int BM = 256;         // output tile rows
+constexpr int BN = 256;         // output tile columns
+constexpr int BK = 64;          // K slice
+constexpr int ROWB = BK * 2;    // bytes per LDS row
+constexpr int NSTAGE = 2;
+constexpr int WM = 64, WN = 128;
+constexpr int MI = WM / 32, NJ = WN / 32;
+constexpr int NWAVE = 8;
+constexpr int kThreads = 64 * NWAVE;
+constexpr int kGroups = 8;      // 8-row DMA groups per wavefront (4 wavefronts x 64 rows)
+constexpr int STAGEB = (BM + BN) * ROWB;
+constexpr int LDSB = NSTAGE * STAGEB;
+constexpr int kNumXcd = 8;
+
+enum { DH = 0, DX = 1, WD = 2, WGU = 3 };
+
+struct BwdArgs {
+    const int* perm_src;     // permuted row -> t*k + s
+    const int* tiles;        // (expert, first permuted row, rows) per 256-row tile
+    const int* tile_count;
+    const int* offsets;      // [N+1] first permuted row of each expert
+    int k, N, d, m, Tk;
+    int ntn;                 // DH, DX: 256-column panels per tile
+    const bf16_t* x;
+    const bf16_t* dy;
+    const bf16_t* Wg;
+    const bf16_t* Wu;
+    const bf16_t* Wd;
+    const float* gate;       // [T*k] replay weights, route order
+    bf16_t* AU;              // [T*k, 2m]: a | u in, da | du out
+    bf16_t* Hg;              // [T*k, m]: g * H
+    float* dgp;              // [T*k, m/128] partial gate gradients
+    bf16_t* dxr;             // [T*k, d] per-route input gradients
+    float* dWg;
+    float* dWu;
+    float* dWd;
+};
+
+__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+template <int n>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(n >= 0 && n < 16, "vmcnt field");
+    __builtin_amdgcn_s_waitcnt(0x0f70 | n);
+}
+
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ uint32_t pack_bf(float lo, float hi) {
+    return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+// SwiGLU backward of one element.  H is taken at the precision the forward
+// stores it (rounded to bf16 when round_h), so that dg = <H, G> is the
+// gradient of the computed output.
+__device__ __forceinline__ void swiglu_bwd(float a, float u, float G, float g, bool round_h,
+                                           float& da, float& du, float& hg, float& hG) {
+    const float sig = 1.0f / (1.0f + __expf(-a));
+    const float s = a * sig;
+    float H = s * u;
+    if (round_h) H = bf16_to_f32(f32_to_bf16(H));
+    const float dH = g * G;
+    du = dH * s;
+    da = dH * u * (sig * (1.0f + a * (1.0f - sig)));
+    hg = g * H;
+    hG = H * G;
+}
+
+// One operand whose K index runs along memory rows: this thread's 8 x 8 block
+// covers K values kt*BK + 8*c .. +7 and 8 tile rows starting at column `col`
+// of the source rows.
+struct KRows {
+    const bf16_t* b0;       // rows with K index < ksplit
+    const bf16_t* b1;       // rows with K index >= ksplit (row K index - ksplit)
+    int ksplit;
+    uint32_t ld;            // elements between source rows
+    uint32_t col;           // first element of this thread's 8 columns
+    int rbase;              // first permuted row (direct) or perm_src base (gathered)
+    int klen;               // K values; beyond it the operand is zero
+    bool gather;            // source row = perm_src[rbase + K] / k (a token row)
+};
+
+template <int MODE>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+bwd_gemm(BwdArgs g) {
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[LDSB];
+    constexpr bool kRowTiles = (MODE == DH || MODE == DX);   // C rows are permuted routes
+
+    // ---- work item (XCD-aware: each XCD takes a contiguous logical range)
+    int64_t L;
+    int nct = 1;
+    if (kRowTiles) {
+        L = (int64_t)(*g.tile_count) * g.ntn;
+    } else {
+        const int nrt = MODE == WD ? g.d / BM : 2 * g.m / BM;
+        nct = MODE == WD ? g.m / BN : g.d / BN;
+        L = (int64_t)g.N * nrt * nct;
+    }
+    const int64_t per_xcd = (L + kNumXcd - 1) / kNumXcd;
+    const int64_t local = blockIdx.x / kNumXcd;
+    if (local >= per_xcd) return;
+    const int64_t logical = (int64_t)(blockIdx.x % kNumXcd) * per_xcd + local;
+    if (logical >= L) return;
+
+    int expert, row0 = 0, rows = BM, pn = 0, rt = 0, ct = 0, klen;
+    if (kRowTiles) {
+        const int tile = (int)(logical / g.ntn);
+        pn = (int)(logical % g.ntn);
+        expert = g.tiles[3 * tile + 0];
+        row0 = g.tiles[3 * tile + 1];
+        rows = g.tiles[3 * tile + 2];
+        klen = MODE == DH ? g.d : 2 * g.m;
+    } else {
+        const int per_e = (int)(L / g.N);
+        expert = (int)(logical / per_e);
+        const int tt = (int)(logical % per_e);
+        rt = tt / nct;
+        ct = tt % nct;
+        row0 = g.offsets[expert];
+        klen = g.offsets[expert + 1] - row0;
+    }
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wr = wave >> 1;            // 64-row block of the output tile
+    const int wc = wave & 1;             // 128-column block
+    const int half = wave >> 2;          // operand this wavefront loads: 0 rows, 1 columns
+    const bool active = wr * WM < rows;
+    const bool dma = kRowTiles && half == 0;
+
+    // ---- operand loading
+    const int tt = tid & 255;
+    const int kc = tt & 7;               // K chunk of this thread's block
+    const int rb = tt >> 3;              // 8-row block of the tile
+    KRows kr{};
+    {
+        const int64_t ew = (int64_t)expert * g.m * g.d;   // elements per expert matrix
+        if (half == 1) {
+            if (MODE == DH) {
+                kr = {g.Wd + ew, g.Wd + ew, g.d, (uint32_t)g.m, (uint32_t)(pn * BN + 8 * rb), 0,
+                      g.d, false};
+            } else if (MODE == DX) {
+                kr = {g.Wg + ew, g.Wu + ew, g.m, (uint32_t)g.d, (uint32_t)(pn * BN + 8 * rb), 0,
+                      2 * g.m, false};
+            } else if (MODE == WD) {
+                kr = {g.Hg, g.Hg, klen, (uint32_t)g.m, (uint32_t)(ct * BN + 8 * rb), row0, klen,
+                      false};
+            } else {
+                kr = {g.x, g.x, klen, (uint32_t)g.d, (uint32_t)(ct * BN + 8 * rb), row0, klen, true};
+            }
+        } else if (MODE == WD) {
+            kr = {g.dy, g.dy, klen, (uint32_t)g.d, (uint32_t)(rt * BM + 8 * rb), row0, klen, true};
+        } else if (MODE == WGU) {
+            kr = {g.AU, g.AU, klen, (uint32_t)(2 * g.m), (uint32_t)(rt * BM + 8 * rb), row0, klen,
+                  false};
+        }
+    }
+    u32x4 st[8];
+    auto kload = [&](int kt) {
+        const int kb = kt * BK;
+        const bool hi = kb >= kr.ksplit;
+        const bf16_t* b = hi ? kr.b1 : kr.b0;
+        const int kshift = hi ? kr.ksplit : 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int kk = kb + 8 * kc + i;
+            u32x4 v = {0u, 0u, 0u, 0u};
+            if (kk < kr.klen) {
+                const int row = kr.gather ? g.perm_src[kr.rbase + kk] / g.k : kr.rbase + kk - kshift;
+                v = *(const u32x4*)(b + ((uint32_t)row * kr.ld + kr.col));
+            }
+            st[i] = v;
+        }
+    };
+    auto kstore = [&](int stage) {
+        unsigned char* sb = lds + stage * STAGEB + (half ? BM * ROWB : 0);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int R = 8 * rb + j;
+            const int w = j >> 1;
+            u32x4 o;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                o[q] = (j & 1) ? ((st[2 * q][w] >> 16) | (st[2 * q + 1][w] & 0xffff0000u))
+                               : ((st[2 * q][w] & 0xffffu) | (st[2 * q + 1][w] << 16));
+            *(u32x4*)(sb + R * ROWB + ((kc ^ swz(R)) << 4)) = o;
+        }
+    };
+
+    // direct-to-LDS copies of the K-contiguous row operand (DH: gathered dy, DX: da | du)
+    const bf16_t* sbase = MODE == DH ? g.dy : g.AU;
+    uint32_t soff[kGroups];
+    if (kRowTiles) {
+#pragma unroll
+        for (int i = 0; i < kGroups; ++i) {
+            const int r = (wave & 3) * (kGroups * 8) + i * 8 + lane / 8;
+            const int chunk = (lane % 8) ^ swz(r);
+            const int rr = r < rows ? r : 0;
+            uint32_t off;
+            if (MODE == DH)
+                off = (uint32_t)(min(max(g.perm_src[row0 + rr], 0), g.Tk - 1) / g.k) * (uint32_t)g.d;
+            else
+                off = (uint32_t)(row0 + rr) * (uint32_t)(2 * g.m);
+            soff[i] = off + chunk * 8;
+        }
+    }
+    auto issue = [&](int stage, int k0) {
+#pragma unroll
+        for (int i = 0; i < kGroups; ++i) {
+            const int grp = (wave & 3) * kGroups + i;
+            __builtin_amdgcn_global_load_lds((const void*)(sbase + (soff[i] + (uint32_t)k0)),
+                                             (lds_void*)&lds[stage * STAGEB + grp * 1024], 16, 0,
+                                             0);
+        }
+    };
+
+    f32x16 acc[MI][NJ];
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+    const int lrow = lane & 31;
+    const int sw = swz(lrow);
+    int kpos[BK / 16];
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) kpos[ks] = lrow * ROWB + (((2 * ks + (lane >> 5)) ^ sw) << 4);
+    int a_base[MI], b_base[NJ];
+#pragma unroll
+    for (int i = 0; i < MI; ++i) a_base[i] = (wr * WM + i * 32) * ROWB;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) b_base[j] = (BM + wc * WN + j * 32) * ROWB;
+
+    const int nk = (klen + BK - 1) / BK;
+    if (nk > 0) {
+        if (dma) {
+            issue(0, 0);
+        } else {
+            kload(0);
+            wait_vmcnt<0>();
+            kstore(0);
+        }
+    }
+    for (int kt = 0; kt < nk; ++kt) {
+        wait_vmcnt<0>();
+        __syncthreads();
+        const bool more = kt + 1 < nk;
+        if (more) {
+            if (dma) issue((kt + 1) % NSTAGE, (kt + 1) * BK);
+            else kload(kt + 1);
+        }
+        if (active) {
+            const unsigned char* base = lds + (kt % NSTAGE) * STAGEB;
+            bf16x8 fa[2][MI], fb[2][NJ];
+            auto read_frags = [&](int buf, int ks) {
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+                    fa[buf][i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + a_base[i] + kpos[ks]));
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+                    fb[buf][j] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + b_base[j] + kpos[ks]));
+            };
+            read_frags(0, 0);
+#pragma unroll
+            for (int ks = 0; ks < BK / 16; ++ks) {
+                if (ks + 1 < BK / 16) read_frags((ks + 1) & 1, ks + 1);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            fb[ks & 1][j], fa[ks & 1][i], acc[i][j], 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        if (more && !dma) {
+            wait_vmcnt<0>();
+            kstore((kt + 1) % NSTAGE);
+        }
+    }
+    if (!active) return;
+
+    // ---- epilogues.  Lane l holds output row l%32 of each 32-row block and
+    // columns 8*(v/4) + 4*(l/32) + v%4 of each 32-column block.
+    const int ncol0 = 4 * (lane >> 5);
+    if (MODE == DH) {
+        const int np = g.m / 128;
+        const int64_t ldau = 2 * (int64_t)g.m;
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+            const int r = wr * WM + i * 32 + (lane & 31);
+            const bool ok = r < rows;
+            const int64_t q = row0 + (ok ? r : 0);
+            const float gq = ok ? g.gate[min(max(g.perm_src[q], 0), g.Tk - 1)] : 0.0f;
+            bf16_t* au = g.AU + q * ldau;
+            bf16_t* hg = g.Hg + q * g.m;
+            float part = 0.0f;
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+#pragma unroll
+                for (int a4 = 0; a4 < 4; ++a4) {
+                    const int col = pn * BN + wc * WN + j * 32 + 8 * a4 + ncol0;
+                    if (ok) {
+                        const uint2 av = *(const uint2*)(au + col);
+                        const uint2 uv = *(const uint2*)(au + g.m + col);
+                        const float a[4] = {bf_lo(av.x), bf_hi(av.x), bf_lo(av.y), bf_hi(av.y)};
+                        const float u[4] = {bf_lo(uv.x), bf_hi(uv.x), bf_lo(uv.y), bf_hi(uv.y)};
+                        float da[4], du[4], hgv[4];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            float hG;
+                            swiglu_bwd(a[e], u[e], acc[i][j][4 * a4 + e], gq, true, da[e], du[e],
+                                       hgv[e], hG);
+                            part += hG;
+                        }
+                        *(uint2*)(au + col) = make_uint2(pack_bf(da[0], da[1]), pack_bf(da[2], da[3]));
+                        *(uint2*)(au + g.m + col) =
+                            make_uint2(pack_bf(du[0], du[1]), pack_bf(du[2], du[3]));
+                        *(uint2*)(hg + col) = make_uint2(pack_bf(hgv[0], hgv[1]), pack_bf(hgv[2], hgv[3]));
+                    }
+                }
+            }
+            part += __shfl_xor(part, 32);
+            if (ok && lane < 32) g.dgp[q * np + pn * 2 + wc] = part;
+        }
+    } else if (MODE == DX) {
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+            const int r = wr * WM + i * 32 + (lane & 31);
+            if (r >= rows) continue;
+            bf16_t* orow = g.dxr + ((int64_t)row0 + r) * g.d;
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+#pragma unroll
+                for (int a4 = 0; a4 < 4; ++a4) {
+                    const int col = pn * BN + wc * WN + j * 32 + 8 * a4 + ncol0;
+                    const int v0 = 4 * a4;
+                    *(uint2*)(orow + col) =
+                        make_uint2(pack_bf(acc[i][j][v0], acc[i][j][v0 + 1]),
+                                   pack_bf(acc[i][j][v0 + 2], acc[i][j][v0 + 3]));
+                }
+            }
+        }
+    } else {
+        const int64_t ew = (int64_t)expert * g.m * g.d;
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+            const int R = rt * BM + wr * WM + i * 32 + (lane & 31);
+            float* orow;
+            if (MODE == WD) orow = g.dWd + ew + (int64_t)R * g.m;
+            else orow = (R < g.m ? g.dWg + ew + (int64_t)R * g.d : g.dWu + ew + (int64_t)(R - g.m) * g.d);
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+#pragma unroll
+                for (int a4 = 0; a4 < 4; ++a4) {
+                    const int col = ct * BN + wc * WN + j * 32 + 8 * a4 + ncol0;
+                    const int v0 = 4 * a4;
+                    *(f32x4*)(orow + col) = f32x4{acc[i][j][v0], acc[i][j][v0 + 1],
+                                                  acc[i][j][v0 + 2], acc[i][j][v0 + 3]};
+                }
+            }
+        }
+    }
+}
+
+// ------------------------------------------------------------ generic ----
+// One thread per output element; any shape, bf16 or fp32.
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+dh_generic(const T* dy, const int* perm_src, int k, const T* Wd, const float* gate, int d, int m,
+           const int* tiles, const int* tile_count, T* AU, T* Hg, float* dgp) {
+    const int tile = blockIdx.x;
+    if (tile >= *tile_count) return;
+    const int expert = tiles[3 * tile], row0 = tiles[3 * tile + 1], rows = tiles[3 * tile + 2];
+    const int r = threadIdx.x;
+    const int j = blockIdx.y;
+    if (r >= rows || j >= m) return;
+    const int64_t q = row0 + r;
+    const int src = perm_src[q];
+    const T* dyr = dy + (int64_t)(src / k) * d;
+    const T* w = Wd + (int64_t)expert * d * m + j;
+    float G = 0.0f;
+    for (int i = 0; i < d; ++i) G = fmaf(Act<T>::to_f32(dyr[i]), Act<T>::to_f32(w[(int64_t)i * m]), G);
+    T* au = AU + q * 2 * m;
+    float da, du, hg, hG;
+    swiglu_bwd(Act<T>::to_f32(au[j]), Act<T>::to_f32(au[m + j]), G, gate[src],
+               sizeof(T) == 2, da, du, hg, hG);
+    au[j] = Act<T>::from_f32(da);
+    au[m + j] = Act<T>::from_f32(du);
+    Hg[q * m + j] = Act<T>::from_f32(hg);
+    dgp[q * m + j] = hG;
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+dx_generic(const T* AU, const T* Wg, const T* Wu, int d, int m, const int* tiles,
+           const int* tile_count, T* dxr) {
+    const int tile = blockIdx.x;
+    if (tile >= *tile_count) return;
+    const int expert = tiles[3 * tile], row0 = tiles[3 * tile + 1], rows = tiles[3 * tile + 2];
+    const int r = threadIdx.x;
+    const int i = blockIdx.y;
+    if (r >= rows || i >= d) return;
+    const int64_t q = row0 + r;
+    const T* au = AU + q * 2 * m;
+    const T* wg = Wg + (int64_t)expert * m * d + i;
+    const T* wu = Wu + (int64_t)expert * m * d + i;
+    float acc = 0.0f;
+    for (int j = 0; j < m; ++j) {
+        acc = fmaf(Act<T>::to_f32(au[j]), Act<T>::to_f32(wg[(int64_t)j * d]), acc);
+        acc = fmaf(Act<T>::to_f32(au[m + j]), Act<T>::to_f32(wu[(int64_t)j * d]), acc);
+    }
+    dxr[q * d + i] = Act<T>::from_f32(acc);
+}
+
+// dW_down[e][i][j] = sum over expert e's routes of dy[t][i] * (g H)[q][j]
+template <typename T>
+__global__ void __launch_bounds__(256)
+wd_generic(const T* dy, const T* Hg, const int* perm_src, const int* offsets, int k, int d, int m,
+           float* dWd) {
+    const int e = blockIdx.x;
+    const int i = blockIdx.y;
+    const int q0 = offsets[e], q1 = offsets[e + 1];
+    for (int j = threadIdx.x; j < m; j += blockDim.x) {
+        float acc = 0.0f;
+        for (int q = q0; q < q1; ++q)
+            acc = fmaf(Act<T>::to_f32(dy[(int64_t)(perm_src[q] / k) * d + i]),
+                       Act<T>::to_f32(Hg[(int64_t)q * m + j]), acc);
+        dWd[((int64_t)e * d + i) * m + j] = acc;
+    }
+}
+
+// dW_gate[e][r][i] (r < m) / dW_up[e][r - m][i] = sum over routes of (da | du)[q][r] * x[t][i]
+template <typename T>
+__global__ void __launch_bounds__(256)
+wgu_generic(const T* x, const T* AU, const int* perm_src, const int* offsets, int k, int d, int m,
+            float* dWg, float* dWu) {
+    const int e = blockIdx.x;
+    const int r = blockIdx.y;
+    const int q0 = offsets[e], q1 = offsets[e + 1];
+    float* out = r < m ? dWg + ((int64_t)e * m + r) * d : dWu + ((int64_t)e * m + r - m) * d;
+    for (int i = threadIdx.x; i < d; i += blockDim.x) {
+        float acc = 0.0f;
+        for (int q = q0; q < q1; ++q)
+            acc = fmaf(Act<T>::to_f32(AU[(int64_t)q * 2 * m + r]),
+                       Act<T>::to_f32(x[(int64_t)(perm_src[q] / k) * d + i]), acc);
+        out[i] = acc;
+    }
+}
+
+// ------------------------------------------------------------ router ----
+
+// W_r [d, N] -> [N, d]
+__global__ void __launch_bounds__(256)
+transpose_wr_kernel(const float* W_r, int d, int N, float* wrt) {
+    __shared__ float tile[32][33];
+    const int i0 = blockIdx.x * 32, e0 = blockIdx.y * 32;
+    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+    for (int y = ty; y < 32; y += 8)
+        if (i0 + y < d && e0 + tx < N) tile[y][tx] = W_r[(int64_t)(i0 + y) * N + e0 + tx];
+    __syncthreads();
+    for (int y = ty; y < 32; y += 8)
+        if (e0 + y < N && i0 + tx < d) wrt[(int64_t)(e0 + y) * d + i0 + tx] = tile[tx][y];
+}
+
+// Per token: dg_s = sum of its partials, then the renormalised-softmax backward
+// dp_s = g_s (dg_s - sum_s' g_s' dg_s'), in route and in permuted order.
+__global__ void __launch_bounds__(256)
+gate_grad_kernel(const float* dgp, int np, const int* inv, const float* gate, int64_t T, int k,
+                 float* dp_route, float* dp_perm) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= T) return;
+    float inner = 0.0f;
+    for (int s = 0; s < k; ++s) {
+        const int q = inv[t * k + s];
+        float dg = 0.0f;
+        if (q >= 0)
+            for (int p = 0; p < np; ++p) dg += dgp[(int64_t)q * np + p];
+        dp_route[t * k + s] = dg;
+        inner = fmaf(gate[t * k + s], dg, inner);
+    }
+    for (int s = 0; s < k; ++s) {
+        const float gs = gate[t * k + s];
+        const float dp = gs * (dp_route[t * k + s] - inner);
+        dp_route[t * k + s] = dp;
+        const int q = inv[t * k + s];
+        if (q >= 0) dp_perm[q] = dp;
+    }
+}
+
+// dW_r[:, e] = sum over expert e's routes of dp * x_t, db_r[e] = sum of dp.
+// Block (e, column chunk of 256): 8 row groups of 32 threads, 8 columns per
+// thread, summed across groups in a fixed order.
+template <typename T>
+__global__ void __launch_bounds__(256)
+router_wgrad_kernel(const T* x, const int* perm_src, const int* offsets, const float* dp_perm,
+                    int k, int d, int N, float* dW_r, float* db_r) {
+    __shared__ float red[8][256];
+    __shared__ float dbs[256];
+    const int e = blockIdx.x;
+    const int cg = threadIdx.x & 31, rg = threadIdx.x >> 5;
+    const int i0 = blockIdx.y * 256 + 8 * cg;
+    const int q0 = offsets[e], q1 = offsets[e + 1];
+    float acc[8];
+#pragma unroll
+    for (int v = 0; v < 8; ++v) acc[v] = 0.0f;
+    for (int q = q0 + rg; q < q1; q += 8) {
+        const float w = dp_perm[q];
+        const T* xr = x + (int64_t)(perm_src[q] / k) * d;
+        if (sizeof(T) == 2 && i0 + 8 <= d) {
+            const u32x4 v = *(const u32x4*)(xr + i0);
+#pragma unroll
+            for (int h = 0; h < 4; ++h) {
+                acc[2 * h] = fmaf(w, bf_lo(v[h]), acc[2 * h]);
+                acc[2 * h + 1] = fmaf(w, bf_hi(v[h]), acc[2 * h + 1]);
+            }
+        } else {
+#pragma unroll
+            for (int v = 0; v < 8; ++v)
+                if (i0 + v < d) acc[v] = fmaf(w, Act<T>::to_f32(xr[i0 + v]), acc[v]);
+        }
+    }
+#pragma unroll
+    for (int v = 0; v < 8; ++v) red[rg][8 * cg + v] = acc[v];
+    __syncthreads();
+    {
+        const int c = threadIdx.x;          // column within the chunk
+        float s = 0.0f;
+#pragma unroll
+        for (int r = 0; r < 8; ++r) s += red[r][c];
+        const int i = blockIdx.y * 256 + c;
+        if (i < d) dW_r[(int64_t)i * N + e] = s;
+    }
+    if (db_r && blockIdx.y == 0) {
+        float s = 0.0f;
+        for (int q = q0 + (int)threadIdx.x; q < q1; q += 256) s += dp_perm[q];
+        dbs[threadIdx.x] = s;
+        __syncthreads();
+        for (int w = 128; w > 0; w >>= 1) {
+            if ((int)threadIdx.x < w) dbs[threadIdx.x] += dbs[threadIdx.x + w];
+            __syncthreads();
+        }
+        if (threadIdx.x == 0) db_r[e] = dbs[0];
+    }
+}
+
+// dx_t = sum_s dxr[route (t, s)] + sum_s dp_ts W_r[:, idx_ts], summed in slot order in fp32
+template <typename T>
+__global__ void __launch_bounds__(256)
+dx_combine_kernel(const T* dxr, const int* inv, const float* dp_route, const float* wrt,
+                  const void* idx, int idx_dtype, int64_t ldi, int64_t T_, int k, int d, int N,
+                  T* dx) {
+    const int64_t t = blockIdx.x;
+    if (t >= T_) return;
+    for (int i = threadIdx.x; i < d; i += blockDim.x) {
+        float acc = 0.0f;
+        for (int s = 0; s < k; ++s) {
+            const int q = inv[t * k + s];
+            if (q >= 0) acc += Act<T>::to_f32(dxr[(int64_t)q * d + i]);
+        }
+        for (int s = 0; s < k; ++s) {
+            const int e = load_id(idx, idx_dtype, t * ldi + s);
+            if (e >= 0 && e < N) acc = fmaf(dp_route[t * k + s], wrt[(int64_t)e * d + i], acc);
+        }
+        dx[t * d + i] = Act<T>::from_f32(acc);
+    }
+}
+
+__global__ void __launch_bounds__(256) fill_zero_kernel(float* p, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = 0.0f;
+}
+
+hipError_t zero(float* p, int64_t n, hipStream_t s) {
+    if (!p || n <= 0) return hipSuccess;
+    int64_t blocks = (n + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p, n);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_generic_gemms(const pr2_moe_desc& d, const void* x, const void* Wg,
+                                const void* Wu, const void* Wd, const void* dy, const float* gate,
+                                const BwdWs& ws, const BwdGrads& out, hipStream_t s) {
+    const ReplayWs& w = ws.fw;
+    {
+        LaunchScope scope("bwd_dh_generic", s);
+        hipLaunchKernelGGL(dh_generic<T>, dim3((unsigned)w.max_tiles, (unsigned)d.m), dim3(256), 0,
+                           s, (const T*)dy, w.perm_src, d.k, (const T*)Wd, gate, d.d, d.m, w.tiles,
+                           w.tile_count, (T*)ws.AU, (T*)w.H, ws.dgp);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    {
+        LaunchScope scope("bwd_dx_generic", s);
+        hipLaunchKernelGGL(dx_generic<T>, dim3((unsigned)w.max_tiles, (unsigned)d.d), dim3(256), 0,
+                           s, (const T*)ws.AU, (const T*)Wg, (const T*)Wu, d.d, d.m, w.tiles,
+                           w.tile_count, (T*)w.O);
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    {
+        LaunchScope scope("bwd_wd_generic", s);
+        hipLaunchKernelGGL(wd_generic<T>, dim3((unsigned)d.N, (unsigned)d.d), dim3(256), 0, s,
+                           (const T*)dy, (const T*)w.H, w.perm_src, w.offsets, d.k, d.d, d.m,
+                           out.dW_down);
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    LaunchScope scope("bwd_wgu_generic", s);
+    hipLaunchKernelGGL(wgu_generic<T>, dim3((unsigned)d.N, (unsigned)(2 * d.m)), dim3(256), 0, s,
+                       (const T*)x, (const T*)ws.AU, w.perm_src, w.offsets, d.k, d.d, d.m,
+                       out.dW_gate, out.dW_up);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+bool bwd_mfma_ok(const pr2_moe_desc& d) {
+    const int64_t lim = (int64_t)1 << 31;
+    const int64_t Tk = d.T * (int64_t)d.k;
+    return mfma_shape_ok(d) && d.m % BN == 0 && d.d % BN == 0 && Tk * 2 * d.m < lim;
+}
+
+int bwd_partials(const pr2_moe_desc& d) { return bwd_mfma_ok(d) ? d.m / 128 : d.m; }
+
+hipError_t launch_zero_grads(const pr2_moe_desc& d, const BwdGrads& out, hipStream_t s) {
+    LaunchScope scope("bwd_zero_grads", s);
+    const int64_t wmd = (int64_t)d.N * d.m * d.d;
+    hipError_t e;
+    if ((e = zero(out.dW_r, (int64_t)d.d * d.N, s)) != hipSuccess) return e;
+    if ((e = zero(out.db_r, d.N, s)) != hipSuccess) return e;
+    if ((e = zero(out.dW_gate, wmd, s)) != hipSuccess) return e;
+    if ((e = zero(out.dW_up, wmd, s)) != hipSuccess) return e;
+    return zero(out.dW_down, wmd, s);
+}
+
+hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const void* idx,
+                                  int64_t ldi, const float* W_r, const void* W_gate,
+                                  const void* W_up, const void* W_down, const void* dy,
+                                  const float* gate, const BwdWs& ws, const BwdGrads& out,
+                                  hipStream_t s) {
+    const ReplayWs& w = ws.fw;
+    const bool bf = d.act_dtype == PR2_BF16;
+    hipError_t e = launch_preact(d, x, W_gate, W_up, w, ws.AU, s);
+    if (e != hipSuccess) return e;
+
+    // expert GEMMs: gate gradient partials, SwiGLU backward, per-route input
+    // gradients and the expert weight gradients
+    if (bwd_mfma_ok(d)) {
+        BwdArgs g{};
+        g.perm_src = w.perm_src;
+        g.tiles = w.tiles;
+        g.tile_count = w.tile_count;
+        g.offsets = w.offsets;
+        g.k = d.k;
+        g.N = d.N;
+        g.d = d.d;
+        g.m = d.m;
+        g.Tk = (int)(d.T * d.k);
+        g.x = (const bf16_t*)x;
+        g.dy = (const bf16_t*)dy;
+        g.Wg = (const bf16_t*)W_gate;
+        g.Wu = (const bf16_t*)W_up;
+        g.Wd = (const bf16_t*)W_down;
+        g.gate = gate;
+        g.AU = (bf16_t*)ws.AU;
+        g.Hg = (bf16_t*)w.H;
+        g.dgp = ws.dgp;
+        g.dxr = (bf16_t*)w.O;
+        g.dWg = out.dW_gate;
+        g.dWu = out.dW_up;
+        g.dWd = out.dW_down;
+        auto grid_for = [](int64_t work) {
+            return dim3((unsigned)(((work + kNumXcd - 1) / kNumXcd) * kNumXcd));
+        };
+        g.ntn = d.m / BN;
+        {
+            LaunchScope scope("bwd_dh_swiglu", s);
+            hipLaunchKernelGGL(bwd_gemm<DH>, grid_for(w.max_tiles * g.ntn), dim3(kThreads), 0, s, g);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        g.ntn = d.d / BN;
+        {
+            LaunchScope scope("bwd_dx_gemm", s);
+            hipLaunchKernelGGL(bwd_gemm<DX>, grid_for(w.max_tiles * g.ntn), dim3(kThreads), 0, s, g);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        {
+            LaunchScope scope("bwd_wgrad_down", s);
+            hipLaunchKernelGGL(bwd_gemm<WD>, grid_for((int64_t)d.N * (d.d / BM) * (d.m / BN)),
+                               dim3(kThreads), 0, s, g);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        {
+            LaunchScope scope("bwd_wgrad_gate_up", s);
+            hipLaunchKernelGGL(bwd_gemm<WGU>, grid_for((int64_t)d.N * (2 * d.m / BM) * (d.d / BN)),
+                               dim3(kThreads), 0, s, g);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    } else {
+        e = bf ? launch_generic_gemms<bf16_t>(d, x, W_gate, W_up, W_down, dy, gate, ws, out, s)
+               : launch_generic_gemms<float>(d, x, W_gate, W_up, W_down, dy, gate, ws, out, s);
+        if (e != hipSuccess) return e;
+    }
+
+    // router: logit gradients, then the input-gradient combine and dW_r, db_r
+    {
+        LaunchScope scope("bwd_gate_grad", s);
+        hipLaunchKernelGGL(gate_grad_kernel, dim3((unsigned)((d.T + 255) / 256)), dim3(256), 0, s,
+                           ws.dgp, ws.np, w.inv, gate, d.T, d.k, ws.dp_route, ws.dp_perm);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    {
+        LaunchScope scope("bwd_transpose_wr", s);
+        hipLaunchKernelGGL(transpose_wr_kernel,
+                           dim3((unsigned)((d.d + 31) / 32), (unsigned)((d.N + 31) / 32)), dim3(256),
+                           0, s, W_r, d.d, d.N, ws.wrt);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    {
+        LaunchScope scope("bwd_dx_combine", s);
+        if (bf)
+            hipLaunchKernelGGL(dx_combine_kernel<bf16_t>, dim3((unsigned)d.T), dim3(256), 0, s,
+                               (const bf16_t*)w.O, w.inv, ws.dp_route, ws.wrt, idx, d.idx_dtype, ldi,
+                               d.T, d.k, d.d, d.N, (bf16_t*)out.dx);
+        else
+            hipLaunchKernelGGL(dx_combine_kernel<float>, dim3((unsigned)d.T), dim3(256), 0, s,
+                               (const float*)w.O, w.inv, ws.dp_route, ws.wrt, idx, d.idx_dtype, ldi,
+                               d.T, d.k, d.d, d.N, (float*)out.dx);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    {
+        LaunchScope scope("bwd_router_wgrad", s);
+        dim3 grid((unsigned)d.N, (unsigned)((d.d + 255) / 256));
+        if (bf)
+            hipLaunchKernelGGL(router_wgrad_kernel<bf16_t>, grid, dim3(256), 0, s, (const bf16_t*)x,
+                               w.perm_src, w.offsets, ws.dp_perm, d.k, d.d, d.N, out.dW_r, out.db_r);
+        else
+            hipLaunchKernelGGL(router_wgrad_kernel<float>, grid, dim3(256), 0, s, (const float*)x,
+                               w.perm_src, w.offsets, ws.dp_perm, d.k, d.d, d.N, out.dW_r, out.db_r);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace pr2

@@ -76,6 +76,20 @@ struct ReplayWs {
 
 ReplayWs replay_ws_layout(const pr2_moe_desc& d, void* base);
 
+// the replay segments followed by the backward pass's own
+struct BwdWs {
+    ReplayWs fw;        // fw.H holds g*H, fw.O the per-route input gradients
+    void* AU;           // [T*k, 2m] act: pre-activations a | u, then their gradients
+    float* dgp;         // [T*k, np] partial gate gradients
+    float* dp_route;    // [T*k] router-logit gradient per (token, slot)
+    float* dp_perm;     // [T*k] the same in permuted order
+    float* wrt;         // [N, d] W_r transposed
+    int np;
+    size_t bytes;
+};
+
+BwdWs bwd_ws_layout(const pr2_moe_desc& d, void* base);
+
 // ------------------------------------------------------------ launches ----
 // Every launch goes through this so that measurement events can bracket it.
 struct LaunchScope {
@@ -108,5 +122,26 @@ hipError_t launch_combine(const pr2_moe_desc& d, const ReplayWs& ws, void* y, hi
 hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void* W_gate,
                                const void* W_up, const void* W_down, const float* gate,
                                const ReplayWs& ws, hipStream_t s);
+bool mfma_shape_ok(const pr2_moe_desc& d);
+hipError_t launch_preact(const pr2_moe_desc& d, const void* x, const void* W_gate,
+                         const void* W_up, const ReplayWs& ws, void* AU, hipStream_t s);
+
+// backward.hip
+bool bwd_mfma_ok(const pr2_moe_desc& d);
+int bwd_partials(const pr2_moe_desc& d);    // partial gate-gradient sums per route
+struct BwdGrads {
+    void* dx;
+    float* dW_r;
+    float* db_r;        // may be null
+    float* dW_gate;
+    float* dW_up;
+    float* dW_down;
+};
+hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const void* idx,
+                                  int64_t ldi, const float* W_r, const void* W_gate,
+                                  const void* W_up, const void* W_down, const void* dy,
+                                  const float* gate, const BwdWs& ws, const BwdGrads& out,
+                                  hipStream_t s);
+hipError_t launch_zero_grads(const pr2_moe_desc& d, const BwdGrads& out, hipStream_t s);
 
 }  // namespace pr2

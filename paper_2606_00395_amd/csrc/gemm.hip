@@ -24,6 +24,9 @@
 // straight from registers.  Workgroups are mapped so that each XCD takes a
 // contiguous range of the tile list (same experts, shared L2).
 //
+// A third epilogue serves the backward pass: it stores the pre-activations
+// a = X_e W_gate_e^T and u = X_e W_up_e^T (bf16) instead of H.
+//
 // Other shapes and the fp32 path use a plain one-thread-per-output kernel.
 #include "common.h"
 
@@ -131,7 +134,7 @@ grouped_gemm_mfma(MfmaArgs g) {
     const int wrow0 = wave * kGroups * kRowsPerDma;
     const bf16_t* sbase;
     if (wrow0 < BM) sbase = g.A;
-    else if (MODE == 0) sbase = (wrow0 - BM < 128 ? g.W0 : g.W1) + (int64_t)expert * g.w_stride;
+    else if (MODE != 1) sbase = (wrow0 - BM < 128 ? g.W0 : g.W1) + (int64_t)expert * g.w_stride;
     else sbase = g.W0 + (int64_t)expert * g.w_stride;
     uint32_t soff[kGroups];
 #pragma unroll
@@ -142,11 +145,11 @@ grouped_gemm_mfma(MfmaArgs g) {
         if (r < BM) {
             // rows past the tile's end read a valid row; their results are never stored
             const int rr = r < rows ? r : 0;
-            if (MODE == 0) off = (int64_t)(min(max(g.perm_src[row0 + rr], 0), g.Tk - 1) / g.k) * g.K;
+            if (MODE != 1) off = (int64_t)(min(max(g.perm_src[row0 + rr], 0), g.Tk - 1) / g.k) * g.K;
             else off = ((int64_t)row0 + rr) * g.K;
         } else {
             const int pr = r - BM;
-            off = MODE == 0 ? (int64_t)(pn * 128 + (pr & 127)) * g.K
+            off = MODE != 1 ? (int64_t)(pn * 128 + (pr & 127)) * g.K
                             : (int64_t)(pn * BP + pr) * g.K;
         }
         soff[i] = (uint32_t)(off + chunk * 8);
@@ -183,7 +186,7 @@ grouped_gemm_mfma(MfmaArgs g) {
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
         int prow;
-        if (MODE == 0) prow = (j < NJ / 2 ? 0 : 128) + wc * (WN / 2) + (j % (NJ / 2)) * 32;
+        if (MODE != 1) prow = (j < NJ / 2 ? 0 : 128) + wc * (WN / 2) + (j % (NJ / 2)) * 32;
         else prow = wc * WN + j * 32;
         b_base[j] = (BM + prow) * ROWB;
     }
@@ -254,6 +257,25 @@ grouped_gemm_mfma(MfmaArgs g) {
                     *(uint2*)(orow + col + 8 * a4) = make_uint2(w[0], w[1]);
                 }
             }
+        } else if (MODE == 2) {
+            // pre-activations for the backward pass: a at column col, u at m + col
+#pragma unroll
+            for (int j = 0; j < NJ / 2; ++j) {
+                const int col = pn * 128 + wc * (WN / 2) + j * 32 + ncol0;
+#pragma unroll
+                for (int a4 = 0; a4 < 4; ++a4) {
+#pragma unroll
+                    for (int half = 0; half < 2; ++half) {
+                        const int jj = j + half * (NJ / 2);
+                        const int v0 = 4 * a4;
+                        const uint32_t w0 = (uint32_t)f32_to_bf16(acc[i][jj][v0]) |
+                                            ((uint32_t)f32_to_bf16(acc[i][jj][v0 + 1]) << 16);
+                        const uint32_t w1 = (uint32_t)f32_to_bf16(acc[i][jj][v0 + 2]) |
+                                            ((uint32_t)f32_to_bf16(acc[i][jj][v0 + 3]) << 16);
+                        *(uint2*)(orow + half * (g.n_out / 2) + col + 8 * a4) = make_uint2(w0, w1);
+                    }
+                }
+            }
         } else {
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
@@ -275,6 +297,32 @@ grouped_gemm_mfma(MfmaArgs g) {
 }
 
 // ---------------------------------------------------------------- generic --
+// pre-activations a = x W_gate^T, u = x W_up^T of each permuted row (backward recompute)
+template <typename T>
+__global__ void __launch_bounds__(256)
+preact_generic(const T* x, const int* perm_src, int k, const T* Wg, const T* Wu, int d, int m,
+               const int* tiles, const int* tile_count, T* AU) {
+    const int tile = blockIdx.x;
+    if (tile >= *tile_count) return;
+    const int expert = tiles[3 * tile], row0 = tiles[3 * tile + 1], rows = tiles[3 * tile + 2];
+    const int r = threadIdx.x;
+    const int col = blockIdx.y;
+    if (r >= rows || col >= m) return;
+    const int64_t tok = perm_src[row0 + r] / k;
+    const T* xr = x + tok * d;
+    const T* g = Wg + ((int64_t)expert * m + col) * d;
+    const T* u = Wu + ((int64_t)expert * m + col) * d;
+    float a = 0.0f, b = 0.0f;
+    for (int i = 0; i < d; ++i) {
+        float xv = Act<T>::to_f32(xr[i]);
+        a = fmaf(xv, Act<T>::to_f32(g[i]), a);
+        b = fmaf(xv, Act<T>::to_f32(u[i]), b);
+    }
+    T* o = AU + (int64_t)(row0 + r) * 2 * m;
+    o[col] = Act<T>::from_f32(a);
+    o[m + col] = Act<T>::from_f32(b);
+}
+
 template <typename T>
 __global__ void __launch_bounds__(256)
 gemm1_generic(const T* x, const int* perm_src, int k, const T* Wg, const T* Wu, int d, int m,
@@ -401,6 +449,42 @@ hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void*
                            ws.perm_src, gate, (const float*)W_down, d.d, d.m, ws.tiles,
                            ws.tile_count, (float*)ws.O);
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_preact(const pr2_moe_desc& d, const void* x, const void* W_gate,
+                         const void* W_up, const ReplayWs& ws, void* AU, hipStream_t s) {
+    if (mfma_shape_ok(d)) {
+        MfmaArgs g{};
+        g.A = (const bf16_t*)x;
+        g.perm_src = ws.perm_src;
+        g.k = d.k;
+        g.Tk = (int)(d.T * d.k);
+        g.W0 = (const bf16_t*)W_gate;
+        g.W1 = (const bf16_t*)W_up;
+        g.K = d.d;
+        g.n_out = 2 * d.m;
+        g.ntn = d.m / 128;
+        g.w_stride = (int64_t)d.m * d.d;
+        g.tiles = ws.tiles;
+        g.tile_count = ws.tile_count;
+        g.out = (bf16_t*)AU;
+        const int64_t work = ws.max_tiles * g.ntn;
+        const int64_t grid = ((work + kNumXcd - 1) / kNumXcd) * kNumXcd;
+        LaunchScope scope("bwd_preact_gate_up", s);
+        hipLaunchKernelGGL(grouped_gemm_mfma<2>, dim3((unsigned)grid), dim3(kGemmThreads), 0, s, g);
+        return hipGetLastError();
+    }
+    dim3 grid((unsigned)ws.max_tiles, (unsigned)d.m);
+    LaunchScope scope("bwd_preact_generic", s);
+    if (d.act_dtype == PR2_BF16)
+        hipLaunchKernelGGL(preact_generic<bf16_t>, grid, dim3(256), 0, s, (const bf16_t*)x,
+                           ws.perm_src, d.k, (const bf16_t*)W_gate, (const bf16_t*)W_up, d.d, d.m,
+                           ws.tiles, ws.tile_count, (bf16_t*)AU);
+    else
+        hipLaunchKernelGGL(preact_generic<float>, grid, dim3(256), 0, s, (const float*)x,
+                           ws.perm_src, d.k, (const float*)W_gate, (const float*)W_up, d.d, d.m,
+                           ws.tiles, ws.tile_count, (float*)AU);
     return hipGetLastError();
 }
 

@@ -70,6 +70,20 @@ def replay(d, x=FAKE, idx=FAKE, ldi=None, W=FAKE, b=None, Wg=FAKE, Wu=FAKE, Wd=F
     return st, L.pr2_last_error().decode()
 
 
+def backward(d, x=FAKE, idx=FAKE, ldi=None, W=FAKE, b=None, Wg=FAKE, Wu=FAKE, Wd=FAKE, dy=FAKE,
+             dx=FAKE, dW=FAKE, db=None, dWg=FAKE, dWu=FAKE, dWd=FAKE, ws=FAKE, ws_bytes=None):
+    L = B.lib()
+    ldi = d.k if ldi is None else ldi
+    if ws_bytes is None:
+        ws_bytes = B.workspace_bytes(d, B.OP_REPLAY_BWD)
+    st = L.pr2_moe_replay_backward(byref(d), c_void_p(x), c_void_p(idx), ldi, c_void_p(W),
+                                   c_void_p(b), c_void_p(Wg), c_void_p(Wu), c_void_p(Wd),
+                                   c_void_p(dy), c_void_p(dx), c_void_p(dW), c_void_p(db),
+                                   c_void_p(dWg), c_void_p(dWu), c_void_p(dWd), c_void_p(ws),
+                                   ws_bytes, None)
+    return st, L.pr2_last_error().decode()
+
+
 @pytest.mark.parametrize("kw,status", [
     (dict(k=0), "PR2_ERR_SHAPE"),
     (dict(k=9), "PR2_ERR_SHAPE"),
@@ -146,6 +160,27 @@ def test_replay_rejects_bad_arguments():
     assert B.workspace_bytes(desc(k=0), B.OP_ROUTE) == 0
 
 
+def test_backward_rejects_bad_arguments():
+    d = desc()
+    need = B.workspace_bytes(d, B.OP_REPLAY_BWD)
+    assert need > B.workspace_bytes(d, B.OP_REPLAY_FWD) > 0
+    assert B.STATUS[backward(d, ws_bytes=need - 1)[0]] == "PR2_ERR_WORKSPACE"
+    assert B.STATUS[backward(d, ws=0)[0]] == "PR2_ERR_NULL"
+    for arg in ("x", "idx", "W", "Wg", "Wu", "Wd", "dy", "dx", "dW", "dWg", "dWu", "dWd"):
+        st, msg = backward(d, **{arg: 0})
+        assert B.STATUS[st] == "PR2_ERR_NULL", (arg, msg)
+    assert B.STATUS[backward(d, dx=FAKE + 8)[0]] == "PR2_ERR_ALIGN"
+    assert B.STATUS[backward(d, dWd=FAKE + 4)[0]] == "PR2_ERR_ALIGN"
+    assert B.STATUS[backward(d, db=FAKE + 2)[0]] == "PR2_ERR_ALIGN"
+    assert B.STATUS[backward(d, ldi=1)[0]] == "PR2_ERR_SHAPE"
+    st, msg = backward(desc(renorm=False))
+    assert B.STATUS[st] == "PR2_ERR_UNSUPPORTED" and "renorm" in msg
+    # T = 0 still has weight gradients to zero: those pointers stay required
+    st, _ = backward(desc(T=0), x=0, idx=0, dy=0, dx=0, ws=0, ws_bytes=0, dWg=0)
+    assert B.STATUS[st] == "PR2_ERR_NULL"
+    assert B.workspace_bytes(desc(k=0), B.OP_REPLAY_BWD) == 0
+
+
 def test_valid_call_without_gpu_reports_device():
     import torch
     if torch.cuda.is_available():
@@ -153,6 +188,10 @@ def test_valid_call_without_gpu_reports_device():
     st, msg = route(desc())
     assert B.STATUS[st] == "PR2_ERR_DEVICE", msg
     st, msg = replay(desc())
+    assert B.STATUS[st] == "PR2_ERR_DEVICE", msg
+    st, msg = backward(desc())
+    assert B.STATUS[st] == "PR2_ERR_DEVICE", msg
+    st, msg = backward(desc(T=0), x=0, idx=0, dy=0, dx=0, ws=0, ws_bytes=0)
     assert B.STATUS[st] == "PR2_ERR_DEVICE", msg
 
 

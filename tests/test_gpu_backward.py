@@ -1,0 +1,183 @@
+"""GPU parity of pr2_moe_replay_backward against the float64 oracle's analytic
+backward (itself pinned to central differences): gradients of <dy, y> for the
+replay forward with recorded ids held fixed and renormalised replay weights
+(Sec. 4.1, replay during training; the predictor is bypassed and gets none).
+
+Recorded routes are the current router's top-k with a fraction of tokens
+changed in one slot, so that the replayed set differs from what the current
+router would pick (the situation replay exists for).
+
+Bar: per-tensor Frobenius ratio ||g - g_ref|| / ||g_ref|| <= 2e-2 with bf16
+activations (bf16 pre-activations, g H and per-route input gradients, fp32
+accumulation), <= 1e-4 with fp32 activations; experts that no route uses get
+exactly zero; two runs are bitwise identical."""
+import numpy as np
+import pytest
+
+from oracle import pr2_oracle as O
+import workloads as W
+from tests.parity import to_dev
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"bf16": 2e-2, "f32": 1e-4}
+GRADS = ("dx", "dW_r", "dbeta", "dW_gate", "dW_up", "dW_down")
+
+
+def recorded_route(L, k, flip_frac, seed):
+    """Current router's top-k, with flip_frac of the tokens given one other expert."""
+    p = O.router_logits(L["x"], L["W_r"], L["beta"])
+    idx = O.topk_ids(p, k).copy()
+    T, N = p.shape
+    n = int(round(flip_frac * T))
+    rng = np.random.default_rng([seed, 77])
+    if n and k < N:
+        for t in rng.choice(T, n, replace=False):
+            s = rng.integers(k)
+            free = np.setdiff1d(np.arange(N), idx[t])
+            idx[t, s] = rng.choice(free)
+    return idx
+
+
+def run_bwd(L, idx, dy, act, idx_dtype="int32", ldi_pad=0, ws=None):
+    import torch
+    from paper_2606_00395_amd import binding as B
+    x = to_dev(L["x"], act)
+    Wr = to_dev(L["W_r"])
+    br = to_dev(L["beta"]) if L["beta"] is not None else None
+    Wg, Wu, Wd = (to_dev(L[n], act) for n in ("W_gate", "W_up", "W_down"))
+    dyd = to_dev(dy, act)
+    T, k = idx.shape
+    dt = torch.int16 if idx_dtype == "int16" else torch.int32
+    buf = torch.full((T, k + ldi_pad), -1, dtype=dt, device="cuda")
+    buf[:, :k] = torch.from_numpy(idx.astype(np.int64)).to(dt).to("cuda")
+    nan = float("nan")
+    dx = torch.full_like(x, nan)
+    dWr = torch.full(Wr.shape, nan, device="cuda")
+    dbr = torch.full((Wr.shape[1],), nan, device="cuda")
+    dWg = torch.full(Wg.shape, nan, device="cuda")
+    dWu = torch.full(Wu.shape, nan, device="cuda")
+    dWd = torch.full(Wd.shape, nan, device="cuda")
+    B.moe_replay_backward(x, buf[:, :k], Wr, br, Wg, Wu, Wd, dyd, dx, dWr, dbr, dWg, dWu, dWd,
+                          ws=ws)
+    torch.cuda.synchronize()
+    out = {"dx": dx.float().cpu().numpy(), "dW_r": dWr.cpu().numpy(), "dbeta": dbr.cpu().numpy(),
+           "dW_gate": dWg.cpu().numpy(), "dW_up": dWu.cpu().numpy(), "dW_down": dWd.cpu().numpy()}
+    if ldi_pad:
+        assert torch.all(buf[:, k:] == -1), "the route buffer was written"
+    return out
+
+
+def frob(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def compare(g, ref, act, where, names=GRADS):
+    errs = {}
+    for n in names:
+        assert np.all(np.isfinite(g[n])), f"{where}: {n} has non-finite entries (not written?)"
+        errs[n] = frob(g[n], ref[n])
+    print(f"\n{where}: " + ", ".join(f"{n} {e:.2e}" for n, e in errs.items()))
+    bad = {n: e for n, e in errs.items() if e > TOL[act]}
+    assert not bad, f"{where}: Frobenius ratios over {TOL[act]}: {bad}"
+
+
+def oracle_bwd(L, idx, dy):
+    return O.replay_backward(L["x"], idx, L["W_r"], L["beta"], L["W_gate"], L["W_up"],
+                             L["W_down"], dy, renorm=True)
+
+
+def test_backward_tiny_fp32():
+    s = W.WORKLOADS["tiny_fp32_T256"]
+    L = W.layer_inputs(s, 0)
+    idx = recorded_route(L, s.k, 0.05, 0)
+    dy = W.upstream_grad(s, 0)
+    g = run_bwd(L, idx, dy, "f32")
+    compare(g, oracle_bwd(L, idx, dy), "f32", s.name)
+
+
+CASES = [
+    # (T, d, N, k, m, act, skew, idx_dtype, ldi_pad)
+    (700, 256, 8, 2, 256, "bf16", "hot8", "int32", 0),
+    (1500, 512, 16, 4, 512, "bf16", "zipf", "int16", 3),
+    (333, 256, 64, 8, 256, "bf16", "none", "int32", 0),     # many experts with few or no rows
+    (100, 256, 4, 4, 256, "bf16", "none", "int32", 0),      # k = N
+    (300, 192, 8, 2, 128, "bf16", "hot8", "int32", 0),      # generic kernels (d, m not / 256)
+    (130, 48, 6, 3, 40, "f32", "none", "int16", 1),         # generic fp32, ragged everything
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"T{c[0]}_d{c[1]}_N{c[2]}_k{c[3]}_m{c[4]}_{c[5]}"
+                                              for c in CASES])
+def test_backward_shapes(case):
+    T, d, N, k, m, act, skew, idt, pad = case
+    s = W.LayerShape("case", T=T, d=d, N=N, k=k, m=m, r=0, act=act, skew=skew)
+    L = W.layer_inputs(s, 11)
+    idx = recorded_route(L, k, 0.05, 11)
+    dy = W.upstream_grad(s, 11)
+    g = run_bwd(L, idx, dy, act, idt, pad)
+    ref = oracle_bwd(L, idx, dy)
+    compare(g, ref, act, str(case))
+    unused = np.setdiff1d(np.arange(N), np.unique(idx))
+    for n in ("dW_gate", "dW_up", "dW_down"):
+        assert np.all(g[n][unused] == 0.0), f"{n} of unused experts {unused} is not zero"
+    assert np.all(g["dW_r"][:, unused] == 0.0) and np.all(g["dbeta"][unused] == 0.0)
+
+
+def test_backward_renormalised_logit_gradient_sums_to_zero():
+    """With renormalised weights each token's logit gradient sums to zero over
+    its route (softmax shift invariance), so db_r sums to zero."""
+    s = W.LayerShape("shift", T=512, d=256, N=16, k=4, m=256, r=0, act="bf16", skew="hot8")
+    L = W.layer_inputs(s, 2)
+    idx = recorded_route(L, s.k, 0.1, 2)
+    g = run_bwd(L, idx, W.upstream_grad(s, 2), "bf16")
+    assert abs(g["dbeta"].sum()) <= 1e-4 * np.abs(g["dbeta"]).sum()
+
+
+def test_backward_empty_batch_zeroes_weight_gradients():
+    import torch
+    from paper_2606_00395_amd import binding as B
+    d, N, m, k = 256, 8, 256, 2
+    x = torch.empty((0, d), dtype=torch.bfloat16, device="cuda")
+    idx = torch.empty((0, k), dtype=torch.int32, device="cuda")
+    Wr = torch.zeros((d, N), device="cuda")
+    Wg = torch.zeros((N, m, d), dtype=torch.bfloat16, device="cuda")
+    Wd = torch.zeros((N, d, m), dtype=torch.bfloat16, device="cuda")
+    grads = [torch.full(sh, float("nan"), device="cuda") for sh in
+             ((d, N), (N,), (N, m, d), (N, m, d), (N, d, m))]
+    B.moe_replay_backward(x, idx, Wr, None, Wg, Wg, Wd, x, torch.empty_like(x), *grads)
+    torch.cuda.synchronize()
+    for t in grads:
+        assert torch.all(t == 0)
+
+
+def test_backward_qwen3_30b_sampled_experts():
+    """The full Qwen3-30B-A3B-shaped backward workload (16384 tokens, 5 % of
+    routes changed).  Each expert's weight gradients, its dW_r column and db_r
+    entry depend only on the routes through it, and dx_t only on token t, so the
+    oracle runs on the tokens of three sampled experts (the most loaded, a
+    median one and the least loaded) and checks those exactly; a second run
+    must be bitwise identical."""
+    s = W.WORKLOADS["qwen3_30b_bwd_T16384"]
+    L = W.layer_inputs(s, 0)
+    idx = recorded_route(L, s.k, s.flip_frac, 0)
+    dy = W.upstream_grad(s, 0)
+    g = run_bwd(L, idx, dy, "bf16")
+    load = np.bincount(idx.ravel(), minlength=s.N)
+    order = np.argsort(load, kind="stable")
+    for e in (order[-1], order[s.N // 2], order[0]):
+        toks = np.nonzero((idx == e).any(axis=1))[0]
+        ref = O.replay_backward(L["x"][toks], idx[toks], L["W_r"], L["beta"], L["W_gate"], L["W_up"],
+                                L["W_down"], dy[toks], renorm=True)
+        got = {"dW_gate": g["dW_gate"][e], "dW_up": g["dW_up"][e], "dW_down": g["dW_down"][e],
+               "dW_r": g["dW_r"][:, e], "dbeta": g["dbeta"][e:e + 1], "dx": g["dx"][toks]}
+        want = {"dW_gate": ref["dW_gate"][e], "dW_up": ref["dW_up"][e],
+                "dW_down": ref["dW_down"][e], "dW_r": ref["dW_r"][:, e],
+                "dbeta": ref["dbeta"][e:e + 1], "dx": ref["dx"]}
+        compare(got, want, "bf16", f"{s.name} expert {e} ({load[e]} routes)")
+        del ref
+    g2 = run_bwd(L, idx, dy, "bf16")
+    for n in GRADS:
+        assert np.array_equal(g[n], g2[n]), f"{n} differs between two runs"
