@@ -19,6 +19,9 @@ the paper's sections, equations and algorithms:
                   predictor bypassed           (Sec. 4.1 replay, Eq. pr2_output)
 * predictive loss KL(<rho> || rho_hat)          (Sec. 4.2, Eq. pr2_loss;
                   Alg. 3 in Appendix D)
+* route metrics   agreement |I_hat ∩ I| / k, deviation k - |I_hat ∩ I|,
+                  route KL                      (Sec. 5.4)
+* feature cache   Tc positions by uniform sub-sampling (Appendix E.2)
 * expert E_j      gated MLP: W_down (silu(W_gate h) * W_up h)
                                                (Appendix E.2, FFN-ratio paragraph)
 
@@ -277,10 +280,70 @@ def predictive_kl(p_cur, h_old, p_old, A, B):
 
 # ------------------------------------------------------ route diagnostics --
 
-def route_agreement(idx_cached, idx_current):
-    """|I_hat ∩ I| / k per token (the agreement metric of Sec. 5.4)."""
+def route_overlap(idx_cached, idx_current):
+    """|I_hat ∩ I| per token: how many recorded ids the current top-k also
+    picks (Sec. 5.4, top-k agreement and routing deviation)."""
     a = np.asarray(idx_cached)
     b = np.asarray(idx_current)
-    k = a.shape[1]
-    inter = np.array([len(set(a[t].tolist()) & set(b[t].tolist())) for t in range(a.shape[0])])
-    return inter / k
+    return np.array([len(set(a[t].tolist()) & set(b[t].tolist())) for t in range(a.shape[0])],
+                    dtype=np.int64)
+
+
+def route_agreement(idx_cached, idx_current):
+    """|I_hat ∩ I| / k per token (the agreement metric of Sec. 5.4)."""
+    k = np.asarray(idx_cached).shape[1]
+    return route_overlap(idx_cached, idx_current) / k
+
+
+def route_deviation_histogram(idx_cached, idx_current):
+    """Counts of the deviation k - |I_hat ∩ I| over tokens, for deviations
+    0..k (the routing deviation distribution of Sec. 5.4)."""
+    k = np.asarray(idx_cached).shape[1]
+    dev = k - route_overlap(idx_cached, idx_current)
+    return np.bincount(dev, minlength=k + 1)
+
+
+def route_kl(p_cur, z_ref):
+    """Per-token KL(Softmax(p_cur) || Softmax(z_ref)): the route KL between the
+    current router's distribution and a reference distribution given by its
+    logits (Sec. 5.4; with z_ref = p_old + h_old W_p it is the summand of
+    Eq. pr2_loss)."""
+    rho = softmax(p_cur)
+    zc = _f64(p_cur) - _f64(p_cur).max(axis=1, keepdims=True)
+    log_rho = zc - np.log(np.exp(zc).sum(axis=1, keepdims=True))
+    zr = _f64(z_ref) - _f64(z_ref).max(axis=1, keepdims=True)
+    log_ref = zr - np.log(np.exp(zr).sum(axis=1, keepdims=True))
+    return (rho * (log_rho - log_ref)).sum(axis=1)
+
+
+# -------------------------------------------------------- feature cache ----
+
+_GOLDEN = 0x9E3779B97F4A7C15
+_M64 = (1 << 64) - 1
+
+
+def splitmix64(state):
+    """The SplitMix64 output function of Steele, Lea and Flood (OOPSLA 2014)
+    applied to a 64-bit state: the counter-based generator both sides use to
+    draw feature-cache positions."""
+    z = state & _M64
+    z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & _M64
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & _M64
+    return z ^ (z >> 31)
+
+
+def feature_cache_positions(T, Tc, seed):
+    """Positions retained by a feature cache of length Tc over a rollout of T
+    tokens, drawn by uniform sub-sampling along the rollout (Appendix E.2,
+    feature-cache paragraph): the rollout is cut into Tc strata of (nearly)
+    equal length and one position is drawn uniformly inside stratum i with
+    the i-th SplitMix64 output for the seed.  Tc >= T keeps every position."""
+    if Tc >= T:
+        return np.arange(T, dtype=np.int64)
+    pos = np.empty(Tc, dtype=np.int64)
+    for i in range(Tc):
+        lo = (i * T) // Tc
+        hi = ((i + 1) * T) // Tc
+        r = splitmix64(seed + (i + 1) * _GOLDEN)
+        pos[i] = lo + r % (hi - lo)
+    return pos

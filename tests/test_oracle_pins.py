@@ -429,6 +429,96 @@ def test_workload_generators_are_deterministic_and_row_addressable():
     assert len(fl) == 819 and len(np.unique(fl)) == 819
 
 
+# ------------------------------------------------ route metrics (Sec. 5.4) ---
+
+def test_route_overlap_agreement_and_deviation_brute_force():
+    rng = np.random.default_rng(31)
+    T, N, k = 200, 9, 3
+    a = np.sort(np.array([rng.choice(N, k, replace=False) for _ in range(T)]), axis=1)
+    b = np.sort(np.array([rng.choice(N, k, replace=False) for _ in range(T)]), axis=1)
+    inter = np.array([sum(int(x == y) for x in a[t] for y in b[t]) for t in range(T)])
+    np.testing.assert_array_equal(O.route_overlap(a, b), inter)
+    np.testing.assert_allclose(O.route_agreement(a, b), inter / k)
+    hist = O.route_deviation_histogram(a, b)
+    assert hist.shape == (k + 1,) and hist.sum() == T
+    np.testing.assert_array_equal(hist, [(k - inter == dv).sum() for dv in range(k + 1)])
+    # identical routes: all mass at zero deviation; disjoint: all at k
+    np.testing.assert_array_equal(O.route_deviation_histogram(a, a), [T] + [0] * k)
+    c = np.tile(np.arange(k), (T, 1))
+    dd = np.tile(np.arange(k, 2 * k), (T, 1))
+    np.testing.assert_array_equal(O.route_deviation_histogram(c, dd), [0] * k + [T])
+    # order of ids within a row does not matter
+    np.testing.assert_array_equal(O.route_overlap(a[:, ::-1], b), inter)
+
+
+def test_route_kl_closed_forms():
+    rng = np.random.default_rng(32)
+    p = rand(rng, 50, 7)
+    np.testing.assert_allclose(O.route_kl(p, p), 0.0, atol=1e-13)
+    z = rand(rng, 50, 7)
+    kl = O.route_kl(p, z)
+    assert np.all(kl > 0)
+    # invariant to a per-token shift of either logit vector
+    np.testing.assert_allclose(O.route_kl(p + 3.0, z - 1.5), kl, rtol=1e-10)
+    # two experts: the binary KL of the two sigmoids
+    a, b = rand(rng, 40), rand(rng, 40)
+    s, t = scipy.special.expit(a), scipy.special.expit(b)
+    bern = s * np.log(s / t) + (1 - s) * np.log((1 - s) / (1 - t))
+    np.testing.assert_allclose(O.route_kl(np.stack([a, 0 * a], 1), np.stack([b, 0 * b], 1)), bern,
+                               rtol=1e-10)
+    # scipy's relative entropy of the two softmax vectors
+    ref = scipy.special.rel_entr(scipy.special.softmax(p, axis=1),
+                                 scipy.special.softmax(z, axis=1)).sum(axis=1)
+    np.testing.assert_allclose(kl, ref, rtol=1e-10)
+
+
+def test_route_kl_small_enough_keeps_the_top_k():
+    """Lemma B.2: KL(p || p_hat) < margin^2 / 2 implies TopK(p_hat) = TopK(p),
+    with p, p_hat the two distributions and the margin taken on p."""
+    rng = np.random.default_rng(33)
+    N, k = 12, 4
+    hits = 0
+    for _ in range(400):
+        p = rand(rng, 1, N) * 2.0
+        z = p + rand(rng, 1, N) * 0.02
+        rho = O.softmax(p)[0]
+        srt = np.sort(rho)[::-1]
+        margin = srt[k - 1] - srt[k]
+        if O.route_kl(p, z)[0] < margin ** 2 / 2:
+            hits += 1
+            assert set(O.topk_ids(p, k)[0]) == set(O.topk_ids(z, k)[0])
+    assert hits > 20
+
+
+# ------------------------------------------------ feature cache (App. E.2) ---
+
+def test_splitmix64_published_sequence():
+    """The first outputs of SplitMix64 seeded with 0, as published with the
+    generator's reference implementation."""
+    outs = [O.splitmix64((i + 1) * 0x9E3779B97F4A7C15) for i in range(3)]
+    assert outs == [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F]
+
+
+def test_feature_cache_positions_stratified_uniform():
+    T, Tc = 16384, 2048
+    pos = O.feature_cache_positions(T, Tc, 7)
+    assert pos.shape == (Tc,) and np.all(np.diff(pos) > 0) and pos[0] >= 0 and pos[-1] < T
+    # exactly one retained position per stratum of T / Tc tokens
+    np.testing.assert_array_equal(pos // (T // Tc), np.arange(Tc))
+    np.testing.assert_array_equal(pos, O.feature_cache_positions(T, Tc, 7))
+    assert not np.array_equal(pos, O.feature_cache_positions(T, Tc, 8))
+    # uneven strata still cover [0, T) with one draw each
+    pos2 = O.feature_cache_positions(1000, 7, 1)
+    bounds = [(i * 1000) // 7 for i in range(8)]
+    assert all(bounds[i] <= pos2[i] < bounds[i + 1] for i in range(7))
+    # offsets within a stratum are uniform: chi-square over many seeds
+    off = np.concatenate([O.feature_cache_positions(800, 100, sd) % 8 for sd in range(60)])
+    counts = np.bincount(off, minlength=8)
+    chi2 = ((counts - off.size / 8) ** 2 / (off.size / 8)).sum()
+    assert chi2 < 24.3   # 7 degrees of freedom, p = 0.001
+    np.testing.assert_array_equal(O.feature_cache_positions(50, 64, 3), np.arange(50))
+
+
 # ------------------------------------------------- planted mistakes ----------
 
 def test_pins_catch_planted_mistakes(monkeypatch):
@@ -484,3 +574,14 @@ def test_pins_catch_planted_mistakes(monkeypatch):
     monkeypatch.setattr(O, "replay_backward", bad_backward)
     assert fails(lambda: test_backward_matches_central_differences(True))
     monkeypatch.setattr(O, "replay_backward", bad.replay_backward)
+
+    # route KL taken in the reverse direction
+    monkeypatch.setattr(O, "route_kl", lambda p, z: bad.route_kl(z, p))
+    assert fails(test_route_kl_closed_forms)
+    monkeypatch.setattr(O, "route_kl", bad.route_kl)
+
+    # stratum draw off by one (position may land in the next stratum)
+    monkeypatch.setattr(O, "feature_cache_positions", lambda T, Tc, seed: np.minimum(
+        bad.feature_cache_positions(T, Tc, seed) + 1, T - 1))
+    assert fails(test_feature_cache_positions_stratified_uniform)
+    monkeypatch.setattr(O, "feature_cache_positions", bad.feature_cache_positions)
