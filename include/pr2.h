@@ -64,7 +64,13 @@ enum { PR2_F32 = 0, PR2_BF16 = 1 };
 /* idx_dtype: storage type of recorded expert ids. */
 enum { PR2_I32 = 0, PR2_I16 = 1 };
 /* op codes for pr2_workspace_bytes. */
-enum { PR2_OP_ROUTE = 0, PR2_OP_REPLAY_FWD = 1, PR2_OP_REPLAY_BWD = 2, PR2_OP_ROLLOUT_FWD = 3 };
+enum {
+    PR2_OP_ROUTE = 0,
+    PR2_OP_REPLAY_FWD = 1,
+    PR2_OP_REPLAY_BWD = 2,
+    PR2_OP_ROLLOUT_FWD = 3,
+    PR2_OP_ROUTE_DIAG = 4
+};
 
 /*
  * Layer descriptor.
@@ -143,6 +149,25 @@ pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const
                                   pr2_stream_t stream);
 
 /*
+ * Rollout-phase layer forward (Sec. 4.1 "Route Prediction During Rollout"; Eq. pr2_old_output;
+ * Alg. 2 in Appendix D): route prediction exactly as pr2_route_predict, then the layer output
+ * under the predictive weights,
+ *
+ *   o_old,t = sum_s rho_hat_{t,s} E_{idx[t,s]}(x_t)
+ *
+ * with rho_hat renormalised over the k predicted ids (renorm = 1) or the softmax of the
+ * predictive logits over all N (renorm = 0, the printed equation).  Arguments as for
+ * pr2_route_predict and pr2_moe_replay_forward; idx_out and gate_out receive the recorded
+ * route and its predictive weights (gate_out may be NULL).
+ *   ws       >= pr2_workspace_bytes(desc, PR2_OP_ROLLOUT_FWD)
+ */
+pr2_status pr2_moe_rollout_forward(const pr2_moe_desc* desc, const void* x, const float* W_r,
+                                   const float* b_r, const float* A, const float* B,
+                                   const void* W_gate, const void* W_up, const void* W_down,
+                                   void* idx_out, int64_t ldi, float* gate_out, float* logits_out,
+                                   void* y, void* ws, size_t ws_bytes, pr2_stream_t stream);
+
+/*
  * Replay backward (Sec. 4.1 "Replay During Training": the current experts and router are
  * trained through the replayed routes; Alg. 3 in Appendix D, its backward step).  Gradients
  * of L = sum_t <dy_t, y_t> for the replay forward above, with the recorded ids held fixed and
@@ -174,6 +199,31 @@ pr2_status pr2_moe_replay_backward(const pr2_moe_desc* desc, const void* x, cons
                                    const void* dy, void* dx, float* dW_r, float* db_r,
                                    float* dW_gate, float* dW_up, float* dW_down, void* ws,
                                    size_t ws_bytes, pr2_stream_t stream);
+
+/*
+ * Route-tracking diagnostics (Sec. 5.4: top-k agreement, routing deviation and route KL) of a
+ * recorded route against the current router, the predictor bypassed as in replay:
+ *
+ *   p = x W_r + b_r,  I = TopK(p, k)   (ties to the lower id, decided on the fp32 logits)
+ *   overlap_t = |idx_t ∩ I_t|           (agreement = overlap / k, deviation = k - overlap)
+ *   kl_t = KL(softmax(p_t) || softmax(z_ref_t))
+ *   hist[v] = number of tokens whose deviation is v, v = 0..k
+ *
+ *   x, idx, ldi, W_r, b_r   as for pr2_moe_replay_forward (desc.m, desc.r, desc.renorm unused)
+ *   z_ref        [T, N] fp32 reference logits, e.g. the rollout-time predictive logits; may be
+ *                NULL when kl_out is NULL
+ *   cur_idx_out  [T, k] idx_dtype, the current top-k ascending, or NULL
+ *   overlap_out  [T] int32 or NULL;  kl_out [T] fp32 or NULL
+ *   hist_out     [k + 1] uint64 (8-byte aligned), overwritten with exact counts, or NULL
+ *   ws           >= pr2_workspace_bytes(desc, PR2_OP_ROUTE_DIAG)
+ * The logits are the replay router's (exact bf16 x times fp32 W_r, one rounding to fp32); the
+ * route KL is evaluated in fp64 from them.  T = 0 only zeroes hist_out.
+ */
+pr2_status pr2_route_diagnostics(const pr2_moe_desc* desc, const void* x, const void* idx,
+                                 int64_t ldi, const float* W_r, const float* b_r,
+                                 const float* z_ref, void* cur_idx_out, int32_t* overlap_out,
+                                 float* kl_out, uint64_t* hist_out, void* ws, size_t ws_bytes,
+                                 pr2_stream_t stream);
 
 /* Status name ("PR2_OK", ...); never NULL. */
 const char* pr2_status_string(pr2_status s);

@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(HERE, "libpr2.so")
 
 PR2_F32, PR2_BF16 = 0, 1
 PR2_I32, PR2_I16 = 0, 1
-OP_ROUTE, OP_REPLAY_FWD, OP_REPLAY_BWD, OP_ROLLOUT_FWD = 0, 1, 2, 3
+OP_ROUTE, OP_REPLAY_FWD, OP_REPLAY_BWD, OP_ROLLOUT_FWD, OP_ROUTE_DIAG = 0, 1, 2, 3, 4
 
 STATUS = ["PR2_OK", "PR2_ERR_NULL", "PR2_ERR_SHAPE", "PR2_ERR_DTYPE", "PR2_ERR_ALIGN",
           "PR2_ERR_WORKSPACE", "PR2_ERR_UNSUPPORTED", "PR2_ERR_ROUTE", "PR2_ERR_DEVICE",
@@ -24,7 +24,9 @@ STATUS = ["PR2_OK", "PR2_ERR_NULL", "PR2_ERR_SHAPE", "PR2_ERR_DTYPE", "PR2_ERR_A
 
 # every symbol include/pr2.h declares
 EXPORTS = ["pr2_workspace_bytes", "pr2_route_predict", "pr2_moe_replay_forward",
-           "pr2_moe_replay_backward", "pr2_status_string", "pr2_last_error", "pr2_version", "pr2_profile_enable",
+           "pr2_moe_replay_backward", "pr2_moe_rollout_forward", "pr2_route_diagnostics",
+           "pr2_status_string",
+           "pr2_last_error", "pr2_version", "pr2_profile_enable",
            "pr2_profile_reset", "pr2_profile_collect"]
 
 
@@ -65,6 +67,12 @@ def lib() -> ctypes.CDLL:
     L.pr2_moe_replay_backward.argtypes = [POINTER(MoeDesc), P, P, c_int64, P, P, P, P, P, P, P,
                                           P, P, P, P, P, P, c_size_t, P]
     L.pr2_moe_replay_backward.restype = c_int
+    L.pr2_moe_rollout_forward.argtypes = [POINTER(MoeDesc), P, P, P, P, P, P, P, P, P, c_int64, P,
+                                          P, P, P, c_size_t, P]
+    L.pr2_moe_rollout_forward.restype = c_int
+    L.pr2_route_diagnostics.argtypes = [POINTER(MoeDesc), P, P, c_int64, P, P, P, P, P, P, P, P,
+                                        c_size_t, P]
+    L.pr2_route_diagnostics.restype = c_int
     L.pr2_status_string.argtypes = [c_int]
     L.pr2_status_string.restype = c_char_p
     L.pr2_last_error.argtypes = []
@@ -183,6 +191,50 @@ def moe_replay_forward(x, idx, W_r, b_r, W_gate, W_up, W_down, y, gate_out=None,
                                        _ptr(W_r), _ptr(b_r), _ptr(W_gate), _ptr(W_up),
                                        _ptr(W_down), _ptr(y), _ptr(gate_out), _ptr(ws),
                                        ws.numel(), _stream(stream)))
+
+
+def rollout_workspace(x, W_r, A, W_gate, k, idx_dtype_code=PR2_I32, renorm=True):
+    torch = _torch()
+    T, d = x.shape
+    r = 0 if A is None else A.shape[1]
+    desc = make_desc(T, d, W_r.shape[1], k, W_gate.shape[1], r, _act_code(x), idx_dtype_code,
+                     renorm)
+    return torch.empty(max(1, workspace_bytes(desc, OP_ROLLOUT_FWD)), dtype=torch.uint8,
+                       device=x.device)
+
+
+def moe_rollout_forward(x, W_r, b_r, A, B, W_gate, W_up, W_down, k, idx_out, y, gate_out=None,
+                        logits_out=None, renorm=True, ws=None, stream=None):
+    """pr2_moe_rollout_forward on torch tensors: records the predicted route into ``idx_out``
+    (a [T, k] view, any row stride) and writes the layer output under the predictive weights."""
+    T, d = x.shape
+    N = W_r.shape[1]
+    r = 0 if A is None else A.shape[1]
+    m = W_gate.shape[1]
+    desc = make_desc(T, d, N, k, m, r, _act_code(x), _idx_code(idx_out), renorm)
+    if ws is None:
+        ws = rollout_workspace(x, W_r, A, W_gate, k, _idx_code(idx_out), renorm)
+    check(lib().pr2_moe_rollout_forward(byref(desc), _ptr(x), _ptr(W_r), _ptr(b_r), _ptr(A),
+                                        _ptr(B), _ptr(W_gate), _ptr(W_up), _ptr(W_down),
+                                        _ptr(idx_out), _row_stride(idx_out), _ptr(gate_out),
+                                        _ptr(logits_out), _ptr(y), _ptr(ws), ws.numel(),
+                                        _stream(stream)))
+
+
+def route_diagnostics(x, idx, W_r, b_r, z_ref=None, cur_idx_out=None, overlap_out=None,
+                      kl_out=None, hist_out=None, ws=None, stream=None):
+    """pr2_route_diagnostics on torch tensors; ``hist_out`` is an int64/uint64 tensor of k+1."""
+    torch = _torch()
+    T, d = x.shape
+    k = idx.shape[1]
+    desc = make_desc(T, d, W_r.shape[1], k, 0, 0, _act_code(x), _idx_code(idx))
+    if ws is None:
+        ws = torch.empty(max(1, workspace_bytes(desc, OP_ROUTE_DIAG)), dtype=torch.uint8,
+                         device=x.device)
+    check(lib().pr2_route_diagnostics(byref(desc), _ptr(x), _ptr(idx), _row_stride(idx),
+                                      _ptr(W_r), _ptr(b_r), _ptr(z_ref), _ptr(cur_idx_out),
+                                      _ptr(overlap_out), _ptr(kl_out), _ptr(hist_out), _ptr(ws),
+                                      ws.numel(), _stream(stream)))
 
 
 def backward_workspace(x, idx, W_r, W_gate, renorm=True):

@@ -95,7 +95,19 @@ static pr2_status check_desc(const pr2_moe_desc* d, bool need_m, bool need_idx_d
 // ----------------------------------------------------------- workspace ----
 static size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-ReplayWs replay_ws_layout(const pr2_moe_desc& d, void* base) {
+// Split scratch of the route call: the predictor folded into the router weights (N columns)
+// when no logits are wanted, [W_r | A] (N + r columns) otherwise.
+static size_t route_split_need(const pr2_moe_desc& d) {
+    size_t need = 0;
+    if (router_mfma_ok(d, d.N)) need = router_split_bytes(d.N, d.d);
+    if (router_mfma_ok(d, d.N + d.r)) {
+        size_t b = router_split_bytes(d.N + d.r, d.d);
+        need = b > need ? b : need;
+    }
+    return need;
+}
+
+static ReplayWs moe_ws_layout(const pr2_moe_desc& d, void* base, size_t split_bytes) {
     ReplayWs w{};
     const int64_t Tk = d.T * (int64_t)d.k;
     const int tb = perm_tokens_per_block(d.k);
@@ -119,9 +131,17 @@ ReplayWs replay_ws_layout(const pr2_moe_desc& d, void* base) {
     w.inv = (int*)take(sizeof(int) * Tk);
     w.H = take(ab * Tk * (size_t)d.m);
     w.O = take(ab * Tk * (size_t)d.d);
-    w.wsplit = take(router_mfma_ok(d, d.N) ? router_split_bytes(d.N, d.d) : 0);
+    w.wsplit = take(split_bytes);
     w.bytes = off + 256;   // slack for aligning the caller's base
     return w;
+}
+
+ReplayWs replay_ws_layout(const pr2_moe_desc& d, void* base) {
+    return moe_ws_layout(d, base, router_mfma_ok(d, d.N) ? router_split_bytes(d.N, d.d) : 0);
+}
+
+static ReplayWs rollout_ws_layout(const pr2_moe_desc& d, void* base) {
+    return moe_ws_layout(d, base, route_split_need(d));
 }
 
 BwdWs bwd_ws_layout(const pr2_moe_desc& d, void* base) {
@@ -145,15 +165,12 @@ BwdWs bwd_ws_layout(const pr2_moe_desc& d, void* base) {
     return b;
 }
 
-// The route call folds the predictor into the router weights (N columns) when the
-// caller wants no logits, and projects [W_r | A] (N + r columns) otherwise.
+static size_t diag_ws_bytes(const pr2_moe_desc& d) {
+    return router_mfma_ok(d, d.N) ? router_split_bytes(d.N, d.d) + 256 : 0;
+}
+
 static size_t route_ws_bytes(const pr2_moe_desc& d) {
-    size_t need = 0;
-    if (router_mfma_ok(d, d.N)) need = router_split_bytes(d.N, d.d);
-    if (router_mfma_ok(d, d.N + d.r)) {
-        size_t b = router_split_bytes(d.N + d.r, d.d);
-        need = b > need ? b : need;
-    }
+    const size_t need = route_split_need(d);
     return need ? need + 256 : 0;
 }
 
@@ -231,6 +248,20 @@ size_t pr2_workspace_bytes(const pr2_moe_desc* desc, int op) {
             t_err = saved;
             if (s != PR2_OK) return 0;
             return replay_ws_layout(*desc, nullptr).bytes;
+        }
+        case PR2_OP_ROLLOUT_FWD: {
+            std::string saved = t_err;
+            pr2_status s = check_desc(desc, true, true);
+            t_err = saved;
+            if (s != PR2_OK || desc->r < 0) return 0;
+            return rollout_ws_layout(*desc, nullptr).bytes;
+        }
+        case PR2_OP_ROUTE_DIAG: {
+            std::string saved = t_err;
+            pr2_status s = check_desc(desc, false, true);
+            t_err = saved;
+            if (s != PR2_OK) return 0;
+            return diag_ws_bytes(*desc);
         }
         case PR2_OP_REPLAY_BWD: {
             std::string saved = t_err;
@@ -339,6 +370,56 @@ pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const
     return ok();
 }
 
+pr2_status pr2_moe_rollout_forward(const pr2_moe_desc* desc, const void* x, const float* W_r,
+                                   const float* b_r, const float* A, const float* B,
+                                   const void* W_gate, const void* W_up, const void* W_down,
+                                   void* idx_out, int64_t ldi, float* gate_out, float* logits_out,
+                                   void* y, void* ws, size_t ws_bytes, pr2_stream_t stream) {
+    pr2_status s = check_desc(desc, true, true);
+    if (s != PR2_OK) return s;
+    const pr2_moe_desc& d = *desc;
+    if (d.r > 256) return fail(PR2_ERR_UNSUPPORTED, "predictor rank r = %d > 256", d.r);
+    if (ldi < d.k) return fail(PR2_ERR_SHAPE, "ldi = %lld < k = %d", (long long)ldi, d.k);
+    if (d.T == 0) return ok();
+    if (!x) return fail(PR2_ERR_NULL, "x is NULL");
+    if (!W_r) return fail(PR2_ERR_NULL, "W_r is NULL");
+    if (!idx_out) return fail(PR2_ERR_NULL, "idx_out is NULL");
+    if (d.r > 0 && !A) return fail(PR2_ERR_NULL, "A is NULL with r = %d > 0", d.r);
+    if (d.r > 0 && !B && d.r != d.N)
+        return fail(PR2_ERR_NULL, "B is NULL but r = %d != N = %d (identity needs r == N)", d.r, d.N);
+    if (!W_gate || !W_up || !W_down) return fail(PR2_ERR_NULL, "an expert weight pointer is NULL");
+    if (!y) return fail(PR2_ERR_NULL, "y is NULL");
+    if (!aligned(x, 16) || !aligned(y, 16) || !aligned(W_gate, 16) || !aligned(W_up, 16) ||
+        !aligned(W_down, 16))
+        return fail(PR2_ERR_ALIGN, "x, y and the expert weights must be 16-byte aligned");
+    if (!aligned(W_r, 4) || (b_r && !aligned(b_r, 4)) || (A && !aligned(A, 4)) ||
+        (B && !aligned(B, 4)) || (gate_out && !aligned(gate_out, 4)) ||
+        (logits_out && !aligned(logits_out, 4)))
+        return fail(PR2_ERR_ALIGN, "an fp32 router/predictor/gate/logit tensor is not 4-byte aligned");
+    if (!aligned(idx_out, d.idx_dtype == PR2_I16 ? 2 : 4))
+        return fail(PR2_ERR_ALIGN, "idx_out is not aligned to its element size");
+    const size_t need = rollout_ws_layout(d, nullptr).bytes;
+    if (!ws) return fail(PR2_ERR_NULL, "ws is NULL (need %zu bytes)", need);
+    if (ws_bytes < need)
+        return fail(PR2_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
+    s = device_ready();
+    if (s != PR2_OK) return s;
+
+    hipStream_t st = (hipStream_t)stream;
+    ReplayWs w = rollout_ws_layout(d, ws);
+    float* gate = gate_out ? gate_out : w.gate;
+    hipError_t e = launch_route_predict(d, x, W_r, b_r, A, B, idx_out, ldi, gate, logits_out,
+                                        w.wsplit, st);
+    if (e != hipSuccess) return hip_fail(e, "route_predict launch");
+    e = launch_permute(d, idx_out, ldi, w, st);
+    if (e != hipSuccess) return hip_fail(e, "permute launch");
+    e = launch_expert_gemms(d, x, W_gate, W_up, W_down, gate, w, st);
+    if (e != hipSuccess) return hip_fail(e, "expert GEMM launch");
+    e = launch_combine(d, w, y, st);
+    if (e != hipSuccess) return hip_fail(e, "combine launch");
+    return ok();
+}
+
 pr2_status pr2_moe_replay_backward(const pr2_moe_desc* desc, const void* x, const void* idx,
                                    int64_t ldi, const float* W_r, const float* b_r,
                                    const void* W_gate, const void* W_up, const void* W_down,
@@ -408,6 +489,44 @@ pr2_status pr2_moe_replay_backward(const pr2_moe_desc* desc, const void* x, cons
             return fail(PR2_ERR_ROUTE, "route has %d out-of-range and %d repeated ids",
                         errs[ERR_BAD_ID], errs[ERR_DUP_ID]);
     }
+    return ok();
+}
+
+pr2_status pr2_route_diagnostics(const pr2_moe_desc* desc, const void* x, const void* idx,
+                                 int64_t ldi, const float* W_r, const float* b_r,
+                                 const float* z_ref, void* cur_idx_out, int32_t* overlap_out,
+                                 float* kl_out, uint64_t* hist_out, void* ws, size_t ws_bytes,
+                                 pr2_stream_t stream) {
+    pr2_status s = check_desc(desc, false, true);
+    if (s != PR2_OK) return s;
+    const pr2_moe_desc& d = *desc;
+    if (ldi < d.k) return fail(PR2_ERR_SHAPE, "ldi = %lld < k = %d", (long long)ldi, d.k);
+    if (kl_out && !z_ref) return fail(PR2_ERR_NULL, "kl_out needs z_ref");
+    if (hist_out && !aligned(hist_out, 8)) return fail(PR2_ERR_ALIGN, "hist_out is not 8-byte aligned");
+    if (d.T == 0 && !hist_out) return ok();
+    if (d.T > 0) {
+        if (!x) return fail(PR2_ERR_NULL, "x is NULL");
+        if (!idx) return fail(PR2_ERR_NULL, "idx is NULL");
+        if (!W_r) return fail(PR2_ERR_NULL, "W_r is NULL");
+        if (!aligned(x, 16)) return fail(PR2_ERR_ALIGN, "x is not 16-byte aligned");
+        if (!aligned(W_r, 4) || (b_r && !aligned(b_r, 4)) || (z_ref && !aligned(z_ref, 4)) ||
+            (kl_out && !aligned(kl_out, 4)) || (overlap_out && !aligned(overlap_out, 4)))
+            return fail(PR2_ERR_ALIGN, "an fp32 / int32 tensor is not 4-byte aligned");
+        const size_t ib = d.idx_dtype == PR2_I16 ? 2 : 4;
+        if (!aligned(idx, ib) || (cur_idx_out && !aligned(cur_idx_out, ib)))
+            return fail(PR2_ERR_ALIGN, "an id buffer is not aligned to its element size");
+        const size_t need = diag_ws_bytes(d);
+        if (need && !ws) return fail(PR2_ERR_NULL, "ws is NULL (need %zu bytes)", need);
+        if (ws_bytes < need)
+            return fail(PR2_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
+    }
+    s = device_ready();
+    if (s != PR2_OK) return s;
+    void* split = ws ? (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255) : nullptr;
+    hipError_t e = launch_route_diagnostics(d, x, idx, ldi, W_r, b_r, z_ref, cur_idx_out,
+                                            overlap_out, kl_out, (unsigned long long*)hist_out,
+                                            split, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "route diagnostics launch");
     return ok();
 }
 

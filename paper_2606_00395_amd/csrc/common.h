@@ -113,6 +113,11 @@ hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void*
                                const float* W_r, const float* b_r, float* gate_out, int* err,
                                void* split_ws, hipStream_t s);
 
+hipError_t launch_route_diagnostics(const pr2_moe_desc& d, const void* x, const void* idx,
+                                    int64_t ldi, const float* W_r, const float* b_r,
+                                    const float* z_ref, void* cur_idx, int* overlap, float* kl,
+                                    unsigned long long* hist, void* split_ws, hipStream_t s);
+
 // permute.hip
 hipError_t launch_permute(const pr2_moe_desc& d, const void* idx, int64_t ldi, const ReplayWs& ws,
                           hipStream_t s);

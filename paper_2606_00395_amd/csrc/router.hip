@@ -138,6 +138,55 @@ struct PredictOut {
     float* logits_out;    // [T, N] or null (only when not folded)
 };
 
+// k rounds of a wavefront arg-max over orderable keys (lane l holds ids
+// v*64 + l in key[v]); among equal keys the lower id wins.  Returns the
+// selection as a per-lane bit mask over v and the largest logit in zmax.
+__device__ uint32_t select_topk(const uint32_t* key, int nv, int N, int k, float& zmax) {
+    const int lane = threadIdx.x & 63;
+    uint32_t taken = 0;
+    zmax = 0.0f;
+    for (int it = 0; it < k; ++it) {
+        uint32_t best = 0;
+        for (int v = 0; v < nv; ++v)
+            if (!((taken >> v) & 1u) && key[v] > best) best = key[v];
+        const uint32_t wmax = wave_max_u32(best);
+        int jw = 0;
+        for (int v = 0; v < nv; ++v) {
+            const int j = v * 64 + lane;
+            uint64_t m = __ballot(j < N && !((taken >> v) & 1u) && key[v] == wmax);
+            if (m) {
+                jw = v * 64 + (__ffsll((unsigned long long)m) - 1);
+                break;
+            }
+        }
+        if (it == 0) zmax = from_orderable(wmax);
+        if ((jw & 63) == lane) taken |= 1u << (jw >> 6);
+    }
+    return taken;
+}
+
+// Writes the selected ids ascending from idx + pos0 (and, when gate is not
+// null, e[v] / denom aligned with them).
+__device__ void write_route(uint32_t taken, int nv, void* idx, int idx_dtype, int64_t pos0,
+                            float* gate, const float* e, float denom) {
+    const int lane = threadIdx.x & 63;
+    int before = 0;
+    for (int v = 0; v < nv; ++v) {
+        bool mine = (taken >> v) & 1u;
+        uint64_t bal = __ballot(mine);
+        if (mine) {
+            uint64_t lt = lane ? (bal & ((~0ull) >> (64 - lane))) : 0ull;
+            int rank = before + __popcll(lt);
+            int j = v * 64 + lane;
+            int64_t pos = pos0 + rank;
+            if (idx_dtype == PR2_I16) ((int16_t*)idx)[pos] = (int16_t)j;
+            else ((int32_t*)idx)[pos] = j;
+            if (gate) gate[rank] = e[v] / denom;
+        }
+        before += __popcll(bal);
+    }
+}
+
 // One wavefront: rollout epilogue of token t from its LDS row of logits.
 __device__ void predict_token(const float* row, int64_t t, int N, int r, const PredictOut& o) {
     const int lane = threadIdx.x & 63;
@@ -165,26 +214,8 @@ __device__ void predict_token(const float* row, int64_t t, int N, int r, const P
             key[v] = orderable(z[v]);
         }
     }
-    // k rounds of a wavefront arg-max; among equal logits the lower id wins
-    uint32_t taken = 0;
-    float zmax = 0.0f;
-    for (int it = 0; it < o.k; ++it) {
-        uint32_t best = 0;
-        for (int v = 0; v < nv; ++v)
-            if (!((taken >> v) & 1u) && key[v] > best) best = key[v];
-        const uint32_t wmax = wave_max_u32(best);
-        int jw = 0;
-        for (int v = 0; v < nv; ++v) {
-            const int j = v * 64 + lane;
-            uint64_t m = __ballot(j < N && !((taken >> v) & 1u) && key[v] == wmax);
-            if (m) {
-                jw = v * 64 + (__ffsll((unsigned long long)m) - 1);
-                break;
-            }
-        }
-        if (it == 0) zmax = from_orderable(wmax);
-        if ((jw & 63) == lane) taken |= 1u << (jw >> 6);
-    }
+    float zmax;
+    const uint32_t taken = select_topk(key, nv, N, o.k, zmax);
     float e[kMaxLanesVals];
     float s_sel = 0.0f, s_all = 0.0f;
     for (int v = 0; v < nv; ++v) {
@@ -197,23 +228,18 @@ __device__ void predict_token(const float* row, int64_t t, int N, int r, const P
         }
     }
     const float denom = o.renorm ? wave_sum_f32(s_sel) : wave_sum_f32(s_all);
-    // ids ascending, gates aligned
-    int before = 0;
-    for (int v = 0; v < nv; ++v) {
-        bool mine = (taken >> v) & 1u;
-        uint64_t bal = __ballot(mine);
-        if (mine) {
-            uint64_t lt = lane ? (bal & ((~0ull) >> (64 - lane))) : 0ull;
-            int rank = before + __popcll(lt);
-            int j = v * 64 + lane;
-            int64_t pos = t * o.ldi + rank;
-            if (o.idx_dtype == PR2_I16) ((int16_t*)o.idx_out)[pos] = (int16_t)j;
-            else ((int32_t*)o.idx_out)[pos] = j;
-            if (o.gate_out) o.gate_out[t * o.k + rank] = e[v] / denom;
-        }
-        before += __popcll(bal);
-    }
+    write_route(taken, nv, o.idx_out, o.idx_dtype, t * o.ldi, o.gate_out ? o.gate_out + t * o.k : nullptr,
+                e, denom);
 }
+
+// Route-tracking diagnostics of the recorded route against the current router.
+struct DiagOut {
+    const float* z_ref;            // [T, N] reference logits (for the route KL) or null
+    void* cur_idx;                 // [T, k] current top-k, ascending, idx dtype, or null
+    int* overlap;                  // [T] |recorded ∩ current top-k| or null
+    float* kl;                     // [T] KL(softmax(p) || softmax(z_ref)) or null
+    unsigned long long* hist;      // [k + 1] tokens per deviation k - overlap, or null
+};
 
 struct ReplayOut {
     const float* b_r;
@@ -221,14 +247,91 @@ struct ReplayOut {
     const void* idx;
     int idx_dtype;
     int64_t ldi;
-    float* gate_out;      // [T, k]
+    float* gate_out;      // [T, k] or null (diagnostics only)
     int* err;
     int validate;
+    DiagOut diag;
 };
+
+__device__ __forceinline__ double wave_sum_f64(double v) {
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+__device__ __forceinline__ double wave_max_f64(double v) {
+    for (int off = 32; off >= 1; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+// One wavefront: the current top-k of token t (ties to the lower id, decided on
+// the fp32 logits), its overlap with the recorded ids, and the route KL.
+__device__ void diag_token(const float* row, int64_t t, int N, const ReplayOut& o) {
+    const int lane = threadIdx.x & 63;
+    const int nv = (N + 63) / 64;
+    const DiagOut& g = o.diag;
+    float p[kMaxLanesVals];
+    uint32_t key[kMaxLanesVals];
+    for (int v = 0; v < nv; ++v) {
+        const int j = v * 64 + lane;
+        p[v] = -INFINITY;
+        key[v] = 0;
+        if (j < N) {
+            p[v] = (float)((double)row[j] + (o.b_r ? (double)o.b_r[j] : 0.0));
+            key[v] = orderable(p[v]);
+        }
+    }
+    float pmax;
+    const uint32_t taken = select_topk(key, nv, N, o.k, pmax);
+    if (g.cur_idx) write_route(taken, nv, g.cur_idx, o.idx_dtype, t * o.k, nullptr, nullptr, 1.0f);
+    if (g.overlap || g.hist) {
+        int cnt = 0;
+        for (int s = 0; s < o.k; ++s) {
+            const int id = load_id(o.idx, o.idx_dtype, t * o.ldi + s);
+            if (id >= 0 && id < N && (id & 63) == lane && ((taken >> (id >> 6)) & 1u)) cnt++;
+        }
+        cnt = wave_sum_i32(cnt);
+        if (lane == 0) {
+            if (g.overlap) g.overlap[t] = cnt;
+            if (g.hist) atomicAdd(g.hist + (o.k - cnt), 1ull);
+        }
+    }
+    if (g.kl) {
+        const float* zr = g.z_ref + t * N;
+        double mz = -INFINITY;
+        for (int v = 0; v < nv; ++v) {
+            const int j = v * 64 + lane;
+            if (j < N) mz = fmax(mz, (double)zr[j]);
+        }
+        mz = wave_max_f64(mz);
+        const double mp = (double)pmax;
+        double sp = 0.0, sz = 0.0;
+        for (int v = 0; v < nv; ++v) {
+            const int j = v * 64 + lane;
+            if (j < N) {
+                sp += exp((double)p[v] - mp);
+                sz += exp((double)zr[j] - mz);
+            }
+        }
+        sp = wave_sum_f64(sp);
+        sz = wave_sum_f64(sz);
+        const double shift = (mp + log(sp)) - (mz + log(sz));
+        double acc = 0.0;
+        for (int v = 0; v < nv; ++v) {
+            const int j = v * 64 + lane;
+            if (j < N) {
+                const double lp = (double)p[v] - mp;
+                acc += exp(lp) / sp * (((double)p[v] - (double)zr[j]) - shift);
+            }
+        }
+        acc = wave_sum_f64(acc);
+        if (lane == 0) g.kl[t] = (float)acc;
+    }
+}
 
 // One wavefront: replay weights of token t over its recorded ids from the LDS
 // row of N current-router logits (predictor bypassed).
 __device__ void replay_token(const float* row, int64_t t, int N, const ReplayOut& o) {
+    if (o.diag.cur_idx || o.diag.overlap || o.diag.kl || o.diag.hist) diag_token(row, t, N, o);
+    if (!o.gate_out) return;
     const int lane = threadIdx.x & 63;
     auto logit = [&](int j) {
         return (float)((double)row[j] + (o.b_r ? (double)o.b_r[j] : 0.0));
@@ -567,16 +670,19 @@ hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const floa
     return hipGetLastError();
 }
 
-hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void* idx, int64_t ldi,
-                               const float* W_r, const float* b_r, float* gate_out, int* err,
-                               void* split_ws, hipStream_t s) {
-    const char* v = getenv("PR2_VALIDATE");
-    ReplayOut o{b_r, d.k, d.renorm, idx, d.idx_dtype, ldi, gate_out, err,
-                (v && v[0] == '1') ? 1 : 0};
+namespace {
+
+__global__ void __launch_bounds__(64) zero_u64_kernel(unsigned long long* p, int n) {
+    for (int i = threadIdx.x; i < n; i += 64) p[i] = 0ull;
+}
+
+hipError_t launch_router_replay(const pr2_moe_desc& d, const void* x, const float* W_r,
+                                const ReplayOut& o, void* split_ws, const char* name,
+                                hipStream_t s) {
     if (router_mfma_ok(d, d.N)) {
         hipError_t e = launch_split(W_r, nullptr, nullptr, d, 0, 0, (bf16_t*)split_ws, s);
         if (e != hipSuccess) return e;
-        LaunchScope scope("replay_gates", s);
+        LaunchScope scope(name, s);
         return launch_router_mfma<1>(d, d.N, 0, x, (const bf16_t*)split_ws, PredictOut{}, o, s);
     }
     ProjArgs a;
@@ -591,12 +697,39 @@ hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void*
     pick_tile(a);
     dim3 grid((unsigned)((d.T + a.TM - 1) / a.TM));
     size_t smem = router_smem(a);
-    LaunchScope scope("replay_gates", s);
+    LaunchScope scope(name, s);
     if (d.act_dtype == PR2_BF16)
         hipLaunchKernelGGL(replay_gates_kernel<bf16_t>, grid, dim3(kThreads), smem, s, a, o);
     else
         hipLaunchKernelGGL(replay_gates_kernel<float>, grid, dim3(kThreads), smem, s, a, o);
     return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void* idx, int64_t ldi,
+                               const float* W_r, const float* b_r, float* gate_out, int* err,
+                               void* split_ws, hipStream_t s) {
+    const char* v = getenv("PR2_VALIDATE");
+    ReplayOut o{b_r, d.k, d.renorm, idx, d.idx_dtype, ldi, gate_out, err,
+                (v && v[0] == '1') ? 1 : 0, DiagOut{}};
+    return launch_router_replay(d, x, W_r, o, split_ws, "replay_gates", s);
+}
+
+hipError_t launch_route_diagnostics(const pr2_moe_desc& d, const void* x, const void* idx,
+                                    int64_t ldi, const float* W_r, const float* b_r,
+                                    const float* z_ref, void* cur_idx, int* overlap, float* kl,
+                                    unsigned long long* hist, void* split_ws, hipStream_t s) {
+    if (hist) {
+        LaunchScope scope("route_diagnostics_zero", s);
+        hipLaunchKernelGGL(zero_u64_kernel, dim3(1), dim3(64), 0, s, hist, d.k + 1);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (d.T == 0) return hipSuccess;
+    ReplayOut o{b_r, d.k, 1, idx, d.idx_dtype, ldi, nullptr, nullptr, 0,
+                DiagOut{z_ref, cur_idx, overlap, kl, hist}};
+    return launch_router_replay(d, x, W_r, o, split_ws, "route_diagnostics", s);
 }
 
 }  // namespace pr2
