@@ -262,17 +262,36 @@ def predictive_kl(p_cur, h_old, p_old, A, B):
     rho = Softmax(p_cur) under stop-gradient and
     rho_hat = Softmax(p_old + h_old A B) rebuilt from the feature cache.
 
-    Returns (kl [T], dA, dB) where dA, dB are gradients of mean_t kl."""
-    rho = softmax(p_cur)
+    B = None means the identity (a full-rank predictor W_p = A, r = N).
+    Returns (kl [T], dA, dB) where dA, dB are gradients of mean_t kl (dB is
+    None for the identity)."""
     u = _f64(h_old) @ _f64(A)
-    zhat = _f64(p_old) + u @ _f64(B)
+    zhat = _f64(p_old) + (u if B is None else u @ _f64(B))
+    return _kl_and_grads(softmax(p_cur), zhat, u, h_old, B)
+
+
+def delta_matching_kl(p_cur, h_old, p_old, A, B):
+    """The delta-matching alternative of the predictive loss (Appendix F,
+    predictive-objective ablation): per-token
+    KL(Softmax(<p_cur - p_old>) || Softmax(h_old W_p)), W_p = A B (B = None:
+    identity).  Returns (kl [T], dA, dB) like predictive_kl."""
+    u = _f64(h_old) @ _f64(A)
+    b = u if B is None else u @ _f64(B)
+    return _kl_and_grads(softmax(_f64(p_cur) - _f64(p_old)), b, u, h_old, B)
+
+
+def _kl_and_grads(target, zhat, u, h_old, B):
+    """KL(target || Softmax(zhat)) per token and the gradients of its mean
+    through zhat = const + u B, u = h_old A."""
     rho_hat = softmax(zhat)
-    log_rho = np.log(np.where(rho > 0, rho, 1.0))
+    log_t = np.log(np.where(target > 0, target, 1.0))
     log_rho_hat = zhat - zhat.max(axis=1, keepdims=True)
     log_rho_hat = log_rho_hat - np.log(np.exp(log_rho_hat).sum(axis=1, keepdims=True))
-    kl = (rho * (log_rho - log_rho_hat)).sum(axis=1)
+    kl = (target * (log_t - log_rho_hat)).sum(axis=1)
     T = zhat.shape[0]
-    dz = (rho_hat - rho) / T          # d mean KL / d zhat
+    dz = (rho_hat - target) / T       # d mean KL / d zhat
+    if B is None:
+        return kl, _f64(h_old).T @ dz, None
     dB = u.T @ dz
     dA = _f64(h_old).T @ (dz @ _f64(B).T)
     return kl, dA, dB

@@ -372,6 +372,56 @@ def test_predictive_kl_zero_when_predictor_matches_and_gradients():
         np.testing.assert_allclose(G, fd, rtol=1e-6, atol=1e-9)
 
 
+def _fd_mean(fn, M, eps=1e-6):
+    fd = np.zeros_like(M)
+    for i in range(M.size):
+        o = M.flat[i]
+        M.flat[i] = o + eps
+        lp = fn()[0].mean()
+        M.flat[i] = o - eps
+        lm = fn()[0].mean()
+        M.flat[i] = o
+        fd.flat[i] = (lp - lm) / (2 * eps)
+    return fd
+
+
+def test_predictive_kl_full_rank_identity():
+    """B = None (W_p = A, r = N) equals passing the identity matrix."""
+    rng = np.random.default_rng(20)
+    T, d, N = 15, 5, 6
+    h_old, p_old, p_cur = rand(rng, T, d), rand(rng, T, N), rand(rng, T, N)
+    A = rand(rng, d, N, std=0.3)
+    kl, dA, dB = O.predictive_kl(p_cur, h_old, p_old, A, None)
+    kl2, dA2, _ = O.predictive_kl(p_cur, h_old, p_old, A, np.eye(N))
+    np.testing.assert_allclose(kl, kl2, rtol=1e-12)
+    np.testing.assert_allclose(dA, dA2, rtol=1e-12, atol=1e-15)
+    assert dB is None
+    np.testing.assert_allclose(dA, _fd_mean(lambda: O.predictive_kl(p_cur, h_old, p_old, A, None), A),
+                               rtol=1e-6, atol=1e-9)
+
+
+def test_delta_matching_kl_closed_forms_and_gradients():
+    rng = np.random.default_rng(21)
+    T, d, N, r = 20, 6, 5, 3
+    h_old, p_old = rand(rng, T, d), rand(rng, T, N)
+    A, B = rand(rng, d, r, std=0.3), rand(rng, r, N, std=0.3)
+    # the current logits moved by exactly the predicted residual: zero loss and gradient
+    p_cur = p_old + h_old @ A @ B + rand(rng, T, 1)
+    kl, dA, dB = O.delta_matching_kl(p_cur, h_old, p_old, A, B)
+    np.testing.assert_allclose(kl, 0.0, atol=1e-12)
+    np.testing.assert_allclose(dB, 0.0, atol=1e-12)
+    p_cur = rand(rng, T, N)
+    kl, dA, dB = O.delta_matching_kl(p_cur, h_old, p_old, A, B)
+    ref = scipy.special.rel_entr(scipy.special.softmax(p_cur - p_old, 1),
+                                 scipy.special.softmax(h_old @ A @ B, 1)).sum(1)
+    np.testing.assert_allclose(kl, ref, rtol=1e-10)
+    # it differs from the standard objective (which keeps p_old inside rho_hat)
+    assert not np.allclose(kl, O.predictive_kl(p_cur, h_old, p_old, A, B)[0])
+    fn = lambda: O.delta_matching_kl(p_cur, h_old, p_old, A, B)
+    np.testing.assert_allclose(dA, _fd_mean(fn, A), rtol=1e-6, atol=1e-9)
+    np.testing.assert_allclose(dB, _fd_mean(fn, B), rtol=1e-6, atol=1e-9)
+
+
 # ------------------------------------------------- Table 3 cost formulas ----
 
 def test_table3_overheads_reproduce():
@@ -585,3 +635,9 @@ def test_pins_catch_planted_mistakes(monkeypatch):
         bad.feature_cache_positions(T, Tc, seed) + 1, T - 1))
     assert fails(test_feature_cache_positions_stratified_uniform)
     monkeypatch.setattr(O, "feature_cache_positions", bad.feature_cache_positions)
+
+    # delta-matching target without the old logits subtracted
+    monkeypatch.setattr(O, "delta_matching_kl", lambda p_cur, h_old, p_old, A, B:
+                        bad.delta_matching_kl(p_cur, h_old, 0 * p_old, A, B))
+    assert fails(test_delta_matching_kl_closed_forms_and_gradients)
+    monkeypatch.setattr(O, "delta_matching_kl", bad.delta_matching_kl)
