@@ -69,7 +69,8 @@ enum {
     PR2_OP_REPLAY_FWD = 1,
     PR2_OP_REPLAY_BWD = 2,
     PR2_OP_ROLLOUT_FWD = 3,
-    PR2_OP_ROUTE_DIAG = 4
+    PR2_OP_ROUTE_DIAG = 4,
+    PR2_OP_PREDICTOR_LOSS = 5
 };
 
 /*
@@ -224,6 +225,62 @@ pr2_status pr2_route_diagnostics(const pr2_moe_desc* desc, const void* x, const 
                                  const float* z_ref, void* cur_idx_out, int32_t* overlap_out,
                                  float* kl_out, uint64_t* hist_out, void* ws, size_t ws_bytes,
                                  pr2_stream_t stream);
+
+/*
+ * Feature-cache positions (Appendix E.2, feature-cache paragraph: a fixed number Tc of token
+ * positions per response keep their route-recording features, drawn by uniform
+ * sub-sampling along the rollout).  HOST function, no device work: fills pos_out[0..n) with
+ * n = min(T, Tc) increasing positions in [0, T): Tc >= T keeps every position; otherwise
+ * position i is drawn uniformly inside the stratum [floor(i T / Tc), floor((i+1) T / Tc))
+ * with the i-th output of SplitMix64 (Steele, Lea and Flood, 2014) for `seed`, so the cache
+ * covers the whole rollout evenly.  Returns n, or -1 on a bad argument (pr2_last_error).
+ */
+int64_t pr2_feature_cache_positions(int64_t T, int64_t Tc, uint64_t seed, int64_t* pos_out);
+
+/*
+ * Route prediction with the feature-cache write fused in (Alg. 2 in Appendix D, its caching
+ * step: the predicted ids go to the index cache and the retained tokens' route-recording
+ * features (h_old, p_old) to the feature cache).  Same as pr2_route_predict with
+ * logits_out = NULL, plus: token t with 0 <= cache_row[t] < cache_rows copies its input row
+ * x_t to h_cache[cache_row[t]] ([cache_rows, d] act_dtype, 16-byte aligned) and writes its
+ * router logits p_t (no predictor term) to p_cache[cache_row[t]] ([cache_rows, N] fp32);
+ * tokens with any other cache_row value are not cached.  cache_row is a device int32 [T];
+ * rows must be distinct.  ws >= pr2_workspace_bytes(desc, PR2_OP_ROUTE).
+ */
+pr2_status pr2_route_predict_cached(const pr2_moe_desc* desc, const void* x, const float* W_r,
+                                    const float* b_r, const float* A, const float* B,
+                                    void* idx_out, int64_t ldi, float* gate_out,
+                                    const int32_t* cache_row, void* h_cache, float* p_cache,
+                                    int64_t cache_rows, void* ws, size_t ws_bytes,
+                                    pr2_stream_t stream);
+
+/*
+ * Evolution-predictor loss and gradients on the feature cache (Sec. 4.2, Eq. pr2_loss; Alg. 3
+ * in Appendix D, its predictive-loss steps).  desc.T = number of cached tokens; desc.d, N, r
+ * as for the layer (r >= 1); desc.k must be valid; m, idx_dtype and renorm are unused.
+ *
+ *   p_t = h_t W_r + b_r               the current router on the same tokens (teacher)
+ *   zhat_t = p_old,t + h_old,t A B    rebuilt predictive logits
+ *   loss_kind 0:  kl_t = KL(softmax(p_t) || softmax(zhat_t))                  (Eq. pr2_loss)
+ *   loss_kind 1:  kl_t = KL(softmax(p_t - p_old,t) || softmax(h_old,t A B))   (delta matching,
+ *                 the objective ablation of Appendix F)
+ *   loss = mean_t kl_t;  dA, dB = gradients of loss (the router gets none: stop-gradient)
+ *
+ *   h, h_old   [T, d] act_dtype (16-byte aligned);  W_r [d, N], b_r [N] or NULL, p_old [T, N],
+ *              A [d, r], B [r, N] fp32 (B NULL means the identity, needs r == N; dB unused)
+ *   mini_step  1-based index of the update within the batch: mini_step == 1 is the
+ *              on-policy first step, where the loss is skipped (zeros written, h, h_old, W_r,
+ *              p_old and ws may be NULL)
+ *   kl_out [T] fp32 or NULL;  loss_out [1] fp32;  dA [d, r], dB [r, N] fp32 (overwritten)
+ *   ws         >= pr2_workspace_bytes(desc, PR2_OP_PREDICTOR_LOSS)
+ * p is computed as by the replay router (exact products, one rounding to fp32); everything
+ * after it, including the gradient sums over tokens, in fp64 with a fixed summation order.
+ */
+pr2_status pr2_predictor_loss(const pr2_moe_desc* desc, const void* h, const float* W_r,
+                              const float* b_r, const void* h_old, const float* p_old,
+                              const float* A, const float* B, int loss_kind, int mini_step,
+                              float* kl_out, float* loss_out, float* dA, float* dB, void* ws,
+                              size_t ws_bytes, pr2_stream_t stream);
 
 /* Status name ("PR2_OK", ...); never NULL. */
 const char* pr2_status_string(pr2_status s);

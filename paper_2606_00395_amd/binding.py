@@ -9,14 +9,15 @@ from __future__ import annotations
 
 import ctypes
 import os
-from ctypes import POINTER, byref, c_char_p, c_double, c_int, c_int32, c_int64, c_size_t, c_void_p
+from ctypes import (POINTER, byref, c_char_p, c_double, c_int, c_int32, c_int64, c_size_t,
+                    c_uint64, c_void_p)
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libpr2.so")
 
 PR2_F32, PR2_BF16 = 0, 1
 PR2_I32, PR2_I16 = 0, 1
-OP_ROUTE, OP_REPLAY_FWD, OP_REPLAY_BWD, OP_ROLLOUT_FWD, OP_ROUTE_DIAG = 0, 1, 2, 3, 4
+OP_ROUTE, OP_REPLAY_FWD, OP_REPLAY_BWD, OP_ROLLOUT_FWD, OP_ROUTE_DIAG, OP_PREDICTOR_LOSS = range(6)
 
 STATUS = ["PR2_OK", "PR2_ERR_NULL", "PR2_ERR_SHAPE", "PR2_ERR_DTYPE", "PR2_ERR_ALIGN",
           "PR2_ERR_WORKSPACE", "PR2_ERR_UNSUPPORTED", "PR2_ERR_ROUTE", "PR2_ERR_DEVICE",
@@ -25,6 +26,7 @@ STATUS = ["PR2_OK", "PR2_ERR_NULL", "PR2_ERR_SHAPE", "PR2_ERR_DTYPE", "PR2_ERR_A
 # every symbol include/pr2.h declares
 EXPORTS = ["pr2_workspace_bytes", "pr2_route_predict", "pr2_moe_replay_forward",
            "pr2_moe_replay_backward", "pr2_moe_rollout_forward", "pr2_route_diagnostics",
+           "pr2_feature_cache_positions", "pr2_route_predict_cached", "pr2_predictor_loss",
            "pr2_status_string",
            "pr2_last_error", "pr2_version", "pr2_profile_enable",
            "pr2_profile_reset", "pr2_profile_collect"]
@@ -73,6 +75,14 @@ def lib() -> ctypes.CDLL:
     L.pr2_route_diagnostics.argtypes = [POINTER(MoeDesc), P, P, c_int64, P, P, P, P, P, P, P, P,
                                         c_size_t, P]
     L.pr2_route_diagnostics.restype = c_int
+    L.pr2_feature_cache_positions.argtypes = [c_int64, c_int64, c_uint64, P]
+    L.pr2_feature_cache_positions.restype = c_int64
+    L.pr2_route_predict_cached.argtypes = [POINTER(MoeDesc), P, P, P, P, P, P, c_int64, P, P, P, P,
+                                           c_int64, P, c_size_t, P]
+    L.pr2_route_predict_cached.restype = c_int
+    L.pr2_predictor_loss.argtypes = [POINTER(MoeDesc), P, P, P, P, P, P, P, c_int, c_int, P, P, P,
+                                     P, P, c_size_t, P]
+    L.pr2_predictor_loss.restype = c_int
     L.pr2_status_string.argtypes = [c_int]
     L.pr2_status_string.restype = c_char_p
     L.pr2_last_error.argtypes = []
@@ -235,6 +245,51 @@ def route_diagnostics(x, idx, W_r, b_r, z_ref=None, cur_idx_out=None, overlap_ou
                                       _ptr(W_r), _ptr(b_r), _ptr(z_ref), _ptr(cur_idx_out),
                                       _ptr(overlap_out), _ptr(kl_out), _ptr(hist_out), _ptr(ws),
                                       ws.numel(), _stream(stream)))
+
+
+def feature_cache_positions(T: int, Tc: int, seed: int):
+    """pr2_feature_cache_positions: the retained positions as a numpy int64 array."""
+    import numpy as np
+    n = min(T, Tc)
+    out = np.empty(max(n, 1), dtype=np.int64)
+    got = lib().pr2_feature_cache_positions(T, Tc, seed & ((1 << 64) - 1),
+                                            out.ctypes.data_as(c_void_p))
+    if got < 0:
+        raise Pr2Error(lib().pr2_last_error().decode())
+    return out[:got]
+
+
+def route_predict_cached(x, W_r, b_r, A, B, k, idx_out, cache_row, h_cache, p_cache,
+                         gate_out=None, renorm=True, ws=None, stream=None):
+    """pr2_route_predict_cached on torch tensors: ``cache_row`` int32 [T] on the device."""
+    T, d = x.shape
+    N = W_r.shape[1]
+    r = 0 if A is None else A.shape[1]
+    desc = make_desc(T, d, N, k, 0, r, _act_code(x), _idx_code(idx_out), renorm)
+    if ws is None:
+        ws = route_workspace(x, W_r, A, k, _idx_code(idx_out))
+    check(lib().pr2_route_predict_cached(byref(desc), _ptr(x), _ptr(W_r), _ptr(b_r), _ptr(A),
+                                         _ptr(B), _ptr(idx_out), _row_stride(idx_out),
+                                         _ptr(gate_out), _ptr(cache_row), _ptr(h_cache),
+                                         _ptr(p_cache), h_cache.shape[0], _ptr(ws), ws.numel(),
+                                         _stream(stream)))
+
+
+def predictor_loss(h, W_r, b_r, h_old, p_old, A, B, loss_out, dA, dB=None, kl_out=None,
+                   loss_kind=0, mini_step=2, ws=None, stream=None):
+    """pr2_predictor_loss on torch tensors (h, h_old [Tc, d]; p_old [Tc, N])."""
+    torch = _torch()
+    T, d = h_old.shape
+    N = p_old.shape[1]
+    r = A.shape[1]
+    desc = make_desc(T, d, N, 1, 0, r, _act_code(h_old))
+    if ws is None:
+        ws = torch.empty(max(1, workspace_bytes(desc, OP_PREDICTOR_LOSS)), dtype=torch.uint8,
+                         device=h_old.device)
+    check(lib().pr2_predictor_loss(byref(desc), _ptr(h), _ptr(W_r), _ptr(b_r), _ptr(h_old),
+                                   _ptr(p_old), _ptr(A), _ptr(B), loss_kind, mini_step,
+                                   _ptr(kl_out), _ptr(loss_out), _ptr(dA), _ptr(dB), _ptr(ws),
+                                   ws.numel(), _stream(stream)))
 
 
 def backward_workspace(x, idx, W_r, W_gate, renorm=True):

@@ -169,6 +169,26 @@ static size_t diag_ws_bytes(const pr2_moe_desc& d) {
     return router_mfma_ok(d, d.N) ? router_split_bytes(d.N, d.d) + 256 : 0;
 }
 
+static PredLossWs pred_ws_layout(const pr2_moe_desc& d, void* base) {
+    PredLossWs w{};
+    char* p = base ? (char*)(((uintptr_t)base + 255) & ~(uintptr_t)255) : nullptr;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        char* q = p ? p + off : nullptr;
+        off += up256(bytes);
+        return q;
+    };
+    const size_t T = (size_t)d.T;
+    w.p_cur = (float*)take(sizeof(float) * T * d.N);
+    w.u = (double*)take(sizeof(double) * T * d.r);
+    w.dz = (double*)take(sizeof(double) * T * d.N);
+    w.w = (double*)take(sizeof(double) * T * d.r);
+    w.kl = (double*)take(sizeof(double) * T);
+    w.wsplit = take(router_mfma_ok(d, d.N) ? router_split_bytes(d.N, d.d) : 0);
+    w.bytes = off + 256;
+    return w;
+}
+
 static size_t route_ws_bytes(const pr2_moe_desc& d) {
     const size_t need = route_split_need(d);
     return need ? need + 256 : 0;
@@ -262,6 +282,13 @@ size_t pr2_workspace_bytes(const pr2_moe_desc* desc, int op) {
             t_err = saved;
             if (s != PR2_OK) return 0;
             return diag_ws_bytes(*desc);
+        }
+        case PR2_OP_PREDICTOR_LOSS: {
+            std::string saved = t_err;
+            pr2_status s = check_desc(desc, false, false);
+            t_err = saved;
+            if (s != PR2_OK || desc->r < 1) return 0;
+            return pred_ws_layout(*desc, nullptr).bytes;
         }
         case PR2_OP_REPLAY_BWD: {
             std::string saved = t_err;
@@ -527,6 +554,127 @@ pr2_status pr2_route_diagnostics(const pr2_moe_desc* desc, const void* x, const 
                                             overlap_out, kl_out, (unsigned long long*)hist_out,
                                             split, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "route diagnostics launch");
+    return ok();
+}
+
+int64_t pr2_feature_cache_positions(int64_t T, int64_t Tc, uint64_t seed, int64_t* pos_out) {
+    if (T < 0 || Tc < 1 || T > ((int64_t)1 << 40)) {
+        fail(PR2_ERR_SHAPE, "need T >= 0 (at most 2^40) and Tc >= 1");
+        return -1;
+    }
+    const int64_t n = Tc < T ? Tc : T;
+    if (n > 0 && !pos_out) {
+        fail(PR2_ERR_NULL, "pos_out is NULL");
+        return -1;
+    }
+    if (Tc >= T) {
+        for (int64_t t = 0; t < T; ++t) pos_out[t] = t;
+        ok();
+        return T;
+    }
+    const uint64_t golden = 0x9E3779B97F4A7C15ull;
+    for (int64_t i = 0; i < Tc; ++i) {
+        const int64_t lo = (int64_t)(((__int128)i * T) / Tc);
+        const int64_t hi = (int64_t)(((__int128)(i + 1) * T) / Tc);
+        uint64_t z = seed + (uint64_t)(i + 1) * golden;     // SplitMix64 state of draw i
+        z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+        z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+        z ^= z >> 31;
+        pos_out[i] = lo + (int64_t)(z % (uint64_t)(hi - lo));
+    }
+    ok();
+    return Tc;
+}
+
+pr2_status pr2_route_predict_cached(const pr2_moe_desc* desc, const void* x, const float* W_r,
+                                    const float* b_r, const float* A, const float* B,
+                                    void* idx_out, int64_t ldi, float* gate_out,
+                                    const int32_t* cache_row, void* h_cache, float* p_cache,
+                                    int64_t cache_rows, void* ws, size_t ws_bytes,
+                                    pr2_stream_t stream) {
+    pr2_status s = check_desc(desc, false, true);
+    if (s != PR2_OK) return s;
+    const pr2_moe_desc& d = *desc;
+    if (!cache_row || !h_cache || !p_cache)
+        return fail(PR2_ERR_NULL, "cache_row, h_cache and p_cache are required");
+    if (cache_rows < 0) return fail(PR2_ERR_SHAPE, "cache_rows = %lld < 0", (long long)cache_rows);
+    if (!aligned(h_cache, 16) || !aligned(p_cache, 4) || !aligned(cache_row, 4))
+        return fail(PR2_ERR_ALIGN, "h_cache must be 16-byte, p_cache and cache_row 4-byte aligned");
+    if (d.r > 256) return fail(PR2_ERR_UNSUPPORTED, "predictor rank r = %d > 256", d.r);
+    if (ldi < d.k) return fail(PR2_ERR_SHAPE, "ldi = %lld < k = %d", (long long)ldi, d.k);
+    if (d.T == 0) return ok();
+    if (!x) return fail(PR2_ERR_NULL, "x is NULL");
+    if (!W_r) return fail(PR2_ERR_NULL, "W_r is NULL");
+    if (!idx_out) return fail(PR2_ERR_NULL, "idx_out is NULL");
+    if (d.r > 0 && !A) return fail(PR2_ERR_NULL, "A is NULL with r = %d > 0", d.r);
+    if (d.r > 0 && !B && d.r != d.N)
+        return fail(PR2_ERR_NULL, "B is NULL but r = %d != N = %d (identity needs r == N)", d.r, d.N);
+    if (!aligned(x, 16)) return fail(PR2_ERR_ALIGN, "x is not 16-byte aligned");
+    if (!aligned(W_r, 4) || (b_r && !aligned(b_r, 4)) || (A && !aligned(A, 4)) ||
+        (B && !aligned(B, 4)) || (gate_out && !aligned(gate_out, 4)))
+        return fail(PR2_ERR_ALIGN, "an fp32 router/predictor/gate tensor is not 4-byte aligned");
+    if (!aligned(idx_out, d.idx_dtype == PR2_I16 ? 2 : 4))
+        return fail(PR2_ERR_ALIGN, "idx_out is not aligned to its element size");
+    const size_t need = route_ws_bytes(d);
+    if (need && !ws) return fail(PR2_ERR_NULL, "ws is NULL (need %zu bytes)", need);
+    if (ws_bytes < need)
+        return fail(PR2_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
+    s = device_ready();
+    if (s != PR2_OK) return s;
+    void* split = need ? (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255) : nullptr;
+    const FeatureCache cache{cache_row, h_cache, p_cache, cache_rows};
+    hipError_t e = launch_route_predict(d, x, W_r, b_r, A, B, idx_out, ldi, gate_out, nullptr,
+                                        split, (hipStream_t)stream, cache);
+    if (e != hipSuccess) return hip_fail(e, "route_predict launch");
+    return ok();
+}
+
+pr2_status pr2_predictor_loss(const pr2_moe_desc* desc, const void* h, const float* W_r,
+                              const float* b_r, const void* h_old, const float* p_old,
+                              const float* A, const float* B, int loss_kind, int mini_step,
+                              float* kl_out, float* loss_out, float* dA, float* dB, void* ws,
+                              size_t ws_bytes, pr2_stream_t stream) {
+    pr2_status s = check_desc(desc, false, false);
+    if (s != PR2_OK) return s;
+    const pr2_moe_desc& d = *desc;
+    if (d.r < 1) return fail(PR2_ERR_SHAPE, "the predictor loss needs r >= 1");
+    if (loss_kind != 0 && loss_kind != 1)
+        return fail(PR2_ERR_SHAPE, "loss_kind = %d is not 0 (KL) or 1 (delta matching)", loss_kind);
+    if (mini_step < 1) return fail(PR2_ERR_SHAPE, "mini_step = %d < 1", mini_step);
+    if (!A) return fail(PR2_ERR_NULL, "A is NULL");
+    if (!B && d.r != d.N)
+        return fail(PR2_ERR_NULL, "B is NULL but r = %d != N = %d (identity needs r == N)", d.r, d.N);
+    if (!loss_out || !dA) return fail(PR2_ERR_NULL, "loss_out and dA are required");
+    if (B && !dB) return fail(PR2_ERR_NULL, "dB is NULL");
+    if (!aligned(A, 4) || (B && !aligned(B, 4)) || !aligned(loss_out, 4) || !aligned(dA, 4) ||
+        (dB && !aligned(dB, 4)) || (kl_out && !aligned(kl_out, 4)))
+        return fail(PR2_ERR_ALIGN, "an fp32 tensor is not 4-byte aligned");
+    float* dBo = B ? dB : nullptr;
+    hipStream_t st = (hipStream_t)stream;
+    if (mini_step == 1 || d.T == 0) {
+        // Alg. 3: no predictive loss on the first (on-policy) mini-step
+        s = device_ready();
+        if (s != PR2_OK) return s;
+        hipError_t e = launch_predictor_zero(d, kl_out, loss_out, dA, dBo, st);
+        if (e != hipSuccess) return hip_fail(e, "zero fill launch");
+        return ok();
+    }
+    if (!h || !h_old) return fail(PR2_ERR_NULL, "h and h_old are required");
+    if (!W_r || !p_old) return fail(PR2_ERR_NULL, "W_r and p_old are required");
+    if (!aligned(h, 16) || !aligned(h_old, 16))
+        return fail(PR2_ERR_ALIGN, "h and h_old must be 16-byte aligned");
+    if (!aligned(W_r, 4) || (b_r && !aligned(b_r, 4)) || !aligned(p_old, 4))
+        return fail(PR2_ERR_ALIGN, "W_r, b_r, p_old must be 4-byte aligned");
+    const size_t need = pred_ws_layout(d, nullptr).bytes;
+    if (!ws) return fail(PR2_ERR_NULL, "ws is NULL (need %zu bytes)", need);
+    if (ws_bytes < need)
+        return fail(PR2_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
+    s = device_ready();
+    if (s != PR2_OK) return s;
+    PredLossWs w = pred_ws_layout(d, ws);
+    hipError_t e = launch_predictor_loss(d, h, W_r, b_r, h_old, p_old, A, B, loss_kind, kl_out,
+                                         loss_out, dA, dBo, w, st);
+    if (e != hipSuccess) return hip_fail(e, "predictor loss launch");
     return ok();
 }
 

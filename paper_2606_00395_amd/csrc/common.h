@@ -100,6 +100,16 @@ struct LaunchScope {
     int slot;
 };
 
+// Route-recording features of the retained tokens (feature cache): token t with
+// row[t] in [0, rows) writes its hidden state to h[row[t]] and its router logits
+// to p[row[t]].
+struct FeatureCache {
+    const int* row;     // [T] or null (no feature cache)
+    void* h;            // [rows, d] act
+    float* p;           // [rows, N]
+    int64_t rows;
+};
+
 // router.hip
 // Scratch for the bf16 three-way split of [W_r | A] used by the MFMA router
 // (0 when the shape takes the fp64 vector path).
@@ -108,7 +118,10 @@ bool router_mfma_ok(const pr2_moe_desc& d, int NC);
 hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const float* W_r,
                                 const float* b_r, const float* A, const float* B, void* idx_out,
                                 int64_t ldi, float* gate_out, float* logits_out, void* split_ws,
-                                hipStream_t s);
+                                hipStream_t s, const FeatureCache& cache = FeatureCache{});
+// current router logits p = x W_r + b_r of every token into p_out [T, N]
+hipError_t launch_router_logits(const pr2_moe_desc& d, const void* x, const float* W_r,
+                                const float* b_r, float* p_out, void* split_ws, hipStream_t s);
 hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void* idx, int64_t ldi,
                                const float* W_r, const float* b_r, float* gate_out, int* err,
                                void* split_ws, hipStream_t s);
@@ -130,6 +143,24 @@ hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void*
 bool mfma_shape_ok(const pr2_moe_desc& d);
 hipError_t launch_preact(const pr2_moe_desc& d, const void* x, const void* W_gate,
                          const void* W_up, const ReplayWs& ws, void* AU, hipStream_t s);
+
+// predictor.hip
+struct PredLossWs {
+    float* p_cur;       // [T, N] current router logits
+    double* u;          // [T, r] h_old A
+    double* dz;         // [T, N] d loss / d zhat
+    double* w;          // [T, r] dz B^T
+    double* kl;         // [T]
+    void* wsplit;       // router split (N columns)
+    size_t bytes;
+};
+hipError_t launch_predictor_loss(const pr2_moe_desc& d, const void* h, const float* W_r,
+                                 const float* b_r, const void* h_old, const float* p_old,
+                                 const float* A, const float* B, int kind, float* kl_out,
+                                 float* loss_out, float* dA, float* dB, const PredLossWs& ws,
+                                 hipStream_t s);
+hipError_t launch_predictor_zero(const pr2_moe_desc& d, float* kl_out, float* loss_out, float* dA,
+                                 float* dB, hipStream_t s);
 
 // backward.hip
 bool bwd_mfma_ok(const pr2_moe_desc& d);

@@ -30,6 +30,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kMaxLanesVals = kMaxExperts / 64;
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ uint32_t orderable(float z) {
     if (z == 0.0f) z = 0.0f;                 // -0.0 ties with +0.0
@@ -136,6 +137,10 @@ struct PredictOut {
     int64_t ldi;
     float* gate_out;      // [T, k] or null
     float* logits_out;    // [T, N] or null (only when not folded)
+    FeatureCache cache;   // route-recording features of retained tokens (only when not folded)
+    const void* x;        // the layer input, for the hidden-feature copy
+    int d;
+    int act_dtype;
 };
 
 // k rounds of a wavefront arg-max over orderable keys (lane l holds ids
@@ -191,6 +196,27 @@ __device__ void write_route(uint32_t taken, int nv, void* idx, int idx_dtype, in
 __device__ void predict_token(const float* row, int64_t t, int N, int r, const PredictOut& o) {
     const int lane = threadIdx.x & 63;
     const int nv = (N + 63) / 64;
+    float* lrow = o.logits_out ? o.logits_out + t * N : nullptr;
+    if (o.cache.row) {
+        // feature cache: p_old and h_old of a retained token go to its cache row
+        const int cr = o.cache.row[t];
+        if (cr >= 0 && cr < o.cache.rows) {
+            lrow = o.cache.p + (int64_t)cr * N;
+            const size_t eb = o.act_dtype == PR2_BF16 ? 2 : 4;
+            const size_t bytes = (size_t)o.d * eb;
+            const unsigned char* src = (const unsigned char*)o.x + (size_t)t * bytes;
+            unsigned char* dst = (unsigned char*)o.cache.h + (size_t)cr * bytes;
+            if (bytes % 16 == 0) {
+                for (size_t c = lane; c < bytes / 16; c += 64)
+                    ((u32x4_t*)dst)[c] = ((const u32x4_t*)src)[c];
+            } else {
+                for (size_t c = lane; c < bytes / eb; c += 64) {
+                    if (eb == 2) ((uint16_t*)dst)[c] = ((const uint16_t*)src)[c];
+                    else ((uint32_t*)dst)[c] = ((const uint32_t*)src)[c];
+                }
+            }
+        }
+    }
     float z[kMaxLanesVals];
     uint32_t key[kMaxLanesVals];
     for (int v = 0; v < nv; ++v) {
@@ -209,7 +235,7 @@ __device__ void predict_token(const float* row, int64_t t, int N, int r, const P
                     zz += (double)u[j];      // B = identity (full-rank predictor)
                 }
             }
-            if (o.logits_out) o.logits_out[t * N + j] = (float)p;
+            if (lrow) lrow[j] = (float)p;
             z[v] = (float)zz;
             key[v] = orderable(z[v]);
         }
@@ -239,6 +265,7 @@ struct DiagOut {
     int* overlap;                  // [T] |recorded ∩ current top-k| or null
     float* kl;                     // [T] KL(softmax(p) || softmax(z_ref)) or null
     unsigned long long* hist;      // [k + 1] tokens per deviation k - overlap, or null
+    float* p_out;                  // [T, N] the current logits p, or null
 };
 
 struct ReplayOut {
@@ -277,8 +304,10 @@ __device__ void diag_token(const float* row, int64_t t, int N, const ReplayOut& 
         if (j < N) {
             p[v] = (float)((double)row[j] + (o.b_r ? (double)o.b_r[j] : 0.0));
             key[v] = orderable(p[v]);
+            if (g.p_out) g.p_out[t * N + j] = p[v];
         }
     }
+    if (!(g.cur_idx || g.overlap || g.kl || g.hist)) return;
     float pmax;
     const uint32_t taken = select_topk(key, nv, N, o.k, pmax);
     if (g.cur_idx) write_route(taken, nv, g.cur_idx, o.idx_dtype, t * o.k, nullptr, nullptr, 1.0f);
@@ -330,7 +359,8 @@ __device__ void diag_token(const float* row, int64_t t, int N, const ReplayOut& 
 // One wavefront: replay weights of token t over its recorded ids from the LDS
 // row of N current-router logits (predictor bypassed).
 __device__ void replay_token(const float* row, int64_t t, int N, const ReplayOut& o) {
-    if (o.diag.cur_idx || o.diag.overlap || o.diag.kl || o.diag.hist) diag_token(row, t, N, o);
+    if (o.diag.cur_idx || o.diag.overlap || o.diag.kl || o.diag.hist || o.diag.p_out)
+        diag_token(row, t, N, o);
     if (!o.gate_out) return;
     const int lane = threadIdx.x & 63;
     auto logit = [&](int j) {
@@ -632,17 +662,19 @@ bool router_mfma_ok(const pr2_moe_desc& d, int NC) {
 hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const float* W_r,
                                 const float* b_r, const float* A, const float* B, void* idx_out,
                                 int64_t ldi, float* gate_out, float* logits_out, void* split_ws,
-                                hipStream_t s) {
+                                hipStream_t s, const FeatureCache& cache) {
     const float* Bn = d.r > 0 ? B : nullptr;
-    if (logits_out == nullptr && router_mfma_ok(d, d.N)) {
+    if (logits_out == nullptr && cache.row == nullptr && router_mfma_ok(d, d.N)) {
         // the router logits are not wanted: fold the predictor into the weights
-        PredictOut o{b_r, Bn, d.k, d.renorm, 1, idx_out, d.idx_dtype, ldi, gate_out, nullptr};
+        PredictOut o{b_r, Bn, d.k, d.renorm, 1, idx_out, d.idx_dtype, ldi, gate_out, nullptr,
+                     FeatureCache{}, x, d.d, d.act_dtype};
         hipError_t e = launch_split(W_r, A, Bn, d, d.r, 1, (bf16_t*)split_ws, s);
         if (e != hipSuccess) return e;
         LaunchScope scope("route_predict", s);
         return launch_router_mfma<0>(d, d.N, d.r, x, (const bf16_t*)split_ws, o, ReplayOut{}, s);
     }
-    PredictOut o{b_r, Bn, d.k, d.renorm, 0, idx_out, d.idx_dtype, ldi, gate_out, logits_out};
+    PredictOut o{b_r, Bn, d.k, d.renorm, 0, idx_out, d.idx_dtype, ldi, gate_out, logits_out, cache,
+                 x, d.d, d.act_dtype};
     const int NC = d.N + d.r;
     if (router_mfma_ok(d, NC)) {
         hipError_t e = launch_split(W_r, A, Bn, d, d.r, 0, (bf16_t*)split_ws, s);
@@ -716,6 +748,14 @@ hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void*
     return launch_router_replay(d, x, W_r, o, split_ws, "replay_gates", s);
 }
 
+hipError_t launch_router_logits(const pr2_moe_desc& d, const void* x, const float* W_r,
+                                const float* b_r, float* p_out, void* split_ws, hipStream_t s) {
+    DiagOut g{};
+    g.p_out = p_out;
+    ReplayOut o{b_r, d.k, 1, nullptr, d.idx_dtype, d.k, nullptr, nullptr, 0, g};
+    return launch_router_replay(d, x, W_r, o, split_ws, "router_logits", s);
+}
+
 hipError_t launch_route_diagnostics(const pr2_moe_desc& d, const void* x, const void* idx,
                                     int64_t ldi, const float* W_r, const float* b_r,
                                     const float* z_ref, void* cur_idx, int* overlap, float* kl,
@@ -728,7 +768,7 @@ hipError_t launch_route_diagnostics(const pr2_moe_desc& d, const void* x, const 
     }
     if (d.T == 0) return hipSuccess;
     ReplayOut o{b_r, d.k, 1, idx, d.idx_dtype, ldi, nullptr, nullptr, 0,
-                DiagOut{z_ref, cur_idx, overlap, kl, hist}};
+                DiagOut{z_ref, cur_idx, overlap, kl, hist, nullptr}};
     return launch_router_replay(d, x, W_r, o, split_ws, "route_diagnostics", s);
 }
 

@@ -202,3 +202,65 @@ def test_workspace_grows_with_tokens():
     # H [T*k, m] and O [T*k, d] in bf16 dominate
     d = desc(T=16384, d=2048, N=128, k=8, m=768)
     assert B.workspace_bytes(d, B.OP_REPLAY_FWD) >= 16384 * 8 * (768 + 2048) * 2
+
+
+# ------------------------------------------------ feature cache (host) ----
+
+@pytest.mark.parametrize("T,Tc,seed", [(16384, 2048, 0), (16384, 2048, 12345), (1000, 7, 1),
+                                       (1000, 999, 2**64 - 1), (50, 64, 3), (1, 1, 9),
+                                       (2**20 + 3, 4096, 2**63 + 11)])
+def test_feature_cache_positions_match_oracle(T, Tc, seed):
+    """The library's sampler (host C) and the oracle's (Python integers) draw
+    the same positions: both implement the same stratified rule with
+    SplitMix64."""
+    import numpy as np
+    from oracle import pr2_oracle as O
+    got = B.feature_cache_positions(T, Tc, seed)
+    np.testing.assert_array_equal(got, O.feature_cache_positions(T, Tc, seed))
+
+
+def test_feature_cache_positions_rejects_bad_arguments():
+    L = B.lib()
+    assert L.pr2_feature_cache_positions(-1, 4, 0, None) == -1
+    assert L.pr2_feature_cache_positions(10, 0, 0, None) == -1
+    assert L.pr2_feature_cache_positions(10, 4, 0, None) == -1
+    assert "NULL" in L.pr2_last_error().decode()
+    assert L.pr2_feature_cache_positions(0, 4, 0, None) == 0
+
+
+def test_cached_route_and_predictor_loss_reject_bad_arguments():
+    L = B.lib()
+    d = desc()
+    ws = B.workspace_bytes(d, B.OP_ROUTE)
+
+    def cached(dd=d, row=FAKE, h=FAKE, p=FAKE, rows=16, x=FAKE):
+        st = L.pr2_route_predict_cached(byref(dd), c_void_p(x), c_void_p(FAKE), None,
+                                        c_void_p(FAKE), c_void_p(FAKE), c_void_p(FAKE), dd.k, None,
+                                        c_void_p(row), c_void_p(h), c_void_p(p), rows,
+                                        c_void_p(FAKE), ws, None)
+        return B.STATUS[st]
+    assert cached(row=0) == "PR2_ERR_NULL"
+    assert cached(h=0) == "PR2_ERR_NULL"
+    assert cached(h=FAKE + 4) == "PR2_ERR_ALIGN"
+    assert cached(rows=-1) == "PR2_ERR_SHAPE"
+    assert cached(x=0) == "PR2_ERR_NULL"
+
+    def loss(dd=d, kind=0, step=2, A=FAKE, Bm=FAKE, dB=FAKE, loss_out=FAKE, h=FAKE, ws_bytes=None):
+        wb = B.workspace_bytes(dd, B.OP_PREDICTOR_LOSS) if ws_bytes is None else ws_bytes
+        st = L.pr2_predictor_loss(byref(dd), c_void_p(h), c_void_p(FAKE), None, c_void_p(FAKE),
+                                  c_void_p(FAKE), c_void_p(A), c_void_p(Bm), kind, step, None,
+                                  c_void_p(loss_out), c_void_p(FAKE), c_void_p(dB),
+                                  c_void_p(FAKE), wb, None)
+        return B.STATUS[st]
+    assert B.workspace_bytes(d, B.OP_PREDICTOR_LOSS) > 0
+    assert B.workspace_bytes(desc(r=0), B.OP_PREDICTOR_LOSS) == 0
+    assert loss(desc(r=0)) == "PR2_ERR_SHAPE"
+    assert loss(kind=2) == "PR2_ERR_SHAPE"
+    assert loss(step=0) == "PR2_ERR_SHAPE"
+    assert loss(A=0) == "PR2_ERR_NULL"
+    assert loss(Bm=0) == "PR2_ERR_NULL"            # r != N: B required
+    assert loss(dB=0) == "PR2_ERR_NULL"
+    assert loss(loss_out=0) == "PR2_ERR_NULL"
+    assert loss(h=0) == "PR2_ERR_NULL"
+    assert loss(ws_bytes=1) == "PR2_ERR_WORKSPACE"
+    assert loss(desc(r=8), Bm=0, dB=0) in ("PR2_ERR_DEVICE", "PR2_OK")   # identity, r == N
