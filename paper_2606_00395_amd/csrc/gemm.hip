@@ -12,9 +12,11 @@
 // in flight while one is consumed), 16-byte chunks XOR-swizzled per row so the
 // MFMA operand reads are free of bank conflicts.
 // Eight wavefronts (two per SIMD) in a 4 x 2 arrangement each own 64 rows x 128
-// panel rows as 2 x 4 tiles of v_mfma_f32_32x32x16_bf16 (fp32 accumulation);
+// panel rows as 4 x 8 tiles of v_mfma_f32_16x16x32_bf16 (fp32 accumulation;
+// it issues about 9 % faster than the 32x32x16 form on gfx950 and gives the
+// same sums);
 // operand fragments are double-buffered in registers so the LDS reads of one
-// K=16 step overlap the MFMAs of the previous one; a wavefront whose rows are
+// K=32 step overlap the MFMAs of the previous one; a wavefront whose rows are
 // all past the end of a partial tile skips its MFMAs.
 // GEMM1's epilogue applies SwiGLU in registers (gate and up tiles of the same
 // columns live in the same lanes) and rounds H to bf16; GEMM2's epilogue scales
@@ -38,14 +40,37 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int BM = kTileM;      // 256 rows per tile
 constexpr int BP = 256;         // weight panel rows per tile
-constexpr int BK = 64;          // K slice: 128 bytes per row
+constexpr int BK = 64;          // K slice: 128 bytes per row (32 and 64 supported)
 constexpr int ROWB = BK * 2;    // bytes per LDS row (unpadded; chunks are swizzled)
 constexpr int CHUNKS = ROWB / 16;   // 16-byte chunks per row
-constexpr int NSTAGE = 2;       // LDS stages: slice kt+1 in flight during slice kt
+constexpr int NSTAGE = 2;       // LDS stages: slices kt+1 .. kt+NSTAGE-1 in flight during slice kt
 constexpr int WM = 64;          // token rows per wavefront
 constexpr int WN = 128;         // panel rows per wavefront
-constexpr int MI = WM / 32;     // 32x32 MFMA tiles per wavefront, token direction
-constexpr int NJ = WN / 32;     // 32x32 MFMA tiles per wavefront, panel direction
+constexpr int MT = 16;          // MFMA tile edge: 16 (16x16x32, faster here) or 32 (32x32x16)
+constexpr int MK = 512 / MT;    // K per MFMA
+constexpr int NKS = BK / MK;    // MFMA K sub-steps per slice
+constexpr int ACCN = MT * MT / 64;  // accumulators per lane per tile
+constexpr int MI = WM / MT;     // MFMA tiles per wavefront, token direction
+constexpr int NJ = WN / MT;     // MFMA tiles per wavefront, panel direction
+template <int E> struct MfmaOp;
+template <> struct MfmaOp<32> {
+    typedef f32x16 acc_t;
+    __device__ __forceinline__ static acc_t run(bf16x8 a, bf16x8 b, acc_t c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+    }
+};
+template <> struct MfmaOp<16> {
+    typedef f32x4 acc_t;
+    __device__ __forceinline__ static acc_t run(bf16x8 a, bf16x8 b, acc_t c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    }
+};
+typedef MfmaOp<MT>::acc_t accv;
+static_assert(sizeof(accv) == ACCN * sizeof(float), "accumulator size");
+
+__device__ __forceinline__ accv mfma_bf16(bf16x8 a, bf16x8 b, accv c) {
+    return MfmaOp<MT>::run(a, b, c);
+}
 constexpr int NWAVE = (BM / WM) * (BP / WN);
 constexpr int kGemmThreads = 64 * NWAVE;
 constexpr int kNumXcd = 8;
@@ -80,7 +105,7 @@ __device__ __forceinline__ float silu_f(float a) {
 // 8) consecutive rows read at the same chunk hit disjoint banks.  swz depends
 // on r % 16 only.
 __device__ __forceinline__ int swz(int r) {
-    return CHUNKS == 8 ? (r & 7) ^ ((r >> 3) & 1) : (r >> 2) & 3;
+    return CHUNKS == 8 ? (r & 7) ^ ((r >> 3) & 1) : ((r >> 1) ^ (r >> 2)) & 3;
 }
 
 // wait until at most n of this wavefront's global loads are outstanding
@@ -116,13 +141,13 @@ grouped_gemm_mfma(MfmaArgs g) {
     const int wc = wave % (BP / WN);     // panel block of WN rows
     // a wavefront whose rows are all past the tile's end only helps copy
     const bool active = wr * WM < rows;
-    // each lane's accumulators belong to MI token rows (one per 32-row block);
+    // each lane's accumulators belong to MI token rows (one per MT-row block);
     // GEMM2's route weights for them are fetched now, long before the epilogue
     float gw[MI];
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
         gw[i] = 0.0f;
-        const int r = wr * WM + i * 32 + (lane & 31);
+        const int r = wr * WM + i * MT + (lane % MT);
         if (MODE == 1 && r < rows) gw[i] = g.gate[min(max(g.perm_src[row0 + r], 0), g.Tk - 1)];
     }
 
@@ -164,41 +189,47 @@ grouped_gemm_mfma(MfmaArgs g) {
         }
     };
 
-    f32x16 acc[MI][NJ];
+    accv acc[MI][NJ];
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < NJ; ++j)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+            for (int v = 0; v < ACCN; ++v) acc[i][j][v] = 0.0f;
 
-    // LDS reads for the MFMA operands: lane l reads row (block base + l%32) at
-    // 16-byte position (2*ks + l/32) ^ swz(l%32); block bases are multiples of
-    // 32 rows, so the swizzle is the same for every fragment of the lane.
-    const int lrow = lane & 31;
+    // LDS reads for the MFMA operands: lane l reads row (block base + l%MT),
+    // the 16 bytes of K values MK*ks + 8*(l/MT) .. +7, i.e. chunk
+    // (MK/8)*ks + l/MT, at position chunk ^ swz(row); block bases are
+    // multiples of 16 rows, so the swizzle is the same for every fragment.
+    const int lrow = lane % MT;
     const int sw = swz(lrow);
-    int kpos[BK / 16];
+    int kpos[NKS];
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) kpos[ks] = lrow * ROWB + (((2 * ks + (lane >> 5)) ^ sw) << 4);
+    for (int ks = 0; ks < NKS; ++ks)
+        kpos[ks] = lrow * ROWB + ((((MK / 8) * ks + lane / MT) ^ sw) << 4);
     int a_base[MI], b_base[NJ];
 #pragma unroll
-    for (int i = 0; i < MI; ++i) a_base[i] = (wr * WM + i * 32) * ROWB;
+    for (int i = 0; i < MI; ++i) a_base[i] = (wr * WM + i * MT) * ROWB;
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
         int prow;
-        if (MODE != 1) prow = (j < NJ / 2 ? 0 : 128) + wc * (WN / 2) + (j % (NJ / 2)) * 32;
-        else prow = wc * WN + j * 32;
+        if (MODE != 1) prow = (j < NJ / 2 ? 0 : 128) + wc * (WN / 2) + (j % (NJ / 2)) * MT;
+        else prow = wc * WN + j * MT;
         b_base[j] = (BM + prow) * ROWB;
     }
 
     const int nk = g.K / BK;
-    issue(0, 0);
+#pragma unroll
+    for (int st = 0; st < NSTAGE - 1; ++st)
+        if (st < nk) issue(st, st * BK);
     for (int kt = 0; kt < nk; ++kt) {
-        // slice kt landed and every wavefront is done with slice kt-1, whose
-        // stage is refilled next
-        wait_vmcnt<0>();
+        // slice kt landed (the copies of the later slices may still be in
+        // flight) and every wavefront is done with slice kt-1, whose stage is
+        // refilled next
+        if (kt + NSTAGE - 2 < nk) wait_vmcnt<(NSTAGE - 2) * kGroups>();
+        else wait_vmcnt<0>();
         __syncthreads();
-        if (kt + 1 < nk) issue((kt + 1) % NSTAGE, (kt + 1) * BK);
+        if (kt + NSTAGE - 1 < nk) issue((kt + NSTAGE - 1) % NSTAGE, (kt + NSTAGE - 1) * BK);
         if (active) {
             // fragments double-buffered in registers: the reads for sub-step
             // ks+1 are in flight while the MFMAs of sub-step ks run
@@ -214,16 +245,15 @@ grouped_gemm_mfma(MfmaArgs g) {
             };
             read_frags(0, 0);
 #pragma unroll
-            for (int ks = 0; ks < BK / 16; ++ks) {
-                if (ks + 1 < BK / 16) read_frags((ks + 1) & 1, ks + 1);
+            for (int ks = 0; ks < NKS; ++ks) {
+                if (ks + 1 < NKS) read_frags((ks + 1) & 1, ks + 1);
                 // keep the scheduler from sinking those reads below the MFMAs
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int i = 0; i < MI; ++i)
 #pragma unroll
                     for (int j = 0; j < NJ; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            fb[ks & 1][j], fa[ks & 1][i], acc[i][j], 0, 0, 0);
+                        acc[i][j] = mfma_bf16(fb[ks & 1][j], fa[ks & 1][i], acc[i][j]);
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
@@ -231,21 +261,24 @@ grouped_gemm_mfma(MfmaArgs g) {
     if (!active) return;
 
     // Epilogue.  The MFMA computed the transposed tile (weights x tokens), so
-    // accumulator element v of lane l is output column 8*(v/4) + 4*(l/32) + v%4
-    // of token row l%32 of the 32-row block: four consecutive bf16 per lane,
-    // stored as one 8-byte write.
-    const int ncol0 = 4 * (lane >> 5);
+    // accumulator element v of lane l is, for 32x32 tiles, output column
+    // 8*(v/4) + 4*(l/32) + v%4 of token row l%32, and for 16x16 tiles, column
+    // 4*(l/16) + v of token row l%16: runs of four consecutive bf16 per lane,
+    // each stored as one 8-byte write.
+    const int ncol0 = 4 * (lane / MT);
+    constexpr int NA4 = ACCN / 4;           // runs of four per tile
+    constexpr int A4STEP = MT == 32 ? 8 : 0;
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
-        const int r = wr * WM + i * 32 + (lane & 31);
+        const int r = wr * WM + i * MT + (lane % MT);
         if (r >= rows) continue;
         bf16_t* orow = g.out + ((int64_t)row0 + r) * g.n_out;
         if (MODE == 0) {
 #pragma unroll
             for (int j = 0; j < NJ / 2; ++j) {
-                const int col = pn * 128 + wc * (WN / 2) + j * 32 + ncol0;
+                const int col = pn * 128 + wc * (WN / 2) + j * MT + ncol0;
 #pragma unroll
-                for (int a4 = 0; a4 < 4; ++a4) {
+                for (int a4 = 0; a4 < NA4; ++a4) {
                     uint32_t w[2];
 #pragma unroll
                     for (int h = 0; h < 2; ++h) {
@@ -254,16 +287,16 @@ grouped_gemm_mfma(MfmaArgs g) {
                         const float h1 = silu_f(acc[i][j][v0 + 1]) * acc[i][j + NJ / 2][v0 + 1];
                         w[h] = (uint32_t)f32_to_bf16(h0) | ((uint32_t)f32_to_bf16(h1) << 16);
                     }
-                    *(uint2*)(orow + col + 8 * a4) = make_uint2(w[0], w[1]);
+                    *(uint2*)(orow + col + A4STEP * a4) = make_uint2(w[0], w[1]);
                 }
             }
         } else if (MODE == 2) {
             // pre-activations for the backward pass: a at column col, u at m + col
 #pragma unroll
             for (int j = 0; j < NJ / 2; ++j) {
-                const int col = pn * 128 + wc * (WN / 2) + j * 32 + ncol0;
+                const int col = pn * 128 + wc * (WN / 2) + j * MT + ncol0;
 #pragma unroll
-                for (int a4 = 0; a4 < 4; ++a4) {
+                for (int a4 = 0; a4 < NA4; ++a4) {
 #pragma unroll
                     for (int half = 0; half < 2; ++half) {
                         const int jj = j + half * (NJ / 2);
@@ -272,16 +305,16 @@ grouped_gemm_mfma(MfmaArgs g) {
                                             ((uint32_t)f32_to_bf16(acc[i][jj][v0 + 1]) << 16);
                         const uint32_t w1 = (uint32_t)f32_to_bf16(acc[i][jj][v0 + 2]) |
                                             ((uint32_t)f32_to_bf16(acc[i][jj][v0 + 3]) << 16);
-                        *(uint2*)(orow + half * (g.n_out / 2) + col + 8 * a4) = make_uint2(w0, w1);
+                        *(uint2*)(orow + half * (g.n_out / 2) + col + A4STEP * a4) = make_uint2(w0, w1);
                     }
                 }
             }
         } else {
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
-                const int col = pn * BP + wc * WN + j * 32 + ncol0;
+                const int col = pn * BP + wc * WN + j * MT + ncol0;
 #pragma unroll
-                for (int a4 = 0; a4 < 4; ++a4) {
+                for (int a4 = 0; a4 < NA4; ++a4) {
                     uint32_t w[2];
 #pragma unroll
                     for (int h = 0; h < 2; ++h) {
@@ -289,7 +322,7 @@ grouped_gemm_mfma(MfmaArgs g) {
                         w[h] = (uint32_t)f32_to_bf16(gw[i] * acc[i][j][v0]) |
                                ((uint32_t)f32_to_bf16(gw[i] * acc[i][j][v0 + 1]) << 16);
                     }
-                    *(uint2*)(orow + col + 8 * a4) = make_uint2(w[0], w[1]);
+                    *(uint2*)(orow + col + A4STEP * a4) = make_uint2(w[0], w[1]);
                 }
             }
         }

@@ -60,20 +60,28 @@ __device__ __forceinline__ int wave_incl_scan(int x) {
     return x;
 }
 
+// Exclusive prefix sum over the workgroup's threads: a DPP scan inside each
+// wavefront, then one scan of the wavefront totals (three barriers).  sh needs
+// kScanThreads / 64 + 1 ints.
 __device__ int block_exclusive_scan(int v, int* sh, int* total) {
+    constexpr int kWaves = kScanThreads / 64;
     const int tid = threadIdx.x;
-    sh[tid] = v;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int incl = wave_incl_scan(v);
+    if (lane == 63) sh[wave] = incl;
     __syncthreads();
-    for (int off = 1; off < kScanThreads; off <<= 1) {
-        int add = tid >= off ? sh[tid - off] : 0;
-        __syncthreads();
-        sh[tid] += add;
-        __syncthreads();
+    if (wave == 0) {
+        const int w = lane < kWaves ? sh[lane] : 0;
+        const int wi = wave_incl_scan(w);
+        if (lane < kWaves) sh[lane] = wi - w;
+        if (lane == kWaves - 1) sh[kWaves] = wi;
     }
-    int incl = sh[tid];
-    *total = sh[kScanThreads - 1];
     __syncthreads();
-    return incl - v;
+    const int res = sh[wave] + incl - v;
+    *total = sh[kWaves];
+    __syncthreads();
+    return res;
 }
 
 // counts: [N * nblk] expert-major; rewritten in place with each block's first
@@ -251,9 +259,11 @@ perm_scatter_kernel(const void* idx, int idx_dtype, int64_t ldi, int64_t T, int 
     }
 }
 
-// bf16, d % 8 == 0: each thread owns 8 consecutive columns of TPI tokens per
-// iteration, so TPI*k independent 16-byte loads are in flight per thread
+// bf16, d % 8 == 0: each thread owns 8 consecutive columns of kCombTok tokens
+// per iteration and issues the loads of kCombSlots route slots of each before
+// summing them, so up to kCombTok * kCombSlots 16-byte loads are in flight
 constexpr int kCombTok = 2;
+constexpr int kCombSlots = 8;   // route slots whose loads are in flight together
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __global__ void __launch_bounds__(256)
@@ -266,24 +276,38 @@ combine_bf16_kernel(const bf16_t* O, const int* inv, int64_t ntok, int k, int d,
             for (int u = 0; u < kCombTok; ++u)
 #pragma unroll
                 for (int v = 0; v < 8; ++v) acc[u][v] = 0.0f;
-            for (int s = 0; s < k; ++s) {
-                u32x4 raw[kCombTok];
+            // slots in groups of kCombSlots: all their row indices, then all
+            // their loads are issued before the first is consumed; the sum
+            // still runs in slot order
+            for (int s0 = 0; s0 < k; s0 += kCombSlots) {
+                int r[kCombTok][kCombSlots];
 #pragma unroll
-                for (int u = 0; u < kCombTok; ++u) {
-                    const int64_t t = t0 + u;
-                    const int r = t < ntok ? inv[t * k + s] : -1;
-                    raw[u] = r >= 0 ? __builtin_nontemporal_load((const u32x4*)(O + (int64_t)r * d + c0))
-                                    : u32x4{0, 0, 0, 0};
-                }
+                for (int u = 0; u < kCombTok; ++u)
 #pragma unroll
-                for (int u = 0; u < kCombTok; ++u) {
-                    const uint32_t w[4] = {raw[u][0], raw[u][1], raw[u][2], raw[u][3]};
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        acc[u][2 * v] += __uint_as_float(w[v] << 16);
-                        acc[u][2 * v + 1] += __uint_as_float(w[v] & 0xffff0000u);
+                    for (int j = 0; j < kCombSlots; ++j) {
+                        const int64_t t = t0 + u;
+                        r[u][j] = (t < ntok && s0 + j < k) ? inv[t * k + s0 + j] : -1;
                     }
-                }
+                u32x4 raw[kCombTok][kCombSlots];
+#pragma unroll
+                for (int u = 0; u < kCombTok; ++u)
+#pragma unroll
+                    for (int j = 0; j < kCombSlots; ++j)
+                        raw[u][j] = r[u][j] >= 0
+                            ? __builtin_nontemporal_load((const u32x4*)(O + (int64_t)r[u][j] * d + c0))
+                            : u32x4{0, 0, 0, 0};
+#pragma unroll
+                for (int j = 0; j < kCombSlots; ++j)
+#pragma unroll
+                    for (int u = 0; u < kCombTok; ++u) {
+                        if (r[u][j] < 0) continue;
+                        const uint32_t w[4] = {raw[u][j][0], raw[u][j][1], raw[u][j][2], raw[u][j][3]};
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) {
+                            acc[u][2 * v] += __uint_as_float(w[v] << 16);
+                            acc[u][2 * v + 1] += __uint_as_float(w[v] & 0xffff0000u);
+                        }
+                    }
             }
 #pragma unroll
             for (int u = 0; u < kCombTok; ++u) {

@@ -13,7 +13,10 @@
 // K-tiled ([K/32][3 * columns][32] bf16) so that every K-step reads one
 // contiguous block.  A workgroup of 8 wavefronts owns 64 tokens; each
 // wavefront computes 32 tokens x a quarter of the columns with
-// v_mfma_f32_16x16x32_bf16.
+// v_mfma_f32_16x16x32_bf16.  Token rows and weight rows of a K step are copied
+// straight from global memory into LDS (16-byte copies, 64-byte rows with
+// XOR-swizzled chunks), three or four steps deep, so the copies of later steps
+// are in flight while one step is consumed.
 //
 // fp64 vector path (fp32 x or other shapes): each thread accumulates a 4-token
 // x 4-column micro-tile in fp64 from LDS-staged slices.
@@ -451,11 +454,11 @@ replay_gates_kernel(ProjArgs a, ReplayOut o) {
 // ---------------------------------------------------------- MFMA path -----
 constexpr int kRTM = 64;                  // tokens per workgroup
 constexpr int kRBK = 32;                  // K step
-constexpr int kRStride = kRBK + 8;        // bf16 per LDS row (16 B pad)
 constexpr int kRThreads = 512;            // 8 wavefronts: 2 token halves x 4 column quarters
 constexpr int kRMaxNTW = 3;               // 16-column tiles per wavefront (<= 192 columns)
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
 
 // Ws[kt][p * NCp + c][kk] = part p of column c at K index kt*32 + kk (zero for c >= NC).
 // Columns: folded -> W_r + A B (or W_r + A when B is null); else [W_r | A].
@@ -498,44 +501,71 @@ router_split_kernel(const float* W_r, const float* A, const float* B, int d, int
     }
 }
 
+// 16-byte chunk c of a 64-byte LDS row r sits at position c ^ rswz(r): 16
+// consecutive rows read at one chunk hit 16 different 16-byte bank groups.
+__device__ __forceinline__ int rswz(int r) { return ((r >> 1) ^ (r >> 2)) & 3; }
+
+template <int n>
+__device__ __forceinline__ void router_wait_vmcnt() {
+    static_assert(n >= 0 && n < 16, "vmcnt field");
+    __builtin_amdgcn_s_waitcnt(0x0f70 | n);
+}
+
+template <int NTW>
+struct RouterTile {
+    static constexpr int NCp = 64 * NTW;
+    static constexpr int ROWS = kRTM + 3 * NCp;          // x rows, then hi | mid | lo weight rows
+    static constexpr int STAGEB = ROWS * 64;             // one K step of 32 bf16 per row
+    static constexpr int NSTAGE = NTW <= 2 ? 4 : 3;      // K steps in flight: NSTAGE - 1
+    static constexpr int GROUPS = ROWS / 16;             // 1 KiB copies (16 rows) per stage
+    static constexpr int GPW = (GROUPS + 7) / 8;         // copies per wavefront (uniform)
+};
+
 template <int NTW, int MODE>   // MODE 0: rollout, 1: replay
 __global__ void __launch_bounds__(kRThreads)
 router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, int r, int NC,
                    PredictOut po, ReplayOut ro) {
-    constexpr int NCp = 64 * NTW;
-    constexpr int WROWS = 3 * NCp;
-    constexpr int WCH = (WROWS * 4 + kRThreads - 1) / kRThreads;
-    __shared__ __attribute__((aligned(16))) bf16_t xs[2][kRTM * kRStride];
-    __shared__ __attribute__((aligned(16))) bf16_t wsb[2][WROWS * kRStride];
-    static_assert(sizeof(bf16_t) * 2 * WROWS * kRStride >= sizeof(float) * kRTM * NCp,
-                  "logit tile must fit over the weight buffers");
+    using RT = RouterTile<NTW>;
+    constexpr int NCp = RT::NCp;
+    constexpr int NSTAGE = RT::NSTAGE;
+    constexpr int GPW = RT::GPW;
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[NSTAGE * RT::STAGEB];
+    static_assert(NSTAGE * RT::STAGEB >= (int)sizeof(float) * kRTM * NCp,
+                  "logit tile must fit over the copy stages");
     const int64_t t0 = (int64_t)blockIdx.x * kRTM;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int wr = wave >> 2, wc = wave & 3;
 
-    // copies: x 64 rows x 4 chunks (threads 0..255); weights WROWS x 4 chunks, contiguous
-    const int xr = (tid & 255) >> 2, xc = tid & 3;
-    const bool x_thread = tid < 256;
-    const bool x_ok = x_thread && t0 + xr < T;
-    const bf16_t* xsrc = x + (x_ok ? (t0 + xr) : 0) * (int64_t)d + xc * 8;
-    u32x4 rx, rw[WCH];
-    auto load_global = [&](int kt) {
-        rx = x_ok ? *(const u32x4*)(xsrc + kt * kRBK) : u32x4{0, 0, 0, 0};
-        const bf16_t* wk = Ws + (int64_t)kt * WROWS * kRBK;
+    // Copies straight into LDS, 16 bytes per lane: copy slot i of wavefront w
+    // moves 16-row group g = w + 8 i (groups past the end repeat the last
+    // groups: the same bytes to the same place), lane l row 16 g + l/4 at
+    // position l%4.  Rows below kRTM are tokens (past T: the last token, never
+    // written out); the rest are the K-tiled split weights of the step.
+    const bf16_t* src[GPW];
+    int dst[GPW];
 #pragma unroll
-        for (int i = 0; i < WCH; ++i) {
-            int q = tid + kRThreads * i;
-            if (q < WROWS * 4) rw[i] = *(const u32x4*)(wk + q * 8);
+    for (int i = 0; i < GPW; ++i) {
+        int g = wave + 8 * i;
+        if (g >= RT::GROUPS) g = RT::GROUPS - 1 - (g - RT::GROUPS) % 8;
+        const int row = g * 16 + (lane >> 2);
+        const int chunk = (lane & 3) ^ rswz(row);
+        if (row < kRTM) {
+            const int64_t t = t0 + row < T ? t0 + row : T - 1;
+            src[i] = x + t * (int64_t)d + chunk * 8;          // + kt * 32 per step
+        } else {
+            src[i] = Ws + (int64_t)(row - kRTM) * kRBK + chunk * 8;   // + kt * 3 NCp * 32
         }
-    };
-    auto store_lds = [&](int b) {
-        if (x_thread) *(u32x4*)&xs[b][xr * kRStride + xc * 8] = rx;
+        dst[i] = g * 1024;
+    }
+    auto issue = [&](int stage, int kt) {
 #pragma unroll
-        for (int i = 0; i < WCH; ++i) {
-            int q = tid + kRThreads * i;
-            if (q < WROWS * 4) *(u32x4*)&wsb[b][(q >> 2) * kRStride + (q & 3) * 8] = rw[i];
+        for (int i = 0; i < GPW; ++i) {
+            const int64_t step = dst[i] < kRTM * 64 ? (int64_t)kt * kRBK
+                                                     : (int64_t)kt * 3 * NCp * kRBK;
+            __builtin_amdgcn_global_load_lds((const void*)(src[i] + step),
+                                             (lds_void*)&lds[stage * RT::STAGEB + dst[i]], 16, 0, 0);
         }
     };
 
@@ -548,25 +578,33 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
 #pragma unroll
             for (int v = 0; v < 4; ++v) { acc[i][t][v] = 0.0f; acc64[i][t][v] = 0.0; }
 
+    // MFMA operand reads: lane l reads row (base + l%16), chunk l/16
     const int lrow = lane & 15;
-    const int lk = (lane >> 4) * 8;
+    const int lch = lane >> 4;
     const int nk = d / kRBK;
-    load_global(0);
-    store_lds(0);
-    __syncthreads();
+#pragma unroll
+    for (int st = 0; st < NSTAGE - 1; ++st)
+        if (st < nk) issue(st, st);
     for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
-        if (kt + 1 < nk) load_global(kt + 1);
+        // step kt landed (later steps may be in flight) and every wavefront is
+        // done with step kt-1, whose stage is refilled next
+        if (kt + NSTAGE - 2 < nk) router_wait_vmcnt<(NSTAGE - 2) * GPW>();
+        else router_wait_vmcnt<0>();
+        __syncthreads();
+        if (kt + NSTAGE - 1 < nk) issue((kt + NSTAGE - 1) % NSTAGE, kt + NSTAGE - 1);
+        const unsigned char* base = lds + (kt % NSTAGE) * RT::STAGEB;
         bf16x8 fa[2];
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
-            fa[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)&xs[cur][(wr * 32 + i * 16 + lrow) * kRStride + lk]);
+        for (int i = 0; i < 2; ++i) {
+            const int row = wr * 32 + i * 16 + lrow;
+            fa[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + row * 64 + ((lch ^ rswz(row)) << 4)));
+        }
 #pragma unroll
         for (int t = 0; t < NTW; ++t) {
 #pragma unroll
             for (int p = 0; p < 3; ++p) {
-                const int wrow = p * NCp + (wc * NTW + t) * 16 + lrow;
-                bf16x8 fb = __builtin_bit_cast(bf16x8, *(const u32x4*)&wsb[cur][wrow * kRStride + lk]);
+                const int row = kRTM + p * NCp + (wc * NTW + t) * 16 + lrow;
+                bf16x8 fb = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + row * 64 + ((lch ^ rswz(row)) << 4)));
 #pragma unroll
                 for (int i = 0; i < 2; ++i)
                     acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb, acc[i][t], 0, 0, 0);
@@ -583,11 +621,10 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
                         acc[i][t][v] = 0.0f;
                     }
         }
-        if (kt + 1 < nk) store_lds(cur ^ 1);
-        __syncthreads();
     }
+    __syncthreads();
     // logits -> LDS [kRTM][NC]; 16x16 accumulator element v of lane l is C[4*(l/16)+v][l%16]
-    float* lg = (float*)&wsb[0][0];
+    float* lg = (float*)lds;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
