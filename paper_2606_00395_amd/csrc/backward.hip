@@ -51,6 +51,10 @@ struct BwdArgs {
     const int* tiles;        // (expert, first permuted row, rows) per 256-row tile
     const int* tile_count;
     const int* offsets;      // [N+1] first permuted row of each expert
+    const int* order;        // [N] experts by decreasing route count (ties: lower id)
+    const float* dp_perm;    // [T*k] router-logit gradient per permuted row
+    float* dW_r;             // [d, N] (gate/up weight-gradient launch)
+    float* db_r;             // [N] or null
     int k, N, d, m, Tk;
     int ntn;                 // DH, DX: 256-column panels per tile
     const bf16_t* x;
@@ -118,24 +122,17 @@ bwd_gemm(BwdArgs g) {
     __shared__ __attribute__((aligned(1024))) unsigned char lds[LDSB];
     constexpr bool kRowTiles = (MODE == DH || MODE == DX);   // C rows are permuted routes
 
-    // ---- work item (XCD-aware: each XCD takes a contiguous logical range)
-    int64_t L;
+    // ---- work item
     int nct = 1;
-    if (kRowTiles) {
-        L = (int64_t)(*g.tile_count) * g.ntn;
-    } else {
-        const int nrt = MODE == WD ? g.d / BM : 2 * g.m / BM;
-        nct = MODE == WD ? g.m / BN : g.d / BN;
-        L = (int64_t)g.N * nrt * nct;
-    }
-    const int64_t per_xcd = (L + kNumXcd - 1) / kNumXcd;
-    const int64_t local = blockIdx.x / kNumXcd;
-    if (local >= per_xcd) return;
-    const int64_t logical = (int64_t)(blockIdx.x % kNumXcd) * per_xcd + local;
-    if (logical >= L) return;
-
     int expert, row0 = 0, rows = BM, pn = 0, rt = 0, ct = 0, klen;
     if (kRowTiles) {
+        // XCD-aware: XCD b % 8 takes a contiguous range of the (tile, panel) list
+        const int64_t L = (int64_t)(*g.tile_count) * g.ntn;
+        const int64_t per_xcd = (L + kNumXcd - 1) / kNumXcd;
+        const int64_t local = blockIdx.x / kNumXcd;
+        if (local >= per_xcd) return;
+        const int64_t logical = (int64_t)(blockIdx.x % kNumXcd) * per_xcd + local;
+        if (logical >= L) return;
         const int tile = (int)(logical / g.ntn);
         pn = (int)(logical % g.ntn);
         expert = g.tiles[3 * tile + 0];
@@ -143,9 +140,20 @@ bwd_gemm(BwdArgs g) {
         rows = g.tiles[3 * tile + 2];
         klen = MODE == DH ? g.d : 2 * g.m;
     } else {
-        const int per_e = (int)(L / g.N);
-        expert = (int)(logical / per_e);
-        const int tt = (int)(logical % per_e);
+        // Token-contracted: an item's cost grows with its expert's route count.
+        // Experts are dealt to the XCDs round-robin in decreasing count order and
+        // each XCD runs its experts' output tiles biggest first (the dispatcher
+        // starts workgroups in index order), so the busiest experts neither pile
+        // up on one XCD nor start last.
+        const int nrt = MODE == WD ? g.d / BM : 2 * g.m / BM;
+        nct = MODE == WD ? g.m / BN : g.d / BN;
+        const int per_e = nrt * nct;
+        const int xcd = blockIdx.x % kNumXcd;
+        const int local = blockIdx.x / kNumXcd;
+        const int slot = local / per_e;
+        if (xcd + kNumXcd * slot >= g.N) return;
+        expert = g.order[xcd + kNumXcd * slot];
+        const int tt = local % per_e;
         rt = tt / nct;
         ct = tt % nct;
         row0 = g.offsets[expert];
@@ -189,6 +197,15 @@ bwd_gemm(BwdArgs g) {
         }
     }
     u32x4 st[8];
+    // The gate/up weight-gradient items of the first row tile also form the
+    // router gradient from the x rows they stream: dW_r[:, e] = sum_q dp_q x_t(q)
+    // over this item's 256 columns, db_r[e] = sum_q dp_q.
+    const bool rgrad = MODE == WGU && rt == 0 && half == 1;
+    float dpr[8];
+    float racc[8];
+#pragma unroll
+    for (int v = 0; v < 8; ++v) racc[v] = 0.0f;
+    float dbacc = 0.0f;
     auto kload = [&](int kt) {
         const int kb = kt * BK;
         const bool hi = kb >= kr.ksplit;
@@ -198,11 +215,24 @@ bwd_gemm(BwdArgs g) {
         for (int i = 0; i < 8; ++i) {
             const int kk = kb + 8 * kc + i;
             u32x4 v = {0u, 0u, 0u, 0u};
+            dpr[i] = 0.0f;
             if (kk < kr.klen) {
                 const int row = kr.gather ? g.perm_src[kr.rbase + kk] / g.k : kr.rbase + kk - kshift;
                 v = *(const u32x4*)(b + ((uint32_t)row * kr.ld + kr.col));
+                if (rgrad) dpr[i] = g.dp_perm[kr.rbase + kk];
             }
             st[i] = v;
+        }
+    };
+    auto racc_add = [&]() {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                racc[2 * w] = fmaf(dpr[i], bf_lo(st[i][w]), racc[2 * w]);
+                racc[2 * w + 1] = fmaf(dpr[i], bf_hi(st[i][w]), racc[2 * w + 1]);
+            }
+            dbacc += dpr[i];
         }
     };
     auto kstore = [&](int stage) {
@@ -273,6 +303,7 @@ bwd_gemm(BwdArgs g) {
         } else {
             kload(0);
             wait_vmcnt<0>();
+            if (rgrad) racc_add();
             kstore(0);
         }
     }
@@ -311,7 +342,24 @@ bwd_gemm(BwdArgs g) {
         }
         if (more && !dma) {
             wait_vmcnt<0>();
+            if (rgrad) racc_add();
             kstore((kt + 1) % NSTAGE);
+        }
+    }
+    if (rgrad) {
+        // the 8 threads of one 8-column block (consecutive lanes) hold partial
+        // sums over different rows: add them in a fixed butterfly order
+#pragma unroll
+        for (int off = 1; off < 8; off <<= 1) {
+#pragma unroll
+            for (int v = 0; v < 8; ++v) racc[v] += __shfl_xor(racc[v], off, 64);
+            dbacc += __shfl_xor(dbacc, off, 64);
+        }
+        if (kc == 0) {
+#pragma unroll
+            for (int v = 0; v < 8; ++v)
+                g.dW_r[(int64_t)(ct * BN + 8 * rb + v) * g.N + expert] = racc[v];
+            if (g.db_r && ct == 0 && rb == 0) g.db_r[expert] = dbacc;
         }
     }
     if (!active) return;
@@ -396,6 +444,19 @@ bwd_gemm(BwdArgs g) {
                 }
             }
         }
+    }
+}
+
+// Experts by decreasing route count, ties to the lower id (one workgroup).
+__global__ void __launch_bounds__(1024) expert_order_kernel(const int* offsets, int N, int* order) {
+    __shared__ int cnt[kMaxExperts];
+    for (int e = threadIdx.x; e < N; e += blockDim.x) cnt[e] = offsets[e + 1] - offsets[e];
+    __syncthreads();
+    for (int e = threadIdx.x; e < N; e += blockDim.x) {
+        const int c = cnt[e];
+        int rank = 0;
+        for (int f = 0; f < N; ++f) rank += (cnt[f] > c) || (cnt[f] == c && f < e);
+        order[rank] = e;
     }
 }
 
@@ -603,6 +664,74 @@ dx_combine_kernel(const T* dxr, const int* inv, const float* dp_route, const flo
     }
 }
 
+// bf16, d % 8 == 0: each thread owns 8 consecutive columns of kDxTok tokens;
+// per token the k per-route rows are added in slot order, then the router
+// terms dp_ts W_r[:, idx_ts] in slot order (fp32)
+constexpr int kDxTok = 2;
+__global__ void __launch_bounds__(256)
+dx_combine_bf16_kernel(const bf16_t* dxr, const int* inv, const float* dp_route, const float* wrt,
+                       const void* idx, int idx_dtype, int64_t ldi, int64_t T_, int k, int d, int N,
+                       bf16_t* dx) {
+    constexpr int kSlots = 8;
+    const int64_t step = (int64_t)gridDim.x * kDxTok;
+    for (int64_t t0 = (int64_t)blockIdx.x * kDxTok; t0 < T_; t0 += step) {
+        for (int c0 = threadIdx.x * 8; c0 < d; c0 += 256 * 8) {
+            float acc[kDxTok][8];
+#pragma unroll
+            for (int u = 0; u < kDxTok; ++u)
+#pragma unroll
+                for (int v = 0; v < 8; ++v) acc[u][v] = 0.0f;
+            for (int s0 = 0; s0 < k; s0 += kSlots) {
+                int r[kDxTok][kSlots];
+                u32x4 raw[kDxTok][kSlots];
+#pragma unroll
+                for (int u = 0; u < kDxTok; ++u)
+#pragma unroll
+                    for (int j = 0; j < kSlots; ++j) {
+                        const int64_t t = t0 + u;
+                        r[u][j] = (t < T_ && s0 + j < k) ? inv[t * k + s0 + j] : -1;
+                    }
+#pragma unroll
+                for (int u = 0; u < kDxTok; ++u)
+#pragma unroll
+                    for (int j = 0; j < kSlots; ++j)
+                        raw[u][j] = r[u][j] >= 0 ? *(const u32x4*)(dxr + (int64_t)r[u][j] * d + c0)
+                                                 : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+                for (int j = 0; j < kSlots; ++j)
+#pragma unroll
+                    for (int u = 0; u < kDxTok; ++u)
+#pragma unroll
+                        for (int w = 0; w < 4; ++w) {
+                            acc[u][2 * w] += bf_lo(raw[u][j][w]);
+                            acc[u][2 * w + 1] += bf_hi(raw[u][j][w]);
+                        }
+            }
+#pragma unroll
+            for (int u = 0; u < kDxTok; ++u) {
+                const int64_t t = t0 + u;
+                if (t >= T_) continue;
+                for (int s = 0; s < k; ++s) {
+                    const int e = load_id(idx, idx_dtype, t * ldi + s);
+                    if (e < 0 || e >= N) continue;
+                    const float g = dp_route[t * k + s];
+                    const float* wr = wrt + (int64_t)e * d + c0;
+                    const f32x4 w0 = *(const f32x4*)wr;
+                    const f32x4 w1 = *(const f32x4*)(wr + 4);
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        acc[u][v] = fmaf(g, w0[v], acc[u][v]);
+                        acc[u][4 + v] = fmaf(g, w1[v], acc[u][4 + v]);
+                    }
+                }
+                *(uint4*)(dx + t * (int64_t)d + c0) =
+                    make_uint4(pack_bf(acc[u][0], acc[u][1]), pack_bf(acc[u][2], acc[u][3]),
+                               pack_bf(acc[u][4], acc[u][5]), pack_bf(acc[u][6], acc[u][7]));
+            }
+        }
+    }
+}
+
 __global__ void __launch_bounds__(256) fill_zero_kernel(float* p, int64_t n) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
          i += (int64_t)gridDim.x * blockDim.x)
@@ -619,17 +748,11 @@ hipError_t zero(float* p, int64_t n, hipStream_t s) {
 
 template <typename T>
 hipError_t launch_generic_gemms(const pr2_moe_desc& d, const void* x, const void* Wg,
-                                const void* Wu, const void* Wd, const void* dy, const float* gate,
-                                const BwdWs& ws, const BwdGrads& out, hipStream_t s) {
+                                const void* Wu, const void* dy, const BwdWs& ws,
+                                const BwdGrads& out, hipStream_t s) {
+    // the SwiGLU backward (dh_generic) has already run: AU holds da | du, H holds g H
     const ReplayWs& w = ws.fw;
-    {
-        LaunchScope scope("bwd_dh_generic", s);
-        hipLaunchKernelGGL(dh_generic<T>, dim3((unsigned)w.max_tiles, (unsigned)d.m), dim3(256), 0,
-                           s, (const T*)dy, w.perm_src, d.k, (const T*)Wd, gate, d.d, d.m, w.tiles,
-                           w.tile_count, (T*)ws.AU, (T*)w.H, ws.dgp);
-    }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    hipError_t e;
     {
         LaunchScope scope("bwd_dx_generic", s);
         hipLaunchKernelGGL(dx_generic<T>, dim3((unsigned)w.max_tiles, (unsigned)d.d), dim3(256), 0,
@@ -681,42 +804,73 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
                                   hipStream_t s) {
     const ReplayWs& w = ws.fw;
     const bool bf = d.act_dtype == PR2_BF16;
+    const bool mfma = bwd_mfma_ok(d);
     hipError_t e = launch_preact(d, x, W_gate, W_up, w, ws.AU, s);
     if (e != hipSuccess) return e;
 
-    // expert GEMMs: gate gradient partials, SwiGLU backward, per-route input
-    // gradients and the expert weight gradients
-    if (bwd_mfma_ok(d)) {
-        BwdArgs g{};
-        g.perm_src = w.perm_src;
-        g.tiles = w.tiles;
-        g.tile_count = w.tile_count;
-        g.offsets = w.offsets;
-        g.k = d.k;
-        g.N = d.N;
-        g.d = d.d;
-        g.m = d.m;
-        g.Tk = (int)(d.T * d.k);
-        g.x = (const bf16_t*)x;
-        g.dy = (const bf16_t*)dy;
-        g.Wg = (const bf16_t*)W_gate;
-        g.Wu = (const bf16_t*)W_up;
-        g.Wd = (const bf16_t*)W_down;
-        g.gate = gate;
-        g.AU = (bf16_t*)ws.AU;
-        g.Hg = (bf16_t*)w.H;
-        g.dgp = ws.dgp;
-        g.dxr = (bf16_t*)w.O;
-        g.dWg = out.dW_gate;
-        g.dWu = out.dW_up;
-        g.dWd = out.dW_down;
-        auto grid_for = [](int64_t work) {
-            return dim3((unsigned)(((work + kNumXcd - 1) / kNumXcd) * kNumXcd));
-        };
+    BwdArgs g{};
+    g.perm_src = w.perm_src;
+    g.tiles = w.tiles;
+    g.tile_count = w.tile_count;
+    g.offsets = w.offsets;
+    g.order = ws.order;
+    g.dp_perm = ws.dp_perm;
+    g.dW_r = out.dW_r;
+    g.db_r = out.db_r;
+    g.k = d.k;
+    g.N = d.N;
+    g.d = d.d;
+    g.m = d.m;
+    g.Tk = (int)(d.T * d.k);
+    g.x = (const bf16_t*)x;
+    g.dy = (const bf16_t*)dy;
+    g.Wg = (const bf16_t*)W_gate;
+    g.Wu = (const bf16_t*)W_up;
+    g.Wd = (const bf16_t*)W_down;
+    g.gate = gate;
+    g.AU = (bf16_t*)ws.AU;
+    g.Hg = (bf16_t*)w.H;
+    g.dgp = ws.dgp;
+    g.dxr = (bf16_t*)w.O;
+    g.dWg = out.dW_gate;
+    g.dWu = out.dW_up;
+    g.dWd = out.dW_down;
+    auto grid_for = [](int64_t work) {
+        return dim3((unsigned)(((work + kNumXcd - 1) / kNumXcd) * kNumXcd));
+    };
+
+    // gate gradient partials and the SwiGLU backward
+    if (mfma) {
         g.ntn = d.m / BN;
+        LaunchScope scope("bwd_dh_swiglu", s);
+        hipLaunchKernelGGL(bwd_gemm<DH>, grid_for(w.max_tiles * g.ntn), dim3(kThreads), 0, s, g);
+    } else {
+        LaunchScope scope("bwd_dh_generic", s);
+        if (bf)
+            hipLaunchKernelGGL(dh_generic<bf16_t>, dim3((unsigned)w.max_tiles, (unsigned)d.m),
+                               dim3(256), 0, s, (const bf16_t*)dy, w.perm_src, d.k,
+                               (const bf16_t*)W_down, gate, d.d, d.m, w.tiles, w.tile_count,
+                               (bf16_t*)ws.AU, (bf16_t*)w.H, ws.dgp);
+        else
+            hipLaunchKernelGGL(dh_generic<float>, dim3((unsigned)w.max_tiles, (unsigned)d.m),
+                               dim3(256), 0, s, (const float*)dy, w.perm_src, d.k,
+                               (const float*)W_down, gate, d.d, d.m, w.tiles, w.tile_count,
+                               (float*)ws.AU, (float*)w.H, ws.dgp);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // router-logit gradients (needed by the router weight gradient below)
+    {
+        LaunchScope scope("bwd_gate_grad", s);
+        hipLaunchKernelGGL(gate_grad_kernel, dim3((unsigned)((d.T + 255) / 256)), dim3(256), 0, s,
+                           ws.dgp, ws.np, w.inv, gate, d.T, d.k, ws.dp_route, ws.dp_perm);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+
+    if (mfma) {
         {
-            LaunchScope scope("bwd_dh_swiglu", s);
-            hipLaunchKernelGGL(bwd_gemm<DH>, grid_for(w.max_tiles * g.ntn), dim3(kThreads), 0, s, g);
+            LaunchScope scope("bwd_expert_order", s);
+            hipLaunchKernelGGL(expert_order_kernel, dim3(1), dim3(1024), 0, s, w.offsets, d.N,
+                               ws.order);
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
         g.ntn = d.d / BN;
@@ -725,51 +879,26 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
             hipLaunchKernelGGL(bwd_gemm<DX>, grid_for(w.max_tiles * g.ntn), dim3(kThreads), 0, s, g);
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
+        const int64_t experts_per_xcd = (d.N + kNumXcd - 1) / kNumXcd;
         {
             LaunchScope scope("bwd_wgrad_down", s);
-            hipLaunchKernelGGL(bwd_gemm<WD>, grid_for((int64_t)d.N * (d.d / BM) * (d.m / BN)),
+            hipLaunchKernelGGL(bwd_gemm<WD>,
+                               dim3((unsigned)(kNumXcd * experts_per_xcd * (d.d / BM) * (d.m / BN))),
                                dim3(kThreads), 0, s, g);
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
         {
+            // also writes dW_r and db_r
             LaunchScope scope("bwd_wgrad_gate_up", s);
-            hipLaunchKernelGGL(bwd_gemm<WGU>, grid_for((int64_t)d.N * (2 * d.m / BM) * (d.d / BN)),
+            hipLaunchKernelGGL(bwd_gemm<WGU>,
+                               dim3((unsigned)(kNumXcd * experts_per_xcd * (2 * d.m / BM) * (d.d / BN))),
                                dim3(kThreads), 0, s, g);
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
     } else {
-        e = bf ? launch_generic_gemms<bf16_t>(d, x, W_gate, W_up, W_down, dy, gate, ws, out, s)
-               : launch_generic_gemms<float>(d, x, W_gate, W_up, W_down, dy, gate, ws, out, s);
+        e = bf ? launch_generic_gemms<bf16_t>(d, x, W_gate, W_up, dy, ws, out, s)
+               : launch_generic_gemms<float>(d, x, W_gate, W_up, dy, ws, out, s);
         if (e != hipSuccess) return e;
-    }
-
-    // router: logit gradients, then the input-gradient combine and dW_r, db_r
-    {
-        LaunchScope scope("bwd_gate_grad", s);
-        hipLaunchKernelGGL(gate_grad_kernel, dim3((unsigned)((d.T + 255) / 256)), dim3(256), 0, s,
-                           ws.dgp, ws.np, w.inv, gate, d.T, d.k, ws.dp_route, ws.dp_perm);
-    }
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    {
-        LaunchScope scope("bwd_transpose_wr", s);
-        hipLaunchKernelGGL(transpose_wr_kernel,
-                           dim3((unsigned)((d.d + 31) / 32), (unsigned)((d.N + 31) / 32)), dim3(256),
-                           0, s, W_r, d.d, d.N, ws.wrt);
-    }
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    {
-        LaunchScope scope("bwd_dx_combine", s);
-        if (bf)
-            hipLaunchKernelGGL(dx_combine_kernel<bf16_t>, dim3((unsigned)d.T), dim3(256), 0, s,
-                               (const bf16_t*)w.O, w.inv, ws.dp_route, ws.wrt, idx, d.idx_dtype, ldi,
-                               d.T, d.k, d.d, d.N, (bf16_t*)out.dx);
-        else
-            hipLaunchKernelGGL(dx_combine_kernel<float>, dim3((unsigned)d.T), dim3(256), 0, s,
-                               (const float*)w.O, w.inv, ws.dp_route, ws.wrt, idx, d.idx_dtype, ldi,
-                               d.T, d.k, d.d, d.N, (float*)out.dx);
-    }
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    {
         LaunchScope scope("bwd_router_wgrad", s);
         dim3 grid((unsigned)d.N, (unsigned)((d.d + 255) / 256));
         if (bf)
@@ -778,6 +907,31 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
         else
             hipLaunchKernelGGL(router_wgrad_kernel<float>, grid, dim3(256), 0, s, (const float*)x,
                                w.perm_src, w.offsets, ws.dp_perm, d.k, d.d, d.N, out.dW_r, out.db_r);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+
+    // input gradient: per-route rows plus the router term dp W_r^T
+    {
+        LaunchScope scope("bwd_transpose_wr", s);
+        hipLaunchKernelGGL(transpose_wr_kernel,
+                           dim3((unsigned)((d.d + 31) / 32), (unsigned)((d.N + 31) / 32)), dim3(256),
+                           0, s, W_r, d.d, d.N, ws.wrt);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    LaunchScope scope("bwd_dx_combine", s);
+    if (bf && d.d % 8 == 0) {
+        const int64_t want = (d.T + kDxTok - 1) / kDxTok;
+        hipLaunchKernelGGL(dx_combine_bf16_kernel, dim3((unsigned)(want < 8192 ? want : 8192)),
+                           dim3(256), 0, s, (const bf16_t*)w.O, w.inv, ws.dp_route, ws.wrt, idx,
+                           d.idx_dtype, ldi, d.T, d.k, d.d, d.N, (bf16_t*)out.dx);
+    } else if (bf) {
+        hipLaunchKernelGGL(dx_combine_kernel<bf16_t>, dim3((unsigned)d.T), dim3(256), 0, s,
+                           (const bf16_t*)w.O, w.inv, ws.dp_route, ws.wrt, idx, d.idx_dtype, ldi,
+                           d.T, d.k, d.d, d.N, (bf16_t*)out.dx);
+    } else {
+        hipLaunchKernelGGL(dx_combine_kernel<float>, dim3((unsigned)d.T), dim3(256), 0, s,
+                           (const float*)w.O, w.inv, ws.dp_route, ws.wrt, idx, d.idx_dtype, ldi,
+                           d.T, d.k, d.d, d.N, (float*)out.dx);
     }
     return hipGetLastError();
 }

@@ -84,6 +84,7 @@ struct BwdWs {
     float* dp_route;    // [T*k] router-logit gradient per (token, slot)
     float* dp_perm;     // [T*k] the same in permuted order
     float* wrt;         // [N, d] W_r transposed
+    int* order;         // [N] experts by decreasing route count
     int np;
     size_t bytes;
 };
