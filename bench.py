@@ -1,11 +1,23 @@
 """Benchmark of the Pr^2 MoE-layer hot path on one MI355X.
 
-One step = route prediction (router + rank-r evolution predictor, top-k,
-route record) followed by the replay forward of the recorded route (replay
-weights, permutation, grouped SwiGLU expert GEMMs, combine) over one batch of
-synthetic tokens already resident in HBM.  Prints ONE JSON line.
+Default (``--mode forward``): one step = route prediction (router + rank-r
+evolution predictor, top-k, route record) followed by the replay forward of
+the recorded route (replay weights, permutation, grouped SwiGLU expert GEMMs,
+combine) over one batch of synthetic tokens already resident in HBM.
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+``--mode backward``: one step = the replay backward of a recorded route (the
+rollout route of the same layer, which differs from the current router's
+top-k on some tokens): gradients of x, the experts and the router.
+
+``--mode decode``: the decode-style rollout of 256 sequences x 2048 steps, each
+step's route written into an index-stable int16 record, timed per step both
+as separate launches and replayed from one captured HIP graph, then the replay
+forward of 32768-token micro-batches of the record (tokens/s is for those).
+
+Prints ONE JSON line.
+
+    python bench.py [--mode forward|backward|decode] [--steps K] [--warmup W]
+                    [--workload NAME] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -22,26 +34,28 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "MoE-layer tokens/sec (predictive route + replay forward); MFMA util; HBM GB/s"
-DOMINANT = "gemm1_gate_up_swiglu"
+DEFAULT_WORKLOAD = {"forward": "qwen3_30b_T16384", "backward": "qwen3_30b_bwd_T16384",
+                    "decode": "qwen3_30b_decode_256x2048"}
 
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--mode", choices=("forward", "backward", "decode"), default="forward")
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="qwen3_30b_T16384")
+    ap.add_argument("--workload", default=None)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=0,
-                    help="tokens of the oracle's CPU sample (0: whole workload)")
+                    help="tokens of the oracle's CPU sample (0: the mode's default)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="first run a plain device copy of this many MiB (a known-size "
                          "kernel for scaling memory-traffic counters)")
     return ap.parse_args()
 
 
-def profiled_traffic(workload, kernel="grouped_gemm_mfma<0>"):
+def profiled_traffic(workload, kernel="grouped_gemm_mfma<0>", source="gemm.hip"):
     """HBM bytes per launch of the dominant kernel from the committed rocprofv3
     summary (FETCH_SIZE + WRITE_SIZE, copy-calibrated), or None when there is
     no summary for this workload or the kernel source changed since it was taken."""
@@ -50,7 +64,7 @@ def profiled_traffic(workload, kernel="grouped_gemm_mfma<0>"):
         return None
     text = open(path).read()
     m = re.search(r"gemm_source_sha256: ([0-9a-f]+)", text)
-    src = os.path.join(ROOT, "paper_2606_00395_amd", "csrc", "gemm.hip")
+    src = os.path.join(ROOT, "paper_2606_00395_amd", "csrc", source)
     cur = hashlib.sha256(open(src, "rb").read()).hexdigest()
     if not m or m.group(1) != cur:
         return None
@@ -59,50 +73,115 @@ def profiled_traffic(workload, kernel="grouped_gemm_mfma<0>"):
     return int(m.group(1)) + int(m.group(2)) if m else None
 
 
-def cpu_baseline(shape, L, n_tok, min_seconds=10.0):
-    """The float64 oracle (route + replay forward) on the first n_tok tokens,
-    repeated until at least min_seconds of CPU time have been measured."""
-    import numpy as np
-    from oracle import pr2_oracle as O
+def blas_threads():
     try:
         from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()
-                       if p.get("user_api") == "blas"] or [1])
+        return max([p.get("num_threads", 1) for p in threadpool_info()
+                    if p.get("user_api") == "blas"] or [1])
     except Exception:  # pragma: no cover
-        threads = int(os.environ.get("OMP_NUM_THREADS", "1"))
-    x = L["x"][:n_tok]
+        return int(os.environ.get("OMP_NUM_THREADS", "1"))
+
+
+def timed_cpu(fn, n_tok, min_seconds):
     reps = 0
     t0 = time.perf_counter()
     while True:
-        rt = O.route_predict(x, L["W_r"], L["beta"], L["A"], L["B"], shape.k)
-        O.replay_forward(x, rt["idx"], L["W_r"], L["beta"], L["W_gate"], L["W_up"], L["W_down"])
+        fn()
         reps += 1
         dt = time.perf_counter() - t0
         if dt >= min_seconds:
-            break
-    del np
-    return {"value": reps * n_tok / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            return reps, dt
+
+
+def cpu_baseline_forward(shape, L, n_tok, min_seconds=10.0):
+    """The float64 oracle (route + replay forward) on the first n_tok tokens,
+    repeated until at least min_seconds of CPU time have been measured."""
+    from oracle import pr2_oracle as O
+    x = L["x"][:n_tok]
+
+    def run():
+        rt = O.route_predict(x, L["W_r"], L["beta"], L["A"], L["B"], shape.k)
+        O.replay_forward(x, rt["idx"], L["W_r"], L["beta"], L["W_gate"], L["W_up"], L["W_down"])
+    reps, dt = timed_cpu(run, n_tok, min_seconds)
+    return {"value": reps * n_tok / dt, "unit": "tokens/s", "cores": blas_threads(),
+            "kind": "oracle",
             "sample": f"{n_tok} of {shape.T} tokens of {shape.name}, float64 route prediction "
                       f"+ replay forward, {reps} pass(es) in {dt:.1f} s"}
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no "
-              "multi-GPU path", file=sys.stderr)
-        sys.exit(2)
-    import numpy as np
-    import torch
+def cpu_baseline_backward(shape, L, idx, dy, n_tok, min_seconds=10.0):
+    from oracle import pr2_oracle as O
+    x = L["x"][:n_tok]
 
+    def run():
+        O.replay_backward(x, idx[:n_tok], L["W_r"], L["beta"], L["W_gate"], L["W_up"],
+                          L["W_down"], dy[:n_tok])
+    reps, dt = timed_cpu(run, n_tok, min_seconds)
+    return {"value": reps * n_tok / dt, "unit": "tokens/s", "cores": blas_threads(),
+            "kind": "oracle",
+            "sample": f"{n_tok} of {shape.T} tokens of {shape.name}, float64 replay backward, "
+                      f"{reps} pass(es) in {dt:.1f} s"}
+
+
+def cpu_baseline_decode(shape, L, min_seconds=10.0):
+    from oracle import pr2_oracle as O
     import workloads as W
-    from paper_2606_00395_amd import binding as B
-    from paper_2606_00395_amd import costmodel as C
+    xs = [W.decode_step_states(shape, 0, s) for s in range(8)]
+    i = [0]
 
-    shape = W.WORKLOADS[args.workload]
-    dev = torch.device("cuda", 0)
-    torch.cuda.set_device(dev)
-    L = W.layer_inputs(shape, args.seed)
+    def run():
+        O.route_predict(xs[i[0] % 8], L["W_r"], L["beta"], L["A"], L["B"], shape.k)
+        i[0] += 1
+    reps, dt = timed_cpu(run, W.DECODE_SEQS, min_seconds)
+    return {"value": reps * W.DECODE_SEQS / dt, "unit": "routed tokens/s",
+            "cores": blas_threads(), "kind": "oracle",
+            "sample": f"{reps} decode steps of {W.DECODE_SEQS} tokens, float64 route prediction, "
+                      f"in {dt:.1f} s"}
+
+
+def timed_steps(step, steps, warmup, stream, B):
+    """Mean ms per step over `steps` synchronised steps, then the same steps with
+    every kernel bracketed by HIP events on its stream (ms per launch by name)."""
+    import torch
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    B.profile_enable(True)
+    B.profile_reset()
+    torch.cuda.synchronize()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    prof = B.profile_collect()
+    B.profile_enable(False)
+    return ms, {name: tot / n for name, (tot, n) in prof.items()}
+
+
+def base_record(args, metric, value, unit, ms, dtype, config):
+    return {"metric": metric, "value": value, "unit": unit, "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": dtype,
+            "data": "synthetic (seeded N(0,1) tokens, N(0,0.02) weights; see workloads/)",
+            "config": config}
+
+
+def layer_config(shape):
+    return {"workload": shape.name, "tokens": shape.T, "hidden": shape.d, "experts": shape.N,
+            "top_k": shape.k, "expert_intermediate": shape.m, "predictor_rank": shape.r,
+            "router": "fp32", "idx_dtype": shape.idx_dtype, "load_skew": shape.skew}
+
+
+def upload(L, shape, dev):
+    import torch
     tdt = torch.bfloat16 if shape.act == "bf16" else torch.float32
 
     def up(a, act=False):
@@ -110,62 +189,43 @@ def main():
             return None
         t = torch.from_numpy(a)
         return (t.to(tdt) if act else t).to(dev)
+    out = {n: up(L[n]) for n in ("W_r", "beta", "A", "B")}
+    out["x"] = up(L["x"], True)
+    for n in ("W_gate", "W_up", "W_down"):
+        if n in L:
+            out[n] = up(L[n], True)
+    return out, up
 
-    if args.calib_copy_mib:
-        n = args.calib_copy_mib * (1 << 20) // 4
-        a = torch.ones(n, dtype=torch.float32, device=dev)
-        b = torch.empty_like(a)
-        b.copy_(a)
-        torch.cuda.synchronize()
-        del a, b
 
-    x = up(L["x"], True)
-    Wr, br, A, Bm = up(L["W_r"]), up(L["beta"]), up(L["A"]), up(L["B"])
-    Wg, Wu, Wd = up(L["W_gate"], True), up(L["W_up"], True), up(L["W_down"], True)
+def run_forward(args, shape, dev):
+    import torch
+    import workloads as W
+    from paper_2606_00395_amd import binding as B
+    from paper_2606_00395_amd import costmodel as C
+    L = W.layer_inputs(shape, args.seed)
+    G, _ = upload(L, shape, dev)
     T, d, N, k, m, r = shape.T, shape.d, shape.N, shape.k, shape.m, shape.r
     idt = torch.int16 if shape.idx_dtype == "int16" else torch.int32
     idx = torch.empty((T, k), dtype=idt, device=dev)
     gate_roll = torch.empty((T, k), dtype=torch.float32, device=dev)
     gate_rep = torch.empty((T, k), dtype=torch.float32, device=dev)
-    y = torch.empty((T, d), dtype=tdt, device=dev)
-    ws = B.replay_workspace(x, idx, Wr, Wg)
+    y = torch.empty_like(G["x"])
+    ws = B.replay_workspace(G["x"], idx, G["W_r"], G["W_gate"])
     stream = torch.cuda.current_stream()
 
     def step():
-        B.route_predict(x, Wr, br, A, Bm, k, idx, gate_roll, stream=stream)
-        B.moe_replay_forward(x, idx, Wr, br, Wg, Wu, Wd, y, gate_rep, ws=ws, stream=stream)
+        B.route_predict(G["x"], G["W_r"], G["beta"], G["A"], G["B"], k, idx, gate_roll,
+                        stream=stream)
+        B.moe_replay_forward(G["x"], idx, G["W_r"], G["beta"], G["W_gate"], G["W_up"],
+                             G["W_down"], y, gate_rep, ws=ws, stream=stream)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    # timed region: K steps, synchronised on both sides
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record(stream)
-    for _ in range(args.steps):
-        step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
-
-    # the same K steps with every kernel bracketed by events on its own stream
-    B.profile_enable(True)
-    B.profile_reset()
-    torch.cuda.synchronize()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    prof = B.profile_collect()
-    B.profile_enable(False)
-    kern = {name: tot / n for name, (tot, n) in prof.items()}   # ms per launch
-
+    ms, kern = timed_steps(step, args.steps, args.warmup, stream, B)
     ab = 2 if shape.act == "bf16" else 4
     ib = 2 if shape.idx_dtype == "int16" else 4
+    dominant = "gemm1_gate_up_swiglu"
     f_g1 = C.gemm1_flops(T, d, k, m)
     f_g2 = C.gemm2_flops(T, d, k, m)
-    t_g1 = kern.get(DOMINANT, float("nan"))
+    t_g1 = kern.get(dominant, float("nan"))
     t_g2 = kern.get("gemm2_down_scale", float("nan"))
     t_route = kern.get("route_predict", float("nan"))
     t_gates = kern.get("replay_gates", float("nan"))
@@ -174,44 +234,176 @@ def main():
     t_replay = sum(v for n, v in kern.items() if n != "route_predict")
     achieved = f_g1 / (t_g1 * 1e-3) / 1e12
     peak = C.PEAK_BF16_FLOPS / 1e12
-    out = {
-        "metric": METRIC,
-        "value": T / (ms * 1e-3),
-        "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": ms,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16" if shape.act == "bf16" else "f32",
-        "data": "synthetic (seeded N(0,1) tokens, N(0,0.02) weights; see workloads/)",
-        "config": {"workload": shape.name, "tokens": T, "hidden": d, "experts": N, "top_k": k,
-                   "expert_intermediate": m, "predictor_rank": r, "router": "fp32",
-                   "idx_dtype": shape.idx_dtype, "load_skew": shape.skew},
-        "roofline": {"bound": "mfma", "kernel": DOMINANT, "achieved": achieved, "peak": peak,
-                     "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": profiled_traffic(shape.name)},
-        "kernels_ms": {n: round(v, 5) for n, v in kern.items()},
-        "replay_forward": {
-            "ms": t_replay,
-            "mfma_frac_whole_layer": C.expert_flops(T, d, k, m) / (t_replay * 1e-3) / C.PEAK_BF16_FLOPS,
-            "mfma_frac_gemm1": f_g1 / (t_g1 * 1e-3) / C.PEAK_BF16_FLOPS,
-            "mfma_frac_gemm2": f_g2 / (t_g2 * 1e-3) / C.PEAK_BF16_FLOPS,
-        },
-        "hbm_gbps": {
-            "route_predict": C.route_bytes(T, d, N, r, k, ab, ib) / (t_route * 1e-3) / 1e9,
-            "replay_gates": C.replay_gate_bytes(T, d, N, k, ab, ib) / (t_gates * 1e-3) / 1e9,
-            "combine": C.combine_bytes(T, d, k, ab, ab) / (t_comb * 1e-3) / 1e9,
-            "permute_ms": t_perm,
-        },
+    out = base_record(args, METRIC, T / (ms * 1e-3), "tokens/s", ms,
+                      "bf16" if shape.act == "bf16" else "f32", layer_config(shape))
+    out["roofline"] = {"bound": "mfma", "kernel": dominant, "achieved": achieved, "peak": peak,
+                       "unit": "TFLOP/s", "frac": achieved / peak,
+                       "traffic": profiled_traffic(shape.name)}
+    out["kernels_ms"] = {n: round(v, 5) for n, v in kern.items()}
+    out["replay_forward"] = {
+        "ms": t_replay,
+        "mfma_frac_whole_layer": C.expert_flops(T, d, k, m) / (t_replay * 1e-3) / C.PEAK_BF16_FLOPS,
+        "mfma_frac_gemm1": f_g1 / (t_g1 * 1e-3) / C.PEAK_BF16_FLOPS,
+        "mfma_frac_gemm2": f_g2 / (t_g2 * 1e-3) / C.PEAK_BF16_FLOPS,
+    }
+    out["hbm_gbps"] = {
+        "route_predict": C.route_bytes(T, d, N, r, k, ab, ib) / (t_route * 1e-3) / 1e9,
+        "replay_gates": C.replay_gate_bytes(T, d, N, k, ab, ib) / (t_gates * 1e-3) / 1e9,
+        "combine": C.combine_bytes(T, d, k, ab, ab) / (t_comb * 1e-3) / 1e9,
+        "permute_ms": t_perm,
     }
     if not args.no_cpu_baseline:
         n_tok = args.cpu_sample_tokens if args.cpu_sample_tokens > 0 else T
-        out["cpu_baseline"] = cpu_baseline(shape, L, min(n_tok, T))
-    del np
-    print(json.dumps(out))
+        out["cpu_baseline"] = cpu_baseline_forward(shape, L, min(n_tok, T))
+    return out
+
+
+def run_backward(args, shape, dev):
+    import torch
+    import workloads as W
+    from paper_2606_00395_amd import binding as B
+    from paper_2606_00395_amd import costmodel as C
+    L = W.layer_inputs(shape, args.seed)
+    G, up = upload(L, shape, dev)
+    dy_np = W.upstream_grad(shape, args.seed)
+    dy = up(dy_np, True)
+    T, d, N, k, m = shape.T, shape.d, shape.N, shape.k, shape.m
+    idx = torch.empty((T, k), dtype=torch.int32, device=dev)
+    # the recorded route: this layer's rollout route (router + predictor)
+    B.route_predict(G["x"], G["W_r"], G["beta"], G["A"], G["B"], k, idx)
+    dx = torch.empty_like(G["x"])
+    dWr = torch.empty_like(G["W_r"])
+    dbr = torch.empty_like(G["beta"])
+    dWg = torch.empty(G["W_gate"].shape, device=dev)
+    dWu = torch.empty(G["W_up"].shape, device=dev)
+    dWd = torch.empty(G["W_down"].shape, device=dev)
+    ws = B.backward_workspace(G["x"], idx, G["W_r"], G["W_gate"])
+    stream = torch.cuda.current_stream()
+
+    def step():
+        B.moe_replay_backward(G["x"], idx, G["W_r"], G["beta"], G["W_gate"], G["W_up"],
+                              G["W_down"], dy, dx, dWr, dbr, dWg, dWu, dWd, ws=ws, stream=stream)
+
+    ms, kern = timed_steps(step, args.steps, args.warmup, stream, B)
+    flops = {"bwd_preact_gate_up": 4, "bwd_dh_swiglu": 2, "bwd_dx_gemm": 4, "bwd_wgrad_down": 2,
+             "bwd_wgrad_gate_up": 4}
+    unit = T * k * d * m
+    dominant = "bwd_wgrad_gate_up"
+    achieved = flops[dominant] * unit / (kern[dominant] * 1e-3) / 1e12
+    peak = C.PEAK_BF16_FLOPS / 1e12
+    out = base_record(args, "MoE-layer tokens/sec (replay backward: dx, expert and router grads)",
+                      T / (ms * 1e-3), "tokens/s", ms, "bf16", layer_config(shape))
+    out["roofline"] = {"bound": "mfma", "kernel": dominant, "achieved": achieved, "peak": peak,
+                       "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None}
+    out["kernels_ms"] = {n: round(v, 5) for n, v in kern.items()}
+    out["mfma_frac"] = {n: f * unit / (kern[n] * 1e-3) / C.PEAK_BF16_FLOPS
+                        for n, f in flops.items() if n in kern}
+    out["mfma_frac_whole_backward"] = 16 * unit / (ms * 1e-3) / C.PEAK_BF16_FLOPS
+    if not args.no_cpu_baseline:
+        idx_np = idx.cpu().numpy()
+        n_tok = args.cpu_sample_tokens if args.cpu_sample_tokens > 0 else 1024
+        out["cpu_baseline"] = cpu_baseline_backward(shape, L, idx_np, dy_np, min(n_tok, T))
+    return out
+
+
+def run_decode(args, shape, dev):
+    import torch
+    import workloads as W
+    from paper_2606_00395_amd import binding as B
+    from paper_2606_00395_amd import costmodel as C
+    S, P, k = W.DECODE_SEQS, W.DECODE_STEPS, shape.k
+    L = W.layer_inputs(shape.with_(T=S), args.seed)
+    G, _ = upload(L, shape.with_(T=S), dev)
+    X = torch.from_numpy(W.decode_all_states(shape, args.seed)).to(torch.bfloat16).to(dev)
+    Xsteps = X.permute(1, 0, 2).contiguous()                       # [P, S, d]
+    buf = torch.full((S, P, k), -1, dtype=torch.int16, device=dev)
+    ws = B.route_workspace(Xsteps[0], G["W_r"], G["A"], k, B.PR2_I16)
+    stream = torch.cuda.current_stream()
+
+    def record_all(st):
+        for pos in range(P):
+            B.route_predict(Xsteps[pos], G["W_r"], G["beta"], G["A"], G["B"], k, buf[:, pos, :],
+                            ws=ws, stream=st)
+
+    record_all(stream)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    record_all(stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us_launch = e0.elapsed_time(e1) * 1e3 / P
+    # the same 2048 steps captured once and replayed as one HIP graph
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        record_all(torch.cuda.current_stream())      # the capture stream
+    graph.replay()
+    torch.cuda.synchronize()
+    reps = 3
+    e0.record(stream)
+    for _ in range(reps):
+        graph.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us_graph = e0.elapsed_time(e1) * 1e3 / (P * reps)
+    rec_bytes = S * k * 2
+
+    # replay forward of 32768-token micro-batches (16 whole sequences each)
+    Xseq = X.reshape(S * P, shape.d)
+    mb = W.DECODE_MICROBATCH
+    nseq = mb // P
+    y = torch.empty((mb, shape.d), dtype=torch.bfloat16, device=dev)
+    wsr = B.replay_workspace(Xseq[:mb], buf[:nseq].reshape(mb, k), G["W_r"], G["W_gate"])
+    batches = [0, 15]
+
+    def step():
+        for b in batches:
+            B.moe_replay_forward(Xseq[b * mb:(b + 1) * mb], buf[b * nseq:(b + 1) * nseq].reshape(mb, k),
+                                 G["W_r"], G["beta"], G["W_gate"], G["W_up"], G["W_down"], y,
+                                 ws=wsr, stream=stream)
+
+    ms, kern = timed_steps(step, args.steps, args.warmup, stream, B)
+    tok = mb * len(batches)
+    dominant = "gemm1_gate_up_swiglu"
+    achieved = C.gemm1_flops(mb, shape.d, k, shape.m) / (kern[dominant] * 1e-3) / 1e12
+    peak = C.PEAK_BF16_FLOPS / 1e12
+    out = base_record(args, "decode-style route record (us/step) and micro-batch replay "
+                      "tokens/sec", tok / (ms * 1e-3), "tokens/s", ms, "bf16",
+                      dict(layer_config(shape), sequences=S, steps=P, microbatch=mb,
+                           microbatches=batches))
+    out["roofline"] = {"bound": "mfma", "kernel": dominant, "achieved": achieved, "peak": peak,
+                       "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None}
+    out["route_record"] = {"us_per_step_launches": us_launch, "us_per_step_hip_graph": us_graph,
+                           "record_bytes_per_step": rec_bytes,
+                           "record_gbps_graph": rec_bytes / (us_graph * 1e-6) / 1e9}
+    out["kernels_ms"] = {n: round(v, 5) for n, v in kern.items()}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_decode(shape, L)
+    return out
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no "
+              "multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import workloads as W
+
+    shape = W.WORKLOADS[args.workload or DEFAULT_WORKLOAD[args.mode]]
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+    run = {"forward": run_forward, "backward": run_backward, "decode": run_decode}[args.mode]
+    print(json.dumps(run(args, shape, dev)))
 
 
 if __name__ == "__main__":
