@@ -147,39 +147,46 @@ struct PredictOut {
 };
 
 // k rounds of a wavefront arg-max over orderable keys (lane l holds ids
-// v*64 + l in key[v]); among equal keys the lower id wins.  Returns the
-// selection as a per-lane bit mask over v and the largest logit in zmax.
+// v*64 + l in key[v], v < nv <= MAXV); among equal keys the lower id wins.
+// Returns the selection as a per-lane bit mask over v and the largest logit in
+// zmax.  MAXV is a compile-time bound so that every loop unrolls and the
+// per-lane arrays stay in fixed registers.
+template <int MAXV>
 __device__ uint32_t select_topk(const uint32_t* key, int nv, int N, int k, float& zmax) {
     const int lane = threadIdx.x & 63;
     uint32_t taken = 0;
     zmax = 0.0f;
     for (int it = 0; it < k; ++it) {
         uint32_t best = 0;
-        for (int v = 0; v < nv; ++v)
-            if (!((taken >> v) & 1u) && key[v] > best) best = key[v];
+#pragma unroll
+        for (int v = 0; v < MAXV; ++v)
+            if (v < nv && !((taken >> v) & 1u) && key[v] > best) best = key[v];
         const uint32_t wmax = wave_max_u32(best);
-        int jw = 0;
-        for (int v = 0; v < nv; ++v) {
-            const int j = v * 64 + lane;
-            uint64_t m = __ballot(j < N && !((taken >> v) & 1u) && key[v] == wmax);
-            if (m) {
-                jw = v * 64 + (__ffsll((unsigned long long)m) - 1);
-                break;
+        int jw = -1;
+#pragma unroll
+        for (int v = 0; v < MAXV; ++v) {
+            if (v < nv && jw < 0) {
+                const int j = v * 64 + lane;
+                const uint64_t m = __ballot(j < N && !((taken >> v) & 1u) && key[v] == wmax);
+                if (m) jw = v * 64 + (__ffsll((unsigned long long)m) - 1);
             }
         }
         if (it == 0) zmax = from_orderable(wmax);
-        if ((jw & 63) == lane) taken |= 1u << (jw >> 6);
+        if (jw >= 0 && (jw & 63) == lane) taken |= 1u << (jw >> 6);
     }
     return taken;
 }
 
 // Writes the selected ids ascending from idx + pos0 (and, when gate is not
 // null, e[v] / denom aligned with them).
+template <int MAXV>
 __device__ void write_route(uint32_t taken, int nv, void* idx, int idx_dtype, int64_t pos0,
                             float* gate, const float* e, float denom) {
     const int lane = threadIdx.x & 63;
     int before = 0;
-    for (int v = 0; v < nv; ++v) {
+#pragma unroll
+    for (int v = 0; v < MAXV; ++v) {
+        if (v >= nv) break;
         bool mine = (taken >> v) & 1u;
         uint64_t bal = __ballot(mine);
         if (mine) {
@@ -196,7 +203,10 @@ __device__ void write_route(uint32_t taken, int nv, void* idx, int idx_dtype, in
 }
 
 // One wavefront: rollout epilogue of token t from its LDS row of logits.
-__device__ void predict_token(const float* row, int64_t t, int N, int r, const PredictOut& o) {
+// bias: the router bias (in LDS or global memory) or null.
+template <int MAXV>
+__device__ void predict_token(const float* row, int64_t t, int N, int r, const PredictOut& o,
+                              const float* bias) {
     const int lane = threadIdx.x & 63;
     const int nv = (N + 63) / 64;
     float* lrow = o.logits_out ? o.logits_out + t * N : nullptr;
@@ -220,15 +230,16 @@ __device__ void predict_token(const float* row, int64_t t, int N, int r, const P
             }
         }
     }
-    float z[kMaxLanesVals];
-    uint32_t key[kMaxLanesVals];
-    for (int v = 0; v < nv; ++v) {
+    float z[MAXV];
+    uint32_t key[MAXV];
+#pragma unroll
+    for (int v = 0; v < MAXV; ++v) {
         int j = v * 64 + lane;
         z[v] = -INFINITY;
         key[v] = 0;                          // below every real logit's key
         if (j < N) {
             // p = xW + beta and z = p + (xA) B in fp64, one final rounding
-            double p = (double)row[j] + (o.b_r ? (double)o.b_r[j] : 0.0);
+            double p = (double)row[j] + (bias ? (double)bias[j] : 0.0);
             double zz = p;
             if (!o.folded && r > 0) {
                 const float* u = row + N;
@@ -244,10 +255,11 @@ __device__ void predict_token(const float* row, int64_t t, int N, int r, const P
         }
     }
     float zmax;
-    const uint32_t taken = select_topk(key, nv, N, o.k, zmax);
-    float e[kMaxLanesVals];
+    const uint32_t taken = select_topk<MAXV>(key, nv, N, o.k, zmax);
+    float e[MAXV];
     float s_sel = 0.0f, s_all = 0.0f;
-    for (int v = 0; v < nv; ++v) {
+#pragma unroll
+    for (int v = 0; v < MAXV; ++v) {
         int j = v * 64 + lane;
         e[v] = 0.0f;
         if (j < N) {
@@ -257,7 +269,7 @@ __device__ void predict_token(const float* row, int64_t t, int N, int r, const P
         }
     }
     const float denom = o.renorm ? wave_sum_f32(s_sel) : wave_sum_f32(s_all);
-    write_route(taken, nv, o.idx_out, o.idx_dtype, t * o.ldi, o.gate_out ? o.gate_out + t * o.k : nullptr,
+    write_route<MAXV>(taken, nv, o.idx_out, o.idx_dtype, t * o.ldi, o.gate_out ? o.gate_out + t * o.k : nullptr,
                 e, denom);
 }
 
@@ -294,26 +306,29 @@ __device__ __forceinline__ double wave_max_f64(double v) {
 
 // One wavefront: the current top-k of token t (ties to the lower id, decided on
 // the fp32 logits), its overlap with the recorded ids, and the route KL.
-__device__ void diag_token(const float* row, int64_t t, int N, const ReplayOut& o) {
+template <int MAXV>
+__device__ void diag_token(const float* row, int64_t t, int N, const ReplayOut& o,
+                           const float* bias) {
     const int lane = threadIdx.x & 63;
     const int nv = (N + 63) / 64;
     const DiagOut& g = o.diag;
-    float p[kMaxLanesVals];
-    uint32_t key[kMaxLanesVals];
-    for (int v = 0; v < nv; ++v) {
+    float p[MAXV];
+    uint32_t key[MAXV];
+#pragma unroll
+    for (int v = 0; v < MAXV; ++v) {
         const int j = v * 64 + lane;
         p[v] = -INFINITY;
         key[v] = 0;
         if (j < N) {
-            p[v] = (float)((double)row[j] + (o.b_r ? (double)o.b_r[j] : 0.0));
+            p[v] = (float)((double)row[j] + (bias ? (double)bias[j] : 0.0));
             key[v] = orderable(p[v]);
             if (g.p_out) g.p_out[t * N + j] = p[v];
         }
     }
     if (!(g.cur_idx || g.overlap || g.kl || g.hist)) return;
     float pmax;
-    const uint32_t taken = select_topk(key, nv, N, o.k, pmax);
-    if (g.cur_idx) write_route(taken, nv, g.cur_idx, o.idx_dtype, t * o.k, nullptr, nullptr, 1.0f);
+    const uint32_t taken = select_topk<MAXV>(key, nv, N, o.k, pmax);
+    if (g.cur_idx) write_route<MAXV>(taken, nv, g.cur_idx, o.idx_dtype, t * o.k, nullptr, nullptr, 1.0f);
     if (g.overlap || g.hist) {
         int cnt = 0;
         for (int s = 0; s < o.k; ++s) {
@@ -329,14 +344,16 @@ __device__ void diag_token(const float* row, int64_t t, int N, const ReplayOut& 
     if (g.kl) {
         const float* zr = g.z_ref + t * N;
         double mz = -INFINITY;
-        for (int v = 0; v < nv; ++v) {
+    #pragma unroll
+    for (int v = 0; v < MAXV; ++v) {
             const int j = v * 64 + lane;
             if (j < N) mz = fmax(mz, (double)zr[j]);
         }
         mz = wave_max_f64(mz);
         const double mp = (double)pmax;
         double sp = 0.0, sz = 0.0;
-        for (int v = 0; v < nv; ++v) {
+    #pragma unroll
+    for (int v = 0; v < MAXV; ++v) {
             const int j = v * 64 + lane;
             if (j < N) {
                 sp += exp((double)p[v] - mp);
@@ -347,7 +364,8 @@ __device__ void diag_token(const float* row, int64_t t, int N, const ReplayOut& 
         sz = wave_sum_f64(sz);
         const double shift = (mp + log(sp)) - (mz + log(sz));
         double acc = 0.0;
-        for (int v = 0; v < nv; ++v) {
+    #pragma unroll
+    for (int v = 0; v < MAXV; ++v) {
             const int j = v * 64 + lane;
             if (j < N) {
                 const double lp = (double)p[v] - mp;
@@ -360,20 +378,25 @@ __device__ void diag_token(const float* row, int64_t t, int N, const ReplayOut& 
 }
 
 // One wavefront: replay weights of token t over its recorded ids from the LDS
-// row of N current-router logits (predictor bypassed).
-__device__ void replay_token(const float* row, int64_t t, int N, const ReplayOut& o) {
+// row of N current-router logits (predictor bypassed).  bias: the router bias
+// (LDS or global) or null; ids: the token's recorded ids already staged in LDS,
+// or null to read them from the route record.
+template <int MAXV>
+__device__ void replay_token(const float* row, int64_t t, int N, const ReplayOut& o,
+                             const float* bias, const int* ids) {
     if (o.diag.cur_idx || o.diag.overlap || o.diag.kl || o.diag.hist || o.diag.p_out)
-        diag_token(row, t, N, o);
+        diag_token<MAXV>(row, t, N, o, bias);
     if (!o.gate_out) return;
     const int lane = threadIdx.x & 63;
     auto logit = [&](int j) {
-        return (float)((double)row[j] + (o.b_r ? (double)o.b_r[j] : 0.0));
+        return (float)((double)row[j] + (bias ? (double)bias[j] : 0.0));
     };
+    auto id_at = [&](int s) { return ids ? ids[s] : load_id(o.idx, o.idx_dtype, t * o.ldi + s); };
     float ref;
     if (o.renorm) {
         float pmax_sel = -INFINITY;
         for (int s = lane; s < o.k; s += 64) {
-            int id = load_id(o.idx, o.idx_dtype, t * o.ldi + s);
+            int id = id_at(s);
             if (id >= 0 && id < N) pmax_sel = fmaxf(pmax_sel, logit(id));
         }
         ref = wave_max_f32(pmax_sel);
@@ -385,7 +408,7 @@ __device__ void replay_token(const float* row, int64_t t, int N, const ReplayOut
     float part = 0.0f;
     if (o.renorm) {
         for (int s = lane; s < o.k; s += 64) {
-            int id = load_id(o.idx, o.idx_dtype, t * o.ldi + s);
+            int id = id_at(s);
             if (id >= 0 && id < N) part += expf(logit(id) - ref);
         }
     } else {
@@ -394,7 +417,7 @@ __device__ void replay_token(const float* row, int64_t t, int N, const ReplayOut
     const float denom = wave_sum_f32(part);
     int bad = 0;
     for (int s = lane; s < o.k; s += 64) {
-        int id = load_id(o.idx, o.idx_dtype, t * o.ldi + s);
+        int id = id_at(s);
         float g = 0.0f;
         if (id >= 0 && id < N) g = expf(logit(id) - ref) / denom;
         else bad++;
@@ -403,9 +426,9 @@ __device__ void replay_token(const float* row, int64_t t, int N, const ReplayOut
     if (o.validate) {
         int dup = 0;
         for (int s = lane; s < o.k; s += 64) {
-            int id = load_id(o.idx, o.idx_dtype, t * o.ldi + s);
+            int id = id_at(s);
             for (int s2 = 0; s2 < s; ++s2)
-                if (load_id(o.idx, o.idx_dtype, t * o.ldi + s2) == id) dup++;
+                if (id_at(s2) == id) dup++;
         }
         dup = wave_sum_i32(dup);
         int nbad = wave_sum_i32(bad);
@@ -430,7 +453,7 @@ route_predict_kernel(ProjArgs a, PredictOut o) {
     for (int tt = threadIdx.x >> 6; tt < a.TM; tt += kThreads / 64) {
         const int64_t t = t0 + tt;
         if (t >= a.T) break;
-        predict_token(lg + tt * a.NC, t, a.N, a.r, o);
+        predict_token<kMaxLanesVals>(lg + tt * a.NC, t, a.N, a.r, o, o.b_r);
     }
 }
 
@@ -447,7 +470,198 @@ replay_gates_kernel(ProjArgs a, ReplayOut o) {
     for (int tt = threadIdx.x >> 6; tt < a.TM; tt += kThreads / 64) {
         const int64_t t = t0 + tt;
         if (t >= a.T) break;
-        replay_token(lg + tt * a.NC, t, a.N, o);
+        replay_token<kMaxLanesVals>(lg + tt * a.NC, t, a.N, o, o.b_r, nullptr);
+    }
+}
+
+// ------------------------------------------- 16-lane group epilogues ----
+// The MFMA path runs its epilogues four tokens per wavefront: the 16 lanes of
+// group g = lane / 16 own one token, lane l16 = lane % 16 holding experts
+// j = 16 v + l16 (v < MAXV16).  Reductions are butterflies inside the group;
+// sums are then taken from the group's first lane so that every lane uses
+// the same value.
+
+__device__ __forceinline__ uint32_t gmax_u32(uint32_t v) {
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) v = max(v, (uint32_t)__shfl_xor((int)v, off, 16));
+    return v;
+}
+__device__ __forceinline__ int gmin_i32(int v) {
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) v = min(v, __shfl_xor(v, off, 16));
+    return v;
+}
+__device__ __forceinline__ float gmax_f32(float v) {
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) v = fmaxf(v, __shfl_xor(v, off, 16));
+    return v;
+}
+__device__ __forceinline__ float gsum_f32(float v) {
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) v += __shfl_xor(v, off, 16);
+    return __shfl(v, 0, 16);
+}
+__device__ __forceinline__ int gsum_i32(int v) {
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) v += __shfl_xor(v, off, 16);
+    return v;
+}
+
+// Rollout epilogue of token t (valid: t < T) by one 16-lane group.
+template <int MAXV16>
+__device__ void predict_group(const float* row, int64_t t, bool valid, int N, int r,
+                              const PredictOut& o, const float* bias) {
+    const int lane = threadIdx.x & 63;
+    const int l16 = lane & 15, grp = lane >> 4;
+    float* lrow = (valid && o.logits_out) ? o.logits_out + t * N : nullptr;
+    if (valid && o.cache.row) {
+        const int cr = o.cache.row[t];
+        if (cr >= 0 && cr < o.cache.rows) {
+            lrow = o.cache.p + (int64_t)cr * N;
+            const size_t eb = o.act_dtype == PR2_BF16 ? 2 : 4;
+            const size_t bytes = (size_t)o.d * eb;
+            const unsigned char* src = (const unsigned char*)o.x + (size_t)t * bytes;
+            unsigned char* dst = (unsigned char*)o.cache.h + (size_t)cr * bytes;
+            if (bytes % 16 == 0) {
+                for (size_t c = l16; c < bytes / 16; c += 16)
+                    ((u32x4_t*)dst)[c] = ((const u32x4_t*)src)[c];
+            } else {
+                for (size_t c = l16; c < bytes / eb; c += 16) {
+                    if (eb == 2) ((uint16_t*)dst)[c] = ((const uint16_t*)src)[c];
+                    else ((uint32_t*)dst)[c] = ((const uint32_t*)src)[c];
+                }
+            }
+        }
+    }
+    float z[MAXV16];
+    uint32_t key[MAXV16];
+#pragma unroll
+    for (int v = 0; v < MAXV16; ++v) {
+        const int j = v * 16 + l16;
+        z[v] = -INFINITY;
+        key[v] = 0;
+        if (j < N) {
+            const double p = (double)row[j] + (bias ? (double)bias[j] : 0.0);
+            double zz = p;
+            if (!o.folded && r > 0) {
+                const float* u = row + N;
+                if (o.B) {
+                    for (int q = 0; q < r; ++q) zz += (double)u[q] * (double)o.B[(int64_t)q * N + j];
+                } else {
+                    zz += (double)u[j];
+                }
+            }
+            if (lrow) lrow[j] = (float)p;
+            z[v] = (float)zz;
+            key[v] = orderable(z[v]);
+        }
+    }
+    // k rounds of a group arg-max; among equal keys the lower id wins
+    uint32_t taken = 0;
+    float zmax = 0.0f;
+    for (int it = 0; it < o.k; ++it) {
+        uint32_t best = 0;
+#pragma unroll
+        for (int v = 0; v < MAXV16; ++v)
+            if (!((taken >> v) & 1u) && key[v] > best) best = key[v];
+        const uint32_t gm = gmax_u32(best);
+        int cand = 0x7fffffff;
+#pragma unroll
+        for (int v = MAXV16 - 1; v >= 0; --v)
+            if (v * 16 + l16 < N && !((taken >> v) & 1u) && key[v] == gm) cand = v * 16 + l16;
+        const int win = gmin_i32(cand);
+        if (it == 0) zmax = from_orderable(gm);
+        if (win < N && (win & 15) == l16) taken |= 1u << (win >> 4);
+    }
+    float e[MAXV16];
+    float s_sel = 0.0f, s_all = 0.0f;
+#pragma unroll
+    for (int v = 0; v < MAXV16; ++v) {
+        e[v] = 0.0f;
+        if (v * 16 + l16 < N) {
+            e[v] = expf(z[v] - zmax);
+            s_all += e[v];
+            if ((taken >> v) & 1u) s_sel += e[v];
+        }
+    }
+    const float denom = gsum_f32(o.renorm ? s_sel : s_all);
+    // ids ascending (v-major, then lane), gates aligned
+    int before = 0;
+#pragma unroll
+    for (int v = 0; v < MAXV16; ++v) {
+        const bool mine = (taken >> v) & 1u;
+        const uint32_t gbits = (uint32_t)(__ballot(mine) >> (16 * grp)) & 0xffffu;
+        if (mine && valid) {
+            const int rank = before + __popc(gbits & ((1u << l16) - 1u));
+            const int j = v * 16 + l16;
+            const int64_t pos = t * o.ldi + rank;
+            if (o.idx_dtype == PR2_I16) ((int16_t*)o.idx_out)[pos] = (int16_t)j;
+            else ((int32_t*)o.idx_out)[pos] = j;
+            if (o.gate_out) o.gate_out[t * o.k + rank] = e[v] / denom;
+        }
+        before += __popc(gbits);
+    }
+}
+
+// Replay weights of token t over its recorded ids (ids: staged in LDS, or
+// null to read the record) by one 16-lane group.
+template <int MAXV16>
+__device__ void replay_group(const float* row, int64_t t, bool valid, int N, const ReplayOut& o,
+                             const float* bias, const int* ids) {
+    const int lane = threadIdx.x & 63;
+    const int l16 = lane & 15;
+    auto logit = [&](int j) {
+        return (float)((double)row[j] + (bias ? (double)bias[j] : 0.0));
+    };
+    auto id_at = [&](int s) {
+        if (ids) return ids[s];
+        return valid ? load_id(o.idx, o.idx_dtype, t * o.ldi + s) : -1;
+    };
+    float mx = -INFINITY;
+    if (o.renorm) {
+        for (int s = l16; s < o.k; s += 16) {
+            const int id = id_at(s);
+            if (id >= 0 && id < N) mx = fmaxf(mx, logit(id));
+        }
+    } else {
+#pragma unroll
+        for (int v = 0; v < MAXV16; ++v)
+            if (v * 16 + l16 < N) mx = fmaxf(mx, logit(v * 16 + l16));
+    }
+    const float ref = gmax_f32(mx);
+    float part = 0.0f;
+    if (o.renorm) {
+        for (int s = l16; s < o.k; s += 16) {
+            const int id = id_at(s);
+            if (id >= 0 && id < N) part += expf(logit(id) - ref);
+        }
+    } else {
+#pragma unroll
+        for (int v = 0; v < MAXV16; ++v)
+            if (v * 16 + l16 < N) part += expf(logit(v * 16 + l16) - ref);
+    }
+    const float denom = gsum_f32(part);
+    int bad = 0;
+    for (int s = l16; s < o.k; s += 16) {
+        const int id = id_at(s);
+        float g = 0.0f;
+        if (id >= 0 && id < N) g = expf(logit(id) - ref) / denom;
+        else bad++;
+        if (valid) o.gate_out[t * o.k + s] = g;
+    }
+    if (o.validate) {
+        int dup = 0;
+        for (int s = l16; s < o.k; s += 16) {
+            const int id = id_at(s);
+            for (int s2 = 0; s2 < s; ++s2)
+                if (id_at(s2) == id) dup++;
+        }
+        dup = gsum_i32(dup);
+        const int nbad = gsum_i32(bad);
+        if (l16 == 0 && valid) {
+            if (nbad) atomicAdd(o.err + ERR_BAD_ID, nbad);
+            if (dup) atomicAdd(o.err + ERR_DUP_ID, dup);
+        }
     }
 }
 
@@ -530,8 +744,8 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
     constexpr int NSTAGE = RT::NSTAGE;
     constexpr int GPW = RT::GPW;
     __shared__ __attribute__((aligned(1024))) unsigned char lds[NSTAGE * RT::STAGEB];
-    static_assert(NSTAGE * RT::STAGEB >= (int)sizeof(float) * kRTM * NCp,
-                  "logit tile must fit over the copy stages");
+    static_assert(NSTAGE * RT::STAGEB >= (int)sizeof(float) * (kRTM * NCp + NCp + kRTM * 64),
+                  "logit tile, bias and staged ids must fit over the copy stages");
     const int64_t t0 = (int64_t)blockIdx.x * kRTM;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -568,6 +782,22 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
                                              (lds_void*)&lds[stage * RT::STAGEB + dst[i]], 16, 0, 0);
         }
     };
+
+    // replay: the recorded ids of the workgroup's tokens are fetched now and
+    // parked in LDS after the K loop, so the epilogue never waits on them
+    constexpr int kStageK = 64;                       // ids staged when k <= kStageK
+    constexpr int kIdsPerThread = kRTM * kStageK / kRThreads;
+    const bool stage_ids = MODE == 1 && ro.idx != nullptr && ro.k <= kStageK;
+    int pre_ids[kIdsPerThread];
+    if (stage_ids) {
+#pragma unroll
+        for (int i = 0; i < kIdsPerThread; ++i) {
+            const int e = tid + kRThreads * i;
+            const int tok = e / ro.k, slot = e % ro.k;
+            pre_ids[i] = (e < kRTM * ro.k && t0 + tok < T)
+                             ? load_id(ro.idx, ro.idx_dtype, (t0 + tok) * ro.ldi + slot) : -1;
+        }
+    }
 
     f32x4 acc[2][NTW];
     double acc64[2][NTW][4];
@@ -635,12 +865,39 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
                 const int col = (wc * NTW + t) * 16 + (lane & 15);
                 if (col < NC) lg[tok * NC + col] = (float)acc64[i][t][v];
             }
+    // the router bias and (replay) the staged ids go behind the logit tile
+    float* sbias = lg + kRTM * NC;
+    int* sids = (int*)(sbias + N);
+    const float* b_r = MODE == 0 ? po.b_r : ro.b_r;
+    for (int j = tid; j < N; j += kRThreads) sbias[j] = b_r ? b_r[j] : 0.0f;
+    if (stage_ids) {
+#pragma unroll
+        for (int i = 0; i < kIdsPerThread; ++i) {
+            const int e = tid + kRThreads * i;
+            if (e < kRTM * ro.k) sids[e] = pre_ids[i];
+        }
+    }
     __syncthreads();
-    for (int tt = wave; tt < kRTM; tt += kRThreads / 64) {
+    const bool diag = MODE == 1 && (ro.diag.cur_idx || ro.diag.overlap || ro.diag.kl ||
+                                    ro.diag.hist || ro.diag.p_out);
+    if (diag) {
+        // diagnostics: one token per wavefront
+        for (int tt = wave; tt < kRTM; tt += kRThreads / 64) {
+            const int64_t t = t0 + tt;
+            if (t >= T) break;
+            replay_token<NTW>(lg + tt * NC, t, N, ro, sbias, stage_ids ? sids + tt * ro.k : nullptr);
+        }
+        return;
+    }
+    // four tokens per wavefront, one per 16-lane group
+    for (int base = wave * 4; base < kRTM; base += (kRThreads / 64) * 4) {
+        if (t0 + base >= T) break;
+        const int tt = base + (lane >> 4);
         const int64_t t = t0 + tt;
-        if (t >= T) break;
-        if (MODE == 0) predict_token(lg + tt * NC, t, N, r, po);
-        else replay_token(lg + tt * NC, t, N, ro);
+        const bool valid = t < T;
+        if (MODE == 0) predict_group<4 * NTW>(lg + tt * NC, t, valid, N, r, po, sbias);
+        else replay_group<4 * NTW>(lg + tt * NC, t, valid, N, ro, sbias,
+                                   stage_ids ? sids + tt * ro.k : nullptr);
     }
 }
 
