@@ -263,7 +263,7 @@ pr2_status pr2_route_predict_cached(const pr2_moe_desc* desc, const void* x, con
  *   zhat_t = p_old,t + h_old,t A B    rebuilt predictive logits
  *   loss_kind 0:  kl_t = KL(softmax(p_t) || softmax(zhat_t))                  (Eq. pr2_loss)
  *   loss_kind 1:  kl_t = KL(softmax(p_t - p_old,t) || softmax(h_old,t A B))   (delta matching,
- *                 the objective ablation of Appendix F)
+ *                 the objective ablation of Appendix G)
  *   loss = mean_t kl_t;  dA, dB = gradients of loss (the router gets none: stop-gradient)
  *
  *   h, h_old   [T, d] act_dtype (16-byte aligned);  W_r [d, N], b_r [N] or NULL, p_old [T, N],

@@ -271,7 +271,7 @@ def predictive_kl(p_cur, h_old, p_old, A, B):
 
 
 def delta_matching_kl(p_cur, h_old, p_old, A, B):
-    """The delta-matching alternative of the predictive loss (Appendix F,
+    """The delta-matching alternative of the predictive loss (Appendix G,
     predictive-objective ablation): per-token
     KL(Softmax(<p_cur - p_old>) || Softmax(h_old W_p)), W_p = A B (B = None:
     identity).  Returns (kl [T], dA, dB) like predictive_kl."""

@@ -4,7 +4,7 @@
 //   p_t       = h_t W_r + b_r                  current router (the teacher, no gradient)
 //   u_t       = h_old,t A,  b_t = u_t B        predictor residual, W_p = A B
 //   standard:  KL(softmax(p_t) || softmax(p_old,t + b_t))
-//   delta:     KL(softmax(p_t - p_old,t) || softmax(b_t))   (Appendix F ablation)
+//   delta:     KL(softmax(p_t - p_old,t) || softmax(b_t))   (Appendix G ablation)
 //   loss = mean_t KL,  dz_t = (softmax(zhat_t) - target_t) / T
 //   dB = sum_t u_t^T dz_t,  dA = sum_t h_old,t^T (dz_t B^T)
 //

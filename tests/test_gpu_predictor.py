@@ -5,7 +5,7 @@
   the router logits (fp32 rounding of the oracle's), while the recorded
   route follows the usual margin rule;
 * the predictive loss and its gradients (Sec. 4.2, Eq. pr2_loss; Alg. 3) and
-  the delta-matching variant (Appendix F), from a feature cache against a
+  the delta-matching variant (Appendix G), from a feature cache against a
   drifted current router: per-token KL, mean loss, dA and dB within 1e-5
   (Frobenius ratio) of the oracle; zeros at mini-step 1.
 
