@@ -166,6 +166,26 @@ def timed_steps(step, steps, warmup, stream, B):
     return ms, {name: tot / n for name, (tot, n) in prof.items()}
 
 
+def graph_ms_per_step(step_on, steps):
+    """Mean ms per step when the step's launches are captured once into a HIP
+    graph and replayed (no host work or launch gaps between kernels)."""
+    import torch
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step_on(torch.cuda.current_stream())
+    graph.replay()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    st = torch.cuda.current_stream()
+    e0.record(st)
+    for _ in range(steps):
+        graph.replay()
+    e1.record(st)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
 def base_record(args, metric, value, unit, ms, dtype, config):
     return {"metric": metric, "value": value, "unit": unit, "n_gpus": 1, "steps": args.steps,
             "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
@@ -211,15 +231,21 @@ def run_forward(args, shape, dev):
     gate_rep = torch.empty((T, k), dtype=torch.float32, device=dev)
     y = torch.empty_like(G["x"])
     ws = B.replay_workspace(G["x"], idx, G["W_r"], G["W_gate"])
+    ws_r = B.route_workspace(G["x"], G["W_r"], G["A"], k, B.PR2_I16 if shape.idx_dtype == "int16"
+                             else B.PR2_I32)
     stream = torch.cuda.current_stream()
 
-    def step():
-        B.route_predict(G["x"], G["W_r"], G["beta"], G["A"], G["B"], k, idx, gate_roll,
-                        stream=stream)
+    def step_on(st):
+        B.route_predict(G["x"], G["W_r"], G["beta"], G["A"], G["B"], k, idx, gate_roll, ws=ws_r,
+                        stream=st)
         B.moe_replay_forward(G["x"], idx, G["W_r"], G["beta"], G["W_gate"], G["W_up"],
-                             G["W_down"], y, gate_rep, ws=ws, stream=stream)
+                             G["W_down"], y, gate_rep, ws=ws, stream=st)
+
+    def step():
+        step_on(stream)
 
     ms, kern = timed_steps(step, args.steps, args.warmup, stream, B)
+    ms_graph = graph_ms_per_step(step_on, args.steps)
     ab = 2 if shape.act == "bf16" else 4
     ib = 2 if shape.idx_dtype == "int16" else 4
     dominant = "gemm1_gate_up_swiglu"
@@ -239,6 +265,8 @@ def run_forward(args, shape, dev):
     out["roofline"] = {"bound": "mfma", "kernel": dominant, "achieved": achieved, "peak": peak,
                        "unit": "TFLOP/s", "frac": achieved / peak,
                        "traffic": profiled_traffic(shape.name)}
+    out["hip_graph"] = {"ms_per_step": ms_graph, "value": T / (ms_graph * 1e-3),
+                        "note": "the same step captured once and replayed as a HIP graph"}
     out["kernels_ms"] = {n: round(v, 5) for n, v in kern.items()}
     out["replay_forward"] = {
         "ms": t_replay,

@@ -70,6 +70,8 @@ CASES = [
     (200, 72, 6, 6, 40, "f32", "none", True, "int32", 2, "generic_f32_k_eq_N"),
     (130, 256, 1, 1, 128, "bf16", "none", True, "int32", 0, "single_expert"),
     (70, 256, 128, 8, 128, "bf16", "hot8", True, "int32", 0, "few_tokens_many_experts"),
+    (40, 256, 512, 256, 128, "bf16", "none", True, "int32", 0, "k256_N512_max_route"),
+    (33, 64, 1024, 96, 32, "f32", "zipf", False, "int16", 1, "N1024_literal_generic"),
 ]
 
 

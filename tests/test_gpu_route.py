@@ -66,6 +66,8 @@ CASES = [
     (250, 64, 1, 1, 0, "f32", "none", "int32", 0, True, False),         # N = 1
     (200, 64, 64, 2, 64, "bf16", "none", "int32", 0, True, True),       # full-rank W_p = A
     (33, 1024, 128, 8, 256, "bf16", "hot8", "int32", 0, False, False),  # NC > 256, literal
+    (40, 64, 512, 256, 4, "bf16", "none", "int32", 0, True, False),     # k = 256 (maximum)
+    (17, 128, 1024, 256, 0, "f32", "none", "int16", 0, True, False),    # N = 1024, k = 256
 ]
 
 
