@@ -197,16 +197,23 @@ grouped_gemm_mfma(MfmaArgs g) {
 #pragma unroll
             for (int v = 0; v < ACCN; ++v) acc[i][j][v] = 0.0f;
 
-    // LDS reads for the MFMA operands: lane l reads row (block base + l%MT),
-    // the 16 bytes of K values MK*ks + 8*(l/MT) .. +7, i.e. chunk
-    // (MK/8)*ks + l/MT, at position chunk ^ swz(row); block bases are
-    // multiples of 16 rows, so the swizzle is the same for every fragment.
+    // LDS reads for the MFMA operands: lane l reads row (block base + l%MT)
+    // and the 16 bytes of one 8-wide K chunk, at position chunk ^ swz(row);
+    // block bases are multiples of 16 rows, so the swizzle is the same for
+    // every fragment.  Which chunk of the sub-step a lane group g = l/MT
+    // takes is free (A and B fragments use the same assignment, so each MFMA
+    // still sums over the same K values): a ds_read_b128 serves lanes
+    // 8q..8q+7 together with lanes 32+8q..32+8q+7, so for 16x16 tiles groups
+    // g and g+2 take chunks differing in the lowest bit (0,2,1,3), which keeps
+    // the two halves of every LDS cycle in disjoint banks.
     const int lrow = lane % MT;
     const int sw = swz(lrow);
+    const int grp = lane / MT;
+    const int cperm = MT == 16 ? (((grp & 1) << 1) | (grp >> 1)) : grp;
     int kpos[NKS];
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks)
-        kpos[ks] = lrow * ROWB + ((((MK / 8) * ks + lane / MT) ^ sw) << 4);
+        kpos[ks] = lrow * ROWB + ((((MK / 8) * ks + cperm) ^ sw) << 4);
     int a_base[MI], b_base[NJ];
 #pragma unroll
     for (int i = 0; i < MI; ++i) a_base[i] = (wr * WM + i * MT) * ROWB;

@@ -186,9 +186,8 @@ __device__ void write_route(uint32_t taken, int nv, void* idx, int idx_dtype, in
     int before = 0;
 #pragma unroll
     for (int v = 0; v < MAXV; ++v) {
-        if (v >= nv) break;
-        bool mine = (taken >> v) & 1u;
-        uint64_t bal = __ballot(mine);
+        const bool mine = v < nv && ((taken >> v) & 1u);
+        const uint64_t bal = __ballot(mine);
         if (mine) {
             uint64_t lt = lane ? (bal & ((~0ull) >> (64 - lane))) : 0ull;
             int rank = before + __popcll(lt);
