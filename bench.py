@@ -55,18 +55,27 @@ def parse():
     return ap.parse_args()
 
 
-def profiled_traffic(workload, kernel="grouped_gemm_mfma<0>", source="gemm.hip"):
+KERNEL_SOURCES = ("gemm.hip", "common.h")
+
+
+def kernel_source_hash():
+    """sha256 over the sources the forward GEMM kernels are compiled from."""
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, "paper_2606_00395_amd", "csrc", name), "rb").read())
+    return h.hexdigest()
+
+
+def profiled_traffic(workload, kernel="grouped_gemm_mfma<0>"):
     """HBM bytes per launch of the dominant kernel from the committed rocprofv3
     summary (FETCH_SIZE + WRITE_SIZE, copy-calibrated), or None when there is
-    no summary for this workload or the kernel source changed since it was taken."""
+    no summary for this workload or the kernel sources changed since it was taken."""
     path = os.path.join(ROOT, "profiles", f"replay_and_route_kernels_{workload}.txt")
     if not os.path.exists(path):
         return None
     text = open(path).read()
-    m = re.search(r"gemm_source_sha256: ([0-9a-f]+)", text)
-    src = os.path.join(ROOT, "paper_2606_00395_amd", "csrc", source)
-    cur = hashlib.sha256(open(src, "rb").read()).hexdigest()
-    if not m or m.group(1) != cur:
+    m = re.search(r"kernel_source_sha256: ([0-9a-f]+)", text)
+    if not m or m.group(1) != kernel_source_hash():
         return None
     m = re.search(r"traffic_bytes_per_launch\[" + re.escape(kernel) + r"\]: fetch (\d+) write (\d+)",
                   text)

@@ -14,12 +14,13 @@
 //
 // bf16 path: four grouped GEMMs on v_mfma_f32_32x32x16_bf16 with the tile
 // shape of the forward kernels (256 x 256 output tile, K slices of 64, two
-// LDS stages, eight wavefronts of 64 x 128).  An operand whose K index runs
-// along its rows in memory (the weights in the input-gradient GEMMs, both
-// operands of the token-contracted weight-gradient GEMMs) is read with 16-byte
-// loads into registers, one 8 x 8 block per thread, transposed there and
-// written to LDS as 16-byte rows of eight consecutive K values, in the same
-// swizzled layout the direct-to-LDS copies of K-contiguous operands produce.
+// LDS stages, eight wavefronts of 64 x 128), every operand copied global ->
+// LDS by 16-byte direct-to-LDS loads.  An operand whose K index runs along
+// its rows in memory (the weights in the input-gradient GEMMs, both operands
+// of the token-contracted weight-gradient GEMMs) is kept K-major in LDS and
+// its MFMA fragments are read with the transposing LDS read of gfx950
+// (ds_read_b64_tr_b16), so no operand passes through registers on its way in.
+// The router weight gradient is a separate pass over the x rows.
 // Every gradient is written exactly once (no atomics): results are
 // deterministic and overwrite the outputs.
 #include "common.h"
@@ -28,7 +29,9 @@ namespace pr2 {
 namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef short v4s __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) v4s lds_v4s;
 
 constexpr int BM = 256;         // output tile rows
 constexpr int BN = 256;         // output tile columns
@@ -52,9 +55,6 @@ struct BwdArgs {
     const int* tile_count;
     const int* offsets;      // [N+1] first permuted row of each expert
     const int* order;        // [N] experts by decreasing route count (ties: lower id)
-    const float* dp_perm;    // [T*k] router-logit gradient per permuted row
-    float* dW_r;             // [d, N] (gate/up weight-gradient launch)
-    float* db_r;             // [N] or null
     int k, N, d, m, Tk;
     int ntn;                 // DH, DX: 256-column panels per tile
     const bf16_t* x;
@@ -91,7 +91,7 @@ __device__ __forceinline__ uint32_t pack_bf(float lo, float hi) {
 // gradient of the computed output.
 __device__ __forceinline__ void swiglu_bwd(float a, float u, float G, float g, bool round_h,
                                            float& da, float& du, float& hg, float& hG) {
-    const float sig = 1.0f / (1.0f + __expf(-a));
+    const float sig = __builtin_amdgcn_rcpf(1.0f + __expf(-a));   // as the forward's silu
     const float s = a * sig;
     float H = s * u;
     if (round_h) H = bf16_to_f32(f32_to_bf16(H));
@@ -102,19 +102,8 @@ __device__ __forceinline__ void swiglu_bwd(float a, float u, float G, float g, b
     hG = H * G;
 }
 
-// One operand whose K index runs along memory rows: this thread's 8 x 8 block
-// covers K values kt*BK + 8*c .. +7 and 8 tile rows starting at column `col`
-// of the source rows.
-struct KRows {
-    const bf16_t* b0;       // rows with K index < ksplit
-    const bf16_t* b1;       // rows with K index >= ksplit (row K index - ksplit)
-    int ksplit;
-    uint32_t ld;            // elements between source rows
-    uint32_t col;           // first element of this thread's 8 columns
-    int rbase;              // first permuted row (direct) or perm_src base (gathered)
-    int klen;               // K values; beyond it the operand is zero
-    bool gather;            // source row = perm_src[rbase + K] / k (a token row)
-};
+// all-zero source row for the copies of K rows past an expert's last route
+__device__ __attribute__((aligned(16))) const bf16_t kZeroRow[BN] = {};
 
 template <int MODE>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -169,94 +158,27 @@ bwd_gemm(BwdArgs g) {
     const bool active = wr * WM < rows;
     const bool dma = kRowTiles && half == 0;
 
-    // ---- operand loading
-    const int tt = tid & 255;
-    const int kc = tt & 7;               // K chunk of this thread's block
-    const int rb = tt >> 3;              // 8-row block of the tile
-    KRows kr{};
-    {
-        const int64_t ew = (int64_t)expert * g.m * g.d;   // elements per expert matrix
-        if (half == 1) {
-            if (MODE == DH) {
-                kr = {g.Wd + ew, g.Wd + ew, g.d, (uint32_t)g.m, (uint32_t)(pn * BN + 8 * rb), 0,
-                      g.d, false};
-            } else if (MODE == DX) {
-                kr = {g.Wg + ew, g.Wu + ew, g.m, (uint32_t)g.d, (uint32_t)(pn * BN + 8 * rb), 0,
-                      2 * g.m, false};
-            } else if (MODE == WD) {
-                kr = {g.Hg, g.Hg, klen, (uint32_t)g.m, (uint32_t)(ct * BN + 8 * rb), row0, klen,
-                      false};
-            } else {
-                kr = {g.x, g.x, klen, (uint32_t)g.d, (uint32_t)(ct * BN + 8 * rb), row0, klen, true};
-            }
-        } else if (MODE == WD) {
-            kr = {g.dy, g.dy, klen, (uint32_t)g.d, (uint32_t)(rt * BM + 8 * rb), row0, klen, true};
-        } else if (MODE == WGU) {
-            kr = {g.AU, g.AU, klen, (uint32_t)(2 * g.m), (uint32_t)(rt * BM + 8 * rb), row0, klen,
-                  false};
-        }
-    }
-    u32x4 st[8];
-    // The gate/up weight-gradient items of the first row tile also form the
-    // router gradient from the x rows they stream: dW_r[:, e] = sum_q dp_q x_t(q)
-    // over this item's 256 columns, db_r[e] = sum_q dp_q.
-    const bool rgrad = MODE == WGU && rt == 0 && half == 1;
-    float dpr[8];
-    float racc[8];
-#pragma unroll
-    for (int v = 0; v < 8; ++v) racc[v] = 0.0f;
-    float dbacc = 0.0f;
-    auto kload = [&](int kt) {
-        const int kb = kt * BK;
-        const bool hi = kb >= kr.ksplit;
-        const bf16_t* b = hi ? kr.b1 : kr.b0;
-        const int kshift = hi ? kr.ksplit : 0;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int kk = kb + 8 * kc + i;
-            u32x4 v = {0u, 0u, 0u, 0u};
-            dpr[i] = 0.0f;
-            if (kk < kr.klen) {
-                const int row = kr.gather ? g.perm_src[kr.rbase + kk] / g.k : kr.rbase + kk - kshift;
-                v = *(const u32x4*)(b + ((uint32_t)row * kr.ld + kr.col));
-                if (rgrad) dpr[i] = g.dp_perm[kr.rbase + kk];
-            }
-            st[i] = v;
-        }
-    };
-    auto racc_add = [&]() {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-#pragma unroll
-            for (int w = 0; w < 4; ++w) {
-                racc[2 * w] = fmaf(dpr[i], bf_lo(st[i][w]), racc[2 * w]);
-                racc[2 * w + 1] = fmaf(dpr[i], bf_hi(st[i][w]), racc[2 * w + 1]);
-            }
-            dbacc += dpr[i];
-        }
-    };
-    auto kstore = [&](int stage) {
-        unsigned char* sb = lds + stage * STAGEB + (half ? BM * ROWB : 0);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int R = 8 * rb + j;
-            const int w = j >> 1;
-            u32x4 o;
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-                o[q] = (j & 1) ? ((st[2 * q][w] >> 16) | (st[2 * q + 1][w] & 0xffff0000u))
-                               : ((st[2 * q][w] & 0xffffu) | (st[2 * q + 1][w] << 16));
-            *(u32x4*)(sb + R * ROWB + ((kc ^ swz(R)) << 4)) = o;
-        }
-    };
+    // ---- operand loading.  Both operands are copied global -> LDS with
+    // 16-byte direct-to-LDS loads; wavefronts 0-3 copy the row operand (C
+    // rows), 4-7 the column operand.  A K-contiguous operand (the gathered dy
+    // rows of DH, the da | du rows of DX) is stored as 256 tile rows of 128
+    // bytes (64 K values), 16-byte chunks XOR-swizzled per row.  A K-strided
+    // operand (the weights of DH and DX, both operands of WD and WGU) is
+    // stored K-major: 64 K rows of 512 bytes (the tile's 256 columns), chunk c
+    // of K row kr at position c ^ 4 (kr & 3).  Both forms fill 32 KiB.
+    constexpr bool kStridedA = (MODE == WD || MODE == WGU);
+    const bool strided = half == 1 || kStridedA;
+    const int wq = wave & 3;
+    const int64_t ew = (int64_t)expert * g.m * g.d;      // elements per expert matrix
 
-    // direct-to-LDS copies of the K-contiguous row operand (DH: gathered dy, DX: da | du)
+    // K-contiguous rows (DH: gathered dy, DX: da | du): copy group i of this
+    // wavefront moves tile rows 8 (8 wq + i) .. +7
     const bf16_t* sbase = MODE == DH ? g.dy : g.AU;
     uint32_t soff[kGroups];
-    if (kRowTiles) {
+    if (!kStridedA) {
 #pragma unroll
         for (int i = 0; i < kGroups; ++i) {
-            const int r = (wave & 3) * (kGroups * 8) + i * 8 + lane / 8;
+            const int r = wq * (kGroups * 8) + i * 8 + lane / 8;
             const int chunk = (lane % 8) ^ swz(r);
             const int rr = r < rows ? r : 0;
             uint32_t off;
@@ -267,13 +189,60 @@ bwd_gemm(BwdArgs g) {
             soff[i] = off + chunk * 8;
         }
     }
-    auto issue = [&](int stage, int k0) {
+    // K-strided: copy instruction i of this wavefront moves K rows
+    // kr = 16 wq + 2 i (lanes 0-31) and kr + 1 (lanes 32-63) of the slice;
+    // lane l lands at chunk position l % 32 and so loads chunk
+    // (l % 32) ^ 4 (kr & 3) of its K row.  Rows at or past klen read zeros.
+    const int krl = 16 * wq + (lane >> 5);
+    int ccol[kGroups];
+#pragma unroll
+    for (int i = 0; i < kGroups; ++i) ccol[i] = 8 * ((lane & 31) ^ (4 * ((krl + 2 * i) & 3)));
+    // gathered K-strided operand (WD: dy rows, WGU: x rows): token rows of the
+    // next slice to copy, fetched one slice ahead
+    constexpr bool kHasGather = (MODE == WD || MODE == WGU);
+    const bool gathered = (MODE == WD && half == 0) || (MODE == WGU && half == 1);
+    int gtok[kGroups];
+    auto fetch_tok = [&](int kt) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < kGroups; ++i) {
-            const int grp = (wave & 3) * kGroups + i;
-            __builtin_amdgcn_global_load_lds((const void*)(sbase + (soff[i] + (uint32_t)k0)),
-                                             (lds_void*)&lds[stage * STAGEB + grp * 1024], 16, 0,
-                                             0);
+            const int K = kt * BK + krl + 2 * i;
+            gtok[i] = K < klen ? min(max(g.perm_src[row0 + K], 0), g.Tk - 1) / g.k : -1;
+        }
+    };
+    auto issue_strided = [&](int stage, int kt) __attribute__((always_inline)) {
+        unsigned char* dst = lds + stage * STAGEB + (half ? BM * ROWB : 0) + wq * (16 * 512);
+#pragma unroll
+        for (int i = 0; i < kGroups; ++i) {
+            const int K = kt * BK + krl + 2 * i;
+            const bf16_t* src;
+            if (MODE == DH) {
+                src = g.Wd + ew + (int64_t)K * g.m + pn * BN;
+            } else if (MODE == DX) {
+                src = (K < g.m ? g.Wg + ew + (int64_t)K * g.d : g.Wu + ew + (int64_t)(K - g.m) * g.d) +
+                      pn * BN;
+            } else if (MODE == WD) {
+                if (half == 0) src = gtok[i] >= 0 ? g.dy + (int64_t)gtok[i] * g.d + rt * BM : kZeroRow;
+                else src = K < klen ? g.Hg + (int64_t)(row0 + K) * g.m + ct * BN : kZeroRow;
+            } else {
+                if (half == 0) src = K < klen ? g.AU + (int64_t)(row0 + K) * (2 * g.m) + rt * BM : kZeroRow;
+                else src = gtok[i] >= 0 ? g.x + (int64_t)gtok[i] * g.d + ct * BN : kZeroRow;
+            }
+            __builtin_amdgcn_global_load_lds((const void*)(src + ccol[i]), (lds_void*)(dst + i * 1024),
+                                             16, 0, 0);
+        }
+    };
+    auto issue = [&](int stage, int kt) __attribute__((always_inline)) {
+        if (strided) {
+            issue_strided(stage, kt);
+            if (kHasGather && gathered && kt + 1 < (klen + BK - 1) / BK) fetch_tok(kt + 1);
+        } else {
+#pragma unroll
+            for (int i = 0; i < kGroups; ++i) {
+                const int grp = wq * kGroups + i;
+                __builtin_amdgcn_global_load_lds(
+                    (const void*)(sbase + (soff[i] + (uint32_t)(kt * BK))),
+                    (lds_void*)&lds[stage * STAGEB + grp * 1024], 16, 0, 0);
+            }
         }
     };
 
@@ -285,46 +254,57 @@ bwd_gemm(BwdArgs g) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
+    // MFMA fragments: lane l supplies K values 8 (l / 32) .. +7 of the K=16
+    // step for tile row (or column) l % 32 of a 32-block.
+    // K-contiguous: one 16-byte read at the swizzled chunk.
     const int lrow = lane & 31;
     const int sw = swz(lrow);
     int kpos[BK / 16];
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) kpos[ks] = lrow * ROWB + (((2 * ks + (lane >> 5)) ^ sw) << 4);
-    int a_base[MI], b_base[NJ];
+    // K-strided: two ds_read_b64_tr_b16.  Within each group of 16 lanes, lane
+    // s reads 4 values of K row 8 (g/2) + s/4 (+4 for the second read) at
+    // columns 16 (g%2) + 4 (s%4) .. +3 of the block; the instruction hands
+    // lane s value s%4 of the reads of lanes s/4 + 4j, j = 0..3, so each lane
+    // ends up with four consecutive K values of column 16 (g%2) + s.
+    const int s16 = lane & 15, g4 = lane >> 4;
+    const int nl = 16 * (g4 & 1) + 4 * (s16 & 3);
+    const int kl = 8 * (g4 >> 1) + (s16 >> 2);
+    const int tsw = (nl >> 3) ^ (4 * (kl & 3));
+    auto tr_pos = [&](int cb) { return kl * 512 + ((((cb >> 3) ^ tsw)) << 4) + ((nl & 4) << 1); };
+    int a_pos[MI], b_pos[NJ];
 #pragma unroll
-    for (int i = 0; i < MI; ++i) a_base[i] = (wr * WM + i * 32) * ROWB;
+    for (int i = 0; i < MI; ++i)
+        a_pos[i] = kStridedA ? tr_pos(wr * WM + i * 32) : (wr * WM + i * 32) * ROWB;
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) b_base[j] = (BM + wc * WN + j * 32) * ROWB;
+    for (int j = 0; j < NJ; ++j) b_pos[j] = BM * ROWB + tr_pos(wc * WN + j * 32);
 
     const int nk = (klen + BK - 1) / BK;
     if (nk > 0) {
-        if (dma) {
-            issue(0, 0);
-        } else {
-            kload(0);
-            wait_vmcnt<0>();
-            if (rgrad) racc_add();
-            kstore(0);
-        }
+        if (kHasGather && gathered) fetch_tok(0);
+        issue(0, 0);
     }
     for (int kt = 0; kt < nk; ++kt) {
         wait_vmcnt<0>();
         __syncthreads();
-        const bool more = kt + 1 < nk;
-        if (more) {
-            if (dma) issue((kt + 1) % NSTAGE, (kt + 1) * BK);
-            else kload(kt + 1);
-        }
+        if (kt + 1 < nk) issue((kt + 1) % NSTAGE, kt + 1);
         if (active) {
             const unsigned char* base = lds + (kt % NSTAGE) * STAGEB;
             bf16x8 fa[2][MI], fb[2][NJ];
-            auto read_frags = [&](int buf, int ks) {
+            auto tr_frag = [&](int pos, int ks) __attribute__((always_inline)) {
+                const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_v4s*)(base + pos + ks * (16 * 512)));
+                const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_v4s*)(base + pos + ks * (16 * 512) + 4 * 512));
+                return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+            };
+            auto read_frags = [&](int buf, int ks) __attribute__((always_inline)) {
 #pragma unroll
                 for (int i = 0; i < MI; ++i)
-                    fa[buf][i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + a_base[i] + kpos[ks]));
+                    fa[buf][i] = kStridedA ? tr_frag(a_pos[i], ks)
+                                           : __builtin_bit_cast(bf16x8, *(const u32x4*)(base + a_pos[i] + kpos[ks]));
 #pragma unroll
-                for (int j = 0; j < NJ; ++j)
-                    fb[buf][j] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + b_base[j] + kpos[ks]));
+                for (int j = 0; j < NJ; ++j) fb[buf][j] = tr_frag(b_pos[j], ks);
             };
             read_frags(0, 0);
 #pragma unroll
@@ -339,27 +319,6 @@ bwd_gemm(BwdArgs g) {
                             fb[ks & 1][j], fa[ks & 1][i], acc[i][j], 0, 0, 0);
                 __builtin_amdgcn_sched_barrier(0);
             }
-        }
-        if (more && !dma) {
-            wait_vmcnt<0>();
-            if (rgrad) racc_add();
-            kstore((kt + 1) % NSTAGE);
-        }
-    }
-    if (rgrad) {
-        // the 8 threads of one 8-column block (consecutive lanes) hold partial
-        // sums over different rows: add them in a fixed butterfly order
-#pragma unroll
-        for (int off = 1; off < 8; off <<= 1) {
-#pragma unroll
-            for (int v = 0; v < 8; ++v) racc[v] += __shfl_xor(racc[v], off, 64);
-            dbacc += __shfl_xor(dbacc, off, 64);
-        }
-        if (kc == 0) {
-#pragma unroll
-            for (int v = 0; v < 8; ++v)
-                g.dW_r[(int64_t)(ct * BN + 8 * rb + v) * g.N + expert] = racc[v];
-            if (g.db_r && ct == 0 && rb == 0) g.db_r[expert] = dbacc;
         }
     }
     if (!active) return;
@@ -379,14 +338,25 @@ bwd_gemm(BwdArgs g) {
             bf16_t* au = g.AU + q * ldau;
             bf16_t* hg = g.Hg + q * g.m;
             float part = 0.0f;
+            // all of this row's a, u loads first (the stores below write the
+            // same array, so the compiler would not move later loads above them)
+            uint2 avs[NJ][4], uvs[NJ][4];
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                for (int a4 = 0; a4 < 4; ++a4) {
+                    const int col = pn * BN + wc * WN + j * 32 + 8 * a4 + ncol0;
+                    avs[j][a4] = ok ? *(const uint2*)(au + col) : make_uint2(0u, 0u);
+                    uvs[j][a4] = ok ? *(const uint2*)(au + g.m + col) : make_uint2(0u, 0u);
+                }
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
 #pragma unroll
                 for (int a4 = 0; a4 < 4; ++a4) {
                     const int col = pn * BN + wc * WN + j * 32 + 8 * a4 + ncol0;
                     if (ok) {
-                        const uint2 av = *(const uint2*)(au + col);
-                        const uint2 uv = *(const uint2*)(au + g.m + col);
+                        const uint2 av = avs[j][a4];
+                        const uint2 uv = uvs[j][a4];
                         const float a[4] = {bf_lo(av.x), bf_hi(av.x), bf_lo(av.y), bf_hi(av.y)};
                         const float u[4] = {bf_lo(uv.x), bf_hi(uv.x), bf_lo(uv.y), bf_hi(uv.y)};
                         float da[4], du[4], hgv[4];
@@ -602,20 +572,41 @@ router_wgrad_kernel(const T* x, const int* perm_src, const int* offsets, const f
     float acc[8];
 #pragma unroll
     for (int v = 0; v < 8; ++v) acc[v] = 0.0f;
-    for (int q = q0 + rg; q < q1; q += 8) {
-        const float w = dp_perm[q];
-        const T* xr = x + (int64_t)(perm_src[q] / k) * d;
-        if (sizeof(T) == 2 && i0 + 8 <= d) {
-            const u32x4 v = *(const u32x4*)(xr + i0);
+    // each thread sums routes q0 + rg, q0 + rg + 8, ... in that order; the
+    // loads of kRwU consecutive ones are issued together
+    constexpr int kRwU = 8;
+    for (int qb = q0 + rg; qb < q1; qb += 8 * kRwU) {
+        int tok[kRwU];
+        float w[kRwU];
 #pragma unroll
-            for (int h = 0; h < 4; ++h) {
-                acc[2 * h] = fmaf(w, bf_lo(v[h]), acc[2 * h]);
-                acc[2 * h + 1] = fmaf(w, bf_hi(v[h]), acc[2 * h + 1]);
+        for (int u = 0; u < kRwU; ++u) {
+            const int q = qb + 8 * u;
+            tok[u] = q < q1 ? perm_src[q] / k : -1;
+            w[u] = q < q1 ? dp_perm[q] : 0.0f;
+        }
+        if (sizeof(T) == 2 && i0 + 8 <= d) {
+            u32x4 v[kRwU];
+#pragma unroll
+            for (int u = 0; u < kRwU; ++u)
+                v[u] = tok[u] >= 0 ? *(const u32x4*)(x + (int64_t)tok[u] * d + i0) : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int u = 0; u < kRwU; ++u) {
+                if (tok[u] < 0) continue;
+#pragma unroll
+                for (int h = 0; h < 4; ++h) {
+                    acc[2 * h] = fmaf(w[u], bf_lo(v[u][h]), acc[2 * h]);
+                    acc[2 * h + 1] = fmaf(w[u], bf_hi(v[u][h]), acc[2 * h + 1]);
+                }
             }
         } else {
 #pragma unroll
-            for (int v = 0; v < 8; ++v)
-                if (i0 + v < d) acc[v] = fmaf(w, Act<T>::to_f32(xr[i0 + v]), acc[v]);
+            for (int u = 0; u < kRwU; ++u) {
+                if (tok[u] < 0) continue;
+                const T* xr = x + (int64_t)tok[u] * d;
+#pragma unroll
+                for (int v = 0; v < 8; ++v)
+                    if (i0 + v < d) acc[v] = fmaf(w[u], Act<T>::to_f32(xr[i0 + v]), acc[v]);
+            }
         }
     }
 #pragma unroll
@@ -814,9 +805,6 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
     g.tile_count = w.tile_count;
     g.offsets = w.offsets;
     g.order = ws.order;
-    g.dp_perm = ws.dp_perm;
-    g.dW_r = out.dW_r;
-    g.db_r = out.db_r;
     g.k = d.k;
     g.N = d.N;
     g.d = d.d;
@@ -888,7 +876,6 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
         {
-            // also writes dW_r and db_r
             LaunchScope scope("bwd_wgrad_gate_up", s);
             hipLaunchKernelGGL(bwd_gemm<WGU>,
                                dim3((unsigned)(kNumXcd * experts_per_xcd * (2 * d.m / BM) * (d.d / BN))),
@@ -899,6 +886,8 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
         e = bf ? launch_generic_gemms<bf16_t>(d, x, W_gate, W_up, dy, ws, out, s)
                : launch_generic_gemms<float>(d, x, W_gate, W_up, dy, ws, out, s);
         if (e != hipSuccess) return e;
+    }
+    {
         LaunchScope scope("bwd_router_wgrad", s);
         dim3 grid((unsigned)d.N, (unsigned)((d.d + 255) / 256));
         if (bf)

@@ -19,12 +19,11 @@ __device__ __forceinline__ float bf16_to_f32(bf16_t v) {
     return __uint_as_float(((uint32_t)v) << 16);
 }
 
-// round to nearest even; NaN stays NaN
+// round to nearest even, NaN stays a (quiet) NaN: gfx950's v_cvt_pk_bf16_f32,
+// which gives bitwise the integer rounding u + 0x7fff + ((u >> 16) & 1) for
+// every non-NaN pattern and sets the quiet bit of NaNs
 __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (bf16_t)(u >> 16);
+    return __builtin_bit_cast(bf16_t, (__bf16)f);
 }
 
 template <typename T> struct Act;
