@@ -55,27 +55,26 @@ def parse():
     return ap.parse_args()
 
 
-KERNEL_SOURCES = ("gemm.hip", "common.h")
-
-
-def kernel_source_hash():
-    """sha256 over the sources the forward GEMM kernels are compiled from."""
+def kernel_source_hash(names):
+    """sha256 over the given kernel source files of csrc/, in order."""
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
+    for name in names:
         h.update(open(os.path.join(ROOT, "paper_2606_00395_amd", "csrc", name), "rb").read())
     return h.hexdigest()
 
 
-def profiled_traffic(workload, kernel="grouped_gemm_mfma<0>"):
-    """HBM bytes per launch of the dominant kernel from the committed rocprofv3
-    summary (FETCH_SIZE + WRITE_SIZE, copy-calibrated), or None when there is
-    no summary for this workload or the kernel sources changed since it was taken."""
-    path = os.path.join(ROOT, "profiles", f"replay_and_route_kernels_{workload}.txt")
+def profiled_traffic(profile, kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 summary
+    `profiles/<profile>` (FETCH_SIZE + WRITE_SIZE, copy-calibrated), or None
+    when there is no such summary or a source it names changed since it was
+    taken."""
+    path = os.path.join(ROOT, "profiles", profile)
     if not os.path.exists(path):
         return None
     text = open(path).read()
+    srcs = re.search(r"kernel_sources: (.+)", text)
     m = re.search(r"kernel_source_sha256: ([0-9a-f]+)", text)
-    if not m or m.group(1) != kernel_source_hash():
+    if not srcs or not m or m.group(1) != kernel_source_hash(srcs.group(1).split()):
         return None
     m = re.search(r"traffic_bytes_per_launch\[" + re.escape(kernel) + r"\]: fetch (\d+) write (\d+)",
                   text)
@@ -273,7 +272,8 @@ def run_forward(args, shape, dev):
                       "bf16" if shape.act == "bf16" else "f32", layer_config(shape))
     out["roofline"] = {"bound": "mfma", "kernel": dominant, "achieved": achieved, "peak": peak,
                        "unit": "TFLOP/s", "frac": achieved / peak,
-                       "traffic": profiled_traffic(shape.name)}
+                       "traffic": profiled_traffic(f"replay_and_route_kernels_{shape.name}.txt",
+                                                  "grouped_gemm_mfma<0>")}
     out["hip_graph"] = {"ms_per_step": ms_graph, "value": T / (ms_graph * 1e-3),
                         "note": "the same step captured once and replayed as a HIP graph"}
     out["kernels_ms"] = {n: round(v, 5) for n, v in kern.items()}
@@ -331,7 +331,9 @@ def run_backward(args, shape, dev):
     out = base_record(args, "MoE-layer tokens/sec (replay backward: dx, expert and router grads)",
                       T / (ms * 1e-3), "tokens/s", ms, "bf16", layer_config(shape))
     out["roofline"] = {"bound": "mfma", "kernel": dominant, "achieved": achieved, "peak": peak,
-                       "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None}
+                       "unit": "TFLOP/s", "frac": achieved / peak,
+                       "traffic": profiled_traffic(f"replay_backward_kernels_{shape.name}.txt",
+                                                   "bwd_gemm<3>")}
     out["kernels_ms"] = {n: round(v, 5) for n, v in kern.items()}
     out["mfma_frac"] = {n: f * unit / (kern[n] * 1e-3) / C.PEAK_BF16_FLOPS
                         for n, f in flops.items() if n in kern}
