@@ -819,7 +819,12 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
         // done with step kt-1, whose stage is refilled next
         if (kt + NSTAGE - 2 < nk) router_wait_vmcnt<(NSTAGE - 2) * GPW>();
         else router_wait_vmcnt<0>();
-        __syncthreads();
+        // a plain barrier: __syncthreads() would also wait for every copy
+        // still in flight (vmcnt(0)) and undo the pipelining
+        __builtin_amdgcn_s_waitcnt(0xc07f);      // lgkmcnt(0)
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
         if (kt + NSTAGE - 1 < nk) issue((kt + NSTAGE - 1) % NSTAGE, kt + NSTAGE - 1);
         const unsigned char* base = lds + (kt % NSTAGE) * RT::STAGEB;
         bf16x8 fa[2];
