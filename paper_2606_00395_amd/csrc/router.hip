@@ -476,34 +476,47 @@ replay_gates_kernel(ProjArgs a, ReplayOut o) {
 // ------------------------------------------- 16-lane group epilogues ----
 // The MFMA path runs its epilogues four tokens per wavefront: the 16 lanes of
 // group g = lane / 16 own one token, lane l16 = lane % 16 holding experts
-// j = 16 v + l16 (v < MAXV16).  Reductions are butterflies inside the group;
-// sums are then taken from the group's first lane so that every lane uses
-// the same value.
+// j = 16 v + l16 (v < MAXV16).  Reductions inside the group are DPP row
+// rotations (by 8, 4, 2, 1); floating-point sums are then taken from the
+// group's first lane so that every lane uses the same value.
 
+// row_ror:n of the 16-lane row (DPP): every lane reads lane (l16 + n) % 16 of its row
+template <int N_>
+__device__ __forceinline__ int row_ror(int v) {
+    static_assert(N_ >= 1 && N_ < 16, "row rotate");
+    return __builtin_amdgcn_update_dpp(0, v, 0x120 + N_, 0xf, 0xf, false);
+}
 __device__ __forceinline__ uint32_t gmax_u32(uint32_t v) {
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) v = max(v, (uint32_t)__shfl_xor((int)v, off, 16));
-    return v;
+    v = max(v, (uint32_t)row_ror<8>((int)v));
+    v = max(v, (uint32_t)row_ror<4>((int)v));
+    v = max(v, (uint32_t)row_ror<2>((int)v));
+    return max(v, (uint32_t)row_ror<1>((int)v));
 }
 __device__ __forceinline__ int gmin_i32(int v) {
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) v = min(v, __shfl_xor(v, off, 16));
-    return v;
+    v = min(v, row_ror<8>(v));
+    v = min(v, row_ror<4>(v));
+    v = min(v, row_ror<2>(v));
+    return min(v, row_ror<1>(v));
 }
 __device__ __forceinline__ float gmax_f32(float v) {
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) v = fmaxf(v, __shfl_xor(v, off, 16));
-    return v;
+    v = fmaxf(v, __int_as_float(row_ror<8>(__float_as_int(v))));
+    v = fmaxf(v, __int_as_float(row_ror<4>(__float_as_int(v))));
+    v = fmaxf(v, __int_as_float(row_ror<2>(__float_as_int(v))));
+    return fmaxf(v, __int_as_float(row_ror<1>(__float_as_int(v))));
 }
+// each lane adds in its own rotation order; the group's first lane's sum is used by all
 __device__ __forceinline__ float gsum_f32(float v) {
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) v += __shfl_xor(v, off, 16);
+    v += __int_as_float(row_ror<8>(__float_as_int(v)));
+    v += __int_as_float(row_ror<4>(__float_as_int(v)));
+    v += __int_as_float(row_ror<2>(__float_as_int(v)));
+    v += __int_as_float(row_ror<1>(__float_as_int(v)));
     return __shfl(v, 0, 16);
 }
 __device__ __forceinline__ int gsum_i32(int v) {
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) v += __shfl_xor(v, off, 16);
-    return v;
+    v += row_ror<8>(v);
+    v += row_ror<4>(v);
+    v += row_ror<2>(v);
+    return v + row_ror<1>(v);
 }
 
 // Rollout epilogue of token t (valid: t < T) by one 16-lane group.

@@ -147,3 +147,39 @@ def test_route_empty_batch():
     Wr = torch.zeros((64, 8), device="cuda")
     idx = torch.empty((0, 2), dtype=torch.int32, device="cuda")
     B.route_predict(x, Wr, None, None, None, 2, idx)
+
+
+def test_route_is_batch_invariant():
+    """A token's logits, route and weights do not depend on the batch it is
+    routed in: a decode-sized batch (256, 1000 and a single token) gives
+    bitwise the results of the same tokens inside a 2048-token batch, in the
+    rollout (with and without logits, i.e. with the predictor as separate
+    columns or folded into the router weights) and in the replay router
+    (current top-k and route KL of the diagnostics)."""
+    torch = torch_mod()
+    from paper_2606_00395_amd import binding as B
+    s = W.WORKLOADS["qwen3_30b_T16384"].with_(T=2048)
+    L = W.layer_inputs(s, 7, experts=False)
+    for T_small in (256, 1000, 1):
+        Ls = {n: (v[:T_small] if n == "x" else v) for n, v in L.items()}
+        for want_logits in (True, False):
+            big = run_route(L, s, s.k, logits=want_logits)
+            small = run_route(Ls, s.with_(T=T_small), s.k, logits=want_logits)
+            for n in ("idx", "gate") + (("logits",) if want_logits else ()):
+                np.testing.assert_array_equal(small[n], big[n][:T_small],
+                                              err_msg=f"T={T_small} {n} logits={want_logits}")
+        # the replay router: current top-k and route KL against given reference logits
+        x = to_dev(L["x"], s.act)
+        Wr, br = to_dev(L["W_r"]), to_dev(L["beta"])
+        idx = torch.from_numpy(big["idx"]).to("cuda")
+        zref = torch.from_numpy(np.ascontiguousarray(O.router_logits(L["x"], L["W_r"], L["beta"]),
+                                                     dtype=np.float32)).to("cuda")
+        outs = []
+        for T in (s.T, T_small):
+            cur = torch.empty((T, s.k), dtype=torch.int32, device="cuda")
+            kl = torch.empty((T,), dtype=torch.float32, device="cuda")
+            B.route_diagnostics(x[:T], idx[:T], Wr, br, zref[:T], cur_idx_out=cur, kl_out=kl)
+            torch.cuda.synchronize()
+            outs.append((cur.cpu().numpy(), kl.cpu().numpy()))
+        np.testing.assert_array_equal(outs[1][0], outs[0][0][:T_small])
+        np.testing.assert_array_equal(outs[1][1], outs[0][1][:T_small])
