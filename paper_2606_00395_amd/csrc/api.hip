@@ -99,9 +99,9 @@ static size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 // when no logits are wanted, [W_r | A] (N + r columns) otherwise.
 static size_t route_split_need(const pr2_moe_desc& d) {
     size_t need = 0;
-    if (router_mfma_ok(d, d.N)) need = router_split_bytes(d.N, d.d);
+    if (router_mfma_ok(d, d.N)) need = router_split_bytes(d.N, d);
     if (router_mfma_ok(d, d.N + d.r)) {
-        size_t b = router_split_bytes(d.N + d.r, d.d);
+        size_t b = router_split_bytes(d.N + d.r, d);
         need = b > need ? b : need;
     }
     return need;
@@ -137,7 +137,7 @@ static ReplayWs moe_ws_layout(const pr2_moe_desc& d, void* base, size_t split_by
 }
 
 ReplayWs replay_ws_layout(const pr2_moe_desc& d, void* base) {
-    return moe_ws_layout(d, base, router_mfma_ok(d, d.N) ? router_split_bytes(d.N, d.d) : 0);
+    return moe_ws_layout(d, base, router_mfma_ok(d, d.N) ? router_split_bytes(d.N, d) : 0);
 }
 
 static ReplayWs rollout_ws_layout(const pr2_moe_desc& d, void* base) {
@@ -167,7 +167,7 @@ BwdWs bwd_ws_layout(const pr2_moe_desc& d, void* base) {
 }
 
 static size_t diag_ws_bytes(const pr2_moe_desc& d) {
-    return router_mfma_ok(d, d.N) ? router_split_bytes(d.N, d.d) + 256 : 0;
+    return router_mfma_ok(d, d.N) ? router_split_bytes(d.N, d) + 256 : 0;
 }
 
 static PredLossWs pred_ws_layout(const pr2_moe_desc& d, void* base) {
@@ -185,7 +185,7 @@ static PredLossWs pred_ws_layout(const pr2_moe_desc& d, void* base) {
     w.dz = (double*)take(sizeof(double) * T * d.N);
     w.w = (double*)take(sizeof(double) * T * d.r);
     w.kl = (double*)take(sizeof(double) * T);
-    w.wsplit = take(router_mfma_ok(d, d.N) ? router_split_bytes(d.N, d.d) : 0);
+    w.wsplit = take(router_mfma_ok(d, d.N) ? router_split_bytes(d.N, d) : 0);
     w.bytes = off + 256;
     return w;
 }

@@ -113,7 +113,9 @@ struct FeatureCache {
 // router.hip
 // Scratch for the bf16 three-way split of [W_r | A] used by the MFMA router
 // (0 when the shape takes the fp64 vector path).
-size_t router_split_bytes(int NC, int d);
+// router scratch: the split weights and, for small token counts, the split-K
+// pair sums and logits
+size_t router_split_bytes(int NC, const pr2_moe_desc& d);
 bool router_mfma_ok(const pr2_moe_desc& d, int NC);
 hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const float* W_r,
                                 const float* b_r, const float* A, const float* B, void* idx_out,

@@ -688,42 +688,54 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 // Ws[kt][p * NCp + c][kk] = part p of column c at K index kt*32 + kk (zero for c >= NC).
 // Columns: folded -> W_r + A B (or W_r + A when B is null); else [W_r | A].
+// Workgroup (32 columns, K step kt): each thread forms 4 weights (neighbouring
+// threads read neighbouring columns), the parts are transposed through LDS,
+// and each part's 32 x 32 block (2 KiB, contiguous in Ws) is stored 8 bytes
+// per thread.
 __global__ void __launch_bounds__(256)
 router_split_kernel(const float* W_r, const float* A, const float* B, int d, int N, int r,
                     int folded, int NCp, bf16_t* Ws) {
+    __shared__ bf16_t tile[3][32][kRBK + 1];
     const int NC = folded ? N : N + r;
-    const int64_t total = (int64_t)NCp * d;
-    for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < total;
-         q += (int64_t)gridDim.x * 256) {
-        const int kk = (int)(q % kRBK);
-        const int c = (int)((q / kRBK) % NCp);
-        const int kt = (int)(q / ((int64_t)kRBK * NCp));
-        const int kg = kt * kRBK + kk;
+    const int c0 = blockIdx.x * 32, kt = blockIdx.y;
+    const int cl = threadIdx.x & 31, kq = threadIdx.x >> 5;
+    const int c = c0 + cl;
+#pragma unroll
+    for (int e = 0; e < kRBK / 8; ++e) {
+        const int kk = kq + 8 * e;
+        const int64_t kg = (int64_t)kt * kRBK + kk;
         double w = 0.0;
         if (c < NC) {
             if (c < N) {
-                w = (double)W_r[(int64_t)kg * N + c];
+                w = (double)W_r[kg * N + c];
                 if (folded && r > 0) {
                     if (B) {
                         for (int j = 0; j < r; ++j)
-                            w += (double)A[(int64_t)kg * r + j] * (double)B[(int64_t)j * N + c];
+                            w += (double)A[kg * r + j] * (double)B[(int64_t)j * N + c];
                     } else {
-                        w += (double)A[(int64_t)kg * r + c];
+                        w += (double)A[kg * r + c];
                     }
                 }
             } else {
-                w = (double)A[(int64_t)kg * r + (c - N)];
+                w = (double)A[kg * r + (c - N)];
             }
         }
         // three bf16 parts; for a weight representable in fp32 they sum to it exactly
         const bf16_t hi = f32_to_bf16((float)w);
         const double r1 = w - (double)bf16_to_f32(hi);
         const bf16_t mid = f32_to_bf16((float)r1);
-        const bf16_t lo = f32_to_bf16((float)(r1 - (double)bf16_to_f32(mid)));
-        const int64_t base = (int64_t)kt * 3 * NCp * kRBK;
-        Ws[base + ((int64_t)c) * kRBK + kk] = hi;
-        Ws[base + ((int64_t)NCp + c) * kRBK + kk] = mid;
-        Ws[base + ((int64_t)2 * NCp + c) * kRBK + kk] = lo;
+        tile[0][cl][kk] = hi;
+        tile[1][cl][kk] = mid;
+        tile[2][cl][kk] = f32_to_bf16((float)(r1 - (double)bf16_to_f32(mid)));
+    }
+    __syncthreads();
+    const int row = threadIdx.x >> 3, q4 = (threadIdx.x & 7) * 4;
+#pragma unroll
+    for (int p = 0; p < 3; ++p) {
+        const bf16_t* t = &tile[p][row][q4];
+        const uint2 v = make_uint2((uint32_t)t[0] | ((uint32_t)t[1] << 16),
+                                   (uint32_t)t[2] | ((uint32_t)t[3] << 16));
+        *(uint2*)(Ws + ((int64_t)kt * 3 * NCp + (int64_t)p * NCp + c0 + row) * kRBK + q4) = v;
     }
 }
 
@@ -747,10 +759,22 @@ struct RouterTile {
     static constexpr int GPW = (GROUPS + 7) / 8;         // copies per wavefront (uniform)
 };
 
-template <int NTW, int MODE>   // MODE 0: rollout, 1: replay
+// Split-K for small token counts: a few 64-token tiles cannot fill the GPU,
+// and each of them would stream every weight of the projection through one CU.
+// Phase 1 gives workgroup (tile, pair) the two K steps of one K pair and
+// stores their fp32 sum as the fused loop forms it, thread by thread; a
+// reduction kernel adds the pairs of every accumulator in K order in fp64 and
+// rounds once, as the fused loop does; phase 2 takes those logits and runs
+// the epilogue.  The logits are bitwise those of the fused kernel.
+struct SplitK {
+    float* part;       // [npairs][tiles][kRThreads][8 NTW]: phase 1 output
+    float* logit;      // [tiles][kRThreads][8 NTW]: the reduction's output, phase 2 input
+};
+
+template <int NTW, int MODE, int PHASE>   // MODE 0: rollout, 1: replay; PHASE 0: fused, 1, 2: split-K
 __global__ void __launch_bounds__(kRThreads)
 router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, int r, int NC,
-                   PredictOut po, ReplayOut ro) {
+                   PredictOut po, ReplayOut ro, SplitK sk) {
     using RT = RouterTile<NTW>;
     constexpr int NCp = RT::NCp;
     constexpr int NSTAGE = RT::NSTAGE;
@@ -824,13 +848,18 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
     const int lrow = lane & 15;
     const int lch = lane >> 4;
     const int nk = d / kRBK;
+    // K steps of this workgroup: all (fused), one pair (phase 1), none (phase 2)
+    const int kb = PHASE == 1 ? (int)blockIdx.y * 2 : 0;
+    const int ke = PHASE == 1 ? min(nk, kb + 2) : (PHASE == 2 ? 0 : nk);
+    // this thread's accumulators in the split-K buffers: 2 NTW vectors of 4
+    const int64_t my_acc = ((int64_t)blockIdx.x * kRThreads + tid) * (2 * NTW);
 #pragma unroll
     for (int st = 0; st < NSTAGE - 1; ++st)
-        if (st < nk) issue(st, st);
-    for (int kt = 0; kt < nk; ++kt) {
+        if (kb + st < ke) issue(st, kb + st);
+    for (int kt = kb; kt < ke; ++kt) {
         // step kt landed (later steps may be in flight) and every wavefront is
         // done with step kt-1, whose stage is refilled next
-        if (kt + NSTAGE - 2 < nk) router_wait_vmcnt<(NSTAGE - 2) * GPW>();
+        if (kt + NSTAGE - 2 < ke) router_wait_vmcnt<(NSTAGE - 2) * GPW>();
         else router_wait_vmcnt<0>();
         // a plain barrier: __syncthreads() would also wait for every copy
         // still in flight (vmcnt(0)) and undo the pipelining
@@ -838,8 +867,8 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
         __builtin_amdgcn_sched_barrier(0);
         __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_sched_barrier(0);
-        if (kt + NSTAGE - 1 < nk) issue((kt + NSTAGE - 1) % NSTAGE, kt + NSTAGE - 1);
-        const unsigned char* base = lds + (kt % NSTAGE) * RT::STAGEB;
+        if (kt + NSTAGE - 1 < ke) issue((kt - kb + NSTAGE - 1) % NSTAGE, kt + NSTAGE - 1);
+        const unsigned char* base = lds + ((kt - kb) % NSTAGE) * RT::STAGEB;
         bf16x8 fa[2];
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
@@ -857,7 +886,7 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
                     acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb, acc[i][t], 0, 0, 0);
             }
         }
-        if ((kt & 1) || kt + 1 == nk) {
+        if (PHASE == 0 && ((kt & 1) || kt + 1 == nk)) {
 #pragma unroll
             for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -868,6 +897,16 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
                         acc[i][t][v] = 0.0f;
                     }
         }
+    }
+    if (PHASE == 1) {
+        // the pair's sum (no global store inside the loop: the compiler would
+        // then wait for every copy in flight before each LDS read)
+        f32x4* pp = (f32x4*)sk.part + (int64_t)blockIdx.y * gridDim.x * kRThreads * (2 * NTW) + my_acc;
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int t = 0; t < NTW; ++t) pp[i * NTW + t] = acc[i][t];
+        return;
     }
     __syncthreads();
     // logits -> LDS [kRTM][NC]; 16x16 accumulator element v of lane l is C[4*(l/16)+v][l%16]
@@ -880,7 +919,9 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
             for (int v = 0; v < 4; ++v) {
                 const int tok = wr * 32 + i * 16 + 4 * (lane >> 4) + v;
                 const int col = (wc * NTW + t) * 16 + (lane & 15);
-                if (col < NC) lg[tok * NC + col] = (float)acc64[i][t][v];
+                if (col < NC)
+                    lg[tok * NC + col] = PHASE == 2 ? sk.logit[(my_acc + i * NTW + t) * 4 + v]
+                                                    : (float)acc64[i][t][v];
             }
     // the router bias and (replay) the staged ids go behind the logit tile
     float* sbias = lg + kRTM * NC;
@@ -933,15 +974,67 @@ size_t router_smem(const ProjArgs& a) {
 
 int ncp_of(int NC) { return ((NC + 63) / 64) * 64; }
 
+// logit[q] = fp32 of the fp64 sum over K pairs p (in order) of part[p][q]
+__global__ void __launch_bounds__(256)
+router_pair_sum_kernel(const float* part, int npairs, int64_t n, float* logit) {
+    for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < n; q += (int64_t)gridDim.x * 256) {
+        double acc = 0.0;
+        for (int p = 0; p < npairs; ++p) acc += (double)part[(int64_t)p * n + q];
+        logit[q] = (float)acc;
+    }
+}
+
+// split-K below this many 64-token tiles, for K loops of at least kSplitMinSteps
+constexpr int kSplitMaxTiles = 16;
+constexpr int kSplitMinSteps = 8;
+
+bool use_splitk(const pr2_moe_desc& d) {
+    const int64_t tiles = (d.T + kRTM - 1) / kRTM;
+    return d.T > 0 && tiles <= kSplitMaxTiles && d.d / kRBK >= kSplitMinSteps;
+}
+
+size_t split_weight_bytes(int NC, int d) {
+    return ((size_t)3 * ncp_of(NC) * d * sizeof(bf16_t) + 255) & ~(size_t)255;
+}
+
 template <int MODE>
 hipError_t launch_router_mfma(const pr2_moe_desc& d, int NC, int r, const void* x,
                               const bf16_t* Ws, const PredictOut& po, const ReplayOut& ro,
                               hipStream_t s) {
     const int NTW = ncp_of(NC) / 64;
-    dim3 grid((unsigned)((d.T + kRTM - 1) / kRTM));
+    const int64_t tiles = (d.T + kRTM - 1) / kRTM;
+    dim3 grid((unsigned)tiles);
     const bf16_t* xb = (const bf16_t*)x;
+    SplitK sk{nullptr, nullptr};
+    if (!use_splitk(d)) {
+        switch (NTW) {
+#define PR2_CASE(n) case n: hipLaunchKernelGGL((router_mfma_kernel<n, MODE, 0>), grid, dim3(kRThreads), 0, s, xb, Ws, d.T, d.d, d.N, r, NC, po, ro, sk); break;
+            PR2_CASE(1) PR2_CASE(2) PR2_CASE(3)
+#undef PR2_CASE
+            default: return hipErrorInvalidValue;
+        }
+        return hipGetLastError();
+    }
+    const int npairs = (d.d / kRBK + 1) / 2;
+    const int64_t n = tiles * kRTM * ncp_of(NC);     // accumulators of all tiles
+    sk.part = (float*)((char*)Ws + split_weight_bytes(NC, d.d));
+    sk.logit = sk.part + (int64_t)npairs * n;
+    dim3 pgrid((unsigned)tiles, (unsigned)npairs);
     switch (NTW) {
-#define PR2_CASE(n) case n: hipLaunchKernelGGL((router_mfma_kernel<n, MODE>), grid, dim3(kRThreads), 0, s, xb, Ws, d.T, d.d, d.N, r, NC, po, ro); break;
+#define PR2_CASE(n) case n: hipLaunchKernelGGL((router_mfma_kernel<n, 0, 1>), pgrid, dim3(kRThreads), 0, s, xb, Ws, d.T, d.d, d.N, r, NC, po, ro, sk); break;
+        PR2_CASE(1) PR2_CASE(2) PR2_CASE(3)
+#undef PR2_CASE
+        default: return hipErrorInvalidValue;
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    int64_t blocks = (n + 255) / 256;
+    if (blocks > 2048) blocks = 2048;
+    hipLaunchKernelGGL(router_pair_sum_kernel, dim3((unsigned)blocks), dim3(256), 0, s, sk.part,
+                       npairs, n, sk.logit);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    switch (NTW) {
+#define PR2_CASE(n) case n: hipLaunchKernelGGL((router_mfma_kernel<n, MODE, 2>), grid, dim3(kRThreads), 0, s, xb, Ws, d.T, d.d, d.N, r, NC, po, ro, sk); break;
         PR2_CASE(1) PR2_CASE(2) PR2_CASE(3)
 #undef PR2_CASE
         default: return hipErrorInvalidValue;
@@ -953,18 +1046,22 @@ hipError_t launch_split(const float* W_r, const float* A, const float* B, const 
                         int r, int folded, bf16_t* Ws, hipStream_t s) {
     const int NC = folded ? d.N : d.N + r;
     const int NCp = ncp_of(NC);
-    int64_t total = (int64_t)NCp * d.d;
-    int64_t blocks = (total + 255) / 256;
-    if (blocks > 4096) blocks = 4096;
     LaunchScope scope("router_split", s);
-    hipLaunchKernelGGL(router_split_kernel, dim3((unsigned)blocks), dim3(256), 0, s, W_r, A, B,
-                       d.d, d.N, r, folded, NCp, Ws);
+    hipLaunchKernelGGL(router_split_kernel, dim3((unsigned)(NCp / 32), (unsigned)(d.d / kRBK)),
+                       dim3(256), 0, s, W_r, A, B, d.d, d.N, r, folded, NCp, Ws);
     return hipGetLastError();
 }
 
 }  // namespace
 
-size_t router_split_bytes(int NC, int d) { return (size_t)3 * ncp_of(NC) * d * sizeof(bf16_t); }
+size_t router_split_bytes(int NC, const pr2_moe_desc& d) {
+    size_t b = split_weight_bytes(NC, d.d);
+    if (use_splitk(d)) {
+        const int64_t n = (d.T + kRTM - 1) / kRTM * kRTM * ncp_of(NC);
+        b += ((d.d / kRBK + 1) / 2 + 1) * (size_t)n * sizeof(float);   // pair sums, logits
+    }
+    return b;
+}
 
 bool router_mfma_ok(const pr2_moe_desc& d, int NC) {
     return d.act_dtype == PR2_BF16 && d.d % kRBK == 0 && ncp_of(NC) <= 64 * kRMaxNTW;
