@@ -90,6 +90,20 @@ def blas_threads():
         return int(os.environ.get("OMP_NUM_THREADS", "1"))
 
 
+def host_info():
+    """CPU model and the number of CPUs this process may run on."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:  # pragma: no cover
+        pass
+    return {"cpu_model": model, "affinity_cpus": len(os.sched_getaffinity(0))}
+
+
 def timed_cpu(fn, n_tok, min_seconds):
     reps = 0
     t0 = time.perf_counter()
@@ -112,7 +126,7 @@ def cpu_baseline_forward(shape, L, n_tok, min_seconds=10.0):
         O.replay_forward(x, rt["idx"], L["W_r"], L["beta"], L["W_gate"], L["W_up"], L["W_down"])
     reps, dt = timed_cpu(run, n_tok, min_seconds)
     return {"value": reps * n_tok / dt, "unit": "tokens/s", "cores": blas_threads(),
-            "kind": "oracle",
+            "kind": "oracle", "host": host_info(),
             "sample": f"{n_tok} of {shape.T} tokens of {shape.name}, float64 route prediction "
                       f"+ replay forward, {reps} pass(es) in {dt:.1f} s"}
 
@@ -126,7 +140,7 @@ def cpu_baseline_backward(shape, L, idx, dy, n_tok, min_seconds=10.0):
                           L["W_down"], dy[:n_tok])
     reps, dt = timed_cpu(run, n_tok, min_seconds)
     return {"value": reps * n_tok / dt, "unit": "tokens/s", "cores": blas_threads(),
-            "kind": "oracle",
+            "kind": "oracle", "host": host_info(),
             "sample": f"{n_tok} of {shape.T} tokens of {shape.name}, float64 replay backward, "
                       f"{reps} pass(es) in {dt:.1f} s"}
 
@@ -142,7 +156,7 @@ def cpu_baseline_decode(shape, L, min_seconds=10.0):
         i[0] += 1
     reps, dt = timed_cpu(run, W.DECODE_SEQS, min_seconds)
     return {"value": reps * W.DECODE_SEQS / dt, "unit": "routed tokens/s",
-            "cores": blas_threads(), "kind": "oracle",
+            "cores": blas_threads(), "kind": "oracle", "host": host_info(),
             "sample": f"{reps} decode steps of {W.DECODE_SEQS} tokens, float64 route prediction, "
                       f"in {dt:.1f} s"}
 
@@ -172,6 +186,25 @@ def timed_steps(step, steps, warmup, stream, B):
     prof = B.profile_collect()
     B.profile_enable(False)
     return ms, {name: tot / n for name, (tot, n) in prof.items()}
+
+
+def cold_ms_per_step(step, steps, stream):
+    """Mean ms per step when every step follows a 512 MiB device write, which
+    evicts the L2s and the 256 MB last-level cache (inputs come from HBM)."""
+    import torch
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    total = 0.0
+    for _ in range(steps):
+        scratch.fill_(1)
+        e0.record(stream)
+        step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        total += e0.elapsed_time(e1)
+    del scratch
+    return total / steps
 
 
 def graph_ms_per_step(step_on, steps):
@@ -254,6 +287,7 @@ def run_forward(args, shape, dev):
 
     ms, kern = timed_steps(step, args.steps, args.warmup, stream, B)
     ms_graph = graph_ms_per_step(step_on, args.steps)
+    ms_cold = cold_ms_per_step(step, args.steps, stream)
     ab = 2 if shape.act == "bf16" else 4
     ib = 2 if shape.idx_dtype == "int16" else 4
     dominant = "gemm1_gate_up_swiglu"
@@ -276,6 +310,9 @@ def run_forward(args, shape, dev):
                                                   "grouped_gemm_mfma<0>")}
     out["hip_graph"] = {"ms_per_step": ms_graph, "value": T / (ms_graph * 1e-3),
                         "note": "the same step captured once and replayed as a HIP graph"}
+    out["cold_cache"] = {"ms_per_step": ms_cold, "value": T / (ms_cold * 1e-3),
+                         "note": "each step after a 512 MiB device write that evicts L2 and "
+                                 "the 256 MB last-level cache"}
     out["kernels_ms"] = {n: round(v, 5) for n, v in kern.items()}
     out["replay_forward"] = {
         "ms": t_replay,
