@@ -696,10 +696,22 @@ __global__ void __launch_bounds__(256)
 router_split_kernel(const float* W_r, const float* A, const float* B, int d, int N, int r,
                     int folded, int NCp, bf16_t* Ws) {
     __shared__ bf16_t tile[3][32][kRBK + 1];
+    // the predictor factors this workgroup folds in: A rows kt*32.. and B columns c0..
+    constexpr int kStageR = 64;
+    __shared__ float sA[kRBK][kStageR];
+    __shared__ float sB[kStageR][32];
     const int NC = folded ? N : N + r;
     const int c0 = blockIdx.x * 32, kt = blockIdx.y;
     const int cl = threadIdx.x & 31, kq = threadIdx.x >> 5;
     const int c = c0 + cl;
+    const bool staged = folded && B && r > 0 && r <= kStageR;
+    if (staged) {
+        for (int i = threadIdx.x; i < kRBK * r; i += 256)
+            sA[i / r][i % r] = A[((int64_t)kt * kRBK + i / r) * r + i % r];
+        for (int i = threadIdx.x; i < r * 32; i += 256)
+            sB[i / 32][i % 32] = c0 + i % 32 < N ? B[(int64_t)(i / 32) * N + c0 + i % 32] : 0.0f;
+        __syncthreads();
+    }
 #pragma unroll
     for (int e = 0; e < kRBK / 8; ++e) {
         const int kk = kq + 8 * e;
@@ -709,7 +721,9 @@ router_split_kernel(const float* W_r, const float* A, const float* B, int d, int
             if (c < N) {
                 w = (double)W_r[kg * N + c];
                 if (folded && r > 0) {
-                    if (B) {
+                    if (staged) {
+                        for (int j = 0; j < r; ++j) w += (double)sA[kk][j] * (double)sB[j][cl];
+                    } else if (B) {
                         for (int j = 0; j < r; ++j)
                             w += (double)A[kg * r + j] * (double)B[(int64_t)j * N + c];
                     } else {
