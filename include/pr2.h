@@ -91,7 +91,9 @@ typedef struct {
 } pr2_moe_desc;
 
 /* Bytes of workspace an op needs for this descriptor (0 if none).  Never fails: an invalid
- * descriptor yields 0 and the call itself then reports the error. */
+ * descriptor yields 0 and the call itself then reports the error.  The size does not
+ * decrease with T: a workspace sized for a batch also serves any smaller batch of the
+ * same layer shape. */
 size_t pr2_workspace_bytes(const pr2_moe_desc* desc, int op);
 
 /*
@@ -114,8 +116,9 @@ size_t pr2_workspace_bytes(const pr2_moe_desc* desc, int op);
  *   gate_out   [T, k] fp32, aligned with idx_out's order; may be NULL.
  *   logits_out [T, N] fp32 router logits p (without the predictor term); may be NULL.
  *   ws         scratch of at least pr2_workspace_bytes(desc, PR2_OP_ROUTE) bytes (the bf16
- *              three-way split of [W_r | A] that the MFMA router reads; 0 bytes when the shape
- *              takes the fp64 vector path).  Reused freely between calls on one stream.
+ *              three-way split of [W_r | A] that the MFMA router reads, and for batches of at
+ *              most 1024 tokens the partial logits of its split-K form; 0 bytes when the
+ *              shape takes the fp64 vector path).  Reused freely between calls on one stream.
  * Logits are accumulated from exact products (fp32 weights split into three bf16 parts times
  * bf16 x, or fp64 FMA for fp32 x) in fp32 chunks summed in fp64, then rounded once to fp32.
  */

@@ -1068,10 +1068,13 @@ hipError_t launch_split(const float* W_r, const float* A, const float* B, const 
 
 }  // namespace
 
+// The split-K buffers are reserved for min(T, the split-K limit) tokens at
+// every T, so that a workspace sized for some batch also serves any smaller one.
 size_t router_split_bytes(int NC, const pr2_moe_desc& d) {
     size_t b = split_weight_bytes(NC, d.d);
-    if (use_splitk(d)) {
-        const int64_t n = (d.T + kRTM - 1) / kRTM * kRTM * ncp_of(NC);
+    if (d.T > 0 && d.d / kRBK >= kSplitMinSteps) {
+        const int64_t tiles = min((d.T + kRTM - 1) / kRTM, (int64_t)kSplitMaxTiles);
+        const int64_t n = tiles * kRTM * ncp_of(NC);
         b += ((d.d / kRBK + 1) / 2 + 1) * (size_t)n * sizeof(float);   // pair sums, logits
     }
     return b;

@@ -264,3 +264,17 @@ def test_cached_route_and_predictor_loss_reject_bad_arguments():
     assert loss(h=0) == "PR2_ERR_NULL"
     assert loss(ws_bytes=1) == "PR2_ERR_WORKSPACE"
     assert loss(desc(r=8), Bm=0, dB=0) in ("PR2_ERR_DEVICE", "PR2_OK")   # identity, r == N
+
+
+def test_workspace_bytes_do_not_decrease_with_batch():
+    """A workspace sized for a batch also serves every smaller batch of the
+    same layer (decode loops shrink their batch as sequences finish)."""
+    from paper_2606_00395_amd import binding as B
+    for op in (B.OP_ROUTE, B.OP_REPLAY_FWD, B.OP_ROLLOUT_FWD, B.OP_REPLAY_BWD, B.OP_ROUTE_DIAG,
+               B.OP_PREDICTOR_LOSS):
+        prev = 0
+        for T in (1, 63, 64, 65, 256, 1000, 1024, 1025, 2048, 16384):
+            desc = B.make_desc(T, 2048, 128, 8, 768, 16, B.PR2_BF16, B.PR2_I32, 1)
+            n = B.workspace_bytes(desc, op)
+            assert n >= prev, (op, T, n, prev)
+            prev = n
