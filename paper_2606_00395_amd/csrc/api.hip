@@ -162,6 +162,8 @@ BwdWs bwd_ws_layout(const pr2_moe_desc& d, void* base) {
     b.dp_perm = (float*)take(sizeof(float) * Tk);
     b.wrt = (float*)take(sizeof(float) * (size_t)d.N * d.d);
     b.order = (int*)take(sizeof(int) * (size_t)d.N);
+    b.rwpart = (float*)take(sizeof(float) * (size_t)b.fw.max_tiles * d.d);
+    b.rbpart = (float*)take(sizeof(float) * (size_t)b.fw.max_tiles);
     b.bytes = off + 256;
     return b;
 }

@@ -556,24 +556,29 @@ gate_grad_kernel(const float* dgp, int np, const int* inv, const float* gate, in
     }
 }
 
-// dW_r[:, e] = sum over expert e's routes of dp * x_t, db_r[e] = sum of dp.
-// Block (e, column chunk of 256): 8 row groups of 32 threads, 8 columns per
-// thread, summed across groups in a fixed order.
+// dW_r[:, e] = sum over expert e's routes of dp * x_t, db_r[e] = sum of dp, in
+// two passes so that a heavily loaded expert is spread over many workgroups:
+//   partials: workgroup (256-row tile, column chunk of 256) sums the tile's
+//             routes (8 row groups of 32 threads, 8 columns per thread, each
+//             thread over its rows in order, then the groups in a fixed order);
+//   reduce:   each expert's tile partials are added in tile order.
 template <typename T>
 __global__ void __launch_bounds__(256)
-router_wgrad_kernel(const T* x, const int* perm_src, const int* offsets, const float* dp_perm,
-                    int k, int d, int N, float* dW_r, float* db_r) {
+router_wgrad_partial_kernel(const T* x, const int* perm_src, const int* tiles, const int* tile_count,
+                            const float* dp_perm, int k, int d, float* part, float* dbpart) {
     __shared__ float red[8][256];
-    __shared__ float dbs[256];
-    const int e = blockIdx.x;
+    __shared__ float dbs[8];
+    const int tile = blockIdx.x;
+    if (tile >= *tile_count) return;
+    const int q0 = tiles[3 * tile + 1], q1 = q0 + tiles[3 * tile + 2];
     const int cg = threadIdx.x & 31, rg = threadIdx.x >> 5;
     const int i0 = blockIdx.y * 256 + 8 * cg;
-    const int q0 = offsets[e], q1 = offsets[e + 1];
     float acc[8];
 #pragma unroll
     for (int v = 0; v < 8; ++v) acc[v] = 0.0f;
-    // each thread sums routes q0 + rg, q0 + rg + 8, ... in that order; the
-    // loads of kRwU consecutive ones are issued together
+    float dbacc = 0.0f;
+    // each thread sums routes q0 + rg, q0 + rg + 8, ... in that order; the loads
+    // of kRwU consecutive ones are issued together
     constexpr int kRwU = 8;
     for (int qb = q0 + rg; qb < q1; qb += 8 * kRwU) {
         int tok[kRwU];
@@ -608,28 +613,50 @@ router_wgrad_kernel(const T* x, const int* perm_src, const int* offsets, const f
                     if (i0 + v < d) acc[v] = fmaf(w[u], Act<T>::to_f32(xr[i0 + v]), acc[v]);
             }
         }
+#pragma unroll
+        for (int u = 0; u < kRwU; ++u) dbacc += w[u];
     }
 #pragma unroll
     for (int v = 0; v < 8; ++v) red[rg][8 * cg + v] = acc[v];
+    if (cg == 0) dbs[rg] = dbacc;
     __syncthreads();
-    {
-        const int c = threadIdx.x;          // column within the chunk
-        float s = 0.0f;
+    const int c = threadIdx.x;
+    float sum = 0.0f;
 #pragma unroll
-        for (int r = 0; r < 8; ++r) s += red[r][c];
-        const int i = blockIdx.y * 256 + c;
-        if (i < d) dW_r[(int64_t)i * N + e] = s;
+    for (int g = 0; g < 8; ++g) sum += red[g][c];
+    const int i = blockIdx.y * 256 + c;
+    if (i < d) part[(int64_t)tile * d + i] = sum;
+    if (blockIdx.y == 0 && threadIdx.x == 0) {
+        float db = 0.0f;
+        for (int g = 0; g < 8; ++g) db += dbs[g];
+        dbpart[tile] = db;
     }
-    if (db_r && blockIdx.y == 0) {
+}
+
+// dW_r[i][e] = sum of expert e's tile partials in tile order (tiles are expert-major)
+__global__ void __launch_bounds__(256)
+router_wgrad_reduce_kernel(const int* offsets, const float* part, const float* dbpart, int bm,
+                           int d, int N, float* dW_r, float* db_r) {
+    const int e = blockIdx.x;
+    __shared__ int s_t0;
+    if (threadIdx.x == 0) {
+        int t0 = 0;
+        for (int f = 0; f < e; ++f) t0 += (offsets[f + 1] - offsets[f] + bm - 1) / bm;
+        s_t0 = t0;
+    }
+    __syncthreads();
+    const int t0 = s_t0;
+    const int nt = (offsets[e + 1] - offsets[e] + bm - 1) / bm;
+    const int i = blockIdx.y * 256 + threadIdx.x;
+    if (i < d) {
         float s = 0.0f;
-        for (int q = q0 + (int)threadIdx.x; q < q1; q += 256) s += dp_perm[q];
-        dbs[threadIdx.x] = s;
-        __syncthreads();
-        for (int w = 128; w > 0; w >>= 1) {
-            if ((int)threadIdx.x < w) dbs[threadIdx.x] += dbs[threadIdx.x + w];
-            __syncthreads();
-        }
-        if (threadIdx.x == 0) db_r[e] = dbs[0];
+        for (int t = 0; t < nt; ++t) s += part[(int64_t)(t0 + t) * d + i];
+        dW_r[(int64_t)i * N + e] = s;
+    }
+    if (db_r && blockIdx.y == 0 && threadIdx.x == 0) {
+        float s = 0.0f;
+        for (int t = 0; t < nt; ++t) s += dbpart[t0 + t];
+        db_r[e] = s;
     }
 }
 
@@ -889,13 +916,19 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
     }
     {
         LaunchScope scope("bwd_router_wgrad", s);
-        dim3 grid((unsigned)d.N, (unsigned)((d.d + 255) / 256));
+        dim3 grid((unsigned)w.max_tiles, (unsigned)((d.d + 255) / 256));
         if (bf)
-            hipLaunchKernelGGL(router_wgrad_kernel<bf16_t>, grid, dim3(256), 0, s, (const bf16_t*)x,
-                               w.perm_src, w.offsets, ws.dp_perm, d.k, d.d, d.N, out.dW_r, out.db_r);
+            hipLaunchKernelGGL(router_wgrad_partial_kernel<bf16_t>, grid, dim3(256), 0, s,
+                               (const bf16_t*)x, w.perm_src, w.tiles, w.tile_count, ws.dp_perm, d.k,
+                               d.d, ws.rwpart, ws.rbpart);
         else
-            hipLaunchKernelGGL(router_wgrad_kernel<float>, grid, dim3(256), 0, s, (const float*)x,
-                               w.perm_src, w.offsets, ws.dp_perm, d.k, d.d, d.N, out.dW_r, out.db_r);
+            hipLaunchKernelGGL(router_wgrad_partial_kernel<float>, grid, dim3(256), 0, s,
+                               (const float*)x, w.perm_src, w.tiles, w.tile_count, ws.dp_perm, d.k,
+                               d.d, ws.rwpart, ws.rbpart);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(router_wgrad_reduce_kernel, dim3((unsigned)d.N, (unsigned)((d.d + 255) / 256)),
+                           dim3(256), 0, s, w.offsets, ws.rwpart, ws.rbpart, kTileM, d.d, d.N,
+                           out.dW_r, out.db_r);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
 

@@ -84,6 +84,8 @@ struct BwdWs {
     float* dp_perm;     // [T*k] the same in permuted order
     float* wrt;         // [N, d] W_r transposed
     int* order;         // [N] experts by decreasing route count
+    float* rwpart;      // [max_tiles, d] router weight-gradient partials per 256-row tile
+    float* rbpart;      // [max_tiles] router bias-gradient partials
     int np;
     size_t bytes;
 };
