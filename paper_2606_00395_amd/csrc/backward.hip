@@ -729,17 +729,31 @@ dx_combine_bf16_kernel(const bf16_t* dxr, const int* inv, const float* dp_route,
             for (int u = 0; u < kDxTok; ++u) {
                 const int64_t t = t0 + u;
                 if (t >= T_) continue;
-                for (int s = 0; s < k; ++s) {
-                    const int e = load_id(idx, idx_dtype, t * ldi + s);
-                    if (e < 0 || e >= N) continue;
-                    const float g = dp_route[t * k + s];
-                    const float* wr = wrt + (int64_t)e * d + c0;
-                    const f32x4 w0 = *(const f32x4*)wr;
-                    const f32x4 w1 = *(const f32x4*)(wr + 4);
+                // the router rows of kSlots slots are fetched together, then added in slot order
+                for (int s0 = 0; s0 < k; s0 += kSlots) {
+                    int es[kSlots];
+                    float gs[kSlots];
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        acc[u][v] = fmaf(g, w0[v], acc[u][v]);
-                        acc[u][4 + v] = fmaf(g, w1[v], acc[u][4 + v]);
+                    for (int j = 0; j < kSlots; ++j) {
+                        const int e = s0 + j < k ? load_id(idx, idx_dtype, t * ldi + s0 + j) : -1;
+                        es[j] = (e >= 0 && e < N) ? e : -1;
+                        gs[j] = es[j] >= 0 ? dp_route[t * k + s0 + j] : 0.0f;
+                    }
+                    f32x4 w0[kSlots], w1[kSlots];
+#pragma unroll
+                    for (int j = 0; j < kSlots; ++j) {
+                        const float* wr = wrt + (int64_t)(es[j] >= 0 ? es[j] : 0) * d + c0;
+                        w0[j] = *(const f32x4*)wr;
+                        w1[j] = *(const f32x4*)(wr + 4);
+                    }
+#pragma unroll
+                    for (int j = 0; j < kSlots; ++j) {
+                        if (es[j] < 0) continue;
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) {
+                            acc[u][v] = fmaf(gs[j], w0[j][v], acc[u][v]);
+                            acc[u][4 + v] = fmaf(gs[j], w1[j][v], acc[u][4 + v]);
+                        }
                     }
                 }
                 *(uint4*)(dx + t * (int64_t)d + c0) =
