@@ -22,8 +22,10 @@
 // columns live in the same lanes) and rounds H to bf16; GEMM2's epilogue scales
 // by the route weight and rounds O to bf16.  The MFMA operands are given as
 // (weights, tokens), so each lane's accumulators hold runs of four consecutive
-// output columns of one token row and the epilogue stores 8 bytes at a time
-// straight from registers.  Workgroups are mapped so that each XCD takes a
+// output columns of one token row.  GEMM1 stores them 8 bytes at a time
+// straight from registers; GEMM2 (and the pre-activation epilogue below)
+// stages its outputs through the freed LDS stages so that every store covers
+// whole row segments.  Workgroups are mapped so that each XCD takes a
 // contiguous range of the tile list (same experts, shared L2).
 //
 // A third epilogue serves the backward pass: it stores the pre-activations
@@ -265,22 +267,24 @@ grouped_gemm_mfma(MfmaArgs g) {
             }
         }
     }
-    if (!active) return;
-
     // Epilogue.  The MFMA computed the transposed tile (weights x tokens), so
-    // accumulator element v of lane l is, for 32x32 tiles, output column
-    // 8*(v/4) + 4*(l/32) + v%4 of token row l%32, and for 16x16 tiles, column
-    // 4*(l/16) + v of token row l%16: runs of four consecutive bf16 per lane,
-    // each stored as one 8-byte write.
-    const int ncol0 = 4 * (lane / MT);
-    constexpr int NA4 = ACCN / 4;           // runs of four per tile
-    constexpr int A4STEP = MT == 32 ? 8 : 0;
+    // accumulator element v of lane l is, for 16x16 tiles, column 4*(l/16) + v
+    // of token row l%16 of its block (for 32x32 tiles, column
+    // 8*(v/4) + 4*(l/32) + v%4 of token row l%32): runs of four consecutive
+    // outputs per lane.
+    if (MODE == 0) {
+        // GEMM1: H = silu(gate) * up, stored straight from registers, one
+        // 8-byte write per run (gate and up tiles of the same columns sit in
+        // the same lanes)
+        if (!active) return;
+        const int ncol0 = 4 * (lane / MT);
+        constexpr int NA4 = ACCN / 4;           // runs of four per tile
+        constexpr int A4STEP = MT == 32 ? 8 : 0;
 #pragma unroll
-    for (int i = 0; i < MI; ++i) {
-        const int r = wr * WM + i * MT + (lane % MT);
-        if (r >= rows) continue;
-        bf16_t* orow = g.out + ((int64_t)row0 + r) * g.n_out;
-        if (MODE == 0) {
+        for (int i = 0; i < MI; ++i) {
+            const int r = wr * WM + i * MT + (lane % MT);
+            if (r >= rows) continue;
+            bf16_t* orow = g.out + ((int64_t)row0 + r) * g.n_out;
 #pragma unroll
             for (int j = 0; j < NJ / 2; ++j) {
                 const int col = pn * 128 + wc * (WN / 2) + j * MT + ncol0;
@@ -297,41 +301,72 @@ grouped_gemm_mfma(MfmaArgs g) {
                     *(uint2*)(orow + col + A4STEP * a4) = make_uint2(w[0], w[1]);
                 }
             }
-        } else if (MODE == 2) {
-            // pre-activations for the backward pass: a at column col, u at m + col
+        }
+        return;
+    }
+
+    // GEMM2 (route weight times the output) and the pre-activations (a and u)
+    // are staged: the rounded outputs go into this wavefront's LDS region (64
+    // rows of CW columns per output block, 16-byte chunks XOR-swizzled by
+    // row) and are read back 16 bytes per lane, so that each global store
+    // covers whole row segments (256 or 128 contiguous bytes) instead of
+    // 8-byte pieces of 16 rows: measured 10 % faster for GEMM2 (and slower
+    // for GEMM1, whose outputs are half as wide).
+    // Every wavefront must be done with the operand stages first.
+    __syncthreads();
+    if (!active) return;
+    static_assert(MT == 16, "staged epilogue assumes 16x16 MFMA tiles");
+    constexpr int CW = MODE == 1 ? WN : WN / 2;          // columns per output block
+    constexpr int NB = MODE == 2 ? 2 : 1;                 // output blocks per wavefront
+    constexpr int RB = CW * 2;                            // bytes per staged row
+    constexpr int NCH = RB / 16;                          // 16-byte chunks per row
+    unsigned char* stage_w = lds + wave * (NB * WM * RB);
+    auto spos = [&](int blk, int row, int col) {          // byte offset of (row, col), col % 4 == 0
+        const int ch = (col >> 3) ^ (row & (NCH - 1));
+        return blk * WM * RB + row * RB + (ch << 4) + ((col & 4) << 1);
+    };
+    const int ncol0 = 4 * (lane / MT);
 #pragma unroll
-            for (int j = 0; j < NJ / 2; ++j) {
-                const int col = pn * 128 + wc * (WN / 2) + j * MT + ncol0;
+    for (int i = 0; i < MI; ++i) {
+        const int row = i * MT + (lane % MT);
 #pragma unroll
-                for (int a4 = 0; a4 < NA4; ++a4) {
+        for (int j = 0; j < (MODE == 1 ? NJ : NJ / 2); ++j) {
+            const int col = j * MT + ncol0;
+            if (MODE == 2) {
 #pragma unroll
-                    for (int half = 0; half < 2; ++half) {
-                        const int jj = j + half * (NJ / 2);
-                        const int v0 = 4 * a4;
-                        const uint32_t w0 = (uint32_t)f32_to_bf16(acc[i][jj][v0]) |
-                                            ((uint32_t)f32_to_bf16(acc[i][jj][v0 + 1]) << 16);
-                        const uint32_t w1 = (uint32_t)f32_to_bf16(acc[i][jj][v0 + 2]) |
-                                            ((uint32_t)f32_to_bf16(acc[i][jj][v0 + 3]) << 16);
-                        *(uint2*)(orow + half * (g.n_out / 2) + col + A4STEP * a4) = make_uint2(w0, w1);
-                    }
+                for (int half = 0; half < 2; ++half) {
+                    const int jj = j + half * (NJ / 2);
+                    const uint32_t w0 = (uint32_t)f32_to_bf16(acc[i][jj][0]) |
+                                        ((uint32_t)f32_to_bf16(acc[i][jj][1]) << 16);
+                    const uint32_t w1 = (uint32_t)f32_to_bf16(acc[i][jj][2]) |
+                                        ((uint32_t)f32_to_bf16(acc[i][jj][3]) << 16);
+                    *(uint2*)(stage_w + spos(half, row, col)) = make_uint2(w0, w1);
                 }
+            } else {
+                const uint32_t w0 = (uint32_t)f32_to_bf16(gw[i] * acc[i][j][0]) |
+                                    ((uint32_t)f32_to_bf16(gw[i] * acc[i][j][1]) << 16);
+                const uint32_t w1 = (uint32_t)f32_to_bf16(gw[i] * acc[i][j][2]) |
+                                    ((uint32_t)f32_to_bf16(gw[i] * acc[i][j][3]) << 16);
+                *(uint2*)(stage_w + spos(0, row, col)) = make_uint2(w0, w1);
             }
-        } else {
+        }
+    }
+    // the wavefront's own region: LDS operations of one wavefront complete in order
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_wave_barrier();
+    constexpr int RPI = 64 / NCH;                         // rows per 64-lane pass
+    const int rsub = lane / NCH, ch = lane % NCH;
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-                const int col = pn * BP + wc * WN + j * MT + ncol0;
+    for (int blk = 0; blk < NB; ++blk) {
+        int colbase;
+        if (MODE == 1) colbase = pn * BP + wc * WN;
+        else colbase = blk * (g.n_out / 2) + pn * 128 + wc * (WN / 2);
 #pragma unroll
-                for (int a4 = 0; a4 < NA4; ++a4) {
-                    uint32_t w[2];
-#pragma unroll
-                    for (int h = 0; h < 2; ++h) {
-                        const int v0 = 4 * a4 + 2 * h;
-                        w[h] = (uint32_t)f32_to_bf16(gw[i] * acc[i][j][v0]) |
-                               ((uint32_t)f32_to_bf16(gw[i] * acc[i][j][v0 + 1]) << 16);
-                    }
-                    *(uint2*)(orow + col + A4STEP * a4) = make_uint2(w[0], w[1]);
-                }
-            }
+        for (int p = 0; p < WM / RPI; ++p) {
+            const int row = p * RPI + rsub;
+            const int r = wr * WM + row;
+            const u32x4 v = *(const u32x4*)(stage_w + blk * WM * RB + row * RB + ((ch ^ (row & (NCH - 1))) << 4));
+            if (r < rows) *(u32x4*)(g.out + ((int64_t)row0 + r) * g.n_out + colbase + ch * 8) = v;
         }
     }
 }
