@@ -321,11 +321,84 @@ bwd_gemm(BwdArgs g) {
             }
         }
     }
-    if (!active) return;
-
     // ---- epilogues.  Lane l holds output row l%32 of each 32-row block and
     // columns 8*(v/4) + 4*(l/32) + v%4 of each 32-column block.
     const int ncol0 = 4 * (lane >> 5);
+    if (MODE != DH) {
+        // DX (bf16 rows) and WD / WGU (fp32 rows) are staged through this
+        // wavefront's share of the freed LDS stages (16-byte chunks XOR-swizzled
+        // by row) and stored 16 bytes per lane along whole row segments,
+        // instead of 8- or 16-byte pieces of 32 rows per store
+        __syncthreads();
+        if (!active) return;
+        if (MODE == DX) {
+            constexpr int RB = WN * 2, NCH = RB / 16;        // 256-byte staged rows
+            unsigned char* sw = lds + wave * (WM * RB);
+#pragma unroll
+            for (int i = 0; i < MI; ++i) {
+                const int row = i * 32 + (lane & 31);
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                    for (int a4 = 0; a4 < 4; ++a4) {
+                        const int col = j * 32 + 8 * a4 + ncol0;
+                        const int v0 = 4 * a4;
+                        *(uint2*)(sw + row * RB + ((((col >> 3) ^ (row & (NCH - 1)))) << 4) +
+                                  ((col & 4) << 1)) =
+                            make_uint2(pack_bf(acc[i][j][v0], acc[i][j][v0 + 1]),
+                                       pack_bf(acc[i][j][v0 + 2], acc[i][j][v0 + 3]));
+                    }
+            }
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            __builtin_amdgcn_wave_barrier();
+            const int ch = lane % NCH;
+#pragma unroll
+            for (int p = 0; p < WM / (64 / NCH); ++p) {
+                const int row = p * (64 / NCH) + lane / NCH;
+                const int r = wr * WM + row;
+                const u32x4 v = *(const u32x4*)(sw + row * RB + ((ch ^ (row & (NCH - 1))) << 4));
+                if (r < rows)
+                    *(u32x4*)(g.dxr + ((int64_t)row0 + r) * g.d + pn * BN + wc * WN + ch * 8) = v;
+            }
+        } else {
+            // fp32: 512-byte staged rows, one 32-row block at a time
+            constexpr int RB = WN * 4, NCH = RB / 16;
+            unsigned char* sw = lds + wave * (32 * RB);
+            const int64_t ew = (int64_t)expert * g.m * g.d;
+#pragma unroll
+            for (int i = 0; i < MI; ++i) {
+                const int row = lane & 31;
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                    for (int a4 = 0; a4 < 4; ++a4) {
+                        const int col = j * 32 + 8 * a4 + ncol0;
+                        const int v0 = 4 * a4;
+                        *(f32x4*)(sw + row * RB + (((col >> 2) ^ (row & (NCH - 1))) << 4)) =
+                            f32x4{acc[i][j][v0], acc[i][j][v0 + 1], acc[i][j][v0 + 2], acc[i][j][v0 + 3]};
+                    }
+                __builtin_amdgcn_s_waitcnt(0xc07f);
+                __builtin_amdgcn_wave_barrier();
+                const int ch = lane % NCH;
+#pragma unroll
+                for (int p = 0; p < 32 / (64 / NCH); ++p) {
+                    const int row2 = p * (64 / NCH) + lane / NCH;
+                    const int R = rt * BM + wr * WM + i * 32 + row2;
+                    float* orow;
+                    if (MODE == WD) orow = g.dWd + ew + (int64_t)R * g.m;
+                    else orow = (R < g.m ? g.dWg + ew + (int64_t)R * g.d
+                                         : g.dWu + ew + (int64_t)(R - g.m) * g.d);
+                    *(u32x4*)(orow + ct * BN + wc * WN + ch * 4) =
+                        *(const u32x4*)(sw + row2 * RB + ((ch ^ (row2 & (NCH - 1))) << 4));
+                }
+                // the next block overwrites the region
+                __builtin_amdgcn_s_waitcnt(0xc07f);
+                __builtin_amdgcn_wave_barrier();
+            }
+        }
+        return;
+    }
+    if (!active) return;
     if (MODE == DH) {
         const int np = g.m / 128;
         const int64_t ldau = 2 * (int64_t)g.m;
@@ -376,43 +449,6 @@ bwd_gemm(BwdArgs g) {
             }
             part += __shfl_xor(part, 32);
             if (ok && lane < 32) g.dgp[q * np + pn * 2 + wc] = part;
-        }
-    } else if (MODE == DX) {
-#pragma unroll
-        for (int i = 0; i < MI; ++i) {
-            const int r = wr * WM + i * 32 + (lane & 31);
-            if (r >= rows) continue;
-            bf16_t* orow = g.dxr + ((int64_t)row0 + r) * g.d;
-#pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-#pragma unroll
-                for (int a4 = 0; a4 < 4; ++a4) {
-                    const int col = pn * BN + wc * WN + j * 32 + 8 * a4 + ncol0;
-                    const int v0 = 4 * a4;
-                    *(uint2*)(orow + col) =
-                        make_uint2(pack_bf(acc[i][j][v0], acc[i][j][v0 + 1]),
-                                   pack_bf(acc[i][j][v0 + 2], acc[i][j][v0 + 3]));
-                }
-            }
-        }
-    } else {
-        const int64_t ew = (int64_t)expert * g.m * g.d;
-#pragma unroll
-        for (int i = 0; i < MI; ++i) {
-            const int R = rt * BM + wr * WM + i * 32 + (lane & 31);
-            float* orow;
-            if (MODE == WD) orow = g.dWd + ew + (int64_t)R * g.m;
-            else orow = (R < g.m ? g.dWg + ew + (int64_t)R * g.d : g.dWu + ew + (int64_t)(R - g.m) * g.d);
-#pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-#pragma unroll
-                for (int a4 = 0; a4 < 4; ++a4) {
-                    const int col = ct * BN + wc * WN + j * 32 + 8 * a4 + ncol0;
-                    const int v0 = 4 * a4;
-                    *(f32x4*)(orow + col) = f32x4{acc[i][j][v0], acc[i][j][v0 + 1],
-                                                  acc[i][j][v0 + 2], acc[i][j][v0 + 3]};
-                }
-            }
         }
     }
 }
