@@ -327,7 +327,9 @@ bwd_gemm(BwdArgs g) {
     if (MODE != DH) {
         // DX (bf16 rows) and WD / WGU (fp32 rows) are staged through this
         // wavefront's share of the freed LDS stages (16-byte chunks XOR-swizzled
-        // by row) and stored 16 bytes per lane along whole row segments,
+        // by row; for bf16 the 8-byte halves of a chunk are also swapped in rows
+        // with bit 3 set, so the 16 rows of one 8-byte write cycle hit distinct
+        // banks) and stored 16 bytes per lane along whole row segments,
         // instead of 8- or 16-byte pieces of 32 rows per store
         __syncthreads();
         if (!active) return;
@@ -344,7 +346,7 @@ bwd_gemm(BwdArgs g) {
                         const int col = j * 32 + 8 * a4 + ncol0;
                         const int v0 = 4 * a4;
                         *(uint2*)(sw + row * RB + ((((col >> 3) ^ (row & (NCH - 1)))) << 4) +
-                                  ((col & 4) << 1)) =
+                                  (((col & 4) << 1) ^ (row & 8))) =
                             make_uint2(pack_bf(acc[i][j][v0], acc[i][j][v0 + 1]),
                                        pack_bf(acc[i][j][v0 + 2], acc[i][j][v0 + 3]));
                     }
@@ -356,7 +358,8 @@ bwd_gemm(BwdArgs g) {
             for (int p = 0; p < WM / (64 / NCH); ++p) {
                 const int row = p * (64 / NCH) + lane / NCH;
                 const int r = wr * WM + row;
-                const u32x4 v = *(const u32x4*)(sw + row * RB + ((ch ^ (row & (NCH - 1))) << 4));
+                u32x4 v = *(const u32x4*)(sw + row * RB + ((ch ^ (row & (NCH - 1))) << 4));
+                if (row & 8) v = u32x4{v[2], v[3], v[0], v[1]};
                 if (r < rows)
                     *(u32x4*)(g.dxr + ((int64_t)row0 + r) * g.d + pn * BN + wc * WN + ch * 8) = v;
             }
