@@ -80,6 +80,28 @@ __device__ __forceinline__ void wait_vmcnt() {
     __builtin_amdgcn_s_waitcnt(0x0f70 | n);
 }
 
+// Direct global -> LDS copy of 16 bytes per lane: lane l fills dst + 16 l
+// (dst is the same for the whole wavefront).  Written as inline assembly:
+// issued through the compiler builtin, every later LDS read that carries no
+// type-based alias information (the transposing reads do not) is made to wait
+// for all copies in flight, which serialises each K slice's copies with the
+// slice before.  The K loop waits for its own copies explicitly (vmcnt 0 ahead
+// of the barrier that publishes a stage), so nothing relies on that wait.
+// M0 takes the LDS base; the nop covers the M0-write -> LDS-DMA hazard.  The
+// compiler keeps no value of its own in M0 in these kernels (it sets M0 only
+// right before its own LDS-DMA and message instructions, and they use none),
+// so the clobber it warns about is harmless here.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const void* src, const unsigned char* dst) {
+    const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const lds_void*)dst);
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 1\n\tglobal_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(src), "s"(m0)
+                 : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 __device__ __forceinline__ uint32_t pack_bf(float lo, float hi) {
@@ -197,17 +219,21 @@ bwd_gemm(BwdArgs g) {
     int ccol[kGroups];
 #pragma unroll
     for (int i = 0; i < kGroups; ++i) ccol[i] = 8 * ((lane & 31) ^ (4 * ((krl + 2 * i) & 3)));
-    // gathered K-strided operand (WD: dy rows, WGU: x rows): token rows of the
-    // next slice to copy, fetched one slice ahead
+    // gathered K-strided operand (WD: dy rows, WGU: x rows): the route
+    // entries of the next slice's K rows, loaded one slice ahead and only
+    // turned into token rows when that slice's copies are issued, so no load
+    // result is waited for inside the slice (rows past klen load the
+    // expert's last entry and copy zeros)
     constexpr bool kHasGather = (MODE == WD || MODE == WGU);
     const bool gathered = (MODE == WD && half == 0) || (MODE == WGU && half == 1);
-    int gtok[kGroups];
+    int graw[kGroups];
     auto fetch_tok = [&](int kt) __attribute__((always_inline)) {
 #pragma unroll
-        for (int i = 0; i < kGroups; ++i) {
-            const int K = kt * BK + krl + 2 * i;
-            gtok[i] = K < klen ? min(max(g.perm_src[row0 + K], 0), g.Tk - 1) / g.k : -1;
-        }
+        for (int i = 0; i < kGroups; ++i)
+            graw[i] = g.perm_src[row0 + min(kt * BK + krl + 2 * i, klen - 1)];
+    };
+    auto tok_row = [&](int i) __attribute__((always_inline)) {
+        return (int64_t)(min(max(graw[i], 0), g.Tk - 1) / g.k);
     };
     auto issue_strided = [&](int stage, int kt) __attribute__((always_inline)) {
         unsigned char* dst = lds + stage * STAGEB + (half ? BM * ROWB : 0) + wq * (16 * 512);
@@ -221,14 +247,13 @@ bwd_gemm(BwdArgs g) {
                 src = (K < g.m ? g.Wg + ew + (int64_t)K * g.d : g.Wu + ew + (int64_t)(K - g.m) * g.d) +
                       pn * BN;
             } else if (MODE == WD) {
-                if (half == 0) src = gtok[i] >= 0 ? g.dy + (int64_t)gtok[i] * g.d + rt * BM : kZeroRow;
+                if (half == 0) src = K < klen ? g.dy + tok_row(i) * g.d + rt * BM : kZeroRow;
                 else src = K < klen ? g.Hg + (int64_t)(row0 + K) * g.m + ct * BN : kZeroRow;
             } else {
                 if (half == 0) src = K < klen ? g.AU + (int64_t)(row0 + K) * (2 * g.m) + rt * BM : kZeroRow;
-                else src = gtok[i] >= 0 ? g.x + (int64_t)gtok[i] * g.d + ct * BN : kZeroRow;
+                else src = K < klen ? g.x + tok_row(i) * g.d + ct * BN : kZeroRow;
             }
-            __builtin_amdgcn_global_load_lds((const void*)(src + ccol[i]), (lds_void*)(dst + i * 1024),
-                                             16, 0, 0);
+            dma16(src + ccol[i], dst + i * 1024);
         }
     };
     auto issue = [&](int stage, int kt) __attribute__((always_inline)) {
@@ -239,9 +264,7 @@ bwd_gemm(BwdArgs g) {
 #pragma unroll
             for (int i = 0; i < kGroups; ++i) {
                 const int grp = wq * kGroups + i;
-                __builtin_amdgcn_global_load_lds(
-                    (const void*)(sbase + (soff[i] + (uint32_t)(kt * BK))),
-                    (lds_void*)&lds[stage * STAGEB + grp * 1024], 16, 0, 0);
+                dma16(sbase + (soff[i] + (uint32_t)(kt * BK)), &lds[stage * STAGEB + grp * 1024]);
             }
         }
     };
