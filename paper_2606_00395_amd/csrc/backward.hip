@@ -173,7 +173,7 @@ bwd_gemm(BwdArgs g) {
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar branches
     const int wr = wave >> 1;            // 64-row block of the output tile
     const int wc = wave & 1;             // 128-column block
     const int half = wave >> 2;          // operand this wavefront loads: 0 rows, 1 columns

@@ -138,19 +138,27 @@ grouped_gemm_mfma(MfmaArgs g) {
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    // uniform across the wavefront; saying so lets the compiler branch on it
+    // with scalar branches instead of per-lane masks
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wr = wave / (BP / WN);     // token-row block of WM rows
     const int wc = wave % (BP / WN);     // panel block of WN rows
     // a wavefront whose rows are all past the tile's end only helps copy
     const bool active = wr * WM < rows;
     // each lane's accumulators belong to MI token rows (one per MT-row block);
     // GEMM2's route weights for them are fetched now, long before the epilogue
+    // (loads are unconditional, rows clamped into the tile, so that they all
+    // go out together rather than one masked branch at a time)
     float gw[MI];
+    if (MODE == 1) {
+        int src[MI];
 #pragma unroll
-    for (int i = 0; i < MI; ++i) {
-        gw[i] = 0.0f;
-        const int r = wr * WM + i * MT + (lane % MT);
-        if (MODE == 1 && r < rows) gw[i] = g.gate[min(max(g.perm_src[row0 + r], 0), g.Tk - 1)];
+        for (int i = 0; i < MI; ++i) src[i] = g.perm_src[row0 + min(wr * WM + i * MT + (lane % MT), rows - 1)];
+#pragma unroll
+        for (int i = 0; i < MI; ++i) gw[i] = g.gate[min(max(src[i], 0), g.Tk - 1)];
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+            if (wr * WM + i * MT + (lane % MT) >= rows) gw[i] = 0.0f;
     }
 
     // DMA assignments: wavefront w copies row groups w*kGroups .. of the
@@ -163,23 +171,33 @@ grouped_gemm_mfma(MfmaArgs g) {
     if (wrow0 < BM) sbase = g.A;
     else if (MODE != 1) sbase = (wrow0 - BM < 128 ? g.W0 : g.W1) + (int64_t)expert * g.w_stride;
     else sbase = g.W0 + (int64_t)expert * g.w_stride;
+    // (wrow0 < BM holds for a whole wavefront: a scalar branch, and the
+    // gathered route entries are loaded together before any is used)
     uint32_t soff[kGroups];
+    if (wrow0 < BM) {
+        // rows past the tile's end read a valid row; their results are never stored
+        int rsrc[kGroups];
 #pragma unroll
-    for (int i = 0; i < kGroups; ++i) {
-        const int r = wrow0 + i * kRowsPerDma + lane / CHUNKS;  // row in [0, BM + BP)
-        const int chunk = (lane % CHUNKS) ^ swz(r);
-        int64_t off;
-        if (r < BM) {
-            // rows past the tile's end read a valid row; their results are never stored
+        for (int i = 0; i < kGroups; ++i) {
+            const int r = wrow0 + i * kRowsPerDma + lane / CHUNKS;
             const int rr = r < rows ? r : 0;
-            if (MODE != 1) off = (int64_t)(min(max(g.perm_src[row0 + rr], 0), g.Tk - 1) / g.k) * g.K;
-            else off = ((int64_t)row0 + rr) * g.K;
-        } else {
-            const int pr = r - BM;
-            off = MODE != 1 ? (int64_t)(pn * 128 + (pr & 127)) * g.K
-                            : (int64_t)(pn * BP + pr) * g.K;
+            rsrc[i] = MODE != 1 ? g.perm_src[row0 + rr] : row0 + rr;
         }
-        soff[i] = (uint32_t)(off + chunk * 8);
+#pragma unroll
+        for (int i = 0; i < kGroups; ++i) {
+            const int r = wrow0 + i * kRowsPerDma + lane / CHUNKS;
+            const int64_t row = MODE != 1 ? (int64_t)(min(max(rsrc[i], 0), g.Tk - 1) / g.k) : rsrc[i];
+            soff[i] = (uint32_t)(row * g.K + ((lane % CHUNKS) ^ swz(r)) * 8);
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < kGroups; ++i) {
+            const int r = wrow0 + i * kRowsPerDma + lane / CHUNKS;  // row in [BM, BM + BP)
+            const int pr = r - BM;
+            const int64_t off = MODE != 1 ? (int64_t)(pn * 128 + (pr & 127)) * g.K
+                                          : (int64_t)(pn * BP + pr) * g.K;
+            soff[i] = (uint32_t)(off + ((lane % CHUNKS) ^ swz(r)) * 8);
+        }
     }
     auto issue = [&](int stage, int k0) {
 #pragma unroll
