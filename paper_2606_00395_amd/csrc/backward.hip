@@ -102,6 +102,12 @@ __device__ __forceinline__ void dma16(const void* src, const unsigned char* dst)
 }
 #pragma clang diagnostic pop
 
+// value of lane (l + n) mod 16 of this lane's group of 16 (DPP row rotate)
+template <int n>
+__device__ __forceinline__ float row_ror_f(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x120 + n, 0xf, 0xf, false));
+}
+
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 __device__ __forceinline__ uint32_t pack_bf(float lo, float hi) {
@@ -424,57 +430,95 @@ bwd_gemm(BwdArgs g) {
         }
         return;
     }
+    // DH, one 32-row block at a time: G (fp32) goes through this wavefront's
+    // LDS region (512-byte rows, 16-byte chunks XOR-swizzled by row), then each
+    // lane takes 8 consecutive columns of a row, so the loads of a, u and the
+    // stores of da, du and g H are 16 bytes per lane along 256-byte row
+    // segments (reading and writing each lane's own 8-byte pieces of 32 rows
+    // took half the kernel's time).  All of a block's a, u loads go out before
+    // its G is staged.
+    // route weight of the wavefront row this lane's index names, for __shfl
+    const int rl = wr * WM + lane;
+    const int ql = row0 + (rl < rows ? rl : 0);
+    const float gql = g.gate[min(max(g.perm_src[ql], 0), g.Tk - 1)];
+    __syncthreads();
     if (!active) return;
-    if (MODE == DH) {
-        const int np = g.m / 128;
-        const int64_t ldau = 2 * (int64_t)g.m;
+    constexpr int RB = WN * 4;                  // bytes per staged row: 32 chunks of 16
+    unsigned char* stg = lds + wave * (32 * RB);
+    const int np = g.m / 128;
+    const int64_t ldau = 2 * (int64_t)g.m;
+    const int cl = lane & 15, rsub = lane >> 4;
+    const int col = pn * BN + wc * WN + 8 * cl;            // this lane's first column
+    // lanes 4-7 of each group of 8 read their second chunk first, so the 8
+    // lanes of one read cycle hit 8 distinct bank groups
+    const int h0 = (cl >> 2) & 1;
 #pragma unroll
-        for (int i = 0; i < MI; ++i) {
-            const int r = wr * WM + i * 32 + (lane & 31);
-            const bool ok = r < rows;
-            const int64_t q = row0 + (ok ? r : 0);
-            const float gq = ok ? g.gate[min(max(g.perm_src[q], 0), g.Tk - 1)] : 0.0f;
-            bf16_t* au = g.AU + q * ldau;
-            bf16_t* hg = g.Hg + q * g.m;
-            float part = 0.0f;
-            // all of this row's a, u loads first (the stores below write the
-            // same array, so the compiler would not move later loads above them)
-            uint2 avs[NJ][4], uvs[NJ][4];
+    for (int i = 0; i < MI; ++i) {
+        u32x4 av[8], uv[8];
+#pragma unroll
+        for (int p = 0; p < 8; ++p) {
+            const int r = wr * WM + i * 32 + p * 4 + rsub;
+            const int64_t q = row0 + (r < rows ? r : 0);
+            av[p] = *(const u32x4*)(g.AU + q * ldau + col);
+            uv[p] = *(const u32x4*)(g.AU + q * ldau + g.m + col);
+        }
+        {
+            const int row = lane & 31;
 #pragma unroll
             for (int j = 0; j < NJ; ++j)
 #pragma unroll
                 for (int a4 = 0; a4 < 4; ++a4) {
-                    const int col = pn * BN + wc * WN + j * 32 + 8 * a4 + ncol0;
-                    avs[j][a4] = ok ? *(const uint2*)(au + col) : make_uint2(0u, 0u);
-                    uvs[j][a4] = ok ? *(const uint2*)(au + g.m + col) : make_uint2(0u, 0u);
+                    const int c = j * 32 + 8 * a4 + ncol0;
+                    *(f32x4*)(stg + row * RB + (((c >> 2) ^ row) << 4)) =
+                        f32x4{acc[i][j][4 * a4], acc[i][j][4 * a4 + 1], acc[i][j][4 * a4 + 2], acc[i][j][4 * a4 + 3]};
                 }
+        }
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+        __builtin_amdgcn_wave_barrier();
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) {
+        for (int p = 0; p < 8; ++p) {
+            const int row = p * 4 + rsub;
+            const int r = wr * WM + i * 32 + row;
+            const bool ok = r < rows;
+            const int64_t q = row0 + (ok ? r : 0);
+            const f32x4 x0 = *(const f32x4*)(stg + row * RB + (((2 * cl + h0) ^ row) << 4));
+            const f32x4 x1 = *(const f32x4*)(stg + row * RB + (((2 * cl + 1 - h0) ^ row) << 4));
+            const f32x4 G0 = h0 ? x1 : x0, G1 = h0 ? x0 : x1;
+            const float gq = __shfl(gql, i * 32 + row);
+            const float Gv[8] = {G0[0], G0[1], G0[2], G0[3], G1[0], G1[1], G1[2], G1[3]};
+            uint32_t dw[4], uw[4], hw[4];
+            float part = 0.0f;
 #pragma unroll
-                for (int a4 = 0; a4 < 4; ++a4) {
-                    const int col = pn * BN + wc * WN + j * 32 + 8 * a4 + ncol0;
-                    if (ok) {
-                        const uint2 av = avs[j][a4];
-                        const uint2 uv = uvs[j][a4];
-                        const float a[4] = {bf_lo(av.x), bf_hi(av.x), bf_lo(av.y), bf_hi(av.y)};
-                        const float u[4] = {bf_lo(uv.x), bf_hi(uv.x), bf_lo(uv.y), bf_hi(uv.y)};
-                        float da[4], du[4], hgv[4];
+            for (int e2 = 0; e2 < 4; ++e2) {
+                float da[2], du[2], hgv[2];
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            float hG;
-                            swiglu_bwd(a[e], u[e], acc[i][j][4 * a4 + e], gq, true, da[e], du[e],
-                                       hgv[e], hG);
-                            part += hG;
-                        }
-                        *(uint2*)(au + col) = make_uint2(pack_bf(da[0], da[1]), pack_bf(da[2], da[3]));
-                        *(uint2*)(au + g.m + col) =
-                            make_uint2(pack_bf(du[0], du[1]), pack_bf(du[2], du[3]));
-                        *(uint2*)(hg + col) = make_uint2(pack_bf(hgv[0], hgv[1]), pack_bf(hgv[2], hgv[3]));
-                    }
+                for (int h = 0; h < 2; ++h) {
+                    const float a = h ? bf_hi(av[p][e2]) : bf_lo(av[p][e2]);
+                    const float u = h ? bf_hi(uv[p][e2]) : bf_lo(uv[p][e2]);
+                    float hG;
+                    swiglu_bwd(a, u, Gv[2 * e2 + h], gq, true, da[h], du[h], hgv[h], hG);
+                    part += hG;
                 }
+                dw[e2] = pack_bf(da[0], da[1]);
+                uw[e2] = pack_bf(du[0], du[1]);
+                hw[e2] = pack_bf(hgv[0], hgv[1]);
             }
-            part += __shfl_xor(part, 32);
-            if (ok && lane < 32) g.dgp[q * np + pn * 2 + wc] = part;
+            // row sum over the 16 lanes of this row (lane cl = 0 keeps it)
+            part += row_ror_f<8>(part);
+            part += row_ror_f<4>(part);
+            part += row_ror_f<2>(part);
+            part += row_ror_f<1>(part);
+            if (ok) {
+                bf16_t* au = g.AU + q * ldau;
+                *(u32x4*)(au + col) = u32x4{dw[0], dw[1], dw[2], dw[3]};
+                *(u32x4*)(au + g.m + col) = u32x4{uw[0], uw[1], uw[2], uw[3]};
+                *(u32x4*)(g.Hg + q * g.m + col) = u32x4{hw[0], hw[1], hw[2], hw[3]};
+                if (cl == 0) g.dgp[q * np + pn * 2 + wc] = part;
+            }
+        }
+        if (i + 1 < MI) {            // the next block overwrites the region
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            __builtin_amdgcn_wave_barrier();
         }
     }
 }
