@@ -56,6 +56,7 @@ struct BwdArgs {
     const int* offsets;      // [N+1] first permuted row of each expert
     const int* order;        // [N] experts by decreasing route count (ties: lower id)
     int k, N, d, m, Tk;
+    uint32_t kmul;           // ceil(2^32 / k), 0 for k = 1 (token of a route entry by multiply-high)
     int ntn;                 // DH, DX: 256-column panels per tile
     const bf16_t* x;
     const bf16_t* dy;
@@ -218,48 +219,65 @@ bwd_gemm(BwdArgs g) {
         }
     }
     // K-strided: copy instruction i of this wavefront moves K rows
-    // kr = 16 wq + 2 i (lanes 0-31) and kr + 1 (lanes 32-63) of the slice;
-    // lane l lands at chunk position l % 32 and so loads chunk
-    // (l % 32) ^ 4 (kr & 3) of its K row.  Rows at or past klen read zeros.
-    const int krl = 16 * wq + (lane >> 5);
-    int ccol[kGroups];
-#pragma unroll
-    for (int i = 0; i < kGroups; ++i) ccol[i] = 8 * ((lane & 31) ^ (4 * ((krl + 2 * i) & 3)));
-    // gathered K-strided operand (WD: dy rows, WGU: x rows): the route
-    // entries of the next slice's K rows, loaded one slice ahead and only
-    // turned into token rows when that slice's copies are issued, so no load
-    // result is waited for inside the slice (rows past klen load the
-    // expert's last entry and copy zeros)
+    // k0 + 2 i (lanes 0-31) and k0 + 2 i + 1 (lanes 32-63) of the slice,
+    // k0 = 16 wq; lane l lands at chunk position l % 32 and so loads chunk
+    // (l % 32) ^ 4 ((2 i + l / 32) & 3) of its K row: one column pattern for
+    // even i, one for odd.  Rows at or past klen read zeros.  The two rows of
+    // a copy are the same for the whole wavefront, so their addresses are
+    // formed on the scalar unit and each lane only adds its own offset.
+    const int hi = lane >> 5;
+    const int cpat[2] = {8 * ((lane & 31) ^ (4 * hi)), 8 * ((lane & 31) ^ (4 * (hi + 2)))};
     constexpr bool kHasGather = (MODE == WD || MODE == WGU);
     const bool gathered = (MODE == WD && half == 0) || (MODE == WGU && half == 1);
-    int graw[kGroups];
+    // plain strided operand: K row 0 at this tile's columns, row stride ld
+    const bf16_t* rbase = nullptr;
+    int64_t ld = 0;
+    if (MODE == DH) { rbase = g.Wd + ew + pn * BN; ld = g.m; }
+    if (MODE == DX) { rbase = g.Wg + ew + pn * BN; ld = g.d; }
+    if (MODE == WD) { rbase = g.Hg + (int64_t)row0 * g.m + ct * BN; ld = g.m; }
+    if (MODE == WGU) { rbase = g.AU + (int64_t)row0 * (2 * g.m) + rt * BM; ld = 2 * g.m; }
+    const int64_t loff[2] = {hi * ld + cpat[0], hi * ld + cpat[1]};
+    // gathered operand (WD: dy rows, WGU: x rows): lane l holds the route
+    // entry of K row 16 wq + l % 16 of the next slice, loaded one slice ahead
+    // (rows past klen load the expert's last entry and copy zeros)
+    const bf16_t* gbase = MODE == WD ? g.dy + rt * BM : g.x + ct * BN;
+    int gent = 0;
     auto fetch_tok = [&](int kt) __attribute__((always_inline)) {
-#pragma unroll
-        for (int i = 0; i < kGroups; ++i)
-            graw[i] = g.perm_src[row0 + min(kt * BK + krl + 2 * i, klen - 1)];
+        gent = g.perm_src[row0 + min(kt * BK + 16 * wq + (lane & 15), klen - 1)];
     };
-    auto tok_row = [&](int i) __attribute__((always_inline)) {
-        return (int64_t)(min(max(graw[i], 0), g.Tk - 1) / g.k);
+    // token row of a route entry t k + s: multiply-high by kmul = ceil(2^32 / k)
+    // is exact for entries below 2^32 / k (checked on the host); k = 1 has kmul 0
+    auto tok_of = [&](int e) __attribute__((always_inline)) {
+        const uint32_t n = (uint32_t)min(max(e, 0), g.Tk - 1);
+        return (int64_t)(__umulhi(n, g.kmul) + (g.kmul == 0u ? n : 0u));
     };
     auto issue_strided = [&](int stage, int kt) __attribute__((always_inline)) {
         unsigned char* dst = lds + stage * STAGEB + (half ? BM * ROWB : 0) + wq * (16 * 512);
+        const int k0 = kt * BK + 16 * wq;
+        const bool full = kt * BK + BK <= klen;
+        if (kHasGather && gathered) {
 #pragma unroll
-        for (int i = 0; i < kGroups; ++i) {
-            const int K = kt * BK + krl + 2 * i;
-            const bf16_t* src;
-            if (MODE == DH) {
-                src = g.Wd + ew + (int64_t)K * g.m + pn * BN;
-            } else if (MODE == DX) {
-                src = (K < g.m ? g.Wg + ew + (int64_t)K * g.d : g.Wu + ew + (int64_t)(K - g.m) * g.d) +
-                      pn * BN;
-            } else if (MODE == WD) {
-                if (half == 0) src = K < klen ? g.dy + tok_row(i) * g.d + rt * BM : kZeroRow;
-                else src = K < klen ? g.Hg + (int64_t)(row0 + K) * g.m + ct * BN : kZeroRow;
-            } else {
-                if (half == 0) src = K < klen ? g.AU + (int64_t)(row0 + K) * (2 * g.m) + rt * BM : kZeroRow;
-                else src = K < klen ? g.x + tok_row(i) * g.d + ct * BN : kZeroRow;
+            for (int i = 0; i < kGroups; ++i) {
+                const int ka = k0 + 2 * i;
+                const bf16_t* pa = ka < klen ? gbase + tok_of(__builtin_amdgcn_readlane(gent, 2 * i)) * g.d : kZeroRow;
+                const bf16_t* pb =
+                    ka + 1 < klen ? gbase + tok_of(__builtin_amdgcn_readlane(gent, 2 * i + 1)) * g.d : kZeroRow;
+                dma16((hi ? pb : pa) + cpat[i & 1], dst + i * 1024);
             }
-            dma16(src + ccol[i], dst + i * 1024);
+        } else {
+            const bf16_t* rb = rbase;
+            int kr = k0;
+            if (MODE == DX && kt * BK >= g.m) { rb = g.Wu + ew + pn * BN; kr -= g.m; }
+            const bf16_t* p = rb + (int64_t)kr * ld;
+            if (kHasGather && !full) {
+#pragma unroll
+                for (int i = 0; i < kGroups; ++i)
+                    dma16(k0 + 2 * i + hi < klen ? p + 2 * i * ld + loff[i & 1] : kZeroRow + cpat[i & 1],
+                          dst + i * 1024);
+            } else {
+#pragma unroll
+                for (int i = 0; i < kGroups; ++i) dma16(p + 2 * i * ld + loff[i & 1], dst + i * 1024);
+            }
         }
     };
     auto issue = [&](int stage, int kt) __attribute__((always_inline)) {
@@ -919,7 +937,9 @@ hipError_t launch_generic_gemms(const pr2_moe_desc& d, const void* x, const void
 bool bwd_mfma_ok(const pr2_moe_desc& d) {
     const int64_t lim = (int64_t)1 << 31;
     const int64_t Tk = d.T * (int64_t)d.k;
-    return mfma_shape_ok(d) && d.m % BN == 0 && d.d % BN == 0 && Tk * 2 * d.m < lim;
+    // (route entries below 2^32 / k keep the multiply-high token division exact)
+    return mfma_shape_ok(d) && d.m % BN == 0 && d.d % BN == 0 && Tk * 2 * d.m < lim &&
+           Tk * (int64_t)d.k < ((int64_t)1 << 32);
 }
 
 int bwd_partials(const pr2_moe_desc& d) { return bwd_mfma_ok(d) ? d.m / 128 : d.m; }
@@ -953,6 +973,7 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
     g.offsets = w.offsets;
     g.order = ws.order;
     g.k = d.k;
+    g.kmul = d.k == 1 ? 0u : (uint32_t)(0xffffffffull / (uint64_t)d.k + 1);
     g.N = d.N;
     g.d = d.d;
     g.m = d.m;
