@@ -278,3 +278,23 @@ def test_workspace_bytes_do_not_decrease_with_batch():
             n = B.workspace_bytes(desc, op)
             assert n >= prev, (op, T, n, prev)
             prev = n
+
+
+@pytest.mark.parametrize("k", list(range(1, 65)) + [96, 128, 255])
+def test_token_division_by_multiply_high(k):
+    """The backward GEMMs turn a route entry n = t k + s into its token t as
+    mulhi(n, ceil(2^32 / k)) (k = 1: the constant is 0 and t = n); the host
+    keeps T k * k below 2^32, so every entry is below 2^32 / k.  Checked here
+    against integer division at the ends of that range, at multiples of k and
+    their neighbours, and at random entries."""
+    import numpy as np
+    kmul = 0 if k == 1 else (0xFFFFFFFF // k + 1)
+    top = (1 << 32) // k - (1 if (1 << 32) % k == 0 else 0)   # largest n with n k < 2^32
+    rng = np.random.default_rng(k)
+    q = np.arange(0, top // k + 1, max(1, (top // k) // 4096), dtype=np.uint64)
+    n = np.concatenate([q * k, q * k + (k - 1), q * k + 1,
+                        rng.integers(0, top + 1, 20000, dtype=np.uint64),
+                        np.arange(max(0, top - 4096), top + 1, dtype=np.uint64)])
+    n = n[n <= top]
+    t = ((n * np.uint64(kmul)) >> np.uint64(32)) + (n if kmul == 0 else np.uint64(0))
+    assert np.array_equal(t, n // np.uint64(k))
