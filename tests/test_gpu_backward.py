@@ -104,6 +104,9 @@ CASES = [
     (1500, 512, 16, 4, 512, "bf16", "zipf", "int16", 3),
     (333, 256, 64, 8, 256, "bf16", "none", "int32", 0),     # many experts with few or no rows
     (100, 256, 4, 4, 256, "bf16", "none", "int32", 0),      # k = N
+    (400, 256, 8, 1, 256, "bf16", "hot8", "int32", 0),      # k = 1: token of an entry is the entry
+    (520, 256, 12, 3, 256, "bf16", "zipf", "int32", 0),     # odd k: multiply-high token division
+    (260, 512, 16, 6, 256, "bf16", "hot8", "int16", 2),     # k = 6
     (300, 192, 8, 2, 128, "bf16", "hot8", "int32", 0),      # generic kernels (d, m not / 256)
     (130, 48, 6, 3, 40, "f32", "none", "int16", 1),         # generic fp32, ragged everything
 ]
