@@ -104,11 +104,24 @@ perm_scan_kernel(int* counts, int64_t nblk, int N, int bm, int* offsets, int* ti
         // owns blocks [l*P, l*P + P) of each, so one wavefront scan per expert
         // turns the lanes' totals into their starting offsets.
         const int P = ((int)nblk + 63) / 64;
+        // a lane's P block counts are consecutive: when they are 4 or 8
+        // 16-byte aligned ints (nblk a multiple of 256 or 512) they move as
+        // 16-byte vectors, 8x fewer memory instructions through this one CU
+        const bool vec = (P == 4 || P == 8) && nblk == 64 * P;
         int v[kScanE][kScanC];
         int tot[kScanE];
 #pragma unroll
         for (int i = 0; i < kScanE; ++i) {
             const int e = wave + kWaves * i;
+            if (vec) {
+#pragma unroll
+                for (int c4 = 0; c4 < kScanC; c4 += 4) {
+                    int4 q = make_int4(0, 0, 0, 0);
+                    if (e < N && c4 < P) q = *(const int4*)(counts + (int64_t)e * nblk + lane * P + c4);
+                    v[i][c4] = q.x; v[i][c4 + 1] = q.y; v[i][c4 + 2] = q.z; v[i][c4 + 3] = q.w;
+                }
+                continue;
+            }
 #pragma unroll
             for (int c = 0; c < kScanC; ++c) {
                 const int b = lane * P + c;
@@ -147,6 +160,14 @@ perm_scan_kernel(int* counts, int64_t nblk, int N, int bm, int* offsets, int* ti
             const int e = wave + kWaves * i;
             if (e >= N) continue;
             const int add = s_off[e];
+            if (vec) {
+#pragma unroll
+                for (int c4 = 0; c4 < kScanC; c4 += 4)
+                    if (c4 < P)
+                        *(int4*)(counts + (int64_t)e * nblk + lane * P + c4) =
+                            make_int4(v[i][c4] + add, v[i][c4 + 1] + add, v[i][c4 + 2] + add, v[i][c4 + 3] + add);
+                continue;
+            }
 #pragma unroll
             for (int c = 0; c < kScanC; ++c) {
                 const int b = lane * P + c;
