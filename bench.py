@@ -396,10 +396,12 @@ def run_decode(args, shape, dev):
     ws = B.route_workspace(Xsteps[0], G["W_r"], G["A"], k, B.PR2_I16)
     stream = torch.cuda.current_stream()
 
+    # the policy's router and predictor are fixed for the whole rollout: the first step
+    # splits them, the other steps reuse that split (pr2_route_predict_reuse)
     def record_all(st):
         for pos in range(P):
             B.route_predict(Xsteps[pos], G["W_r"], G["beta"], G["A"], G["B"], k, buf[:, pos, :],
-                            ws=ws, stream=st)
+                            ws=ws, stream=st, reuse_split=pos > 0)
 
     record_all(stream)
     torch.cuda.synchronize()

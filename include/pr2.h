@@ -128,6 +128,23 @@ pr2_status pr2_route_predict(const pr2_moe_desc* desc, const void* x, const floa
                              size_t ws_bytes, pr2_stream_t stream);
 
 /*
+ * Route prediction for the later steps of a rollout (Sec. 4.1 "Route Prediction During
+ * Rollout": the policy's router and predictor stay fixed while a batch is generated, so one
+ * decode step follows another with the same W_r, A, B).  Same arguments, checks and results
+ * as pr2_route_predict, except that the bf16 three-way split of the weights is not formed
+ * again: the call reads the split that the previous pr2_route_predict (or _reuse) call on
+ * this workspace left there.  The caller guarantees that since that call the workspace was not
+ * used for anything else, the W_r, A and B values are unchanged, and desc differs at most in T
+ * and logits_out has the same NULL-ness (the two choices store the split in different
+ * layouts).  Otherwise the logits are those of the stale weights; nothing detects it.  Shapes
+ * that take the fp64 vector path keep no split and behave exactly as pr2_route_predict.
+ */
+pr2_status pr2_route_predict_reuse(const pr2_moe_desc* desc, const void* x, const float* W_r,
+                                   const float* b_r, const float* A, const float* B,
+                                   void* idx_out, int64_t ldi, float* gate_out, float* logits_out,
+                                   void* ws, size_t ws_bytes, pr2_stream_t stream);
+
+/*
  * Replay forward during training (Sec. 4.1 "Replay During Training"; Eq. pr2_output;
  * Alg. 3 in Appendix D, its first two steps).  No fresh top-k: the recorded ids are used as
  * given, in any order; the weights come from the current router with the predictor bypassed:

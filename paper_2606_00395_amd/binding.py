@@ -24,7 +24,8 @@ STATUS = ["PR2_OK", "PR2_ERR_NULL", "PR2_ERR_SHAPE", "PR2_ERR_DTYPE", "PR2_ERR_A
           "PR2_ERR_HIP"]
 
 # every symbol include/pr2.h declares
-EXPORTS = ["pr2_workspace_bytes", "pr2_route_predict", "pr2_moe_replay_forward",
+EXPORTS = ["pr2_workspace_bytes", "pr2_route_predict", "pr2_route_predict_reuse",
+           "pr2_moe_replay_forward",
            "pr2_moe_replay_backward", "pr2_moe_rollout_forward", "pr2_route_diagnostics",
            "pr2_feature_cache_positions", "pr2_route_predict_cached", "pr2_predictor_loss",
            "pr2_status_string",
@@ -63,6 +64,8 @@ def lib() -> ctypes.CDLL:
     L.pr2_route_predict.argtypes = [POINTER(MoeDesc), P, P, P, P, P, P, c_int64, P, P, P,
                                     c_size_t, P]
     L.pr2_route_predict.restype = c_int
+    L.pr2_route_predict_reuse.argtypes = L.pr2_route_predict.argtypes
+    L.pr2_route_predict_reuse.restype = c_int
     L.pr2_moe_replay_forward.argtypes = [POINTER(MoeDesc), P, P, c_int64, P, P, P, P, P, P, P,
                                          P, c_size_t, P]
     L.pr2_moe_replay_forward.restype = c_int
@@ -164,18 +167,23 @@ def route_workspace(x, W_r, A, k, idx_dtype_code=PR2_I32):
 
 
 def route_predict(x, W_r, b_r, A, B, k, idx_out, gate_out=None, logits_out=None, renorm=True,
-                  ws=None, stream=None):
+                  ws=None, stream=None, reuse_split=False):
     """pr2_route_predict on torch tensors.  ``idx_out`` is a [T, k] view (any row stride)
-    of int16/int32; A/B may be None (no predictor); B None with A given means identity."""
+    of int16/int32; A/B may be None (no predictor); B None with A given means identity.
+    ``reuse_split`` calls pr2_route_predict_reuse: ``ws`` must hold the weight split of the
+    previous call with the same weights (see include/pr2.h)."""
     T, d = x.shape
     N = W_r.shape[1]
     r = 0 if A is None else A.shape[1]
     desc = make_desc(T, d, N, k, 0, r, _act_code(x), _idx_code(idx_out), renorm)
     if ws is None:
         ws = route_workspace(x, W_r, A, k, _idx_code(idx_out))
-    check(lib().pr2_route_predict(byref(desc), _ptr(x), _ptr(W_r), _ptr(b_r), _ptr(A), _ptr(B),
-                                  _ptr(idx_out), _row_stride(idx_out), _ptr(gate_out),
-                                  _ptr(logits_out), _ptr(ws), ws.numel(), _stream(stream)))
+    if reuse_split and ws is None:
+        raise ValueError("reuse_split needs the workspace of the previous call")
+    fn = lib().pr2_route_predict_reuse if reuse_split else lib().pr2_route_predict
+    check(fn(byref(desc), _ptr(x), _ptr(W_r), _ptr(b_r), _ptr(A), _ptr(B), _ptr(idx_out),
+             _row_stride(idx_out), _ptr(gate_out), _ptr(logits_out), _ptr(ws), ws.numel(),
+             _stream(stream)))
 
 
 def replay_workspace(x, idx, W_r, W_gate, renorm=True):

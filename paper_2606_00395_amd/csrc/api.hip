@@ -305,10 +305,11 @@ size_t pr2_workspace_bytes(const pr2_moe_desc* desc, int op) {
     }
 }
 
-pr2_status pr2_route_predict(const pr2_moe_desc* desc, const void* x, const float* W_r,
-                             const float* b_r, const float* A, const float* B, void* idx_out,
-                             int64_t ldi, float* gate_out, float* logits_out, void* ws,
-                             size_t ws_bytes, pr2_stream_t stream) {
+static pr2_status route_predict_impl(const pr2_moe_desc* desc, const void* x, const float* W_r,
+                                     const float* b_r, const float* A, const float* B,
+                                     void* idx_out, int64_t ldi, float* gate_out,
+                                     float* logits_out, void* ws, size_t ws_bytes,
+                                     pr2_stream_t stream, bool reuse_split) {
     pr2_status s = check_desc(desc, false, true);
     if (s != PR2_OK) return s;
     const pr2_moe_desc& d = *desc;
@@ -337,9 +338,25 @@ pr2_status pr2_route_predict(const pr2_moe_desc* desc, const void* x, const floa
     if (s != PR2_OK) return s;
     void* split = need ? (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255) : nullptr;
     hipError_t e = launch_route_predict(d, x, W_r, b_r, A, B, idx_out, ldi, gate_out, logits_out,
-                                        split, (hipStream_t)stream);
+                                        split, (hipStream_t)stream, FeatureCache{}, reuse_split);
     if (e != hipSuccess) return hip_fail(e, "route_predict launch");
     return ok();
+}
+
+pr2_status pr2_route_predict(const pr2_moe_desc* desc, const void* x, const float* W_r,
+                             const float* b_r, const float* A, const float* B, void* idx_out,
+                             int64_t ldi, float* gate_out, float* logits_out, void* ws,
+                             size_t ws_bytes, pr2_stream_t stream) {
+    return route_predict_impl(desc, x, W_r, b_r, A, B, idx_out, ldi, gate_out, logits_out, ws,
+                              ws_bytes, stream, false);
+}
+
+pr2_status pr2_route_predict_reuse(const pr2_moe_desc* desc, const void* x, const float* W_r,
+                                   const float* b_r, const float* A, const float* B,
+                                   void* idx_out, int64_t ldi, float* gate_out, float* logits_out,
+                                   void* ws, size_t ws_bytes, pr2_stream_t stream) {
+    return route_predict_impl(desc, x, W_r, b_r, A, B, idx_out, ldi, gate_out, logits_out, ws,
+                              ws_bytes, stream, true);
 }
 
 pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const void* idx,

@@ -122,7 +122,8 @@ bool router_mfma_ok(const pr2_moe_desc& d, int NC);
 hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const float* W_r,
                                 const float* b_r, const float* A, const float* B, void* idx_out,
                                 int64_t ldi, float* gate_out, float* logits_out, void* split_ws,
-                                hipStream_t s, const FeatureCache& cache = FeatureCache{});
+                                hipStream_t s, const FeatureCache& cache = FeatureCache{},
+                                bool reuse_split = false);
 // current router logits p = x W_r + b_r of every token into p_out [T, N]
 hipError_t launch_router_logits(const pr2_moe_desc& d, const void* x, const float* W_r,
                                 const float* b_r, float* p_out, void* split_ws, hipStream_t s);

@@ -1087,14 +1087,17 @@ bool router_mfma_ok(const pr2_moe_desc& d, int NC) {
 hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const float* W_r,
                                 const float* b_r, const float* A, const float* B, void* idx_out,
                                 int64_t ldi, float* gate_out, float* logits_out, void* split_ws,
-                                hipStream_t s, const FeatureCache& cache) {
+                                hipStream_t s, const FeatureCache& cache, bool reuse_split) {
+    // reuse_split: split_ws already holds this call's split (same weights, same layout)
     const float* Bn = d.r > 0 ? B : nullptr;
     if (logits_out == nullptr && cache.row == nullptr && router_mfma_ok(d, d.N)) {
         // the router logits are not wanted: fold the predictor into the weights
         PredictOut o{b_r, Bn, d.k, d.renorm, 1, idx_out, d.idx_dtype, ldi, gate_out, nullptr,
                      FeatureCache{}, x, d.d, d.act_dtype};
-        hipError_t e = launch_split(W_r, A, Bn, d, d.r, 1, (bf16_t*)split_ws, s);
-        if (e != hipSuccess) return e;
+        if (!reuse_split) {
+            hipError_t e = launch_split(W_r, A, Bn, d, d.r, 1, (bf16_t*)split_ws, s);
+            if (e != hipSuccess) return e;
+        }
         LaunchScope scope("route_predict", s);
         return launch_router_mfma<0>(d, d.N, d.r, x, (const bf16_t*)split_ws, o, ReplayOut{}, s);
     }
@@ -1102,8 +1105,10 @@ hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const floa
                  x, d.d, d.act_dtype};
     const int NC = d.N + d.r;
     if (router_mfma_ok(d, NC)) {
-        hipError_t e = launch_split(W_r, A, Bn, d, d.r, 0, (bf16_t*)split_ws, s);
-        if (e != hipSuccess) return e;
+        if (!reuse_split) {
+            hipError_t e = launch_split(W_r, A, Bn, d, d.r, 0, (bf16_t*)split_ws, s);
+            if (e != hipSuccess) return e;
+        }
         LaunchScope scope("route_predict", s);
         return launch_router_mfma<0>(d, NC, d.r, x, (const bf16_t*)split_ws, o, ReplayOut{}, s);
     }

@@ -298,3 +298,22 @@ def test_token_division_by_multiply_high(k):
     n = n[n <= top]
     t = ((n * np.uint64(kmul)) >> np.uint64(32)) + (n if kmul == 0 else np.uint64(0))
     assert np.array_equal(t, n // np.uint64(k))
+
+
+def test_route_reuse_rejects_bad_arguments():
+    """pr2_route_predict_reuse runs pr2_route_predict's checks before anything else."""
+    L = B.lib()
+    d = desc()
+    ws_bytes = B.workspace_bytes(d, B.OP_ROUTE)
+
+    def reuse(x=FAKE, idx=FAKE, ldi=d.k, ws=FAKE, nbytes=ws_bytes):
+        st = L.pr2_route_predict_reuse(byref(d), c_void_p(x), c_void_p(FAKE), None,
+                                       c_void_p(FAKE), c_void_p(FAKE), c_void_p(idx), ldi, None,
+                                       None, c_void_p(ws), nbytes, None)
+        return B.STATUS[st], L.pr2_last_error().decode()
+
+    assert reuse(x=0)[0] == "PR2_ERR_NULL"
+    assert reuse(idx=0)[0] == "PR2_ERR_NULL"
+    assert reuse(ldi=1)[0] == "PR2_ERR_SHAPE"
+    assert reuse(x=FAKE + 2)[0] == "PR2_ERR_ALIGN"
+    assert reuse(nbytes=ws_bytes - 1)[0] == "PR2_ERR_WORKSPACE"

@@ -31,14 +31,16 @@ def test_decode_record_then_replay():
     Wr, br, A, Bm = (to_dev(L[n]) for n in ("W_r", "beta", "A", "B"))
     buf = torch.full((S, P, k), -1, dtype=torch.int16, device=dev)
     ws = B.route_workspace(Xsteps[0], Wr, A, k, B.PR2_I16)
+    # as a rollout runs it: the first step splits the weights, the others reuse the split
     for pos in range(P):
         # the step writes row s of its [S, k] view at buf[s, pos, :] (row stride P*k)
-        B.route_predict(Xsteps[pos], Wr, br, A, Bm, k, buf[:, pos, :], ws=ws)
+        B.route_predict(Xsteps[pos], Wr, br, A, Bm, k, buf[:, pos, :], ws=ws, reuse_split=pos > 0)
     torch.cuda.synchronize()
     rec = buf.cpu().numpy()
     assert rec.min() >= 0 and rec.max() < s.N, "some route slot was never written"
 
     # index stability: a step recorded into a contiguous buffer gives the same rows
+    # (each such call forms the split afresh, so this also checks the reused split)
     for pos in (0, 777, P - 1):
         one = torch.empty((S, k), dtype=torch.int16, device=dev)
         B.route_predict(Xsteps[pos], Wr, br, A, Bm, k, one, ws=ws)

@@ -183,3 +183,42 @@ def test_route_is_batch_invariant():
             outs.append((cur.cpu().numpy(), kl.cpu().numpy()))
         np.testing.assert_array_equal(outs[1][0], outs[0][0][:T_small])
         np.testing.assert_array_equal(outs[1][1], outs[0][1][:T_small])
+
+
+@pytest.mark.parametrize("logits", [False, True], ids=["folded", "with_logits"])
+def test_route_reuse_split_matches_fresh_calls(logits):
+    """Decode-style steps: the first call splits the weights, the later ones
+    (pr2_route_predict_reuse) read that split.  Every step's ids, gates (and
+    logits) equal those of a fresh pr2_route_predict on the same tokens, bit
+    for bit, and the ids match the oracle's; covers both split layouts (the
+    predictor folded into the weights, and kept apart when logits are wanted)
+    and a batch size that changes between steps."""
+    torch = torch_mod()
+    from paper_2606_00395_amd import binding as B
+    s = W.LayerShape("reuse", T=384, d=512, N=64, k=4, m=8, r=16, act="bf16", skew="hot8")
+    L = W.layer_inputs(s, 21, experts=False)
+    Wr, br, A, Bm = to_dev(L["W_r"]), to_dev(L["beta"]), to_dev(L["A"]), to_dev(L["B"])
+    x_all = to_dev(L["x"], s.act)
+    ws = B.route_workspace(x_all, Wr, A, s.k)
+    steps = [(0, 256), (256, 384), (0, 100), (100, 356)]   # token ranges of four steps
+    for n, (a, b) in enumerate(steps):
+        T = b - a
+        outs = []
+        for reuse in (n > 0, False):
+            idx = torch.full((T, s.k), -1, dtype=torch.int32, device="cuda")
+            gate = torch.empty((T, s.k), dtype=torch.float32, device="cuda")
+            lg = torch.empty((T, s.N), dtype=torch.float32, device="cuda") if logits else None
+            if reuse or n == 0:
+                B.route_predict(x_all[a:b], Wr, br, A, Bm, s.k, idx, gate, lg, ws=ws,
+                                reuse_split=reuse)
+            else:
+                B.route_predict(x_all[a:b], Wr, br, A, Bm, s.k, idx, gate, lg)   # own workspace
+            torch.cuda.synchronize()
+            outs.append((idx.cpu(), gate.cpu(), None if lg is None else lg.cpu()))
+        (i0, g0, l0), (i1, g1, l1) = outs
+        assert torch.equal(i0, i1) and torch.equal(g0, g1), f"step {n}"
+        if logits:
+            assert torch.equal(l0, l1), f"step {n} logits"
+        Ls = dict(L, x=L["x"][a:b])
+        ref = oracle_route(Ls, s.k)
+        assert compare_route(i0.numpy(), g0.numpy(), ref, s.k, f"reuse step {n}") == 0
