@@ -185,17 +185,19 @@ def test_route_is_batch_invariant():
         np.testing.assert_array_equal(outs[1][1], outs[0][1][:T_small])
 
 
-@pytest.mark.parametrize("logits", [False, True], ids=["folded", "with_logits"])
-def test_route_reuse_split_matches_fresh_calls(logits):
+@pytest.mark.parametrize("logits,act", [(False, "bf16"), (True, "bf16"), (False, "f32")],
+                         ids=["folded", "with_logits", "fp32_vector_path"])
+def test_route_reuse_split_matches_fresh_calls(logits, act):
     """Decode-style steps: the first call splits the weights, the later ones
     (pr2_route_predict_reuse) read that split.  Every step's ids, gates (and
     logits) equal those of a fresh pr2_route_predict on the same tokens, bit
     for bit, and the ids match the oracle's; covers both split layouts (the
-    predictor folded into the weights, and kept apart when logits are wanted)
-    and a batch size that changes between steps."""
+    predictor folded into the weights, and kept apart when logits are wanted),
+    a batch size that changes between steps, and fp32 activations (the fp64
+    vector path, which keeps no split)."""
     torch = torch_mod()
     from paper_2606_00395_amd import binding as B
-    s = W.LayerShape("reuse", T=384, d=512, N=64, k=4, m=8, r=16, act="bf16", skew="hot8")
+    s = W.LayerShape("reuse", T=384, d=512, N=64, k=4, m=8, r=16, act=act, skew="hot8")
     L = W.layer_inputs(s, 21, experts=False)
     Wr, br, A, Bm = to_dev(L["W_r"]), to_dev(L["beta"]), to_dev(L["A"]), to_dev(L["B"])
     x_all = to_dev(L["x"], s.act)
