@@ -657,6 +657,36 @@ transpose_wr_kernel(const float* W_r, int d, int N, float* wrt) {
 
 // Per token: dg_s = sum of its partials, then the renormalised-softmax backward
 // dp_s = g_s (dg_s - sum_s' g_s' dg_s'), in route and in permuted order.
+// One lane per route: the k routes of a token sit in an aligned group of
+// 2^kp_log2 >= k lanes of one wavefront (k <= 64), and every lane forms the
+// token's inner product from its group by shuffles, in slot order, so the sums
+// are those of a serial loop over the slots.
+__global__ void __launch_bounds__(256)
+gate_grad_lanes_kernel(const float* dgp, int np, const int* inv, const float* gate, int64_t T,
+                       int k, int kp_log2, float* dp_route, float* dp_perm) {
+    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t t = gid >> kp_log2;
+    const int s = (int)(gid & ((1 << kp_log2) - 1));
+    const bool valid = t < T && s < k;
+    float dg = 0.0f, gs = 0.0f;
+    int q = -1;
+    if (valid) {
+        q = inv[t * k + s];
+        gs = gate[t * k + s];
+        if (q >= 0)
+            for (int p = 0; p < np; ++p) dg += dgp[(int64_t)q * np + p];
+    }
+    const int base = (threadIdx.x & 63) & ~((1 << kp_log2) - 1);
+    float inner = 0.0f;
+    for (int j = 0; j < k; ++j)
+        inner = fmaf(__shfl(gs, base + j, 64), __shfl(dg, base + j, 64), inner);
+    if (valid) {
+        const float dp = gs * (dg - inner);
+        dp_route[t * k + s] = dp;
+        if (q >= 0) dp_perm[q] = dp;
+    }
+}
+
 __global__ void __launch_bounds__(256)
 gate_grad_kernel(const float* dgp, int np, const int* inv, const float* gate, int64_t T, int k,
                  float* dp_route, float* dp_perm) {
@@ -1017,8 +1047,17 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
     // router-logit gradients (needed by the router weight gradient below)
     {
         LaunchScope scope("bwd_gate_grad", s);
-        hipLaunchKernelGGL(gate_grad_kernel, dim3((unsigned)((d.T + 255) / 256)), dim3(256), 0, s,
-                           ws.dgp, ws.np, w.inv, gate, d.T, d.k, ws.dp_route, ws.dp_perm);
+        int kp_log2 = 0;
+        while ((1 << kp_log2) < d.k) ++kp_log2;
+        if (kp_log2 <= 6) {
+            const int64_t lanes = d.T << kp_log2;
+            hipLaunchKernelGGL(gate_grad_lanes_kernel, dim3((unsigned)((lanes + 255) / 256)), dim3(256),
+                               0, s, ws.dgp, ws.np, w.inv, gate, d.T, d.k, kp_log2, ws.dp_route,
+                               ws.dp_perm);
+        } else {
+            hipLaunchKernelGGL(gate_grad_kernel, dim3((unsigned)((d.T + 255) / 256)), dim3(256), 0, s,
+                               ws.dgp, ws.np, w.inv, gate, d.T, d.k, ws.dp_route, ws.dp_perm);
+        }
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
