@@ -792,12 +792,16 @@ __global__ void __launch_bounds__(256)
 router_wgrad_reduce_kernel(const int* offsets, const float* part, const float* dbpart, int bm,
                            int d, int N, float* dW_r, float* db_r) {
     const int e = blockIdx.x;
+    // first tile of expert e: the tile counts of experts 0 .. e-1, summed by all
+    // threads (integer sums, so the order does not matter)
     __shared__ int s_t0;
-    if (threadIdx.x == 0) {
-        int t0 = 0;
-        for (int f = 0; f < e; ++f) t0 += (offsets[f + 1] - offsets[f] + bm - 1) / bm;
-        s_t0 = t0;
-    }
+    if (threadIdx.x == 0) s_t0 = 0;
+    __syncthreads();
+    int c = 0;
+    for (int f = threadIdx.x; f < e; f += blockDim.x) c += (offsets[f + 1] - offsets[f] + bm - 1) / bm;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off, 64);
+    if ((threadIdx.x & 63) == 0) atomicAdd(&s_t0, c);
     __syncthreads();
     const int t0 = s_t0;
     const int nt = (offsets[e + 1] - offsets[e] + bm - 1) / bm;
