@@ -9,6 +9,13 @@ combine) over one batch of synthetic tokens already resident in HBM.
 rollout route of the same layer, which differs from the current router's
 top-k on some tokens): gradients of x, the experts and the router.
 
+``--mode next``: the method's other per-layer calls on the same layer and
+batch, each timed on its own: the rollout-phase layer output under the
+predictive gates (the step whose tokens/s is reported), the route with the
+feature-cache write of 2048 sub-sampled positions, the predictive KL loss and
+its delta-matching variant with dA, dB over those positions, and the route
+diagnostics (current top-k, overlap, deviation histogram, route KL).
+
 ``--mode decode``: the decode-style rollout of 256 sequences x 2048 steps, each
 step's route written into an index-stable int16 record, timed per step both
 as separate launches and replayed from one captured HIP graph, then the replay
@@ -16,7 +23,7 @@ forward of 32768-token micro-batches of the record (tokens/s is for those).
 
 Prints ONE JSON line.
 
-    python bench.py [--mode forward|backward|decode] [--steps K] [--warmup W]
+    python bench.py [--mode forward|backward|decode|next] [--steps K] [--warmup W]
                     [--workload NAME] [--no-cpu-baseline]
 """
 from __future__ import annotations
@@ -35,13 +42,14 @@ if ROOT not in sys.path:
 
 METRIC = "MoE-layer tokens/sec (predictive route + replay forward); MFMA util; HBM GB/s"
 DEFAULT_WORKLOAD = {"forward": "qwen3_30b_T16384", "backward": "qwen3_30b_bwd_T16384",
-                    "decode": "qwen3_30b_decode_256x2048"}
+                    "decode": "qwen3_30b_decode_256x2048", "next": "qwen3_30b_T16384"}
+FEATURE_CACHE_POSITIONS = 2048      # cached positions per 16384-token response (App. E.2)
 
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--mode", choices=("forward", "backward", "decode"), default="forward")
+    ap.add_argument("--mode", choices=("forward", "backward", "decode", "next"), default="forward")
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=None)
@@ -143,6 +151,21 @@ def cpu_baseline_backward(shape, L, idx, dy, n_tok, min_seconds=10.0):
             "kind": "oracle", "host": host_info(),
             "sample": f"{n_tok} of {shape.T} tokens of {shape.name}, float64 replay backward, "
                       f"{reps} pass(es) in {dt:.1f} s"}
+
+
+def cpu_baseline_rollout(shape, L, n_tok, min_seconds=10.0):
+    from oracle import pr2_oracle as O
+    x = L["x"][:n_tok]
+
+    def run():
+        O.rollout_forward(x, L["W_r"], L["beta"], L["A"], L["B"], shape.k, L["W_gate"],
+                          L["W_up"], L["W_down"])
+    reps, dt = timed_cpu(run, n_tok, min_seconds)
+    return {"value": reps * n_tok / dt, "unit": "tokens/s", "cores": blas_threads(),
+            "kind": "oracle", "host": host_info(),
+            "sample": f"{n_tok} of {shape.T} tokens of {shape.name}, float64 rollout forward "
+                      f"(route prediction + layer output under the predictive gates), {reps} "
+                      f"pass(es) in {dt:.1f} s"}
 
 
 def cpu_baseline_decode(shape, L, min_seconds=10.0):
@@ -461,6 +484,128 @@ def run_decode(args, shape, dev):
     return out
 
 
+def run_next(args, shape, dev):
+    import numpy as np
+    import torch
+    import workloads as W
+    from paper_2606_00395_amd import binding as B
+    from paper_2606_00395_amd import costmodel as C
+    L = W.layer_inputs(shape, args.seed)
+    G, up = upload(L, shape, dev)
+    T, d, N, k, m, r = shape.T, shape.d, shape.N, shape.k, shape.m, shape.r
+    ab = 2 if shape.act == "bf16" else 4
+    x = G["x"]
+    stream = torch.cuda.current_stream()
+
+    def measure(step):
+        ms, kern = timed_steps(step, args.steps, args.warmup, stream, B)
+        return ms, {n: round(v, 5) for n, v in kern.items()}
+
+    # f2: rollout-phase layer output (route prediction, record, experts under the
+    # predictive gates), renormalised and paper-literal
+    idx = torch.empty((T, k), dtype=torch.int32, device=dev)
+    gate = torch.empty((T, k), dtype=torch.float32, device=dev)
+    y = torch.empty_like(x)
+    ws_ro = B.rollout_workspace(x, G["W_r"], G["A"], G["W_gate"], k)
+    ws_lit = B.rollout_workspace(x, G["W_r"], G["A"], G["W_gate"], k, renorm=False)
+
+    def rollout(renorm, ws):
+        def step():
+            B.moe_rollout_forward(x, G["W_r"], G["beta"], G["A"], G["B"], G["W_gate"], G["W_up"],
+                                  G["W_down"], k, idx, y, gate, renorm=renorm, ws=ws,
+                                  stream=stream)
+        return step
+    ms_lit, kern_lit = measure(rollout(False, ws_lit))
+    ms, kern = measure(rollout(True, ws_ro))
+    dominant = "gemm1_gate_up_swiglu"
+    achieved = C.gemm1_flops(T, d, k, m) / (kern[dominant] * 1e-3) / 1e12
+    peak = C.PEAK_BF16_FLOPS / 1e12
+    out = base_record(args, "MoE-layer tokens/sec (rollout forward: predictive route, record, "
+                      "layer output under the predictive gates)", T / (ms * 1e-3), "tokens/s", ms,
+                      "bf16" if shape.act == "bf16" else "f32", layer_config(shape))
+    out["roofline"] = {"bound": "mfma", "kernel": dominant, "achieved": achieved, "peak": peak,
+                       "unit": "TFLOP/s", "frac": achieved / peak,
+                       "traffic": profiled_traffic(f"replay_and_route_kernels_{shape.name}.txt",
+                                                  "grouped_gemm_mfma<0>")}
+    out["kernels_ms"] = kern
+    out["rollout_paper_literal_gates"] = {"ms": ms_lit, "value": T / (ms_lit * 1e-3),
+                                          "kernels_ms": kern_lit}
+
+    # f1: route with the feature-cache write of Tc sub-sampled positions
+    Tc = min(FEATURE_CACHE_POSITIONS, T)
+    pos = B.feature_cache_positions(T, Tc, args.seed + 5)
+    row = np.full(T, -1, dtype=np.int32)
+    row[pos] = np.arange(len(pos), dtype=np.int32)
+    cache_row = torch.from_numpy(row).to(dev)
+    h_cache = torch.empty((len(pos), d), dtype=x.dtype, device=dev)
+    p_cache = torch.empty((len(pos), N), dtype=torch.float32, device=dev)
+    ws_r = B.route_workspace(x, G["W_r"], G["A"], k)
+
+    def cached():
+        B.route_predict_cached(x, G["W_r"], G["beta"], G["A"], G["B"], k, idx, cache_row, h_cache,
+                               p_cache, gate, ws=ws_r, stream=stream)
+    ms_c, kern_c = measure(cached)
+    t_route = kern_c.get("route_predict", float("nan"))
+    rbytes = C.route_bytes(T, d, N, r, k, ab, 4) + len(pos) * (d * ab + N * 4)
+    out["feature_cache_route"] = {
+        "ms": ms_c, "cached_positions": len(pos), "kernels_ms": kern_c,
+        "roofline": {"bound": "hbm", "kernel": "route_predict", "achieved": rbytes / (t_route * 1e-3)
+                     / 1e9, "peak": C.PEAK_HBM_BYTES / 1e9, "unit": "GB/s",
+                     "frac": rbytes / (t_route * 1e-3) / C.PEAK_HBM_BYTES}}
+
+    # f1 / f4: predictor loss over the cached positions, current router drifted from
+    # the rollout's, standard and delta-matching forms
+    rng = np.random.default_rng([args.seed, 601])
+    W_cur = up((L["W_r"] + 0.002 * rng.standard_normal(L["W_r"].shape)).astype(np.float32))
+    h_cur = x[torch.from_numpy(pos).to(dev)].contiguous()
+    loss = torch.empty((1,), dtype=torch.float32, device=dev)
+    dA = torch.empty((d, r), dtype=torch.float32, device=dev)
+    dB = torch.empty((r, N), dtype=torch.float32, device=dev)
+    kl = torch.empty((len(pos),), dtype=torch.float32, device=dev)
+    desc = B.make_desc(len(pos), d, N, 1, 0, r, B._act_code(x))
+    ws_p = torch.empty(max(1, B.workspace_bytes(desc, B.OP_PREDICTOR_LOSS)), dtype=torch.uint8,
+                       device=dev)
+    pflops = 2 * len(pos) * d * N + 4 * len(pos) * d * r + 4 * len(pos) * r * N
+    pbytes = len(pos) * (2 * d * ab + N * 4 + 4) + (d * N + 2 * d * r + 2 * r * N) * 4
+    for kind, name in ((0, "predictor_loss"), (1, "delta_matching_loss")):
+        def loss_step():
+            B.predictor_loss(h_cur, W_cur, G["beta"], h_cache, p_cache, G["A"], G["B"], loss, dA,
+                             dB, kl, loss_kind=kind, mini_step=2, ws=ws_p, stream=stream)
+        ms_p, kern_p = measure(loss_step)
+        out[name] = {"ms": ms_p, "cached_positions": len(pos), "kernels_ms": kern_p,
+                     "flops": pflops, "algorithmic_bytes": pbytes,
+                     "hbm_gbps": pbytes / (ms_p * 1e-3) / 1e9}
+
+    # f3: route diagnostics of the recorded rollout route under the drifted router
+    z_ref = torch.empty((T, N), dtype=torch.float32, device=dev)
+    B.route_predict(x, G["W_r"], G["beta"], G["A"], G["B"], k, idx, gate, logits_out=z_ref,
+                    stream=stream)
+    cur = torch.empty((T, k), dtype=torch.int32, device=dev)
+    ov = torch.empty((T,), dtype=torch.int32, device=dev)
+    kl_t = torch.empty((T,), dtype=torch.float32, device=dev)
+    hist = torch.empty((k + 1,), dtype=torch.int64, device=dev)
+    desc = B.make_desc(T, d, N, k, 0, 0, B._act_code(x))
+    ws_d = torch.empty(max(1, B.workspace_bytes(desc, B.OP_ROUTE_DIAG)), dtype=torch.uint8,
+                       device=dev)
+
+    def diag():
+        B.route_diagnostics(x, idx, W_cur, G["beta"], z_ref, cur, ov, kl_t, hist, ws=ws_d,
+                            stream=stream)
+    ms_d, kern_d = measure(diag)
+    t_diag = kern_d.get("route_diagnostics", float("nan"))
+    dbytes = T * d * ab + T * N * 4 + T * k * 4 * 2 + T * 8 + (k + 1) * 8
+    out["route_diagnostics"] = {
+        "ms": ms_d, "kernels_ms": kern_d,
+        "agreement": float(ov.double().mean().item() / k), "hist": hist.cpu().tolist(),
+        "roofline": {"bound": "hbm", "kernel": "route_diagnostics",
+                     "achieved": dbytes / (t_diag * 1e-3) / 1e9, "peak": C.PEAK_HBM_BYTES / 1e9,
+                     "unit": "GB/s", "frac": dbytes / (t_diag * 1e-3) / C.PEAK_HBM_BYTES}}
+    if not args.no_cpu_baseline:
+        n_tok = args.cpu_sample_tokens if args.cpu_sample_tokens > 0 else 4096
+        out["cpu_baseline"] = cpu_baseline_rollout(shape, L, min(n_tok, T))
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -480,7 +625,8 @@ def main():
         b.copy_(a)
         torch.cuda.synchronize()
         del a, b
-    run = {"forward": run_forward, "backward": run_backward, "decode": run_decode}[args.mode]
+    run = {"forward": run_forward, "backward": run_backward, "decode": run_decode,
+           "next": run_next}[args.mode]
     print(json.dumps(run(args, shape, dev)))
 
 

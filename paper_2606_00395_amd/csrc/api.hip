@@ -187,6 +187,7 @@ static PredLossWs pred_ws_layout(const pr2_moe_desc& d, void* base) {
     w.dz = (double*)take(sizeof(double) * T * d.N);
     w.w = (double*)take(sizeof(double) * T * d.r);
     w.kl = (double*)take(sizeof(double) * T);
+    w.part = (double*)take(sizeof(double) * predictor_partial_doubles(d));
     w.wsplit = take(router_mfma_ok(d, d.N) ? router_split_bytes(d.N, d) : 0);
     w.bytes = off + 256;
     return w;

@@ -156,9 +156,11 @@ struct PredLossWs {
     double* dz;         // [T, N] d loss / d zhat
     double* w;          // [T, r] dz B^T
     double* kl;         // [T]
+    double* part;       // per-slice partial products (predictor_partial_doubles)
     void* wsplit;       // router split (N columns)
     size_t bytes;
 };
+size_t predictor_partial_doubles(const pr2_moe_desc& d);
 hipError_t launch_predictor_loss(const pr2_moe_desc& d, const void* h, const float* W_r,
                                  const float* b_r, const void* h_old, const float* p_old,
                                  const float* A, const float* B, int kind, float* kl_out,

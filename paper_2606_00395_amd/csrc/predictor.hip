@@ -9,11 +9,14 @@
 //   dB = sum_t u_t^T dz_t,  dA = sum_t h_old,t^T (dz_t B^T)
 //
 // p comes from the replay router kernels (exact products, one rounding to fp32).
-// Everything after it runs in fp64: u by an fp64 dot product per (token,
-// column), one wavefront per token for the two softmaxes, the KL and dz, and
-// one thread per gradient entry summing over the tokens in a fixed order.
-// Sizes are those of a feature cache (thousands of tokens), so these are small
-// kernels; the sums are deterministic (no atomics).
+// Everything after it runs in fp64.  The three products u = h_old A,
+// dB = u^T dz and dA = h_old^T w go through one tiled kernel: a workgroup forms
+// a 64 x 16 output tile over one slice of the summed index, staging both
+// operands through LDS as fp64, and a second kernel adds the slices in slice
+// order.  The two softmaxes, the KL and dz take one wavefront per token.  The
+// sums are deterministic (no atomics).
+#include <algorithm>
+
 #include "common.h"
 
 namespace pr2 {
@@ -30,20 +33,119 @@ __device__ __forceinline__ double wmax(double v) {
     return v;
 }
 
-// u[t][q] = sum_i h_old[t][i] A[i][q]; one wavefront per token, lanes over q
-template <typename XT>
-__global__ void __launch_bounds__(256)
-proj_u_kernel(const XT* h, int64_t T, int d, const float* A, int r, double* u) {
-    const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int lane = threadIdx.x & 63;
-    if (t >= T) return;
-    const XT* hr = h + t * d;
-    for (int q = lane; q < r; q += 64) {
-        double acc = 0.0;
-        for (int i = 0; i < d; ++i)
-            acc = fma((double)Act<XT>::to_f32(hr[i]), (double)A[(int64_t)i * r + q], acc);
-        u[t * r + q] = acc;
+__device__ __forceinline__ double to_f64(bf16_t v) { return (double)Act<bf16_t>::to_f32(v); }
+__device__ __forceinline__ double to_f64(float v) { return (double)v; }
+__device__ __forceinline__ double to_f64(double v) { return v; }
+
+constexpr int kPM = 64, kPN = 16, kPK = 32;     // output tile and staged slice of the sum
+
+// C[m][n] = sum_k a(m, k) b(k, n), operands addressed through strides:
+// a(m, k) = a[m*a_m + k*a_k], b(k, n) = b[k*b_k + n*b_n].
+struct ProdArgs {
+    const void* a;
+    int64_t a_m, a_k;
+    const void* b;
+    int64_t b_k, b_n;
+    int M, Nc;
+    int64_t K, kslice;
+    double* part;       // [slices][M][Nc]
+};
+
+// workgroup (m tile, n tile, slice); thread (tm, tn) keeps rows 4tm..4tm+3 of column tn
+template <typename TA, typename TB>
+__global__ void __launch_bounds__(256) prod_f64_kernel(ProdArgs p) {
+    __shared__ double sa[kPK][kPM + 1];
+    __shared__ double sb[kPK][kPN];
+    const int tid = threadIdx.x;
+    const int tn = tid & 15, tm = tid >> 4;
+    const int m0 = blockIdx.x * kPM, n0 = blockIdx.y * kPN;
+    const int64_t k0 = (int64_t)blockIdx.z * p.kslice;
+    const int64_t k1 = min(p.K, k0 + p.kslice);
+    const TA* a = (const TA*)p.a;
+    const TB* b = (const TB*)p.b;
+    const bool a_kfast = p.a_k == 1;
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int64_t kc = k0; kc < k1; kc += kPK) {
+        for (int e = tid; e < kPM * kPK; e += 256) {
+            const int kk = a_kfast ? (e & (kPK - 1)) : e / kPM;
+            const int mm = a_kfast ? e / kPK : (e & (kPM - 1));
+            const int64_t k = kc + kk;
+            const int m = m0 + mm;
+            sa[kk][mm] = (m < p.M && k < k1) ? to_f64(a[(int64_t)m * p.a_m + k * p.a_k]) : 0.0;
+        }
+        for (int e = tid; e < kPN * kPK; e += 256) {
+            const int kk = e / kPN, nn = e & (kPN - 1);
+            const int64_t k = kc + kk;
+            const int n = n0 + nn;
+            sb[kk][nn] = (n < p.Nc && k < k1) ? to_f64(b[k * p.b_k + (int64_t)n * p.b_n]) : 0.0;
+        }
+        __syncthreads();
+#pragma unroll 8
+        for (int kk = 0; kk < kPK; ++kk) {
+            const double bv = sb[kk][tn];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[i] = fma(sa[kk][tm * 4 + i], bv, acc[i]);
+        }
+        __syncthreads();
     }
+    const int n = n0 + tn;
+    if (n >= p.Nc) return;
+    double* out = p.part + (int64_t)blockIdx.z * p.M * p.Nc;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int m = m0 + tm * 4 + i;
+        if (m < p.M) out[(int64_t)m * p.Nc + n] = acc[i];
+    }
+}
+
+// out[e] = sum over slices of part[s][e], slice order
+template <typename OT>
+__global__ void __launch_bounds__(256)
+sum_slices_kernel(const double* part, int slices, int64_t n, OT* out) {
+    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (e >= n) return;
+    double acc = 0.0;
+    int s = 0;
+    for (; s + 8 <= slices; s += 8) {       // eight loads in flight, added in slice order
+        double v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = part[(int64_t)(s + i) * n + e];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc += v[i];
+    }
+    for (; s < slices; ++s) acc += part[(int64_t)s * n + e];
+    out[e] = (OT)acc;
+}
+
+// slices of the summed index: about 1024 workgroups in all, each slice a whole
+// number of staged chunks, at most 64 slices
+int64_t prod_kslice(int M, int Nc, int64_t K) {
+    const int64_t tiles = (int64_t)((M + kPM - 1) / kPM) * ((Nc + kPN - 1) / kPN);
+    const int64_t chunks = (K + kPK - 1) / kPK;
+    int64_t s = (1024 + tiles - 1) / tiles;
+    s = std::max<int64_t>(1, std::min<int64_t>({s, chunks, 64}));
+    return std::max<int64_t>(1, (chunks + s - 1) / s) * kPK;
+}
+
+int prod_slices(int M, int Nc, int64_t K) {
+    return (int)std::max<int64_t>(1, (K + prod_kslice(M, Nc, K) - 1) / prod_kslice(M, Nc, K));
+}
+
+template <typename TA, typename TB, typename OT>
+hipError_t launch_prod(const TA* a, int64_t a_m, int64_t a_k, const TB* b, int64_t b_k,
+                       int64_t b_n, int M, int Nc, int64_t K, double* part, OT* out,
+                       hipStream_t s) {
+    if (M <= 0 || Nc <= 0) return hipSuccess;
+    ProdArgs p{a, a_m, a_k, b, b_k, b_n, M, Nc, K, prod_kslice(M, Nc, K), part};
+    const int slices = prod_slices(M, Nc, K);
+    dim3 grid((unsigned)((M + kPM - 1) / kPM), (unsigned)((Nc + kPN - 1) / kPN), (unsigned)slices);
+    hipLaunchKernelGGL((prod_f64_kernel<TA, TB>), grid, dim3(256), 0, s, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t n = (int64_t)M * Nc;
+    hipLaunchKernelGGL(sum_slices_kernel<OT>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                       part, slices, n, out);
+    return hipGetLastError();
 }
 
 struct LossArgs {
@@ -59,27 +161,40 @@ struct LossArgs {
     double* w;              // [T, r]  dz B^T (unused for the identity)
 };
 
-// one wavefront per token
+constexpr int kLdsB = 4096;      // B entries staged in LDS (r N <= 4096)
+
+// one wavefront per token; B in LDS and the token's u in lanes when they fit
 __global__ void __launch_bounds__(256) pred_loss_kernel(LossArgs a) {
+    __shared__ float sB[kLdsB];
+    const int N = a.N, r = a.r;
+    const bool b_lds = a.B && r * N <= kLdsB;
+    if (b_lds) {
+        for (int e = threadIdx.x; e < r * N; e += 256) sB[e] = a.B[e];
+        __syncthreads();
+    }
+    const float* Bm = b_lds ? sB : a.B;
     const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (t >= a.T) return;
-    const int N = a.N, r = a.r;
     const int nv = (N + 63) / 64;
     const double* ut = a.u + t * r;
+    const bool u_lanes = r <= 64;
+    const double ul = (u_lanes && lane < r) ? ut[lane] : 0.0;
     double zh[kMaxVals], tl[kMaxVals];
     double mz = -INFINITY, mt = -INFINITY;
     for (int v = 0; v < nv; ++v) {
         const int j = v * 64 + lane;
+        const int jc = j < N ? j : N - 1;       // every lane takes part in the shuffles
+        double b = 0.0;
+        if (a.B) {
+            for (int q = 0; q < r; ++q)
+                b = fma(u_lanes ? __shfl(ul, q, 64) : ut[q], (double)Bm[(int64_t)q * N + jc], b);
+        } else {
+            b = ut[jc];
+        }
         zh[v] = -INFINITY;
         tl[v] = -INFINITY;
         if (j < N) {
-            double b = 0.0;
-            if (a.B) {
-                for (int q = 0; q < r; ++q) b = fma(ut[q], (double)a.B[(int64_t)q * N + j], b);
-            } else {
-                b = ut[j];
-            }
             const double po = (double)a.p_old[t * N + j];
             const double pc = (double)a.p_cur[t * N + j];
             zh[v] = a.kind == 0 ? po + b : b;
@@ -123,7 +238,7 @@ __global__ void __launch_bounds__(256) pred_loss_kernel(LossArgs a) {
             double part = 0.0;
             for (int v = 0; v < nv; ++v) {
                 const int j = v * 64 + lane;
-                if (j < N) part = fma(zh[v], (double)a.B[(int64_t)q * N + j], part);
+                if (j < N) part = fma(zh[v], (double)Bm[(int64_t)q * N + j], part);
             }
             part = wsum(part);
             if (lane == (q & 63)) a.w[t * r + q] = part;
@@ -145,30 +260,6 @@ __global__ void __launch_bounds__(256) mean_kernel(const double* kl, int64_t T, 
     if (threadIdx.x == 0) out[0] = T > 0 ? (float)(s[0] / (double)T) : 0.0f;
 }
 
-// dB[q][j] = sum_t u[t][q] dz[t][j]
-__global__ void __launch_bounds__(256)
-grad_b_kernel(const double* u, const double* dz, int64_t T, int r, int N, float* dB) {
-    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (e >= (int64_t)r * N) return;
-    const int q = (int)(e / N), j = (int)(e % N);
-    double acc = 0.0;
-    for (int64_t t = 0; t < T; ++t) acc = fma(u[t * r + q], dz[t * N + j], acc);
-    dB[e] = (float)acc;
-}
-
-// dA[i][q] = sum_t h_old[t][i] g[t][q], g = dz B^T (or dz for the identity)
-template <typename XT>
-__global__ void __launch_bounds__(256)
-grad_a_kernel(const XT* h, const double* g, int64_t T, int d, int r, float* dA) {
-    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (e >= (int64_t)d * r) return;
-    const int q = (int)(e / d), i = (int)(e % d);    // i fastest: coalesced reads of h
-    double acc = 0.0;
-    for (int64_t t = 0; t < T; ++t)
-        acc = fma((double)Act<XT>::to_f32(h[t * d + i]), g[t * r + q], acc);
-    dA[(int64_t)i * r + q] = (float)acc;
-}
-
 __global__ void __launch_bounds__(256) fill_f32_kernel(float* p, int64_t n) {
     for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
         p[i] = 0.0f;
@@ -182,9 +273,15 @@ hipError_t fill0(float* p, int64_t n, hipStream_t s) {
     return hipGetLastError();
 }
 
-dim3 blocks_for(int64_t n) { return dim3((unsigned)((n + 255) / 256)); }
-
 }  // namespace
+
+size_t predictor_partial_doubles(const pr2_moe_desc& d) {
+    const int64_t T = d.T;
+    const size_t pu = (size_t)prod_slices((int)T, d.r, d.d) * (size_t)T * d.r;
+    const size_t pb = (size_t)prod_slices(d.r, d.N, T) * (size_t)d.r * d.N;
+    const size_t pa = (size_t)prod_slices(d.d, d.r, T) * (size_t)d.d * d.r;
+    return std::max({pu, pb, pa});
+}
 
 hipError_t launch_predictor_zero(const pr2_moe_desc& d, float* kl_out, float* loss_out, float* dA,
                                  float* dB, hipStream_t s) {
@@ -206,15 +303,14 @@ hipError_t launch_predictor_loss(const pr2_moe_desc& d, const void* h, const flo
     const bool bf = d.act_dtype == PR2_BF16;
     dim3 tok((unsigned)((d.T + 3) / 4));
     {
+        // u = h_old A: (token, column) entries summed over the hidden index
         LaunchScope scope("predictor_proj_u", s);
-        if (bf)
-            hipLaunchKernelGGL(proj_u_kernel<bf16_t>, tok, dim3(256), 0, s, (const bf16_t*)h_old,
-                               d.T, d.d, A, d.r, ws.u);
-        else
-            hipLaunchKernelGGL(proj_u_kernel<float>, tok, dim3(256), 0, s, (const float*)h_old, d.T,
-                               d.d, A, d.r, ws.u);
+        e = bf ? launch_prod((const bf16_t*)h_old, d.d, 1, A, d.r, 1, (int)d.T, d.r, d.d, ws.part,
+                             ws.u, s)
+               : launch_prod((const float*)h_old, d.d, 1, A, d.r, 1, (int)d.T, d.r, d.d, ws.part,
+                             ws.u, s);
     }
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (e != hipSuccess) return e;
     LossArgs a{ws.p_cur, p_old, ws.u, B, d.T, d.N, d.r, kind, kl_out, ws.kl, ws.dz, ws.w};
     {
         LaunchScope scope("predictor_kl", s);
@@ -227,20 +323,16 @@ hipError_t launch_predictor_loss(const pr2_moe_desc& d, const void* h, const flo
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (B) {
+        // dB[q][j] = sum_t u[t][q] dz[t][j]
         LaunchScope scope("predictor_grad_b", s);
-        hipLaunchKernelGGL(grad_b_kernel, blocks_for((int64_t)d.r * d.N), dim3(256), 0, s, ws.u,
-                           ws.dz, d.T, d.r, d.N, dB);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
+        e = launch_prod(ws.u, 1, d.r, ws.dz, d.N, 1, d.r, d.N, d.T, ws.part, dB, s);
+        if (e != hipSuccess) return e;
     }
+    // dA[i][q] = sum_t h_old[t][i] g[t][q], g = dz B^T (dz itself for the identity)
     const double* g = B ? ws.w : ws.dz;
     LaunchScope scope("predictor_grad_a", s);
-    if (bf)
-        hipLaunchKernelGGL(grad_a_kernel<bf16_t>, blocks_for((int64_t)d.d * d.r), dim3(256), 0, s,
-                           (const bf16_t*)h_old, g, d.T, d.d, d.r, dA);
-    else
-        hipLaunchKernelGGL(grad_a_kernel<float>, blocks_for((int64_t)d.d * d.r), dim3(256), 0, s,
-                           (const float*)h_old, g, d.T, d.d, d.r, dA);
-    return hipGetLastError();
+    return bf ? launch_prod((const bf16_t*)h_old, 1, d.d, g, d.r, 1, d.d, d.r, d.T, ws.part, dA, s)
+              : launch_prod((const float*)h_old, 1, d.d, g, d.r, 1, d.d, d.r, d.T, ws.part, dA, s);
 }
 
 }  // namespace pr2

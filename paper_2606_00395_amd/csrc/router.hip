@@ -307,7 +307,7 @@ __device__ __forceinline__ double wave_max_f64(double v) {
 // the fp32 logits), its overlap with the recorded ids, and the route KL.
 template <int MAXV>
 __device__ void diag_token(const float* row, int64_t t, int N, const ReplayOut& o,
-                           const float* bias) {
+                           const float* bias, const int* ids, unsigned int* lhist) {
     const int lane = threadIdx.x & 63;
     const int nv = (N + 63) / 64;
     const DiagOut& g = o.diag;
@@ -331,13 +331,18 @@ __device__ void diag_token(const float* row, int64_t t, int N, const ReplayOut& 
     if (g.overlap || g.hist) {
         int cnt = 0;
         for (int s = 0; s < o.k; ++s) {
-            const int id = load_id(o.idx, o.idx_dtype, t * o.ldi + s);
+            const int id = ids ? ids[s] : load_id(o.idx, o.idx_dtype, t * o.ldi + s);
             if (id >= 0 && id < N && (id & 63) == lane && ((taken >> (id >> 6)) & 1u)) cnt++;
         }
         cnt = wave_sum_i32(cnt);
         if (lane == 0) {
             if (g.overlap) g.overlap[t] = cnt;
-            if (g.hist) atomicAdd(g.hist + (o.k - cnt), 1ull);
+            // the workgroup's LDS histogram when there is one (flushed once per
+            // bin by the kernel), else the global counters directly
+            if (g.hist) {
+                if (lhist) atomicAdd(lhist + (o.k - cnt), 1u);
+                else atomicAdd(g.hist + (o.k - cnt), 1ull);
+            }
         }
     }
     if (g.kl) {
@@ -382,9 +387,9 @@ __device__ void diag_token(const float* row, int64_t t, int N, const ReplayOut& 
 // or null to read them from the route record.
 template <int MAXV>
 __device__ void replay_token(const float* row, int64_t t, int N, const ReplayOut& o,
-                             const float* bias, const int* ids) {
+                             const float* bias, const int* ids, unsigned int* lhist = nullptr) {
     if (o.diag.cur_idx || o.diag.overlap || o.diag.kl || o.diag.hist || o.diag.p_out)
-        diag_token<MAXV>(row, t, N, o, bias);
+        diag_token<MAXV>(row, t, N, o, bias, ids, lhist);
     if (!o.gate_out) return;
     const int lane = threadIdx.x & 63;
     auto logit = [&](int j) {
@@ -794,8 +799,9 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
     constexpr int NSTAGE = RT::NSTAGE;
     constexpr int GPW = RT::GPW;
     __shared__ __attribute__((aligned(1024))) unsigned char lds[NSTAGE * RT::STAGEB];
-    static_assert(NSTAGE * RT::STAGEB >= (int)sizeof(float) * (kRTM * NCp + NCp + kRTM * 64),
-                  "logit tile, bias and staged ids must fit over the copy stages");
+    static_assert(NSTAGE * RT::STAGEB >= (int)sizeof(float) * (kRTM * NCp + NCp + kRTM * 64 + 257),
+                  "logit tile, bias, staged ids and the deviation histogram must fit over the "
+                  "copy stages");
     const int64_t t0 = (int64_t)blockIdx.x * kRTM;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -942,6 +948,11 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
     int* sids = (int*)(sbias + N);
     const float* b_r = MODE == 0 ? po.b_r : ro.b_r;
     for (int j = tid; j < N; j += kRThreads) sbias[j] = b_r ? b_r[j] : 0.0f;
+    // diagnostics: the workgroup's deviation histogram (k + 1 <= 257 bins)
+    unsigned int* shist = (unsigned int*)(sids + kRTM * 64);
+    const bool lds_hist = MODE == 1 && ro.diag.hist != nullptr;
+    if (lds_hist)
+        for (int i = tid; i <= ro.k; i += kRThreads) shist[i] = 0u;
     if (stage_ids) {
 #pragma unroll
         for (int i = 0; i < kIdsPerThread; ++i) {
@@ -957,7 +968,13 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
         for (int tt = wave; tt < kRTM; tt += kRThreads / 64) {
             const int64_t t = t0 + tt;
             if (t >= T) break;
-            replay_token<NTW>(lg + tt * NC, t, N, ro, sbias, stage_ids ? sids + tt * ro.k : nullptr);
+            replay_token<NTW>(lg + tt * NC, t, N, ro, sbias, stage_ids ? sids + tt * ro.k : nullptr,
+                              lds_hist ? shist : nullptr);
+        }
+        if (lds_hist) {
+            __syncthreads();
+            for (int i = tid; i <= ro.k; i += kRThreads)
+                if (shist[i]) atomicAdd(ro.diag.hist + i, (unsigned long long)shist[i]);
         }
         return;
     }

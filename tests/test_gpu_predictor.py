@@ -97,7 +97,8 @@ def run_loss(L, s, Tc, kind, identity=False, mini_step=2):
 
 @pytest.mark.parametrize("name,Tc,kind", [("tiny_fp32_T256", 256, 0), ("tiny_fp32_T256", 100, 1),
                                           ("qwen3_30b_T16384", 2048, 0),
-                                          ("qwen3_30b_T16384", 2048, 1)])
+                                          ("qwen3_30b_T16384", 2048, 1),
+                                          ("qwen3_30b_T16384", 1000, 0)])
 def test_predictor_loss_matches_oracle(name, Tc, kind):
     s = W.WORKLOADS[name]
     L = W.layer_inputs(s, 0, experts=False)
