@@ -275,9 +275,16 @@ hipError_t fill0(float* p, int64_t n, hipStream_t s) {
 
 }  // namespace
 
+// Partial sums of the three products.  The u product's slice count falls as
+// its row tiles grow, so its part is bounded by a size that does not decrease
+// with T (slices <= 1024 / tiles + 1 with tiles >= T ntiles / 64, and
+// slices <= min(64, K chunks)): a workspace sized for a batch serves every
+// smaller one.
 size_t predictor_partial_doubles(const pr2_moe_desc& d) {
     const int64_t T = d.T;
-    const size_t pu = (size_t)prod_slices((int)T, d.r, d.d) * (size_t)T * d.r;
+    const int64_t ntiles = (d.r + kPN - 1) / kPN;
+    const int64_t su_max = std::min<int64_t>(64, std::max<int64_t>(1, (d.d + kPK - 1) / kPK));
+    const size_t pu = (size_t)std::min<int64_t>(su_max * T, 1024 * kPM / ntiles + T) * d.r;
     const size_t pb = (size_t)prod_slices(d.r, d.N, T) * (size_t)d.r * d.N;
     const size_t pa = (size_t)prod_slices(d.d, d.r, T) * (size_t)d.d * d.r;
     return std::max({pu, pb, pa});
