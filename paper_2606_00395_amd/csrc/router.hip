@@ -325,6 +325,14 @@ __device__ void diag_token(const float* row, int64_t t, int N, const ReplayOut& 
         }
     }
     if (!(g.cur_idx || g.overlap || g.kl || g.hist)) return;
+    // the reference logits are fetched before the top-k so that their latency
+    // overlaps the selection
+    float zv[MAXV];
+#pragma unroll
+    for (int v = 0; v < MAXV; ++v) {
+        const int j = v * 64 + lane;
+        zv[v] = (g.kl && j < N) ? g.z_ref[t * N + j] : 0.0f;
+    }
     float pmax;
     const uint32_t taken = select_topk<MAXV>(key, nv, N, o.k, pmax);
     if (g.cur_idx) write_route<MAXV>(taken, nv, g.cur_idx, o.idx_dtype, t * o.k, nullptr, nullptr, 1.0f);
@@ -346,34 +354,33 @@ __device__ void diag_token(const float* row, int64_t t, int N, const ReplayOut& 
         }
     }
     if (g.kl) {
-        const float* zr = g.z_ref + t * N;
         double mz = -INFINITY;
-    #pragma unroll
-    for (int v = 0; v < MAXV; ++v) {
+#pragma unroll
+        for (int v = 0; v < MAXV; ++v) {
             const int j = v * 64 + lane;
-            if (j < N) mz = fmax(mz, (double)zr[j]);
+            if (j < N) mz = fmax(mz, (double)zv[v]);
         }
         mz = wave_max_f64(mz);
         const double mp = (double)pmax;
         double sp = 0.0, sz = 0.0;
-    #pragma unroll
-    for (int v = 0; v < MAXV; ++v) {
+#pragma unroll
+        for (int v = 0; v < MAXV; ++v) {
             const int j = v * 64 + lane;
             if (j < N) {
                 sp += exp((double)p[v] - mp);
-                sz += exp((double)zr[j] - mz);
+                sz += exp((double)zv[v] - mz);
             }
         }
         sp = wave_sum_f64(sp);
         sz = wave_sum_f64(sz);
         const double shift = (mp + log(sp)) - (mz + log(sz));
         double acc = 0.0;
-    #pragma unroll
-    for (int v = 0; v < MAXV; ++v) {
+#pragma unroll
+        for (int v = 0; v < MAXV; ++v) {
             const int j = v * 64 + lane;
             if (j < N) {
                 const double lp = (double)p[v] - mp;
-                acc += exp(lp) / sp * (((double)p[v] - (double)zr[j]) - shift);
+                acc += exp(lp) / sp * (((double)p[v] - (double)zv[v]) - shift);
             }
         }
         acc = wave_sum_f64(acc);
@@ -1010,13 +1017,21 @@ __global__ void __launch_bounds__(256)
 router_pair_sum_kernel(const float* part, int npairs, int64_t n, float* logit) {
     for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < n; q += (int64_t)gridDim.x * 256) {
         double acc = 0.0;
-        for (int p = 0; p < npairs; ++p) acc += (double)part[(int64_t)p * n + q];
+        int p = 0;
+        for (; p + 8 <= npairs; p += 8) {      // eight loads in flight, added in K order
+            float v[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) v[i] = part[(int64_t)(p + i) * n + q];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) acc += (double)v[i];
+        }
+        for (; p < npairs; ++p) acc += (double)part[(int64_t)p * n + q];
         logit[q] = (float)acc;
     }
 }
 
 // split-K below this many 64-token tiles, for K loops of at least kSplitMinSteps
-constexpr int kSplitMaxTiles = 16;
+constexpr int kSplitMaxTiles = 32;
 constexpr int kSplitMinSteps = 8;
 
 bool use_splitk(const pr2_moe_desc& d) {

@@ -151,16 +151,17 @@ def test_route_empty_batch():
 
 def test_route_is_batch_invariant():
     """A token's logits, route and weights do not depend on the batch it is
-    routed in: a decode-sized batch (256, 1000 and a single token) gives
-    bitwise the results of the same tokens inside a 2048-token batch, in the
+    routed in: batches small enough for the split-K path (2048, 1000, 256 and
+    a single token) give bitwise the results of the same tokens inside a
+    4096-token batch, which takes the fused path, in the
     rollout (with and without logits, i.e. with the predictor as separate
     columns or folded into the router weights) and in the replay router
     (current top-k and route KL of the diagnostics)."""
     torch = torch_mod()
     from paper_2606_00395_amd import binding as B
-    s = W.WORKLOADS["qwen3_30b_T16384"].with_(T=2048)
+    s = W.WORKLOADS["qwen3_30b_T16384"].with_(T=4096)
     L = W.layer_inputs(s, 7, experts=False)
-    for T_small in (256, 1000, 1):
+    for T_small in (2048, 256, 1000, 1):
         Ls = {n: (v[:T_small] if n == "x" else v) for n, v in L.items()}
         for want_logits in (True, False):
             big = run_route(L, s, s.k, logits=want_logits)
