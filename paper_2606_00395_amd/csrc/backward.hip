@@ -807,8 +807,17 @@ router_wgrad_reduce_kernel(const int* offsets, const float* part, const float* d
     const int nt = (offsets[e + 1] - offsets[e] + bm - 1) / bm;
     const int i = blockIdx.y * 256 + threadIdx.x;
     if (i < d) {
+        // the expert's tile sums in tile order, eight loads in flight
         float s = 0.0f;
-        for (int t = 0; t < nt; ++t) s += part[(int64_t)(t0 + t) * d + i];
+        int t = 0;
+        for (; t + 8 <= nt; t += 8) {
+            float v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[j] = part[(int64_t)(t0 + t + j) * d + i];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) s += v[j];
+        }
+        for (; t < nt; ++t) s += part[(int64_t)(t0 + t) * d + i];
         dW_r[(int64_t)i * N + e] = s;
     }
     if (db_r && blockIdx.y == 0 && threadIdx.x == 0) {

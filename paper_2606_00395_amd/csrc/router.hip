@@ -362,12 +362,15 @@ __device__ void diag_token(const float* row, int64_t t, int N, const ReplayOut& 
         }
         mz = wave_max_f64(mz);
         const double mp = (double)pmax;
-        double sp = 0.0, sz = 0.0;
+        // KL = sum_j e_j / sp * ((p_j - z_j) - shift), e_j = exp(p_j - max p)
+        double sp = 0.0, sz = 0.0, ep[MAXV];
 #pragma unroll
         for (int v = 0; v < MAXV; ++v) {
             const int j = v * 64 + lane;
+            ep[v] = 0.0;
             if (j < N) {
-                sp += exp((double)p[v] - mp);
+                ep[v] = exp((double)p[v] - mp);
+                sp += ep[v];
                 sz += exp((double)zv[v] - mz);
             }
         }
@@ -378,12 +381,9 @@ __device__ void diag_token(const float* row, int64_t t, int N, const ReplayOut& 
 #pragma unroll
         for (int v = 0; v < MAXV; ++v) {
             const int j = v * 64 + lane;
-            if (j < N) {
-                const double lp = (double)p[v] - mp;
-                acc += exp(lp) / sp * (((double)p[v] - (double)zv[v]) - shift);
-            }
+            if (j < N) acc += ep[v] * (((double)p[v] - (double)zv[v]) - shift);
         }
-        acc = wave_sum_f64(acc);
+        acc = wave_sum_f64(acc) / sp;
         if (lane == 0) g.kl[t] = (float)acc;
     }
 }
