@@ -153,6 +153,60 @@ def cpu_baseline_backward(shape, L, idx, dy, n_tok, min_seconds=10.0):
                       f"{reps} pass(es) in {dt:.1f} s"}
 
 
+def measured_peaks(dev):
+    """A plain 1 GiB device copy (GB/s, read + write) and a dense 8192^3 bf16
+    library GEMM (TFLOP/s), as this GPU runs them now: context for the
+    published peaks the rooflines use."""
+    import torch
+    n = 1 << 28
+    a = torch.ones(n, dtype=torch.float32, device=dev)
+    b = torch.empty_like(a)
+    m = 8192
+    x = torch.randn(m, m, dtype=torch.bfloat16, device=dev)
+    w = torch.randn(m, m, dtype=torch.bfloat16, device=dev)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    out = {}
+    for name, fn, work in (("copy_gbps", lambda: b.copy_(a), 2 * 4 * n / 1e9),
+                           ("library_gemm_bf16_tflops", lambda: torch.matmul(x, w),
+                            2 * m ** 3 / 1e12)):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(10):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        out[name] = work / (e0.elapsed_time(e1) / 10 * 1e-3)
+    del a, b, x, w
+    return out
+
+
+def cpu_baseline_small_1thread(min_seconds=2.0):
+    """The oracle on the 256-token fp32 configuration with one BLAS thread."""
+    import workloads as W
+    from oracle import pr2_oracle as O
+    s = W.WORKLOADS["tiny_fp32_T256"]
+    L = W.layer_inputs(s, 0)
+    import contextlib
+    try:
+        from threadpoolctl import threadpool_limits
+        ctx = threadpool_limits(limits=1, user_api="blas")
+    except ImportError:  # pragma: no cover
+        ctx = contextlib.nullcontext()
+
+    def run():
+        rt = O.route_predict(L["x"], L["W_r"], L["beta"], L["A"], L["B"], s.k)
+        O.replay_forward(L["x"], rt["idx"], L["W_r"], L["beta"], L["W_gate"], L["W_up"],
+                         L["W_down"])
+    with ctx:
+        reps, dt = timed_cpu(run, s.T, min_seconds)
+    return {"value": reps * s.T / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"{s.name}: float64 route prediction + replay forward, {reps} pass(es) "
+                      f"in {dt:.1f} s"}
+
+
 def cpu_baseline_rollout(shape, L, n_tok, min_seconds=10.0):
     from oracle import pr2_oracle as O
     x = L["x"][:n_tok]
@@ -200,6 +254,17 @@ def timed_steps(step, steps, warmup, stream, B):
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
+    # the same steps each between its own pair of events, for the median
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    for a, b in evs:
+        a.record(stream)
+        step()
+        b.record(stream)
+    torch.cuda.synchronize()
+    per = sorted(a.elapsed_time(b) for a, b in evs)
+    timed_steps.median_ms = per[len(per) // 2] if len(per) % 2 else 0.5 * (
+        per[len(per) // 2 - 1] + per[len(per) // 2])
     B.profile_enable(True)
     B.profile_reset()
     torch.cuda.synchronize()
@@ -336,7 +401,9 @@ def run_forward(args, shape, dev):
     out["cold_cache"] = {"ms_per_step": ms_cold, "value": T / (ms_cold * 1e-3),
                          "note": "each step after a 512 MiB device write that evicts L2 and "
                                  "the 256 MB last-level cache"}
+    out["ms_per_step_median"] = timed_steps.median_ms
     out["kernels_ms"] = {n: round(v, 5) for n, v in kern.items()}
+    out["measured_peaks"] = measured_peaks(dev)
     out["replay_forward"] = {
         "ms": t_replay,
         "mfma_frac_whole_layer": C.expert_flops(T, d, k, m) / (t_replay * 1e-3) / C.PEAK_BF16_FLOPS,
@@ -352,6 +419,7 @@ def run_forward(args, shape, dev):
     if not args.no_cpu_baseline:
         n_tok = args.cpu_sample_tokens if args.cpu_sample_tokens > 0 else T
         out["cpu_baseline"] = cpu_baseline_forward(shape, L, min(n_tok, T))
+        out["cpu_baseline_small_1thread"] = cpu_baseline_small_1thread()
     return out
 
 
