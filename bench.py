@@ -374,8 +374,16 @@ def run_forward(args, shape, dev):
         step_on(stream)
 
     ms, kern = timed_steps(step, args.steps, args.warmup, stream, B)
+    median = timed_steps.median_ms
     ms_graph = graph_ms_per_step(step_on, args.steps)
     ms_cold = cold_ms_per_step(step, args.steps, stream)
+    # the same step with every launch on the caller's stream (no side stream for the
+    # replay gates), for comparison
+    os.environ["PR2_NO_SIDE_STREAM"] = "1"
+    try:
+        ms_inorder, _ = timed_steps(step, args.steps, 2, stream, B)
+    finally:
+        del os.environ["PR2_NO_SIDE_STREAM"]
     ab = 2 if shape.act == "bf16" else 4
     ib = 2 if shape.idx_dtype == "int16" else 4
     dominant = "gemm1_gate_up_swiglu"
@@ -401,7 +409,10 @@ def run_forward(args, shape, dev):
     out["cold_cache"] = {"ms_per_step": ms_cold, "value": T / (ms_cold * 1e-3),
                          "note": "each step after a 512 MiB device write that evicts L2 and "
                                  "the 256 MB last-level cache"}
-    out["ms_per_step_median"] = timed_steps.median_ms
+    out["ms_per_step_median"] = median
+    out["in_order"] = {"ms_per_step": ms_inorder,
+                       "note": "the replay gates on the caller's stream instead of the side "
+                               "stream (PR2_NO_SIDE_STREAM=1)"}
     out["kernels_ms"] = {n: round(v, 5) for n, v in kern.items()}
     out["measured_peaks"] = measured_peaks(dev)
     out["replay_forward"] = {

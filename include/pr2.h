@@ -162,6 +162,11 @@ pr2_status pr2_route_predict_reuse(const pr2_moe_desc* desc, const void* x, cons
  * bf16 expert GEMMs use MFMA with fp32 accumulation; the SwiGLU activation is rounded to
  * act_dtype before the down projection and the weighted expert outputs are rounded to
  * act_dtype before the combine, which sums each token's k terms in slot order in fp32.
+ * Streams: the replay weights are formed on a second stream that the library owns (one per
+ * device, created at the first call made outside a HIP graph capture).  That stream is forked
+ * from `stream` with an event and joined back before the down projection, so the work stays
+ * ordered with respect to `stream` and can be captured into a HIP graph.  With the
+ * environment variable PR2_NO_SIDE_STREAM=1, every launch goes on `stream`.
  */
 pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const void* idx,
                                   int64_t ldi, const float* W_r, const float* b_r,

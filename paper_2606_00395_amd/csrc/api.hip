@@ -65,6 +65,48 @@ static pr2_status device_ready() {
     return PR2_OK;
 }
 
+// ------------------------------------------------------ side stream ----
+// A second stream per device for work that can run beside the caller's: it
+// is forked from the caller's stream and joined back with events, so the
+// caller's ordering (and HIP graph capture, which follows such event edges)
+// is kept.  Created once per device, outside any capture, and kept for the
+// life of the process; g_side_mu is held from a call's fork to its join wait
+// so that calls from several threads cannot interleave the two events.
+struct SideStream {
+    hipStream_t s = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+};
+static std::mutex g_side_mu;
+
+static SideStream* side_stream_for(hipStream_t st) {      // caller holds g_side_mu
+    static std::map<int, SideStream> per_dev;
+    const char* off = getenv("PR2_NO_SIDE_STREAM");
+    if (off && off[0] == '1') return nullptr;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    auto it = per_dev.find(dev);
+    if (it != per_dev.end()) return &it->second;
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) {
+        (void)hipGetLastError();
+        return nullptr;                 // not created during a capture: run in order
+    }
+    SideStream ss;
+    if (hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking) != hipSuccess ||
+        hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&ss.join, hipEventDisableTiming) != hipSuccess) {
+        (void)hipGetLastError();
+        if (ss.join) (void)hipEventDestroy(ss.join);
+        if (ss.fork) (void)hipEventDestroy(ss.fork);
+        if (ss.s) (void)hipStreamDestroy(ss.s);
+        return nullptr;
+    }
+    return &per_dev.emplace(dev, ss).first->second;
+}
+
 static pr2_status hip_fail(hipError_t e, const char* what) {
     return fail(PR2_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
@@ -398,12 +440,40 @@ pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const
         if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
     }
     float* gate = gate_out ? gate_out : w.gate;
-    e = launch_replay_gates(d, x, idx, ldi, W_r, b_r, gate, w.err, w.wsplit, st);
-    if (e != hipSuccess) return hip_fail(e, "replay_gates launch");
-    e = launch_permute(d, idx, ldi, w, st);
-    if (e != hipSuccess) return hip_fail(e, "permute launch");
-    e = launch_expert_gemms(d, x, W_gate, W_up, W_down, gate, w, st);
-    if (e != hipSuccess) return hip_fail(e, "expert GEMM launch");
+    {
+        // Only the down projection reads the replay gates: they are formed on
+        // the side stream beside the permutation and the gate/up GEMM, and the
+        // caller's stream waits for them before GEMM 2.
+        std::lock_guard<std::mutex> side_lk(g_side_mu);
+        SideStream* side = side_stream_for(st);
+        hipStream_t gst = st;
+        if (side) {
+            e = hipEventRecord(side->fork, st);
+            if (e == hipSuccess) e = hipStreamWaitEvent(side->s, side->fork, 0);
+            if (e != hipSuccess) return hip_fail(e, "side stream fork");
+            gst = side->s;
+        }
+        e = launch_replay_gates(d, x, idx, ldi, W_r, b_r, gate, w.err, w.wsplit, gst);
+        hipEvent_t gates_done = nullptr;
+        if (side) {
+            // joined even when the launch failed, so no forked work is left behind
+            hipError_t ej = hipEventRecord(side->join, side->s);
+            if (ej == hipSuccess) gates_done = side->join;
+            if (e == hipSuccess) e = ej;
+            if (e != hipSuccess && gates_done) (void)hipStreamWaitEvent(st, gates_done, 0);
+        }
+        if (e != hipSuccess) return hip_fail(e, "replay_gates launch");
+        e = launch_permute(d, idx, ldi, w, st);
+        if (e != hipSuccess) {
+            if (gates_done) (void)hipStreamWaitEvent(st, gates_done, 0);
+            return hip_fail(e, "permute launch");
+        }
+        e = launch_expert_gemms(d, x, W_gate, W_up, W_down, gate, w, st, gates_done);
+        if (e != hipSuccess) {
+            if (gates_done) (void)hipStreamWaitEvent(st, gates_done, 0);
+            return hip_fail(e, "expert GEMM launch");
+        }
+    }
     e = launch_combine(d, w, y, st);
     if (e != hipSuccess) return hip_fail(e, "combine launch");
     if (validate) {

@@ -144,7 +144,7 @@ hipError_t launch_combine(const pr2_moe_desc& d, const ReplayWs& ws, void* y, hi
 // gemm.hip
 hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void* W_gate,
                                const void* W_up, const void* W_down, const float* gate,
-                               const ReplayWs& ws, hipStream_t s);
+                               const ReplayWs& ws, hipStream_t s, hipEvent_t before_gemm2 = nullptr);
 bool mfma_shape_ok(const pr2_moe_desc& d);
 hipError_t launch_preact(const pr2_moe_desc& d, const void* x, const void* W_gate,
                          const void* W_up, const ReplayWs& ws, void* AU, hipStream_t s);
