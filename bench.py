@@ -461,6 +461,11 @@ def run_backward(args, shape, dev):
                               G["W_down"], dy, dx, dWr, dbr, dWg, dWu, dWd, ws=ws, stream=stream)
 
     ms, kern = timed_steps(step, args.steps, args.warmup, stream, B)
+    os.environ["PR2_NO_SIDE_STREAM"] = "1"
+    try:
+        ms_inorder, _ = timed_steps(step, args.steps, 2, stream, B)
+    finally:
+        del os.environ["PR2_NO_SIDE_STREAM"]
     flops = {"bwd_preact_gate_up": 4, "bwd_dh_swiglu": 2, "bwd_dx_gemm": 4, "bwd_wgrad_down": 2,
              "bwd_wgrad_gate_up": 4}
     unit = T * k * d * m
@@ -477,6 +482,9 @@ def run_backward(args, shape, dev):
     out["mfma_frac"] = {n: f * unit / (kern[n] * 1e-3) / C.PEAK_BF16_FLOPS
                         for n, f in flops.items() if n in kern}
     out["mfma_frac_whole_backward"] = 16 * unit / (ms * 1e-3) / C.PEAK_BF16_FLOPS
+    out["in_order"] = {"ms_per_step": ms_inorder,
+                       "note": "the router and input-gradient tail on the caller's stream after "
+                               "the weight-gradient GEMMs (PR2_NO_SIDE_STREAM=1)"}
     if not args.no_cpu_baseline:
         idx_np = idx.cpu().numpy()
         n_tok = args.cpu_sample_tokens if args.cpu_sample_tokens > 0 else 1024

@@ -596,7 +596,15 @@ pr2_status pr2_moe_replay_backward(const pr2_moe_desc* desc, const void* x, cons
     if (e != hipSuccess) return hip_fail(e, "replay_gates launch");
     e = launch_permute(d, idx, ldi, w.fw, st);
     if (e != hipSuccess) return hip_fail(e, "permute launch");
-    e = launch_replay_backward(d, x, idx, ldi, W_r, W_gate, W_up, W_down, dy, w.fw.gate, w, out, st);
+    {
+        // the router and input-gradient tail runs on the side stream beside the
+        // expert weight-gradient GEMMs (forked and joined inside)
+        std::lock_guard<std::mutex> side_lk(g_side_mu);
+        SideStream* side = side_stream_for(st);
+        e = launch_replay_backward(d, x, idx, ldi, W_r, W_gate, W_up, W_down, dy, w.fw.gate, w,
+                                   out, st, side ? side->s : nullptr, side ? side->fork : nullptr,
+                                   side ? side->join : nullptr);
+    }
     if (e != hipSuccess) return hip_fail(e, "backward launch");
     if (validate) {
         int errs[ERR_WORDS];

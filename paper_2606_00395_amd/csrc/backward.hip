@@ -1002,7 +1002,8 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
                                   int64_t ldi, const float* W_r, const void* W_gate,
                                   const void* W_up, const void* W_down, const void* dy,
                                   const float* gate, const BwdWs& ws, const BwdGrads& out,
-                                  hipStream_t s) {
+                                  hipStream_t s, hipStream_t side, hipEvent_t fork,
+                                  hipEvent_t join) {
     const ReplayWs& w = ws.fw;
     const bool bf = d.act_dtype == PR2_BF16;
     const bool mfma = bwd_mfma_ok(d);
@@ -1074,6 +1075,55 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
+    // The router weight gradient and the input gradient's combine read neither
+    // the outputs of the expert weight-gradient GEMMs nor write their inputs:
+    // with a side stream they run on it, beside those GEMMs.
+    auto tail = [&](hipStream_t ts) -> hipError_t {
+        hipError_t e = hipSuccess;
+        {
+            LaunchScope scope("bwd_router_wgrad", ts);
+            dim3 grid((unsigned)w.max_tiles, (unsigned)((d.d + 255) / 256));
+            if (bf)
+                hipLaunchKernelGGL(router_wgrad_partial_kernel<bf16_t>, grid, dim3(256), 0, ts,
+                                   (const bf16_t*)x, w.perm_src, w.tiles, w.tile_count, ws.dp_perm, d.k,
+                                   d.d, ws.rwpart, ws.rbpart);
+            else
+                hipLaunchKernelGGL(router_wgrad_partial_kernel<float>, grid, dim3(256), 0, ts,
+                                   (const float*)x, w.perm_src, w.tiles, w.tile_count, ws.dp_perm, d.k,
+                                   d.d, ws.rwpart, ws.rbpart);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            hipLaunchKernelGGL(router_wgrad_reduce_kernel, dim3((unsigned)d.N, (unsigned)((d.d + 255) / 256)),
+                               dim3(256), 0, ts, w.offsets, ws.rwpart, ws.rbpart, kTileM, d.d, d.N,
+                               out.dW_r, out.db_r);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+
+        // input gradient: per-route rows plus the router term dp W_r^T
+        {
+            LaunchScope scope("bwd_transpose_wr", ts);
+            hipLaunchKernelGGL(transpose_wr_kernel,
+                               dim3((unsigned)((d.d + 31) / 32), (unsigned)((d.N + 31) / 32)), dim3(256),
+                               0, ts, W_r, d.d, d.N, ws.wrt);
+        }
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        LaunchScope scope("bwd_dx_combine", ts);
+        if (bf && d.d % 8 == 0) {
+            const int64_t want = (d.T + kDxTok - 1) / kDxTok;
+            hipLaunchKernelGGL(dx_combine_bf16_kernel, dim3((unsigned)(want < 8192 ? want : 8192)),
+                               dim3(256), 0, ts, (const bf16_t*)w.O, w.inv, ws.dp_route, ws.wrt, idx,
+                               d.idx_dtype, ldi, d.T, d.k, d.d, d.N, (bf16_t*)out.dx);
+        } else if (bf) {
+            hipLaunchKernelGGL(dx_combine_kernel<bf16_t>, dim3((unsigned)d.T), dim3(256), 0, ts,
+                               (const bf16_t*)w.O, w.inv, ws.dp_route, ws.wrt, idx, d.idx_dtype, ldi,
+                               d.T, d.k, d.d, d.N, (bf16_t*)out.dx);
+        } else {
+            hipLaunchKernelGGL(dx_combine_kernel<float>, dim3((unsigned)d.T), dim3(256), 0, ts,
+                               (const float*)w.O, w.inv, ws.dp_route, ws.wrt, idx, d.idx_dtype, ldi,
+                               d.T, d.k, d.d, d.N, (float*)out.dx);
+        }
+        return hipGetLastError();
+    };
+
     if (mfma) {
         {
             LaunchScope scope("bwd_expert_order", s);
@@ -1087,6 +1137,18 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
             hipLaunchKernelGGL(bwd_gemm<DX>, grid_for(w.max_tiles * g.ntn), dim3(kThreads), 0, s, g);
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
+        if (side) {
+            if ((e = hipEventRecord(fork, s)) != hipSuccess) return e;
+            if ((e = hipStreamWaitEvent(side, fork, 0)) != hipSuccess) return e;
+            e = tail(side);
+            const hipError_t ej = hipEventRecord(join, side);
+            if (e == hipSuccess) e = ej;
+            if (e != hipSuccess) {
+                // joined even when a launch failed, so no forked work is left behind
+                if (ej == hipSuccess) (void)hipStreamWaitEvent(s, join, 0);
+                return e;
+            }
+        }
         const int64_t experts_per_xcd = (d.N + kNumXcd - 1) / kNumXcd;
         {
             LaunchScope scope("bwd_wgrad_down", s);
@@ -1094,61 +1156,29 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
                                dim3((unsigned)(kNumXcd * experts_per_xcd * (d.d / BM) * (d.m / BN))),
                                dim3(kThreads), 0, s, g);
         }
-        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = hipGetLastError()) != hipSuccess) {
+            if (side) (void)hipStreamWaitEvent(s, join, 0);
+            return e;
+        }
         {
             LaunchScope scope("bwd_wgrad_gate_up", s);
             hipLaunchKernelGGL(bwd_gemm<WGU>,
                                dim3((unsigned)(kNumXcd * experts_per_xcd * (2 * d.m / BM) * (d.d / BN))),
                                dim3(kThreads), 0, s, g);
         }
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    } else {
-        e = bf ? launch_generic_gemms<bf16_t>(d, x, W_gate, W_up, dy, ws, out, s)
-               : launch_generic_gemms<float>(d, x, W_gate, W_up, dy, ws, out, s);
+        e = hipGetLastError();
+        // the caller's stream takes the side stream's work back (also after an error)
+        if (side) {
+            const hipError_t ew = hipStreamWaitEvent(s, join, 0);
+            return e != hipSuccess ? e : ew;
+        }
         if (e != hipSuccess) return e;
+        return tail(s);
     }
-    {
-        LaunchScope scope("bwd_router_wgrad", s);
-        dim3 grid((unsigned)w.max_tiles, (unsigned)((d.d + 255) / 256));
-        if (bf)
-            hipLaunchKernelGGL(router_wgrad_partial_kernel<bf16_t>, grid, dim3(256), 0, s,
-                               (const bf16_t*)x, w.perm_src, w.tiles, w.tile_count, ws.dp_perm, d.k,
-                               d.d, ws.rwpart, ws.rbpart);
-        else
-            hipLaunchKernelGGL(router_wgrad_partial_kernel<float>, grid, dim3(256), 0, s,
-                               (const float*)x, w.perm_src, w.tiles, w.tile_count, ws.dp_perm, d.k,
-                               d.d, ws.rwpart, ws.rbpart);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        hipLaunchKernelGGL(router_wgrad_reduce_kernel, dim3((unsigned)d.N, (unsigned)((d.d + 255) / 256)),
-                           dim3(256), 0, s, w.offsets, ws.rwpart, ws.rbpart, kTileM, d.d, d.N,
-                           out.dW_r, out.db_r);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
-
-    // input gradient: per-route rows plus the router term dp W_r^T
-    {
-        LaunchScope scope("bwd_transpose_wr", s);
-        hipLaunchKernelGGL(transpose_wr_kernel,
-                           dim3((unsigned)((d.d + 31) / 32), (unsigned)((d.N + 31) / 32)), dim3(256),
-                           0, s, W_r, d.d, d.N, ws.wrt);
-    }
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    LaunchScope scope("bwd_dx_combine", s);
-    if (bf && d.d % 8 == 0) {
-        const int64_t want = (d.T + kDxTok - 1) / kDxTok;
-        hipLaunchKernelGGL(dx_combine_bf16_kernel, dim3((unsigned)(want < 8192 ? want : 8192)),
-                           dim3(256), 0, s, (const bf16_t*)w.O, w.inv, ws.dp_route, ws.wrt, idx,
-                           d.idx_dtype, ldi, d.T, d.k, d.d, d.N, (bf16_t*)out.dx);
-    } else if (bf) {
-        hipLaunchKernelGGL(dx_combine_kernel<bf16_t>, dim3((unsigned)d.T), dim3(256), 0, s,
-                           (const bf16_t*)w.O, w.inv, ws.dp_route, ws.wrt, idx, d.idx_dtype, ldi,
-                           d.T, d.k, d.d, d.N, (bf16_t*)out.dx);
-    } else {
-        hipLaunchKernelGGL(dx_combine_kernel<float>, dim3((unsigned)d.T), dim3(256), 0, s,
-                           (const float*)w.O, w.inv, ws.dp_route, ws.wrt, idx, d.idx_dtype, ldi,
-                           d.T, d.k, d.d, d.N, (float*)out.dx);
-    }
-    return hipGetLastError();
+    e = bf ? launch_generic_gemms<bf16_t>(d, x, W_gate, W_up, dy, ws, out, s)
+           : launch_generic_gemms<float>(d, x, W_gate, W_up, dy, ws, out, s);
+    if (e != hipSuccess) return e;
+    return tail(s);
 }
 
 }  // namespace pr2

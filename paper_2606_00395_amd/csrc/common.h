@@ -184,7 +184,9 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
                                   int64_t ldi, const float* W_r, const void* W_gate,
                                   const void* W_up, const void* W_down, const void* dy,
                                   const float* gate, const BwdWs& ws, const BwdGrads& out,
-                                  hipStream_t s);
+                                  hipStream_t s,
+                                  hipStream_t side = nullptr, hipEvent_t fork = nullptr,
+                                  hipEvent_t join = nullptr);
 hipError_t launch_zero_grads(const pr2_moe_desc& d, const BwdGrads& out, hipStream_t s);
 
 }  // namespace pr2
