@@ -1,0 +1,137 @@
+"""The library's side stream (the replay weights of the forward, the router and
+input-gradient tail of the backward) keeps every call ordered with respect to
+the caller's stream:
+
+* calls made at the same time from two host threads, each on its own stream
+  and workspace, give bitwise the outputs of the same calls made one after
+  the other (the fork and join of one call are not interleaved with the
+  other's);
+* a replay backward captured into a HIP graph (fork and join inside the
+  capture) gives, on every replay, bitwise the gradients of the eager call;
+* PR2_NO_SIDE_STREAM=1 (every launch on the caller's stream) gives bitwise
+  the same outputs."""
+import os
+import threading
+
+import pytest
+
+import workloads as W
+from tests.parity import to_dev
+
+pytestmark = pytest.mark.gpu
+
+SHAPE = W.LayerShape("streams", T=3000, d=512, N=32, k=4, m=256, r=8, act="bf16", skew="hot8")
+
+
+class Problem:
+    """One layer's inputs, outputs and workspaces on the device."""
+
+    def __init__(self, seed):
+        import torch
+        from paper_2606_00395_amd import binding as B
+        s = SHAPE
+        L = W.layer_inputs(s, seed)
+        self.x = to_dev(L["x"], "bf16")
+        self.Wr, self.br, self.A, self.Bm = (to_dev(L[n]) for n in ("W_r", "beta", "A", "B"))
+        self.Wg, self.Wu, self.Wd = (to_dev(L[n], "bf16") for n in ("W_gate", "W_up", "W_down"))
+        self.dy = to_dev(W.upstream_grad(s, seed), "bf16")
+        self.idx = torch.empty((s.T, s.k), dtype=torch.int32, device="cuda")
+        B.route_predict(self.x, self.Wr, self.br, self.A, self.Bm, s.k, self.idx)
+        self.y = torch.empty_like(self.x)
+        self.gate = torch.empty((s.T, s.k), device="cuda")
+        self.grads = [torch.empty_like(self.x), torch.empty_like(self.Wr), torch.empty_like(self.br),
+                      torch.empty(self.Wg.shape, device="cuda"), torch.empty(self.Wu.shape, device="cuda"),
+                      torch.empty(self.Wd.shape, device="cuda")]
+        self.ws_f = B.replay_workspace(self.x, self.idx, self.Wr, self.Wg)
+        self.ws_b = B.backward_workspace(self.x, self.idx, self.Wr, self.Wg)
+        torch.cuda.synchronize()
+
+    def forward(self, st):
+        from paper_2606_00395_amd import binding as B
+        B.moe_replay_forward(self.x, self.idx, self.Wr, self.br, self.Wg, self.Wu, self.Wd, self.y,
+                             self.gate, ws=self.ws_f, stream=st)
+
+    def backward(self, st):
+        from paper_2606_00395_amd import binding as B
+        B.moe_replay_backward(self.x, self.idx, self.Wr, self.br, self.Wg, self.Wu, self.Wd,
+                              self.dy, *self.grads, ws=self.ws_b, stream=st)
+
+    def outputs(self):
+        return [t.clone() for t in [self.y, self.gate] + self.grads]
+
+
+def same(a, b):
+    import torch
+    return all(torch.equal(u, v) for u, v in zip(a, b))
+
+
+def test_concurrent_calls_from_two_threads_match_serial_calls():
+    import torch
+    probs = [Problem(21), Problem(22)]
+    st = torch.cuda.current_stream()
+    ref = []
+    for p in probs:
+        p.forward(st)
+        p.backward(st)
+        torch.cuda.synchronize()
+        ref.append(p.outputs())
+    errors = []
+    streams = [torch.cuda.Stream() for _ in probs]
+
+    def run(i):
+        try:
+            p, s = probs[i], streams[i]
+            for it in range(6):
+                p.forward(s)
+                p.backward(s)
+                s.synchronize()
+                if not same(p.outputs(), ref[i]):
+                    errors.append(f"thread {i} iteration {it}: outputs differ")
+        except Exception as e:  # reported below
+            errors.append(f"thread {i}: {e!r}")
+
+    threads = [threading.Thread(target=run, args=(i,)) for i in range(len(probs))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+
+
+def test_backward_graph_replays_match_eager_call():
+    import torch
+    p = Problem(23)
+    st = torch.cuda.current_stream()
+    p.backward(st)
+    torch.cuda.synchronize()
+    eager = p.outputs()[2:]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        p.backward(torch.cuda.current_stream())
+    for rep in range(3):
+        for g in p.grads:
+            g.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        assert same(p.outputs()[2:], eager), f"replay {rep}"
+        p.forward(st)             # eager work between replays
+        torch.cuda.synchronize()
+
+
+def test_in_order_launches_match_side_stream():
+    import torch
+    p = Problem(24)
+    st = torch.cuda.current_stream()
+    p.forward(st)
+    p.backward(st)
+    torch.cuda.synchronize()
+    side = p.outputs()
+    os.environ["PR2_NO_SIDE_STREAM"] = "1"
+    try:
+        p.forward(st)
+        p.backward(st)
+        torch.cuda.synchronize()
+    finally:
+        del os.environ["PR2_NO_SIDE_STREAM"]
+    assert same(p.outputs(), side)
