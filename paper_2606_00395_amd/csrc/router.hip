@@ -629,6 +629,121 @@ __device__ void predict_group(const float* row, int64_t t, bool valid, int N, in
 
 // Replay weights of token t over its recorded ids (ids: staged in LDS, or
 // null to read the record) by one 16-lane group.
+// Diagnostics of token t by one 16-lane group (lane l16 holds experts
+// j = 16 v + l16): current top-k (ties to the lower id), overlap with the
+// recorded ids, deviation histogram (LDS, lhist) and route KL in fp64.  The
+// fp64 sums run over the group as an xor butterfly, which leaves every lane
+// with the same bits.
+__device__ __forceinline__ double gsum_f64(double v) {
+    v += __shfl_xor(v, 8, 64);
+    v += __shfl_xor(v, 4, 64);
+    v += __shfl_xor(v, 2, 64);
+    return v + __shfl_xor(v, 1, 64);
+}
+
+template <int MAXV16>
+__device__ void diag_group(const float* row, int64_t t, bool valid, int N, const ReplayOut& o,
+                           const float* bias, const int* ids, unsigned int* lhist) {
+    const int lane = threadIdx.x & 63;
+    const int l16 = lane & 15, grp = lane >> 4;
+    const DiagOut& g = o.diag;
+    float p[MAXV16], zv[MAXV16];
+    uint32_t key[MAXV16];
+#pragma unroll
+    for (int v = 0; v < MAXV16; ++v) {
+        const int j = v * 16 + l16;
+        p[v] = -INFINITY;
+        zv[v] = 0.0f;
+        key[v] = 0;
+        if (j < N) {
+            p[v] = (float)((double)row[j] + (bias ? (double)bias[j] : 0.0));
+            key[v] = orderable(p[v]);
+            if (valid && g.p_out) g.p_out[t * N + j] = p[v];
+            if (valid && g.kl) zv[v] = g.z_ref[t * N + j];
+        }
+    }
+    if (!(g.cur_idx || g.overlap || g.kl || g.hist)) return;
+    uint32_t taken = 0;
+    float pmax = 0.0f;
+    for (int it = 0; it < o.k; ++it) {
+        uint32_t best = 0;
+#pragma unroll
+        for (int v = 0; v < MAXV16; ++v)
+            if (!((taken >> v) & 1u) && key[v] > best) best = key[v];
+        const uint32_t gm = gmax_u32(best);
+        int cand = 0x7fffffff;
+#pragma unroll
+        for (int v = MAXV16 - 1; v >= 0; --v)
+            if (v * 16 + l16 < N && !((taken >> v) & 1u) && key[v] == gm) cand = v * 16 + l16;
+        const int win = gmin_i32(cand);
+        if (it == 0) pmax = from_orderable(gm);
+        if (win < N && (win & 15) == l16) taken |= 1u << (win >> 4);
+    }
+    if (g.cur_idx) {
+        int before = 0;
+#pragma unroll
+        for (int v = 0; v < MAXV16; ++v) {
+            const bool mine = (taken >> v) & 1u;
+            const uint32_t gbits = (uint32_t)(__ballot(mine) >> (16 * grp)) & 0xffffu;
+            if (mine && valid) {
+                const int rank = before + __popc(gbits & ((1u << l16) - 1u));
+                const int64_t pos = t * o.k + rank;
+                if (o.idx_dtype == PR2_I16) ((int16_t*)g.cur_idx)[pos] = (int16_t)(v * 16 + l16);
+                else ((int32_t*)g.cur_idx)[pos] = v * 16 + l16;
+            }
+            before += __popc(gbits);
+        }
+    }
+    if (g.overlap || g.hist) {
+        int cnt = 0;
+        if (valid) {
+            for (int s = 0; s < o.k; ++s) {
+                const int id = ids ? ids[s] : load_id(o.idx, o.idx_dtype, t * o.ldi + s);
+                if (id >= 0 && id < N && (id & 15) == l16 && ((taken >> (id >> 4)) & 1u)) cnt++;
+            }
+        }
+        cnt = gsum_i32(cnt);
+        if (valid && l16 == 0) {
+            if (g.overlap) g.overlap[t] = cnt;
+            if (g.hist) {
+                if (lhist) atomicAdd(lhist + (o.k - cnt), 1u);
+                else atomicAdd(g.hist + (o.k - cnt), 1ull);
+            }
+        }
+    }
+    if (g.kl) {
+        // KL(softmax(p) || softmax(z_ref)) = sum_j e_j / sp * ((p_j - z_j) - shift)
+        float zm = -INFINITY;
+#pragma unroll
+        for (int v = 0; v < MAXV16; ++v)
+            if (v * 16 + l16 < N) zm = fmaxf(zm, zv[v]);
+        zm = fmaxf(zm, __shfl_xor(zm, 8, 64));
+        zm = fmaxf(zm, __shfl_xor(zm, 4, 64));
+        zm = fmaxf(zm, __shfl_xor(zm, 2, 64));
+        zm = fmaxf(zm, __shfl_xor(zm, 1, 64));
+        const double mz = (double)zm, mp = (double)pmax;
+        double sp = 0.0, sz = 0.0, ep[MAXV16];
+#pragma unroll
+        for (int v = 0; v < MAXV16; ++v) {
+            ep[v] = 0.0;
+            if (v * 16 + l16 < N) {
+                ep[v] = exp((double)p[v] - mp);
+                sp += ep[v];
+                sz += exp((double)zv[v] - mz);
+            }
+        }
+        sp = gsum_f64(sp);
+        sz = gsum_f64(sz);
+        const double shift = (mp + log(sp)) - (mz + log(sz));
+        double acc = 0.0;
+#pragma unroll
+        for (int v = 0; v < MAXV16; ++v)
+            if (v * 16 + l16 < N) acc += ep[v] * (((double)p[v] - (double)zv[v]) - shift);
+        acc = gsum_f64(acc) / sp;
+        if (valid && l16 == 0) g.kl[t] = (float)acc;
+    }
+}
+
 template <int MAXV16>
 __device__ void replay_group(const float* row, int64_t t, bool valid, int N, const ReplayOut& o,
                              const float* bias, const int* ids) {
@@ -971,12 +1086,16 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
     const bool diag = MODE == 1 && (ro.diag.cur_idx || ro.diag.overlap || ro.diag.kl ||
                                     ro.diag.hist || ro.diag.p_out);
     if (diag) {
-        // diagnostics: one token per wavefront
-        for (int tt = wave; tt < kRTM; tt += kRThreads / 64) {
+        // diagnostics: four tokens per wavefront, one per 16-lane group
+        for (int base = wave * 4; base < kRTM; base += (kRThreads / 64) * 4) {
+            if (t0 + base >= T) break;
+            const int tt = base + (lane >> 4);
             const int64_t t = t0 + tt;
-            if (t >= T) break;
-            replay_token<NTW>(lg + tt * NC, t, N, ro, sbias, stage_ids ? sids + tt * ro.k : nullptr,
-                              lds_hist ? shist : nullptr);
+            const bool valid = t < T;
+            const int* tids = stage_ids ? sids + tt * ro.k : nullptr;
+            diag_group<4 * NTW>(lg + tt * NC, t, valid, N, ro, sbias, tids,
+                                lds_hist ? shist : nullptr);
+            if (ro.gate_out) replay_group<4 * NTW>(lg + tt * NC, t, valid, N, ro, sbias, tids);
         }
         if (lds_hist) {
             __syncthreads();
