@@ -218,8 +218,9 @@ pr2_status pr2_moe_rollout_forward(const pr2_moe_desc* desc, const void* x, cons
  * are recomputed (nothing is saved from the forward call); on the bf16 MFMA path
  * (d % 256 == 0, m % 256 == 0) a, u, their gradients, g H and the per-route input gradients
  * are held in bf16, with fp32 accumulation everywhere.
- * Streams: on the MFMA path, the router weight gradient and the combine of the input
- * gradient run on the library's side stream beside the expert weight-gradient GEMMs.  The
+ * Streams: the replay weights (beside the permutation and the pre-activation GEMM) and, on
+ * the MFMA path, the router weight gradient and the combine of the input gradient (beside
+ * the expert weight-gradient GEMMs) run on the library's side stream.  The
  * side stream is forked from `stream` and joined back before the call's last launch, the
  * same stream and rules as pr2_moe_replay_forward.
  */

@@ -74,7 +74,7 @@ static pr2_status device_ready() {
 // so that calls from several threads cannot interleave the two events.
 struct SideStream {
     hipStream_t s = nullptr;
-    hipEvent_t fork = nullptr, join = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr, mid = nullptr;
 };
 static std::mutex g_side_mu;
 
@@ -97,8 +97,10 @@ static SideStream* side_stream_for(hipStream_t st) {      // caller holds g_side
     SideStream ss;
     if (hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking) != hipSuccess ||
         hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&ss.join, hipEventDisableTiming) != hipSuccess) {
+        hipEventCreateWithFlags(&ss.join, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&ss.mid, hipEventDisableTiming) != hipSuccess) {
         (void)hipGetLastError();
+        if (ss.mid) (void)hipEventDestroy(ss.mid);
         if (ss.join) (void)hipEventDestroy(ss.join);
         if (ss.fork) (void)hipEventDestroy(ss.fork);
         if (ss.s) (void)hipStreamDestroy(ss.s);
@@ -592,18 +594,36 @@ pr2_status pr2_moe_replay_backward(const pr2_moe_desc* desc, const void* x, cons
         e = hipMemsetAsync(w.fw.err, 0, sizeof(int) * ERR_WORDS, st);
         if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
     }
-    e = launch_replay_gates(d, x, idx, ldi, W_r, b_r, w.fw.gate, w.fw.err, w.fw.wsplit, st);
-    if (e != hipSuccess) return hip_fail(e, "replay_gates launch");
-    e = launch_permute(d, idx, ldi, w.fw, st);
-    if (e != hipSuccess) return hip_fail(e, "permute launch");
     {
-        // the router and input-gradient tail runs on the side stream beside the
-        // expert weight-gradient GEMMs (forked and joined inside)
+        // On the side stream: the replay weights beside the permutation and the
+        // pre-activation GEMM (the dh kernel waits for them), then the router and
+        // input-gradient tail beside the expert weight-gradient GEMMs (forked and
+        // joined inside the backward launch).
         std::lock_guard<std::mutex> side_lk(g_side_mu);
         SideStream* side = side_stream_for(st);
+        hipStream_t gst = st;
+        if (side) {
+            e = hipEventRecord(side->fork, st);
+            if (e == hipSuccess) e = hipStreamWaitEvent(side->s, side->fork, 0);
+            if (e != hipSuccess) return hip_fail(e, "side stream fork");
+            gst = side->s;
+        }
+        e = launch_replay_gates(d, x, idx, ldi, W_r, b_r, w.fw.gate, w.fw.err, w.fw.wsplit, gst);
+        hipEvent_t gates_done = nullptr;
+        if (side) {
+            const hipError_t ej = hipEventRecord(side->mid, side->s);
+            if (ej == hipSuccess) gates_done = side->mid;
+            if (e == hipSuccess) e = ej;
+        }
+        if (e == hipSuccess) e = launch_permute(d, idx, ldi, w.fw, st);
+        if (e != hipSuccess) {
+            if (gates_done) (void)hipStreamWaitEvent(st, gates_done, 0);
+            return hip_fail(e, "replay_gates / permute launch");
+        }
         e = launch_replay_backward(d, x, idx, ldi, W_r, W_gate, W_up, W_down, dy, w.fw.gate, w,
                                    out, st, side ? side->s : nullptr, side ? side->fork : nullptr,
-                                   side ? side->join : nullptr);
+                                   side ? side->join : nullptr, gates_done);
+        if (e != hipSuccess && gates_done) (void)hipStreamWaitEvent(st, gates_done, 0);
     }
     if (e != hipSuccess) return hip_fail(e, "backward launch");
     if (validate) {

@@ -1003,7 +1003,7 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
                                   const void* W_up, const void* W_down, const void* dy,
                                   const float* gate, const BwdWs& ws, const BwdGrads& out,
                                   hipStream_t s, hipStream_t side, hipEvent_t fork,
-                                  hipEvent_t join) {
+                                  hipEvent_t join, hipEvent_t gates_ready) {
     const ReplayWs& w = ws.fw;
     const bool bf = d.act_dtype == PR2_BF16;
     const bool mfma = bwd_mfma_ok(d);
@@ -1040,6 +1040,9 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
     };
 
     // gate gradient partials and the SwiGLU backward
+    // the dh kernel reads the replay weights: when they come from another
+    // stream, wait for them here
+    if (gates_ready && (e = hipStreamWaitEvent(s, gates_ready, 0)) != hipSuccess) return e;
     if (mfma) {
         g.ntn = d.m / BN;
         LaunchScope scope("bwd_dh_swiglu", s);

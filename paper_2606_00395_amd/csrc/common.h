@@ -186,7 +186,7 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
                                   const float* gate, const BwdWs& ws, const BwdGrads& out,
                                   hipStream_t s,
                                   hipStream_t side = nullptr, hipEvent_t fork = nullptr,
-                                  hipEvent_t join = nullptr);
+                                  hipEvent_t join = nullptr, hipEvent_t gates_ready = nullptr);
 hipError_t launch_zero_grads(const pr2_moe_desc& d, const BwdGrads& out, hipStream_t s);
 
 }  // namespace pr2
