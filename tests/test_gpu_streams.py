@@ -135,3 +135,4 @@ def test_in_order_launches_match_side_stream():
     finally:
         del os.environ["PR2_NO_SIDE_STREAM"]
     assert same(p.outputs(), side)
+
