@@ -29,7 +29,8 @@
  *     touch memory out of bounds for any id value: an out-of-range id is skipped and counted.
  *     With the environment variable PR2_VALIDATE=1 each call that reads a route also
  *     synchronises its stream and returns PR2_ERR_ROUTE if any id was out of range or
- *     repeated within its row.
+ *     repeated within its row (PR2_ERR_UNSUPPORTED, nothing enqueued, if the stream is
+ *     being captured into a HIP graph).
  *   - Inputs must be finite; NaN or Inf give unspecified (but memory-safe) results.
  */
 #ifndef PR2_H
@@ -117,7 +118,7 @@ size_t pr2_workspace_bytes(const pr2_moe_desc* desc, int op);
  *   logits_out [T, N] fp32 router logits p (without the predictor term); may be NULL.
  *   ws         scratch of at least pr2_workspace_bytes(desc, PR2_OP_ROUTE) bytes (the bf16
  *              three-way split of [W_r | A] that the MFMA router reads, and for batches of at
- *              most 1024 tokens the partial logits of its split-K form; 0 bytes when the
+ *              most 2048 tokens the partial logits of its split-K form; 0 bytes when the
  *              shape takes the fp64 vector path).  Reused freely between calls on one stream.
  * Logits are accumulated from exact products (fp32 weights split into three bf16 parts times
  * bf16 x, or fp64 FMA for fp32 x) in fp32 chunks summed in fp64, then rounded once to fp32.
@@ -133,11 +134,14 @@ pr2_status pr2_route_predict(const pr2_moe_desc* desc, const void* x, const floa
  * decode step follows another with the same W_r, A, B).  Same arguments, checks and results
  * as pr2_route_predict, except that the bf16 three-way split of the weights is not formed
  * again: the call reads the split that the previous pr2_route_predict (or _reuse) call on
- * this workspace left there.  The caller guarantees that since that call the workspace was not
- * used for anything else, the W_r, A and B values are unchanged, and desc differs at most in T
- * and logits_out has the same NULL-ness (the two choices store the split in different
- * layouts).  Otherwise the logits are those of the stale weights; nothing detects it.  Shapes
- * that take the fp64 vector path keep no split and behave exactly as pr2_route_predict.
+ * this workspace left there.  The library keeps a host-side record per workspace address of
+ * the split it holds (device, W_r, A, B pointers, d, N, r and the layout, which depends on the
+ * NULL-ness of logits_out); any other call that takes the workspace drops the records inside
+ * it.  The call returns PR2_ERR_WORKSPACE, with nothing enqueued, when ws holds no record or
+ * one that differs from this call in any of those.  The caller still guarantees that the
+ * VALUES of W_r, A and B did not change since the split was formed (only pointers are
+ * compared).  Shapes that take the fp64 vector path keep no split and behave exactly as
+ * pr2_route_predict.
  */
 pr2_status pr2_route_predict_reuse(const pr2_moe_desc* desc, const void* x, const float* W_r,
                                    const float* b_r, const float* A, const float* B,
@@ -173,6 +177,32 @@ pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const
                                   const void* W_gate, const void* W_up, const void* W_down,
                                   void* y, float* gate_out, void* ws, size_t ws_bytes,
                                   pr2_stream_t stream);
+
+/*
+ * Replay forward with the route-tracking diagnostics of Sec. 5.4 (top-k agreement, routing
+ * deviation, route KL) formed in the same pass: the replay-weight epilogue already holds all N
+ * current router logits of each token, so it also selects their top-k and compares it with the
+ * recorded ids.  Everything pr2_moe_replay_forward does, plus (each output may be NULL):
+ *
+ *   p = x W_r + b_r (the replay router, predictor bypassed),  I = TopK(p, k) (ties to the lower
+ *   id, decided on the fp32 logits)
+ *   cur_idx_out [T, k] idx_dtype   I, ascending
+ *   overlap_out [T] int32          |idx_t ∩ I_t|   (agreement = overlap / k, deviation = k - overlap)
+ *   kl_out      [T] fp32           KL(softmax(p_t) || softmax(z_ref_t)), evaluated in fp64
+ *   hist_out    [k + 1] uint64     tokens per deviation value, overwritten (8-byte aligned)
+ *   z_ref       [T, N] fp32 reference logits (e.g. the rollout's predictive logits); needed only
+ *               with kl_out
+ * Same workspace, streams and checks as pr2_moe_replay_forward; y and gate_out are bitwise
+ * those of pr2_moe_replay_forward, and the diagnostics bitwise those of pr2_route_diagnostics
+ * on the same inputs.  T = 0 only zeroes hist_out.
+ */
+pr2_status pr2_moe_replay_forward_diag(const pr2_moe_desc* desc, const void* x, const void* idx,
+                                       int64_t ldi, const float* W_r, const float* b_r,
+                                       const void* W_gate, const void* W_up, const void* W_down,
+                                       void* y, float* gate_out, const float* z_ref,
+                                       void* cur_idx_out, int32_t* overlap_out, float* kl_out,
+                                       uint64_t* hist_out, void* ws, size_t ws_bytes,
+                                       pr2_stream_t stream);
 
 /*
  * Rollout-phase layer forward (Sec. 4.1 "Route Prediction During Rollout"; Eq. pr2_old_output;

@@ -25,7 +25,7 @@ STATUS = ["PR2_OK", "PR2_ERR_NULL", "PR2_ERR_SHAPE", "PR2_ERR_DTYPE", "PR2_ERR_A
 
 # every symbol include/pr2.h declares
 EXPORTS = ["pr2_workspace_bytes", "pr2_route_predict", "pr2_route_predict_reuse",
-           "pr2_moe_replay_forward",
+           "pr2_moe_replay_forward", "pr2_moe_replay_forward_diag",
            "pr2_moe_replay_backward", "pr2_moe_rollout_forward", "pr2_route_diagnostics",
            "pr2_feature_cache_positions", "pr2_route_predict_cached", "pr2_predictor_loss",
            "pr2_status_string",
@@ -69,6 +69,9 @@ def lib() -> ctypes.CDLL:
     L.pr2_moe_replay_forward.argtypes = [POINTER(MoeDesc), P, P, c_int64, P, P, P, P, P, P, P,
                                          P, c_size_t, P]
     L.pr2_moe_replay_forward.restype = c_int
+    L.pr2_moe_replay_forward_diag.argtypes = [POINTER(MoeDesc), P, P, c_int64, P, P, P, P, P, P,
+                                              P, P, P, P, P, P, P, c_size_t, P]
+    L.pr2_moe_replay_forward_diag.restype = c_int
     L.pr2_moe_replay_backward.argtypes = [POINTER(MoeDesc), P, P, c_int64, P, P, P, P, P, P, P,
                                           P, P, P, P, P, P, c_size_t, P]
     L.pr2_moe_replay_backward.restype = c_int
@@ -146,7 +149,107 @@ def _stream(stream):
 def _row_stride(idx):
     if idx.dim() != 2 or idx.stride(1) != 1:
         raise ValueError("ids must be a 2-D view [T, k] with unit stride along k")
+    if idx.shape[0] > 1 and idx.stride(0) < idx.shape[1]:
+        raise ValueError("id rows overlap: row stride below k")
     return idx.stride(0)
+
+
+def _need(t, name, shape, dtype=None, device=None, optional=False):
+    """Checks that tensor ``t`` is what the C ABI will read or write through its
+    pointer: the given shape, dtype and device, row-major and contiguous."""
+    torch = _torch()
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous (row-major)")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
+def _need_ids(idx, name, T, k, device):
+    torch = _torch()
+    if tuple(idx.shape) != (T, k):
+        raise ValueError(f"{name} has shape {tuple(idx.shape)}, expected {(T, k)}")
+    if idx.dtype not in (torch.int16, torch.int32):
+        raise TypeError(f"{name} must be int16 or int32, got {idx.dtype}")
+    if idx.device != device:
+        raise ValueError(f"{name} is on {idx.device}, expected {device}")
+    return _row_stride(idx)
+
+
+def _need_act(x, name="x"):
+    torch = _torch()
+    if x.dim() != 2:
+        raise ValueError(f"{name} must be 2-D [T, d]")
+    _act_code(x)
+    if not x.is_contiguous():
+        raise ValueError(f"{name} must be contiguous (row-major)")
+    if x.device.type != "cuda":
+        raise ValueError(f"{name} must be a CUDA (HIP) tensor")
+    return x.shape[0], x.shape[1], x.dtype, x.device
+
+
+def _need_ws(ws, device):
+    torch = _torch()
+    if ws is None:
+        return
+    if ws.dtype != torch.uint8 or not ws.is_contiguous() or ws.device != device:
+        raise ValueError("ws must be a contiguous uint8 tensor on the inputs' device")
+
+
+def _new_ws(nbytes, device, stream):
+    """A workspace of nbytes; allocated on ``stream`` when one is given, so that
+    the caching allocator does not hand its memory to another stream while the
+    call may still be using it."""
+    torch = _torch()
+    if stream is None:
+        return torch.empty(max(1, nbytes), dtype=torch.uint8, device=device)
+    with torch.cuda.stream(stream):
+        return torch.empty(max(1, nbytes), dtype=torch.uint8, device=device)
+
+
+def _experts(W_gate, W_up, W_down, N, d, dtype, device):
+    if W_gate.dim() != 3:
+        raise ValueError("W_gate must be [N, m, d]")
+    m = W_gate.shape[1]
+    _need(W_gate, "W_gate", (N, m, d), dtype, device)
+    _need(W_up, "W_up", (N, m, d), dtype, device)
+    _need(W_down, "W_down", (N, d, m), dtype, device)
+    return m
+
+
+def _router(W_r, b_r, d, device):
+    torch = _torch()
+    if W_r.dim() != 2 or W_r.shape[0] != d:
+        raise ValueError(f"W_r must be [d={d}, N]")
+    N = W_r.shape[1]
+    _need(W_r, "W_r", (d, N), torch.float32, device)
+    _need(b_r, "b_r", (N,), torch.float32, device, optional=True)
+    return N
+
+
+def _predictor(A, B, d, N, device):
+    torch = _torch()
+    if A is None:
+        if B is not None:
+            raise ValueError("B given without A")
+        return 0
+    if A.dim() != 2 or A.shape[0] != d:
+        raise ValueError(f"A must be [d={d}, r]")
+    r = A.shape[1]
+    _need(A, "A", (d, r), torch.float32, device)
+    if B is None and r != N:
+        raise ValueError("B may be omitted only for a full-rank predictor (r == N)")
+    _need(B, "B", (r, N), torch.float32, device, optional=True)
+    return r
 
 
 def make_desc(T, d, N, k, m=0, r=0, act=PR2_BF16, idx=PR2_I32, renorm=True) -> MoeDesc:
@@ -157,13 +260,11 @@ def workspace_bytes(desc: MoeDesc, op: int) -> int:
     return int(lib().pr2_workspace_bytes(byref(desc), op))
 
 
-def route_workspace(x, W_r, A, k, idx_dtype_code=PR2_I32):
-    torch = _torch()
+def route_workspace(x, W_r, A, k, idx_dtype_code=PR2_I32, stream=None):
     T, d = x.shape
     r = 0 if A is None else A.shape[1]
     desc = make_desc(T, d, W_r.shape[1], k, 0, r, _act_code(x), idx_dtype_code)
-    n = workspace_bytes(desc, OP_ROUTE)
-    return torch.empty(max(1, n), dtype=torch.uint8, device=x.device)
+    return _new_ws(workspace_bytes(desc, OP_ROUTE), x.device, stream)
 
 
 def route_predict(x, W_r, b_r, A, B, k, idx_out, gate_out=None, logits_out=None, renorm=True,
@@ -172,69 +273,114 @@ def route_predict(x, W_r, b_r, A, B, k, idx_out, gate_out=None, logits_out=None,
     of int16/int32; A/B may be None (no predictor); B None with A given means identity.
     ``reuse_split`` calls pr2_route_predict_reuse: ``ws`` must hold the weight split of the
     previous call with the same weights (see include/pr2.h)."""
-    T, d = x.shape
-    N = W_r.shape[1]
-    r = 0 if A is None else A.shape[1]
-    desc = make_desc(T, d, N, k, 0, r, _act_code(x), _idx_code(idx_out), renorm)
-    if ws is None:
-        ws = route_workspace(x, W_r, A, k, _idx_code(idx_out))
+    torch = _torch()
     if reuse_split and ws is None:
         raise ValueError("reuse_split needs the workspace of the previous call")
+    T, d, _, dev = _need_act(x)
+    N = _router(W_r, b_r, d, dev)
+    r = _predictor(A, B, d, N, dev)
+    ldi = _need_ids(idx_out, "idx_out", T, k, dev)
+    _need(gate_out, "gate_out", (T, k), torch.float32, dev, optional=True)
+    _need(logits_out, "logits_out", (T, N), torch.float32, dev, optional=True)
+    _need_ws(ws, dev)
+    desc = make_desc(T, d, N, k, 0, r, _act_code(x), _idx_code(idx_out), renorm)
+    if ws is None:
+        ws = route_workspace(x, W_r, A, k, _idx_code(idx_out), stream)
     fn = lib().pr2_route_predict_reuse if reuse_split else lib().pr2_route_predict
     check(fn(byref(desc), _ptr(x), _ptr(W_r), _ptr(b_r), _ptr(A), _ptr(B), _ptr(idx_out),
-             _row_stride(idx_out), _ptr(gate_out), _ptr(logits_out), _ptr(ws), ws.numel(),
-             _stream(stream)))
+             ldi, _ptr(gate_out), _ptr(logits_out), _ptr(ws), ws.numel(), _stream(stream)))
 
 
-def replay_workspace(x, idx, W_r, W_gate, renorm=True):
-    torch = _torch()
+def replay_workspace(x, idx, W_r, W_gate, renorm=True, stream=None):
     T, d = x.shape
     desc = make_desc(T, d, W_r.shape[1], idx.shape[1], W_gate.shape[1], 0, _act_code(x),
                      _idx_code(idx), renorm)
-    return torch.empty(max(1, workspace_bytes(desc, OP_REPLAY_FWD)), dtype=torch.uint8,
-                       device=x.device)
+    return _new_ws(workspace_bytes(desc, OP_REPLAY_FWD), x.device, stream)
 
 
 def moe_replay_forward(x, idx, W_r, b_r, W_gate, W_up, W_down, y, gate_out=None, ws=None,
                        renorm=True, stream=None):
     """pr2_moe_replay_forward on torch tensors.  ``idx`` is a [T, k] view (any row stride)."""
-    T, d = x.shape
-    N = W_r.shape[1]
-    k = idx.shape[1]
-    m = W_gate.shape[1]
+    torch = _torch()
+    T, d, adt, dev = _need_act(x)
+    N = _router(W_r, b_r, d, dev)
+    k = idx.shape[1] if idx.dim() == 2 else -1
+    ldi = _need_ids(idx, "idx", T, k, dev)
+    m = _experts(W_gate, W_up, W_down, N, d, adt, dev)
+    _need(y, "y", (T, d), adt, dev)
+    _need(gate_out, "gate_out", (T, k), torch.float32, dev, optional=True)
+    _need_ws(ws, dev)
     desc = make_desc(T, d, N, k, m, 0, _act_code(x), _idx_code(idx), renorm)
     if ws is None:
-        ws = replay_workspace(x, idx, W_r, W_gate, renorm)
-    check(lib().pr2_moe_replay_forward(byref(desc), _ptr(x), _ptr(idx), _row_stride(idx),
+        ws = replay_workspace(x, idx, W_r, W_gate, renorm, stream)
+    check(lib().pr2_moe_replay_forward(byref(desc), _ptr(x), _ptr(idx), ldi,
                                        _ptr(W_r), _ptr(b_r), _ptr(W_gate), _ptr(W_up),
                                        _ptr(W_down), _ptr(y), _ptr(gate_out), _ptr(ws),
                                        ws.numel(), _stream(stream)))
 
 
-def rollout_workspace(x, W_r, A, W_gate, k, idx_dtype_code=PR2_I32, renorm=True):
+def moe_replay_forward_diag(x, idx, W_r, b_r, W_gate, W_up, W_down, y, gate_out=None,
+                            z_ref=None, cur_idx_out=None, overlap_out=None, kl_out=None,
+                            hist_out=None, ws=None, renorm=True, stream=None):
+    """pr2_moe_replay_forward_diag: the replay forward plus the route diagnostics
+    (current top-k, overlap, route KL against ``z_ref``, deviation histogram)."""
     torch = _torch()
+    T, d, adt, dev = _need_act(x)
+    N = _router(W_r, b_r, d, dev)
+    k = idx.shape[1] if idx.dim() == 2 else -1
+    ldi = _need_ids(idx, "idx", T, k, dev)
+    m = _experts(W_gate, W_up, W_down, N, d, adt, dev)
+    _need(y, "y", (T, d), adt, dev)
+    _need(gate_out, "gate_out", (T, k), torch.float32, dev, optional=True)
+    _need(z_ref, "z_ref", (T, N), torch.float32, dev, optional=True)
+    if cur_idx_out is not None:
+        _need(cur_idx_out, "cur_idx_out", (T, k), idx.dtype, dev)
+    _need(overlap_out, "overlap_out", (T,), torch.int32, dev, optional=True)
+    _need(kl_out, "kl_out", (T,), torch.float32, dev, optional=True)
+    if hist_out is not None:
+        _need(hist_out, "hist_out", (k + 1,), None, dev)
+        if hist_out.dtype not in (torch.int64, torch.uint64):
+            raise TypeError("hist_out must be int64 or uint64")
+    _need_ws(ws, dev)
+    desc = make_desc(T, d, N, k, m, 0, _act_code(x), _idx_code(idx), renorm)
+    if ws is None:
+        ws = replay_workspace(x, idx, W_r, W_gate, renorm, stream)
+    check(lib().pr2_moe_replay_forward_diag(byref(desc), _ptr(x), _ptr(idx), ldi, _ptr(W_r),
+                                            _ptr(b_r), _ptr(W_gate), _ptr(W_up), _ptr(W_down),
+                                            _ptr(y), _ptr(gate_out), _ptr(z_ref),
+                                            _ptr(cur_idx_out), _ptr(overlap_out), _ptr(kl_out),
+                                            _ptr(hist_out), _ptr(ws), ws.numel(),
+                                            _stream(stream)))
+
+
+def rollout_workspace(x, W_r, A, W_gate, k, idx_dtype_code=PR2_I32, renorm=True, stream=None):
     T, d = x.shape
     r = 0 if A is None else A.shape[1]
     desc = make_desc(T, d, W_r.shape[1], k, W_gate.shape[1], r, _act_code(x), idx_dtype_code,
                      renorm)
-    return torch.empty(max(1, workspace_bytes(desc, OP_ROLLOUT_FWD)), dtype=torch.uint8,
-                       device=x.device)
+    return _new_ws(workspace_bytes(desc, OP_ROLLOUT_FWD), x.device, stream)
 
 
 def moe_rollout_forward(x, W_r, b_r, A, B, W_gate, W_up, W_down, k, idx_out, y, gate_out=None,
                         logits_out=None, renorm=True, ws=None, stream=None):
     """pr2_moe_rollout_forward on torch tensors: records the predicted route into ``idx_out``
     (a [T, k] view, any row stride) and writes the layer output under the predictive weights."""
-    T, d = x.shape
-    N = W_r.shape[1]
-    r = 0 if A is None else A.shape[1]
-    m = W_gate.shape[1]
+    torch = _torch()
+    T, d, adt, dev = _need_act(x)
+    N = _router(W_r, b_r, d, dev)
+    r = _predictor(A, B, d, N, dev)
+    ldi = _need_ids(idx_out, "idx_out", T, k, dev)
+    m = _experts(W_gate, W_up, W_down, N, d, adt, dev)
+    _need(y, "y", (T, d), adt, dev)
+    _need(gate_out, "gate_out", (T, k), torch.float32, dev, optional=True)
+    _need(logits_out, "logits_out", (T, N), torch.float32, dev, optional=True)
+    _need_ws(ws, dev)
     desc = make_desc(T, d, N, k, m, r, _act_code(x), _idx_code(idx_out), renorm)
     if ws is None:
-        ws = rollout_workspace(x, W_r, A, W_gate, k, _idx_code(idx_out), renorm)
+        ws = rollout_workspace(x, W_r, A, W_gate, k, _idx_code(idx_out), renorm, stream)
     check(lib().pr2_moe_rollout_forward(byref(desc), _ptr(x), _ptr(W_r), _ptr(b_r), _ptr(A),
                                         _ptr(B), _ptr(W_gate), _ptr(W_up), _ptr(W_down),
-                                        _ptr(idx_out), _row_stride(idx_out), _ptr(gate_out),
+                                        _ptr(idx_out), ldi, _ptr(gate_out),
                                         _ptr(logits_out), _ptr(y), _ptr(ws), ws.numel(),
                                         _stream(stream)))
 
@@ -243,13 +389,24 @@ def route_diagnostics(x, idx, W_r, b_r, z_ref=None, cur_idx_out=None, overlap_ou
                       kl_out=None, hist_out=None, ws=None, stream=None):
     """pr2_route_diagnostics on torch tensors; ``hist_out`` is an int64/uint64 tensor of k+1."""
     torch = _torch()
-    T, d = x.shape
-    k = idx.shape[1]
-    desc = make_desc(T, d, W_r.shape[1], k, 0, 0, _act_code(x), _idx_code(idx))
+    T, d, _, dev = _need_act(x)
+    N = _router(W_r, b_r, d, dev)
+    k = idx.shape[1] if idx.dim() == 2 else -1
+    ldi = _need_ids(idx, "idx", T, k, dev)
+    _need(z_ref, "z_ref", (T, N), torch.float32, dev, optional=True)
+    if cur_idx_out is not None:
+        _need(cur_idx_out, "cur_idx_out", (T, k), idx.dtype, dev)
+    _need(overlap_out, "overlap_out", (T,), torch.int32, dev, optional=True)
+    _need(kl_out, "kl_out", (T,), torch.float32, dev, optional=True)
+    if hist_out is not None:
+        _need(hist_out, "hist_out", (k + 1,), None, dev)
+        if hist_out.dtype not in (torch.int64, torch.uint64):
+            raise TypeError("hist_out must be int64 or uint64")
+    _need_ws(ws, dev)
+    desc = make_desc(T, d, N, k, 0, 0, _act_code(x), _idx_code(idx))
     if ws is None:
-        ws = torch.empty(max(1, workspace_bytes(desc, OP_ROUTE_DIAG)), dtype=torch.uint8,
-                         device=x.device)
-    check(lib().pr2_route_diagnostics(byref(desc), _ptr(x), _ptr(idx), _row_stride(idx),
+        ws = _new_ws(workspace_bytes(desc, OP_ROUTE_DIAG), dev, stream)
+    check(lib().pr2_route_diagnostics(byref(desc), _ptr(x), _ptr(idx), ldi,
                                       _ptr(W_r), _ptr(b_r), _ptr(z_ref), _ptr(cur_idx_out),
                                       _ptr(overlap_out), _ptr(kl_out), _ptr(hist_out), _ptr(ws),
                                       ws.numel(), _stream(stream)))
@@ -270,14 +427,22 @@ def feature_cache_positions(T: int, Tc: int, seed: int):
 def route_predict_cached(x, W_r, b_r, A, B, k, idx_out, cache_row, h_cache, p_cache,
                          gate_out=None, renorm=True, ws=None, stream=None):
     """pr2_route_predict_cached on torch tensors: ``cache_row`` int32 [T] on the device."""
-    T, d = x.shape
-    N = W_r.shape[1]
-    r = 0 if A is None else A.shape[1]
+    torch = _torch()
+    T, d, adt, dev = _need_act(x)
+    N = _router(W_r, b_r, d, dev)
+    r = _predictor(A, B, d, N, dev)
+    ldi = _need_ids(idx_out, "idx_out", T, k, dev)
+    _need(gate_out, "gate_out", (T, k), torch.float32, dev, optional=True)
+    _need(cache_row, "cache_row", (T,), torch.int32, dev)
+    rows = h_cache.shape[0]
+    _need(h_cache, "h_cache", (rows, d), adt, dev)
+    _need(p_cache, "p_cache", (rows, N), torch.float32, dev)
+    _need_ws(ws, dev)
     desc = make_desc(T, d, N, k, 0, r, _act_code(x), _idx_code(idx_out), renorm)
     if ws is None:
-        ws = route_workspace(x, W_r, A, k, _idx_code(idx_out))
+        ws = route_workspace(x, W_r, A, k, _idx_code(idx_out), stream)
     check(lib().pr2_route_predict_cached(byref(desc), _ptr(x), _ptr(W_r), _ptr(b_r), _ptr(A),
-                                         _ptr(B), _ptr(idx_out), _row_stride(idx_out),
+                                         _ptr(B), _ptr(idx_out), ldi,
                                          _ptr(gate_out), _ptr(cache_row), _ptr(h_cache),
                                          _ptr(p_cache), h_cache.shape[0], _ptr(ws), ws.numel(),
                                          _stream(stream)))
@@ -287,40 +452,58 @@ def predictor_loss(h, W_r, b_r, h_old, p_old, A, B, loss_out, dA, dB=None, kl_ou
                    loss_kind=0, mini_step=2, ws=None, stream=None):
     """pr2_predictor_loss on torch tensors (h, h_old [Tc, d]; p_old [Tc, N])."""
     torch = _torch()
-    T, d = h_old.shape
-    N = p_old.shape[1]
-    r = A.shape[1]
+    T, d, adt, dev = _need_act(h_old, "h_old")
+    N = p_old.shape[1] if p_old.dim() == 2 else -1
+    _need(p_old, "p_old", (T, N), torch.float32, dev)
+    _need(h, "h", (T, d), adt, dev)
+    _router(W_r, b_r, d, dev)
+    if W_r.shape[1] != N:
+        raise ValueError("W_r and p_old disagree on N")
+    r = _predictor(A, B, d, N, dev)
+    _need(loss_out, "loss_out", (1,), torch.float32, dev)
+    _need(dA, "dA", (d, r), torch.float32, dev)
+    if B is not None:
+        _need(dB, "dB", (r, N), torch.float32, dev)
+    _need(kl_out, "kl_out", (T,), torch.float32, dev, optional=True)
+    _need_ws(ws, dev)
     desc = make_desc(T, d, N, 1, 0, r, _act_code(h_old))
     if ws is None:
-        ws = torch.empty(max(1, workspace_bytes(desc, OP_PREDICTOR_LOSS)), dtype=torch.uint8,
-                         device=h_old.device)
+        ws = _new_ws(workspace_bytes(desc, OP_PREDICTOR_LOSS), dev, stream)
     check(lib().pr2_predictor_loss(byref(desc), _ptr(h), _ptr(W_r), _ptr(b_r), _ptr(h_old),
                                    _ptr(p_old), _ptr(A), _ptr(B), loss_kind, mini_step,
                                    _ptr(kl_out), _ptr(loss_out), _ptr(dA), _ptr(dB), _ptr(ws),
                                    ws.numel(), _stream(stream)))
 
 
-def backward_workspace(x, idx, W_r, W_gate, renorm=True):
-    torch = _torch()
+def backward_workspace(x, idx, W_r, W_gate, renorm=True, stream=None):
     T, d = x.shape
     desc = make_desc(T, d, W_r.shape[1], idx.shape[1], W_gate.shape[1], 0, _act_code(x),
                      _idx_code(idx), renorm)
-    return torch.empty(max(1, workspace_bytes(desc, OP_REPLAY_BWD)), dtype=torch.uint8,
-                       device=x.device)
+    return _new_ws(workspace_bytes(desc, OP_REPLAY_BWD), x.device, stream)
 
 
 def moe_replay_backward(x, idx, W_r, b_r, W_gate, W_up, W_down, dy, dx, dW_r, db_r, dW_gate,
                         dW_up, dW_down, ws=None, renorm=True, stream=None):
     """pr2_moe_replay_backward on torch tensors; every gradient tensor is overwritten.
     ``db_r`` may be None."""
-    T, d = x.shape
-    N = W_r.shape[1]
-    k = idx.shape[1]
-    m = W_gate.shape[1]
+    torch = _torch()
+    T, d, adt, dev = _need_act(x)
+    N = _router(W_r, b_r, d, dev)
+    k = idx.shape[1] if idx.dim() == 2 else -1
+    ldi = _need_ids(idx, "idx", T, k, dev)
+    m = _experts(W_gate, W_up, W_down, N, d, adt, dev)
+    _need(dy, "dy", (T, d), adt, dev)
+    _need(dx, "dx", (T, d), adt, dev)
+    _need(dW_r, "dW_r", (d, N), torch.float32, dev)
+    _need(db_r, "db_r", (N,), torch.float32, dev, optional=True)
+    _need(dW_gate, "dW_gate", (N, m, d), torch.float32, dev)
+    _need(dW_up, "dW_up", (N, m, d), torch.float32, dev)
+    _need(dW_down, "dW_down", (N, d, m), torch.float32, dev)
+    _need_ws(ws, dev)
     desc = make_desc(T, d, N, k, m, 0, _act_code(x), _idx_code(idx), renorm)
     if ws is None:
-        ws = backward_workspace(x, idx, W_r, W_gate, renorm)
-    check(lib().pr2_moe_replay_backward(byref(desc), _ptr(x), _ptr(idx), _row_stride(idx),
+        ws = backward_workspace(x, idx, W_r, W_gate, renorm, stream)
+    check(lib().pr2_moe_replay_backward(byref(desc), _ptr(x), _ptr(idx), ldi,
                                         _ptr(W_r), _ptr(b_r), _ptr(W_gate), _ptr(W_up),
                                         _ptr(W_down), _ptr(dy), _ptr(dx), _ptr(dW_r), _ptr(db_r),
                                         _ptr(dW_gate), _ptr(dW_up), _ptr(dW_down), _ptr(ws),

@@ -17,7 +17,7 @@ namespace pr2 {
 // ------------------------------------------------------------- errors ----
 static thread_local std::string t_err;
 
-static pr2_status fail(pr2_status s, const char* fmt, ...) {
+pr2_status fail(pr2_status s, const char* fmt, ...) {
     char buf[512];
     va_list ap;
     va_start(ap, fmt);
@@ -27,7 +27,7 @@ static pr2_status fail(pr2_status s, const char* fmt, ...) {
     return s;
 }
 
-static pr2_status ok() {
+pr2_status ok() {
     t_err.clear();
     return PR2_OK;
 }
@@ -41,8 +41,22 @@ static bool validate_env() {
     return v && v[0] == '1';
 }
 
+// PR2_VALIDATE=1 waits for the stream, which a HIP graph capture forbids
+static pr2_status validation_allowed(bool validate, hipStream_t st) {
+    if (!validate) return PR2_OK;
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st, &cs) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(PR2_ERR_HIP, "hipStreamIsCapturing failed");
+    }
+    if (cs != hipStreamCaptureStatusNone)
+        return fail(PR2_ERR_UNSUPPORTED, "PR2_VALIDATE=1 synchronises the stream, which is not "
+                    "allowed while it is captured into a HIP graph");
+    return PR2_OK;
+}
+
 // ------------------------------------------------------- device check ----
-static pr2_status device_ready() {
+pr2_status device_ready() {
     static std::mutex mu;
     static std::map<int, int> ok_dev;  // device -> 1 gfx950, 0 not
     int dev = -1;
@@ -109,7 +123,37 @@ static SideStream* side_stream_for(hipStream_t st) {      // caller holds g_side
     return &per_dev.emplace(dev, ss).first->second;
 }
 
-static pr2_status hip_fail(hipError_t e, const char* what) {
+// ------------------------------------------------ weight-split records ----
+// pr2_route_predict_reuse reads the bf16 split of the router (and predictor)
+// weights that an earlier route call left in the same workspace.  Each route
+// call that forms a split records what it was formed from (device, weight
+// pointers, layout, shape) under the workspace's address; every other call
+// that writes into a workspace drops the records inside it.  The reuse call
+// refuses a workspace without a matching record.  (Changed weight values under
+// the same pointers stay undetectable: the caller guarantees them.)
+struct SplitRecord {
+    uintptr_t end;          // ws + ws_bytes of the recording call
+    int dev;
+    const float* W_r;
+    const float* A;
+    const float* B;
+    int d, N, r;
+    bool folded;            // predictor folded into N columns (no logits wanted)
+};
+static std::mutex g_split_mu;
+static std::map<uintptr_t, SplitRecord> g_splits;   // keyed by workspace address
+
+static void drop_split_records(const void* ws, size_t bytes) {
+    if (!ws) return;
+    const uintptr_t lo = (uintptr_t)ws, hi = lo + (bytes ? bytes : 1);
+    std::lock_guard<std::mutex> lk(g_split_mu);
+    for (auto it = g_splits.begin(); it != g_splits.end();) {
+        if (it->first < hi && lo < it->second.end) it = g_splits.erase(it);
+        else ++it;
+    }
+}
+
+pr2_status hip_fail(hipError_t e, const char* what) {
     return fail(PR2_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
@@ -274,6 +318,38 @@ LaunchScope::~LaunchScope() {
     g_prof.pending.push_back({name, slot});
 }
 
+// Argument checks of the route calls; *empty is set for T == 0 (a no-op).
+pr2_status check_route_args(const pr2_moe_desc* desc, const void* x, const float* W_r,
+                                   const float* b_r, const float* A, const float* B,
+                                   void* idx_out, int64_t ldi, float* gate_out,
+                                   float* logits_out, bool* empty) {
+    *empty = false;
+    pr2_status s = check_desc(desc, false, true);
+    if (s != PR2_OK) return s;
+    const pr2_moe_desc& d = *desc;
+    if (d.r > 256) return fail(PR2_ERR_UNSUPPORTED, "predictor rank r = %d > 256", d.r);
+    if (ldi < d.k) return fail(PR2_ERR_SHAPE, "ldi = %lld < k = %d", (long long)ldi, d.k);
+    if (d.T == 0) {
+        *empty = true;
+        return PR2_OK;
+    }
+    if (!x) return fail(PR2_ERR_NULL, "x is NULL");
+    if (!W_r) return fail(PR2_ERR_NULL, "W_r is NULL");
+    if (!idx_out) return fail(PR2_ERR_NULL, "idx_out is NULL");
+    if (d.r > 0 && !A) return fail(PR2_ERR_NULL, "A is NULL with r = %d > 0", d.r);
+    if (d.r > 0 && !B && d.r != d.N)
+        return fail(PR2_ERR_NULL, "B is NULL but r = %d != N = %d (identity needs r == N)", d.r, d.N);
+    if (!aligned(x, 16)) return fail(PR2_ERR_ALIGN, "x is not 16-byte aligned");
+    if (!aligned(W_r, 4) || (b_r && !aligned(b_r, 4)) || (A && !aligned(A, 4)) ||
+        (B && !aligned(B, 4)))
+        return fail(PR2_ERR_ALIGN, "an fp32 router/predictor tensor is not 4-byte aligned");
+    if (!aligned(idx_out, d.idx_dtype == PR2_I16 ? 2 : 4))
+        return fail(PR2_ERR_ALIGN, "idx_out is not aligned to its element size");
+    if ((gate_out && !aligned(gate_out, 4)) || (logits_out && !aligned(logits_out, 4)))
+        return fail(PR2_ERR_ALIGN, "gate_out / logits_out is not 4-byte aligned");
+    return PR2_OK;
+}
+
 }  // namespace pr2
 
 using namespace pr2;
@@ -355,36 +431,55 @@ static pr2_status route_predict_impl(const pr2_moe_desc* desc, const void* x, co
                                      void* idx_out, int64_t ldi, float* gate_out,
                                      float* logits_out, void* ws, size_t ws_bytes,
                                      pr2_stream_t stream, bool reuse_split) {
-    pr2_status s = check_desc(desc, false, true);
+    bool empty = false;
+    pr2_status s = check_route_args(desc, x, W_r, b_r, A, B, idx_out, ldi, gate_out, logits_out,
+                                    &empty);
     if (s != PR2_OK) return s;
+    if (empty) return ok();
     const pr2_moe_desc& d = *desc;
-    if (d.r > 256) return fail(PR2_ERR_UNSUPPORTED, "predictor rank r = %d > 256", d.r);
-    if (ldi < d.k) return fail(PR2_ERR_SHAPE, "ldi = %lld < k = %d", (long long)ldi, d.k);
-    if (d.T == 0) return ok();
-    if (!x) return fail(PR2_ERR_NULL, "x is NULL");
-    if (!W_r) return fail(PR2_ERR_NULL, "W_r is NULL");
-    if (!idx_out) return fail(PR2_ERR_NULL, "idx_out is NULL");
-    if (d.r > 0 && !A) return fail(PR2_ERR_NULL, "A is NULL with r = %d > 0", d.r);
-    if (d.r > 0 && !B && d.r != d.N)
-        return fail(PR2_ERR_NULL, "B is NULL but r = %d != N = %d (identity needs r == N)", d.r, d.N);
-    if (!aligned(x, 16)) return fail(PR2_ERR_ALIGN, "x is not 16-byte aligned");
-    if (!aligned(W_r, 4) || (b_r && !aligned(b_r, 4)) || (A && !aligned(A, 4)) ||
-        (B && !aligned(B, 4)))
-        return fail(PR2_ERR_ALIGN, "an fp32 router/predictor tensor is not 4-byte aligned");
-    if (!aligned(idx_out, d.idx_dtype == PR2_I16 ? 2 : 4))
-        return fail(PR2_ERR_ALIGN, "idx_out is not aligned to its element size");
-    if ((gate_out && !aligned(gate_out, 4)) || (logits_out && !aligned(logits_out, 4)))
-        return fail(PR2_ERR_ALIGN, "gate_out / logits_out is not 4-byte aligned");
     const size_t need = route_ws_bytes(d);
     if (need && !ws) return fail(PR2_ERR_NULL, "ws is NULL (need %zu bytes)", need);
     if (ws_bytes < need)
         return fail(PR2_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
+    // the split this call reads or forms: none on the fp64 vector path
+    const bool folded = logits_out == nullptr && router_mfma_ok(d, d.N);
+    const bool has_split = folded || router_mfma_ok(d, d.N + d.r);
+    const float* A_key = d.r > 0 ? A : nullptr;
+    const float* B_key = d.r > 0 ? B : nullptr;
+    SplitRecord want{(uintptr_t)ws + ws_bytes, -1, W_r, A_key, B_key, d.d, d.N, d.r, folded};
+    if (reuse_split && has_split) {
+        std::lock_guard<std::mutex> lk(g_split_mu);
+        auto it = g_splits.find((uintptr_t)ws);
+        if (it == g_splits.end())
+            return fail(PR2_ERR_WORKSPACE, "ws holds no router split: call pr2_route_predict "
+                        "with this workspace first");
+        const SplitRecord& h = it->second;
+        if (h.W_r != W_r || h.A != A_key || h.B != B_key || h.d != d.d || h.N != d.N ||
+            h.r != d.r || h.folded != folded)
+            return fail(PR2_ERR_WORKSPACE, "ws holds the split of other weights, shape or layout "
+                        "(W_r, A, B, d, N, r and the NULL-ness of logits_out must match the "
+                        "call that formed it)");
+        want.dev = h.dev;
+    }
     s = device_ready();
     if (s != PR2_OK) return s;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(PR2_ERR_DEVICE, "no usable HIP device");
+    }
+    if (reuse_split && has_split && want.dev != dev)
+        return fail(PR2_ERR_WORKSPACE, "ws holds a split formed on device %d, not %d", want.dev, dev);
+    if (!reuse_split) drop_split_records(ws, ws_bytes);
     void* split = need ? (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255) : nullptr;
     hipError_t e = launch_route_predict(d, x, W_r, b_r, A, B, idx_out, ldi, gate_out, logits_out,
                                         split, (hipStream_t)stream, FeatureCache{}, reuse_split);
     if (e != hipSuccess) return hip_fail(e, "route_predict launch");
+    if (!reuse_split && has_split) {
+        want.dev = dev;
+        std::lock_guard<std::mutex> lk(g_split_mu);
+        g_splits[(uintptr_t)ws] = want;
+    }
     return ok();
 }
 
@@ -404,15 +499,36 @@ pr2_status pr2_route_predict_reuse(const pr2_moe_desc* desc, const void* x, cons
                               ws_bytes, stream, true);
 }
 
-pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const void* idx,
-                                  int64_t ldi, const float* W_r, const float* b_r,
-                                  const void* W_gate, const void* W_up, const void* W_down,
-                                  void* y, float* gate_out, void* ws, size_t ws_bytes,
-                                  pr2_stream_t stream) {
+static pr2_status check_diag_outputs(const pr2_moe_desc& d, const float* z_ref,
+                                     const void* cur_idx_out, const int32_t* overlap_out,
+                                     const float* kl_out, const uint64_t* hist_out) {
+    if (kl_out && !z_ref) return fail(PR2_ERR_NULL, "kl_out needs z_ref");
+    if (hist_out && !aligned(hist_out, 8)) return fail(PR2_ERR_ALIGN, "hist_out is not 8-byte aligned");
+    if ((z_ref && !aligned(z_ref, 4)) || (kl_out && !aligned(kl_out, 4)) ||
+        (overlap_out && !aligned(overlap_out, 4)))
+        return fail(PR2_ERR_ALIGN, "z_ref, kl_out and overlap_out must be 4-byte aligned");
+    if (cur_idx_out && !aligned(cur_idx_out, d.idx_dtype == PR2_I16 ? 2 : 4))
+        return fail(PR2_ERR_ALIGN, "cur_idx_out is not aligned to its element size");
+    return PR2_OK;
+}
+
+static pr2_status replay_forward_impl(const pr2_moe_desc* desc, const void* x, const void* idx,
+                                      int64_t ldi, const float* W_r, const float* b_r,
+                                      const void* W_gate, const void* W_up, const void* W_down,
+                                      void* y, float* gate_out, const RouteDiag* diag, void* ws,
+                                      size_t ws_bytes, pr2_stream_t stream) {
     pr2_status s = check_desc(desc, true, true);
     if (s != PR2_OK) return s;
     const pr2_moe_desc& d = *desc;
     if (ldi < d.k) return fail(PR2_ERR_SHAPE, "ldi = %lld < k = %d", (long long)ldi, d.k);
+    if (diag && diag->hist && d.T == 0) {
+        // the histogram of an empty batch is all zeros
+        s = device_ready();
+        if (s != PR2_OK) return s;
+        hipError_t e = launch_zero_i32((int*)diag->hist, 2 * (d.k + 1), (hipStream_t)stream);
+        if (e != hipSuccess) return hip_fail(e, "histogram reset");
+        return ok();
+    }
     if (d.T == 0) return ok();
     if (!x) return fail(PR2_ERR_NULL, "x is NULL");
     if (!idx) return fail(PR2_ERR_NULL, "idx is NULL");
@@ -436,10 +552,13 @@ pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const
     hipStream_t st = (hipStream_t)stream;
     ReplayWs w = replay_ws_layout(d, ws);
     const bool validate = validate_env();
+    s = validation_allowed(validate, st);
+    if (s != PR2_OK) return s;
+    drop_split_records(ws, ws_bytes);
     hipError_t e;
     if (validate) {
-        e = hipMemsetAsync(w.err, 0, sizeof(int) * ERR_WORDS, st);
-        if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
+        e = launch_zero_i32(w.err, ERR_WORDS, st);
+        if (e != hipSuccess) return hip_fail(e, "error-word reset");
     }
     float* gate = gate_out ? gate_out : w.gate;
     {
@@ -455,7 +574,7 @@ pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const
             if (e != hipSuccess) return hip_fail(e, "side stream fork");
             gst = side->s;
         }
-        e = launch_replay_gates(d, x, idx, ldi, W_r, b_r, gate, w.err, w.wsplit, gst);
+        e = launch_replay_gates(d, x, idx, ldi, W_r, b_r, gate, w.err, w.wsplit, gst, diag);
         hipEvent_t gates_done = nullptr;
         if (side) {
             // joined even when the launch failed, so no forked work is left behind
@@ -488,6 +607,33 @@ pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const
                         errs[ERR_BAD_ID], errs[ERR_DUP_ID]);
     }
     return ok();
+}
+
+pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const void* idx,
+                                  int64_t ldi, const float* W_r, const float* b_r,
+                                  const void* W_gate, const void* W_up, const void* W_down,
+                                  void* y, float* gate_out, void* ws, size_t ws_bytes,
+                                  pr2_stream_t stream) {
+    return replay_forward_impl(desc, x, idx, ldi, W_r, b_r, W_gate, W_up, W_down, y, gate_out,
+                               nullptr, ws, ws_bytes, stream);
+}
+
+pr2_status pr2_moe_replay_forward_diag(const pr2_moe_desc* desc, const void* x, const void* idx,
+                                       int64_t ldi, const float* W_r, const float* b_r,
+                                       const void* W_gate, const void* W_up, const void* W_down,
+                                       void* y, float* gate_out, const float* z_ref,
+                                       void* cur_idx_out, int32_t* overlap_out, float* kl_out,
+                                       uint64_t* hist_out, void* ws, size_t ws_bytes,
+                                       pr2_stream_t stream) {
+    pr2_status s = check_desc(desc, true, true);
+    if (s != PR2_OK) return s;
+    s = check_diag_outputs(*desc, z_ref, cur_idx_out, overlap_out, kl_out, hist_out);
+    if (s != PR2_OK) return s;
+    const RouteDiag diag{kl_out ? z_ref : nullptr, cur_idx_out, overlap_out, kl_out,
+                         (unsigned long long*)hist_out};
+    const bool any = cur_idx_out || overlap_out || kl_out || hist_out;
+    return replay_forward_impl(desc, x, idx, ldi, W_r, b_r, W_gate, W_up, W_down, y, gate_out,
+                               any ? &diag : nullptr, ws, ws_bytes, stream);
 }
 
 pr2_status pr2_moe_rollout_forward(const pr2_moe_desc* desc, const void* x, const float* W_r,
@@ -527,6 +673,7 @@ pr2_status pr2_moe_rollout_forward(const pr2_moe_desc* desc, const void* x, cons
 
     hipStream_t st = (hipStream_t)stream;
     ReplayWs w = rollout_ws_layout(d, ws);
+    drop_split_records(ws, ws_bytes);
     float* gate = gate_out ? gate_out : w.gate;
     hipError_t e = launch_route_predict(d, x, W_r, b_r, A, B, idx_out, ldi, gate, logits_out,
                                         w.wsplit, st);
@@ -589,10 +736,13 @@ pr2_status pr2_moe_replay_backward(const pr2_moe_desc* desc, const void* x, cons
 
     BwdWs w = bwd_ws_layout(d, ws);
     const bool validate = validate_env();
+    s = validation_allowed(validate, st);
+    if (s != PR2_OK) return s;
+    drop_split_records(ws, ws_bytes);
     hipError_t e;
     if (validate) {
-        e = hipMemsetAsync(w.fw.err, 0, sizeof(int) * ERR_WORDS, st);
-        if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
+        e = launch_zero_i32(w.fw.err, ERR_WORDS, st);
+        if (e != hipSuccess) return hip_fail(e, "error-word reset");
     }
     {
         // On the side stream: the replay weights beside the permutation and the
@@ -668,6 +818,7 @@ pr2_status pr2_route_diagnostics(const pr2_moe_desc* desc, const void* x, const 
     }
     s = device_ready();
     if (s != PR2_OK) return s;
+    drop_split_records(ws, ws_bytes);
     void* split = ws ? (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255) : nullptr;
     hipError_t e = launch_route_diagnostics(d, x, idx, ldi, W_r, b_r, z_ref, cur_idx_out,
                                             overlap_out, kl_out, (unsigned long long*)hist_out,
@@ -740,6 +891,7 @@ pr2_status pr2_route_predict_cached(const pr2_moe_desc* desc, const void* x, con
         return fail(PR2_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
     s = device_ready();
     if (s != PR2_OK) return s;
+    drop_split_records(ws, ws_bytes);
     void* split = need ? (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255) : nullptr;
     const FeatureCache cache{cache_row, h_cache, p_cache, cache_rows};
     hipError_t e = launch_route_predict(d, x, W_r, b_r, A, B, idx_out, ldi, gate_out, nullptr,
@@ -790,6 +942,7 @@ pr2_status pr2_predictor_loss(const pr2_moe_desc* desc, const void* h, const flo
         return fail(PR2_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
     s = device_ready();
     if (s != PR2_OK) return s;
+    drop_split_records(ws, ws_bytes);
     PredLossWs w = pred_ws_layout(d, ws);
     hipError_t e = launch_predictor_loss(d, h, W_r, b_r, h_old, p_old, A, B, loss_kind, kl_out,
                                          loss_out, dA, dBo, w, st);

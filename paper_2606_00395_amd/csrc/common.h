@@ -92,6 +92,18 @@ struct BwdWs {
 
 BwdWs bwd_ws_layout(const pr2_moe_desc& d, void* base);
 
+// ------------------------------------------------- host helpers (api.hip) ----
+// fail() records a sentence for pr2_last_error and returns s; ok() clears it.
+pr2_status fail(pr2_status s, const char* fmt, ...);
+pr2_status ok();
+pr2_status hip_fail(hipError_t e, const char* what);
+// the current device is usable and is a gfx950
+pr2_status device_ready();
+// argument checks shared by the route calls; *empty is set for T == 0 (a no-op)
+pr2_status check_route_args(const pr2_moe_desc* desc, const void* x, const float* W_r,
+                            const float* b_r, const float* A, const float* B, void* idx_out,
+                            int64_t ldi, float* gate_out, float* logits_out, bool* empty);
+
 // ------------------------------------------------------------ launches ----
 // Every launch goes through this so that measurement events can bracket it.
 struct LaunchScope {
@@ -118,18 +130,32 @@ struct FeatureCache {
 // router scratch: the split weights and, for small token counts, the split-K
 // pair sums and logits
 size_t router_split_bytes(int NC, const pr2_moe_desc& d);
+// the split weights alone (what the fused, non-split-K router reads)
+size_t router_split_weight_bytes(int NC, const pr2_moe_desc& d);
 bool router_mfma_ok(const pr2_moe_desc& d, int NC);
+// splitk_ok = false keeps every batch size on the fused kernel (same logits
+// bit for bit), so split_ws needs only router_split_weight_bytes
 hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const float* W_r,
                                 const float* b_r, const float* A, const float* B, void* idx_out,
                                 int64_t ldi, float* gate_out, float* logits_out, void* split_ws,
                                 hipStream_t s, const FeatureCache& cache = FeatureCache{},
-                                bool reuse_split = false);
+                                bool reuse_split = false, bool splitk_ok = true);
 // current router logits p = x W_r + b_r of every token into p_out [T, N]
 hipError_t launch_router_logits(const pr2_moe_desc& d, const void* x, const float* W_r,
                                 const float* b_r, float* p_out, void* split_ws, hipStream_t s);
+// Route-tracking diagnostics a replay-weight pass can form from the same logits
+// (current top-k, overlap with the recorded ids, route KL against z_ref, the
+// deviation histogram); any field may be null.
+struct RouteDiag {
+    const float* z_ref;         // [T, N] reference logits (needed by kl)
+    void* cur_idx;              // [T, k] idx_dtype
+    int* overlap;               // [T]
+    float* kl;                  // [T]
+    unsigned long long* hist;   // [k + 1], zeroed by the launch
+};
 hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void* idx, int64_t ldi,
                                const float* W_r, const float* b_r, float* gate_out, int* err,
-                               void* split_ws, hipStream_t s);
+                               void* split_ws, hipStream_t s, const RouteDiag* diag = nullptr);
 
 hipError_t launch_route_diagnostics(const pr2_moe_desc& d, const void* x, const void* idx,
                                     int64_t ldi, const float* W_r, const float* b_r,
@@ -140,6 +166,8 @@ hipError_t launch_route_diagnostics(const pr2_moe_desc& d, const void* x, const 
 hipError_t launch_permute(const pr2_moe_desc& d, const void* idx, int64_t ldi, const ReplayWs& ws,
                           hipStream_t s);
 hipError_t launch_combine(const pr2_moe_desc& d, const ReplayWs& ws, void* y, hipStream_t s);
+// p[0..n) = 0 (one workgroup; for the few error words)
+hipError_t launch_zero_i32(int* p, int n, hipStream_t s);
 
 // gemm.hip
 hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void* W_gate,

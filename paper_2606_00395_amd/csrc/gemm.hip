@@ -73,6 +73,9 @@ static_assert(sizeof(accv) == ACCN * sizeof(float), "accumulator size");
 __device__ __forceinline__ accv mfma_bf16(bf16x8 a, bf16x8 b, accv c) {
     return MfmaOp<MT>::run(a, b, c);
 }
+// tiles per group of the work order (1: tile-major, every panel of a tile in turn)
+constexpr int kGroupGemm1 = 1;
+constexpr int kGroupGemm2 = 1;
 constexpr int NWAVE = (BM / WM) * (BP / WN);
 constexpr int kGemmThreads = 64 * NWAVE;
 constexpr int kNumXcd = 8;
@@ -96,6 +99,7 @@ struct MfmaArgs {
     const int* tile_count;
     const float* gate;      // GEMM2
     bf16_t* out;
+    int group;              // work order: groups of this many tiles, panel-major inside
 };
 
 // silu(a) = a / (1 + e^-a) with the hardware reciprocal (about 1 ulp; H is rounded to bf16)
@@ -123,15 +127,23 @@ grouped_gemm_mfma(MfmaArgs g) {
     __shared__ __attribute__((aligned(1024))) unsigned char lds[LDSB];
 
     // XCD-aware mapping: physical block b runs on XCD b % 8; give each XCD a
-    // contiguous range of the (tile, panel) work list.
-    const int64_t L = (int64_t)(*g.tile_count) * g.ntn;
+    // contiguous range of the (tile, panel) work list.  The list runs over
+    // groups of g.group consecutive tiles (the last group may be smaller); inside
+    // a group it is panel-major, so the workgroups that start together share
+    // one weight panel and the group's gathered rows stay in that XCD's L2.
+    const int ntile = *g.tile_count;
+    const int64_t L = (int64_t)ntile * g.ntn;
     const int64_t per_xcd = (L + kNumXcd - 1) / kNumXcd;
     const int64_t local = blockIdx.x / kNumXcd;
     if (local >= per_xcd) return;
     const int64_t logical = (int64_t)(blockIdx.x % kNumXcd) * per_xcd + local;
     if (logical >= L) return;
-    const int tile = (int)(logical / g.ntn);
-    const int pn = (int)(logical % g.ntn);
+    const int64_t wgrp = logical / ((int64_t)g.group * g.ntn);
+    const int first = (int)(wgrp * g.group);
+    const int gsz = min(g.group, ntile - first);
+    const int within = (int)(logical - wgrp * g.group * g.ntn);
+    const int tile = first + within % gsz;
+    const int pn = within / gsz;
     const int expert = g.tiles[3 * tile + 0];
     const int row0 = g.tiles[3 * tile + 1];
     const int rows = g.tiles[3 * tile + 2];
@@ -199,10 +211,15 @@ grouped_gemm_mfma(MfmaArgs g) {
             soff[i] = (uint32_t)(off + ((lane % CHUNKS) ^ swz(r)) * 8);
         }
     }
+    // A groups of 8 token rows wholly past the end of a partial tile are not
+    // copied: no stored output depends on those LDS rows (a wavefront-uniform,
+    // scalar test; the K loop's waits are for all copies in flight, so the count
+    // issued does not matter)
     auto issue = [&](int stage, int k0) {
 #pragma unroll
         for (int i = 0; i < kGroups; ++i) {
             const int grp = wave * kGroups + i;
+            if (wrow0 < BM && wrow0 + i * kRowsPerDma >= rows) continue;
             __builtin_amdgcn_global_load_lds((const void*)(sbase + (soff[i] + (uint32_t)k0)),
                                              (lds_void*)&lds[stage * STAGEB + grp * 1024], 16,
                                              0, 0);
@@ -493,6 +510,7 @@ hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void*
         g1.tile_count = ws.tile_count;
         g1.gate = gate;
         g1.out = (bf16_t*)ws.H;
+        g1.group = kGroupGemm1;
         int64_t work = ws.max_tiles * g1.ntn;
         int64_t grid = ((work + kNumXcd - 1) / kNumXcd) * kNumXcd;
         {
@@ -510,6 +528,7 @@ hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void*
         g2.n_out = d.d;
         g2.ntn = d.d / BP;
         g2.out = (bf16_t*)ws.O;
+        g2.group = kGroupGemm2;
         work = ws.max_tiles * g2.ntn;
         grid = ((work + kNumXcd - 1) / kNumXcd) * kNumXcd;
         if ((e = wait_gates()) != hipSuccess) return e;
@@ -572,6 +591,7 @@ hipError_t launch_preact(const pr2_moe_desc& d, const void* x, const void* W_gat
         g.tiles = ws.tiles;
         g.tile_count = ws.tile_count;
         g.out = (bf16_t*)AU;
+        g.group = kGroupGemm1;
         const int64_t work = ws.max_tiles * g.ntn;
         const int64_t grid = ((work + kNumXcd - 1) / kNumXcd) * kNumXcd;
         LaunchScope scope("bwd_preact_gate_up", s);

@@ -7,12 +7,13 @@
 //   scan    one block turns the expert-major counts into the exclusive prefix
 //           over (expert, block), which is each block's first output position
 //           per expert; it also writes the expert offsets and the tile list
-//           (expert, first row, rows) of 128-row grouped-GEMM tiles;
+//           (expert, first row, rows) of kTileM-row (256) grouped-GEMM tiles;
 //   scatter one wavefront per chunk walks its entries 64 at a time; lanes with
 //           the same expert find each other with ballots over the id bits, so
 //           each entry's position is its block base + the entries of the same
 //           expert before it.  perm_src[pos] = t*k + s, inv[t*k + s] = pos.
-// Out-of-range ids are not dispatched (inv = -1) and are counted.
+// Out-of-range ids are not dispatched (inv = -1); the count pass is the one
+// place that counts them (in the workspace's error words).
 //
 // Combine: y_t = sum over slots s (in slot order) of the weighted expert output
 // row O[inv[t*k + s]], accumulated in fp32 (Eq. pr2_output).
@@ -386,6 +387,19 @@ hipError_t launch_permute(const pr2_moe_desc& d, const void* idx, int64_t ldi, c
                            d.idx_dtype, ldi, d.T, d.k, d.N, tb, ws.nblk, ws.bcount, ws.perm_src,
                            ws.inv);
     }
+    return hipGetLastError();
+}
+
+namespace {
+__global__ void __launch_bounds__(64) zero_i32_kernel(int* p, int n) {
+    for (int i = threadIdx.x; i < n; i += 64) p[i] = 0;
+}
+}  // namespace
+
+// A fill kernel rather than hipMemsetAsync, so that a captured HIP graph holds
+// no memset node.
+hipError_t launch_zero_i32(int* p, int n, hipStream_t s) {
+    hipLaunchKernelGGL(zero_i32_kernel, dim3(1), dim3(64), 0, s, p, n);
     return hipGetLastError();
 }
 

@@ -426,14 +426,14 @@ __device__ void replay_token(const float* row, int64_t t, int N, const ReplayOut
         for (int j = lane; j < N; j += 64) part += expf(logit(j) - ref);
     }
     const float denom = wave_sum_f32(part);
-    int bad = 0;
     for (int s = lane; s < o.k; s += 64) {
         int id = id_at(s);
         float g = 0.0f;
         if (id >= 0 && id < N) g = expf(logit(id) - ref) / denom;
-        else bad++;
         o.gate_out[t * o.k + s] = g;
     }
+    // out-of-range ids are counted by the permutation's count pass alone;
+    // repeated ids of a row are counted here
     if (o.validate) {
         int dup = 0;
         for (int s = lane; s < o.k; s += 64) {
@@ -442,11 +442,7 @@ __device__ void replay_token(const float* row, int64_t t, int N, const ReplayOut
                 if (id_at(s2) == id) dup++;
         }
         dup = wave_sum_i32(dup);
-        int nbad = wave_sum_i32(bad);
-        if (lane == 0) {
-            if (nbad) atomicAdd(o.err + ERR_BAD_ID, nbad);
-            if (dup) atomicAdd(o.err + ERR_DUP_ID, dup);
-        }
+        if (lane == 0 && dup) atomicAdd(o.err + ERR_DUP_ID, dup);
     }
 }
 
@@ -780,14 +776,14 @@ __device__ void replay_group(const float* row, int64_t t, bool valid, int N, con
             if (v * 16 + l16 < N) part += expf(logit(v * 16 + l16) - ref);
     }
     const float denom = gsum_f32(part);
-    int bad = 0;
     for (int s = l16; s < o.k; s += 16) {
         const int id = id_at(s);
         float g = 0.0f;
         if (id >= 0 && id < N) g = expf(logit(id) - ref) / denom;
-        else bad++;
         if (valid) o.gate_out[t * o.k + s] = g;
     }
+    // out-of-range ids are counted by the permutation's count pass alone;
+    // repeated ids of a row are counted here
     if (o.validate) {
         int dup = 0;
         for (int s = l16; s < o.k; s += 16) {
@@ -796,11 +792,7 @@ __device__ void replay_group(const float* row, int64_t t, bool valid, int N, con
                 if (id_at(s2) == id) dup++;
         }
         dup = gsum_i32(dup);
-        const int nbad = gsum_i32(bad);
-        if (l16 == 0 && valid) {
-            if (nbad) atomicAdd(o.err + ERR_BAD_ID, nbad);
-            if (dup) atomicAdd(o.err + ERR_DUP_ID, dup);
-        }
+        if (l16 == 0 && valid && dup) atomicAdd(o.err + ERR_DUP_ID, dup);
     }
 }
 
@@ -1165,13 +1157,13 @@ size_t split_weight_bytes(int NC, int d) {
 template <int MODE>
 hipError_t launch_router_mfma(const pr2_moe_desc& d, int NC, int r, const void* x,
                               const bf16_t* Ws, const PredictOut& po, const ReplayOut& ro,
-                              hipStream_t s) {
+                              hipStream_t s, bool splitk_ok = true) {
     const int NTW = ncp_of(NC) / 64;
     const int64_t tiles = (d.T + kRTM - 1) / kRTM;
     dim3 grid((unsigned)tiles);
     const bf16_t* xb = (const bf16_t*)x;
     SplitK sk{nullptr, nullptr};
-    if (!use_splitk(d)) {
+    if (!splitk_ok || !use_splitk(d)) {
         switch (NTW) {
 #define PR2_CASE(n) case n: hipLaunchKernelGGL((router_mfma_kernel<n, MODE, 0>), grid, dim3(kRThreads), 0, s, xb, Ws, d.T, d.d, d.N, r, NC, po, ro, sk); break;
             PR2_CASE(1) PR2_CASE(2) PR2_CASE(3)
@@ -1221,6 +1213,10 @@ hipError_t launch_split(const float* W_r, const float* A, const float* B, const 
 
 // The split-K buffers are reserved for min(T, the split-K limit) tokens at
 // every T, so that a workspace sized for some batch also serves any smaller one.
+size_t router_split_weight_bytes(int NC, const pr2_moe_desc& d) {
+    return split_weight_bytes(NC, d.d);
+}
+
 size_t router_split_bytes(int NC, const pr2_moe_desc& d) {
     size_t b = split_weight_bytes(NC, d.d);
     if (d.T > 0 && d.d / kRBK >= kSplitMinSteps) {
@@ -1238,7 +1234,8 @@ bool router_mfma_ok(const pr2_moe_desc& d, int NC) {
 hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const float* W_r,
                                 const float* b_r, const float* A, const float* B, void* idx_out,
                                 int64_t ldi, float* gate_out, float* logits_out, void* split_ws,
-                                hipStream_t s, const FeatureCache& cache, bool reuse_split) {
+                                hipStream_t s, const FeatureCache& cache, bool reuse_split,
+                                bool splitk_ok) {
     // reuse_split: split_ws already holds this call's split (same weights, same layout)
     const float* Bn = d.r > 0 ? B : nullptr;
     if (logits_out == nullptr && cache.row == nullptr && router_mfma_ok(d, d.N)) {
@@ -1250,7 +1247,8 @@ hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const floa
             if (e != hipSuccess) return e;
         }
         LaunchScope scope("route_predict", s);
-        return launch_router_mfma<0>(d, d.N, d.r, x, (const bf16_t*)split_ws, o, ReplayOut{}, s);
+        return launch_router_mfma<0>(d, d.N, d.r, x, (const bf16_t*)split_ws, o, ReplayOut{}, s,
+                                     splitk_ok);
     }
     PredictOut o{b_r, Bn, d.k, d.renorm, 0, idx_out, d.idx_dtype, ldi, gate_out, logits_out, cache,
                  x, d.d, d.act_dtype};
@@ -1261,7 +1259,8 @@ hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const floa
             if (e != hipSuccess) return e;
         }
         LaunchScope scope("route_predict", s);
-        return launch_router_mfma<0>(d, NC, d.r, x, (const bf16_t*)split_ws, o, ReplayOut{}, s);
+        return launch_router_mfma<0>(d, NC, d.r, x, (const bf16_t*)split_ws, o, ReplayOut{}, s,
+                                     splitk_ok);
     }
     ProjArgs a;
     a.x = x;
@@ -1322,10 +1321,21 @@ hipError_t launch_router_replay(const pr2_moe_desc& d, const void* x, const floa
 
 hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void* idx, int64_t ldi,
                                const float* W_r, const float* b_r, float* gate_out, int* err,
-                               void* split_ws, hipStream_t s) {
+                               void* split_ws, hipStream_t s, const RouteDiag* diag) {
     const char* v = getenv("PR2_VALIDATE");
+    DiagOut g{};
+    if (diag) {
+        // the diagnostics epilogue runs on the same logits, before the weights
+        g = DiagOut{diag->z_ref, diag->cur_idx, diag->overlap, diag->kl, diag->hist, nullptr};
+        if (diag->hist) {
+            LaunchScope scope("replay_diagnostics_zero", s);
+            hipLaunchKernelGGL(zero_u64_kernel, dim3(1), dim3(64), 0, s, diag->hist, d.k + 1);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
+    }
     ReplayOut o{b_r, d.k, d.renorm, idx, d.idx_dtype, ldi, gate_out, err,
-                (v && v[0] == '1') ? 1 : 0, DiagOut{}};
+                (v && v[0] == '1') ? 1 : 0, g};
     return launch_router_replay(d, x, W_r, o, split_ws, "replay_gates", s);
 }
 

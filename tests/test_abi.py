@@ -317,3 +317,27 @@ def test_route_reuse_rejects_bad_arguments():
     assert reuse(ldi=1)[0] == "PR2_ERR_SHAPE"
     assert reuse(x=FAKE + 2)[0] == "PR2_ERR_ALIGN"
     assert reuse(nbytes=ws_bytes - 1)[0] == "PR2_ERR_WORKSPACE"
+
+
+def route_reuse(d, x=FAKE, W=FAKE, b=None, A=FAKE, Bm=FAKE, idx=FAKE, logits=None, ws=FAKE):
+    L = B.lib()
+    st = L.pr2_route_predict_reuse(byref(d), c_void_p(x), c_void_p(W), c_void_p(b), c_void_p(A),
+                                   c_void_p(Bm), c_void_p(idx), d.k, None, c_void_p(logits),
+                                   c_void_p(ws), B.workspace_bytes(d, B.OP_ROUTE), None)
+    return st, L.pr2_last_error().decode()
+
+
+def test_reuse_needs_a_recorded_split():
+    """pr2_route_predict_reuse refuses a workspace that holds no split formed by a
+    route call (checked on the host, before any HIP call)."""
+    d = desc()                                    # bf16, d % 32 == 0: the MFMA router's split
+    assert B.workspace_bytes(d, B.OP_ROUTE) > 0
+    st, msg = route_reuse(d, ws=FAKE + 0x100000)
+    assert B.STATUS[st] == "PR2_ERR_WORKSPACE", msg
+    assert "no router split" in msg
+    # with logits wanted (the unfolded layout) the same
+    st, msg = route_reuse(d, ws=FAKE + 0x200000, logits=FAKE)
+    assert B.STATUS[st] == "PR2_ERR_WORKSPACE", msg
+    # the fp64 vector path keeps no split: nothing to check, the call goes on
+    st, msg = route_reuse(desc(act=B.PR2_F32))
+    assert B.STATUS[st] in ("PR2_ERR_DEVICE", "PR2_OK"), msg

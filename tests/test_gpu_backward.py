@@ -3,14 +3,17 @@ backward (itself pinned to central differences): gradients of <dy, y> for the
 replay forward with recorded ids held fixed and renormalised replay weights
 (Sec. 4.1, replay during training; the predictor is bypassed and gets none).
 
-Recorded routes are the current router's top-k with a fraction of tokens
-changed in one slot, so that the replayed set differs from what the current
-router would pick (the situation replay exists for).
+Recorded routes are the current router's top-k with 5 % of the tokens
+recording the (k+1)-th ranked expert in place of the k-th, so that the
+replayed set differs from what the current router would pick (the situation
+replay exists for).  The ranking comes from the oracle's router logits.
 
 Bar: per-tensor Frobenius ratio ||g - g_ref|| / ||g_ref|| <= 2e-2 with bf16
 activations (bf16 pre-activations, g H and per-route input gradients, fp32
-accumulation), <= 1e-4 with fp32 activations; experts that no route uses get
-exactly zero; two runs are bitwise identical."""
+accumulation), <= 1e-4 with fp32 activations; at the full Qwen3-30B-A3B shape
+the same bar holds for every expert's slice of each expert-weight gradient,
+every column of dW_r and every token row of dx; experts that no route uses
+get exactly zero; two runs are bitwise identical."""
 import numpy as np
 import pytest
 
@@ -24,19 +27,16 @@ TOL = {"bf16": 2e-2, "f32": 1e-4}
 GRADS = ("dx", "dW_r", "dbeta", "dW_gate", "dW_up", "dW_down")
 
 
-def recorded_route(L, k, flip_frac, seed):
-    """Current router's top-k, with flip_frac of the tokens given one other expert."""
+def recorded_route(L, shape, seed):
+    """The current router's top-k (oracle logits, fp32 decision, ties to the lower
+    id) with flip_frac of the tokens recording the (k+1)-th ranked expert instead
+    of the k-th (workloads.flip_route)."""
     p = O.router_logits(L["x"], L["W_r"], L["beta"])
-    idx = O.topk_ids(p, k).copy()
-    T, N = p.shape
-    n = int(round(flip_frac * T))
-    rng = np.random.default_rng([seed, 77])
-    if n and k < N:
-        for t in rng.choice(T, n, replace=False):
-            s = rng.integers(k)
-            free = np.setdiff1d(np.arange(N), idx[t])
-            idx[t, s] = rng.choice(free)
-    return idx
+    k, N = shape.k, p.shape[1]
+    if k == N:
+        return O.topk_ids(p, k)
+    ranked = np.argsort(-p.astype(np.float32), axis=1, kind="stable")[:, :k + 1]
+    return W.flip_route(ranked, W.flip_tokens(shape, seed), k)
 
 
 def run_bwd(L, idx, dy, act, idx_dtype="int32", ldi_pad=0, ws=None):
@@ -92,7 +92,7 @@ def oracle_bwd(L, idx, dy):
 def test_backward_tiny_fp32():
     s = W.WORKLOADS["tiny_fp32_T256"]
     L = W.layer_inputs(s, 0)
-    idx = recorded_route(L, s.k, 0.05, 0)
+    idx = recorded_route(L, s.with_(flip_frac=0.05), 0)
     dy = W.upstream_grad(s, 0)
     g = run_bwd(L, idx, dy, "f32")
     compare(g, oracle_bwd(L, idx, dy), "f32", s.name)
@@ -116,9 +116,9 @@ CASES = [
                                               for c in CASES])
 def test_backward_shapes(case):
     T, d, N, k, m, act, skew, idt, pad = case
-    s = W.LayerShape("case", T=T, d=d, N=N, k=k, m=m, r=0, act=act, skew=skew)
+    s = W.LayerShape("case", T=T, d=d, N=N, k=k, m=m, r=0, act=act, skew=skew, flip_frac=0.05)
     L = W.layer_inputs(s, 11)
-    idx = recorded_route(L, k, 0.05, 11)
+    idx = recorded_route(L, s, 11)
     dy = W.upstream_grad(s, 11)
     g = run_bwd(L, idx, dy, act, idt, pad)
     ref = oracle_bwd(L, idx, dy)
@@ -132,9 +132,10 @@ def test_backward_shapes(case):
 def test_backward_renormalised_logit_gradient_sums_to_zero():
     """With renormalised weights each token's logit gradient sums to zero over
     its route (softmax shift invariance), so db_r sums to zero."""
-    s = W.LayerShape("shift", T=512, d=256, N=16, k=4, m=256, r=0, act="bf16", skew="hot8")
+    s = W.LayerShape("shift", T=512, d=256, N=16, k=4, m=256, r=0, act="bf16", skew="hot8",
+                     flip_frac=0.1)
     L = W.layer_inputs(s, 2)
-    idx = recorded_route(L, s.k, 0.1, 2)
+    idx = recorded_route(L, s, 2)
     g = run_bwd(L, idx, W.upstream_grad(s, 2), "bf16")
     assert abs(g["dbeta"].sum()) <= 1e-4 * np.abs(g["dbeta"]).sum()
 
@@ -156,31 +157,52 @@ def test_backward_empty_batch_zeroes_weight_gradients():
         assert torch.all(t == 0)
 
 
-def test_backward_qwen3_30b_sampled_experts():
-    """The full Qwen3-30B-A3B-shaped backward workload (16384 tokens, 5 % of
-    routes changed).  Each expert's weight gradients, its dW_r column and db_r
-    entry depend only on the routes through it, and dx_t only on token t, so the
-    oracle runs on the tokens of three sampled experts (the most loaded, a
-    median one and the least loaded) and checks those exactly; a second run
-    must be bitwise identical."""
+def frob_rows(g, ref):
+    """||g_i - ref_i|| / ||ref_i|| over the leading axis (slices, rows or columns)."""
+    g = np.asarray(g, dtype=np.float64).reshape(g.shape[0], -1)
+    ref = np.asarray(ref, dtype=np.float64).reshape(ref.shape[0], -1)
+    num = np.linalg.norm(g - ref, axis=1)
+    den = np.linalg.norm(ref, axis=1)
+    return num, den
+
+
+def test_backward_qwen3_30b_full():
+    """The full Qwen3-30B-A3B-shaped backward workload: 16384 tokens, 5 % of them
+    (819) recording the (k+1)-th ranked expert instead of the k-th.  Every
+    expert's dW_gate / dW_up / dW_down slice, every dW_r column and every dx row
+    is held to the 2e-2 relative bar (exact zeros where the oracle has none);
+    a second run is bitwise identical."""
     s = W.WORKLOADS["qwen3_30b_bwd_T16384"]
     L = W.layer_inputs(s, 0)
-    idx = recorded_route(L, s.k, s.flip_frac, 0)
+    idx = recorded_route(L, s, 0)
+    assert (O.route_overlap(idx, O.topk_ids(O.router_logits(L["x"], L["W_r"], L["beta"]), s.k))
+            < s.k).sum() == 819
     dy = W.upstream_grad(s, 0)
     g = run_bwd(L, idx, dy, "bf16")
-    load = np.bincount(idx.ravel(), minlength=s.N)
-    order = np.argsort(load, kind="stable")
-    for e in (order[-1], order[s.N // 2], order[0]):
-        toks = np.nonzero((idx == e).any(axis=1))[0]
-        ref = O.replay_backward(L["x"][toks], idx[toks], L["W_r"], L["beta"], L["W_gate"], L["W_up"],
-                                L["W_down"], dy[toks], renorm=True)
-        got = {"dW_gate": g["dW_gate"][e], "dW_up": g["dW_up"][e], "dW_down": g["dW_down"][e],
-               "dW_r": g["dW_r"][:, e], "dbeta": g["dbeta"][e:e + 1], "dx": g["dx"][toks]}
-        want = {"dW_gate": ref["dW_gate"][e], "dW_up": ref["dW_up"][e],
-                "dW_down": ref["dW_down"][e], "dW_r": ref["dW_r"][:, e],
-                "dbeta": ref["dbeta"][e:e + 1], "dx": ref["dx"]}
-        compare(got, want, "bf16", f"{s.name} expert {e} ({load[e]} routes)")
-        del ref
+    ref = oracle_bwd(L, idx, dy)
+    tol = TOL["bf16"]
+    report = {}
+    for n, axis_name in (("dW_gate", "expert"), ("dW_up", "expert"), ("dW_down", "expert"),
+                         ("dx", "row")):
+        num, den = frob_rows(g[n], ref[n])
+        zero = den == 0
+        assert np.all(num[zero] == 0), f"{n}: a {axis_name} with a zero oracle gradient is not zero"
+        rel = num[~zero] / den[~zero]
+        worst = int(np.flatnonzero(~zero)[np.argmax(rel)])
+        report[n] = (rel.max(), worst)
+        assert rel.max() <= tol, f"{n}: {axis_name} {worst} rel err {rel.max():.3e} > {tol}"
+    num, den = frob_rows(g["dW_r"].T, ref["dW_r"].T)           # per expert column
+    zero = den == 0
+    assert np.all(num[zero] == 0)
+    rel = num[~zero] / den[~zero]
+    report["dW_r"] = (rel.max(), int(np.flatnonzero(~zero)[np.argmax(rel)]))
+    assert rel.max() <= tol, f"dW_r: column rel err {rel.max():.3e}"
+    e_db = frob(g["dbeta"], ref["dbeta"])
+    assert e_db <= tol, f"dbeta: Frobenius ratio {e_db:.3e}"
+    print(f"\n{s.name}: worst per-slice / per-row / per-column rel err " +
+          ", ".join(f"{n} {v[0]:.2e} (at {v[1]})" for n, v in report.items()) +
+          f", dbeta {e_db:.2e}")
+    del ref
     g2 = run_bwd(L, idx, dy, "bf16")
     for n in GRADS:
         assert np.array_equal(g[n], g2[n]), f"{n} differs between two runs"

@@ -5,8 +5,10 @@ cached for replay; Alg. 2, caching step), then replayed in micro-batches of
 16 whole sequences = 32768 tokens (Sec. 4.1 replay; Alg. 3).
 
 Oracle checks: the routes of sampled steps against the float64 oracle (margin
-rule), and sampled replayed rows against the oracle's replay forward on the
-oracle's own route of those tokens (only where it equals the recorded one)."""
+rule); all 16 micro-batches (the whole 524288-route record) are replayed, and
+in each the first and last rows and 32 random ones are checked against the
+oracle's replay forward on the oracle's own route of those tokens (only where
+it equals the recorded one)."""
 import numpy as np
 import pytest
 
@@ -57,24 +59,34 @@ def test_decode_record_then_replay():
         assert len(bad) == 0, f"step {pos}: sequences {bad[:5]} differ"
     print(f"\ndecode: {len(steps)} steps checked, {excluded} tokens under the margin")
 
-    # replay micro-batches 0 and 15 (16 whole sequences = 32768 tokens each)
+    # replay every micro-batch (16 whole sequences = 32768 tokens each)
     Wg, Wu, Wd = (to_dev(L[n], "bf16") for n in ("W_gate", "W_up", "W_down"))
     Xseq = Xd.reshape(S * P, s.d)                                 # rows (seq, pos), seq-major
+    mbt = W.DECODE_MICROBATCH
+    nseq = mbt // P
+    n_mb = S // nseq
+    assert n_mb == 16
+    ys = torch.empty((S * P, s.d), dtype=torch.bfloat16, device=dev)
+    ws_r = B.replay_workspace(Xseq[:mbt], buf[:nseq].reshape(mbt, k), Wr, Wg)
+    for mb in range(n_mb):
+        lo = mb * mbt
+        B.moe_replay_forward(Xseq[lo:lo + mbt], buf[mb * nseq:(mb + 1) * nseq].reshape(mbt, k),
+                             Wr, br, Wg, Wu, Wd, ys[lo:lo + mbt], ws=ws_r)
+    torch.cuda.synchronize()
+    Y = ys.float().cpu().numpy()
     rng = np.random.default_rng(5)
-    for mb in (0, 15):
-        lo = mb * 16 * P
-        x_mb = Xseq[lo:lo + 16 * P]
-        idx_mb = buf[mb * 16:(mb + 1) * 16].reshape(16 * P, k)
-        y = torch.empty_like(x_mb)
-        B.moe_replay_forward(x_mb, idx_mb, Wr, br, Wg, Wu, Wd, y)
-        torch.cuda.synchronize()
-        rows = np.unique(np.concatenate([[0, 16 * P - 1], rng.choice(16 * P, 96, replace=False)]))
-        seq, pos = mb * 16 + rows // P, rows % P
-        xr = X[seq, pos, :]
-        ref = O.route_predict(xr, L["W_r"], L["beta"], L["A"], L["B"], k)
-        same = (ref["margin"] >= MARGIN_EPS) & np.all(rec[seq, pos, :] == ref["idx"], axis=1)
-        assert same.sum() >= len(rows) - 2
-        keep = rows[same]
-        y_ref, _ = O.replay_forward_rows(keep, xr[same], ref["idx"][same], L["W_r"], L["beta"],
-                                         L["W_gate"], L["W_up"], L["W_down"])
-        compare_rows(y.float().cpu().numpy()[keep], y_ref, "bf16", f"micro-batch {mb}")
+    # sampled rows of every micro-batch, checked in one oracle pass
+    rows = np.concatenate([mb * mbt + np.unique(np.concatenate(
+        [[0, mbt - 1], rng.choice(mbt, 32, replace=False)])) for mb in range(n_mb)])
+    seq, pos = rows // P, rows % P
+    xr = X[seq, pos, :]
+    ref = O.route_predict(xr, L["W_r"], L["beta"], L["A"], L["B"], k)
+    same = (ref["margin"] >= MARGIN_EPS) & np.all(rec[seq, pos, :] == ref["idx"], axis=1)
+    assert same.sum() >= len(rows) - 4
+    for mb in range(n_mb):
+        got = (rows // mbt == mb) & same
+        assert got.sum() >= 30, f"micro-batch {mb}: too few rows to check"
+    y_ref, _ = O.replay_forward_rows(rows[same], xr[same], ref["idx"][same], L["W_r"], L["beta"],
+                                     L["W_gate"], L["W_up"], L["W_down"])
+    err = compare_rows(Y[rows[same]], y_ref, "bf16", "decode micro-batches")
+    print(f"decode replay: {n_mb} micro-batches, {same.sum()} sampled rows, worst rel err {err:.2e}")

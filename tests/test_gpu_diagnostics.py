@@ -2,9 +2,12 @@
 deviation distribution and route KL of the recorded route against the
 current router) with the float64 oracle.
 
-The recorded route is the GPU's predictive route (router + rank-r predictor),
-so it differs from the current router's top-k on some tokens; the reference
-logits for the route KL are the oracle's predictive logits z.  The current
+The recorded route is the oracle's predictive route (router + rank-r
+predictor), so it differs from the current router's top-k on some tokens; the
+reference logits for the route KL are the oracle's predictive logits z.  The
+same checks run on the diagnostics that pr2_moe_replay_forward_diag forms
+inside the replay forward, whose output and weights must equal those of
+pr2_moe_replay_forward bit for bit.  The current
 top-k follows the margin rule on the current logits; overlaps, the deviation
 histogram (exact integer counts) and the per-token KL (fp64 from the fp32
 logits) are compared on every token outside it."""
@@ -38,15 +41,9 @@ def run(L, s, idx_np, z_ref, idx_dtype="int32", ldi_pad=0):
             "kl": kl.cpu().numpy(), "hist": hist.cpu().numpy()}
 
 
-def gpu_route(L, s):
-    import torch
-    from paper_2606_00395_amd import binding as B
-    idx = torch.empty((s.T, s.k), dtype=torch.int32, device="cuda")
-    B.route_predict(to_dev(L["x"], s.act), to_dev(L["W_r"]),
-                    to_dev(L["beta"]) if L["beta"] is not None else None,
-                    to_dev(L["A"]), to_dev(L["B"]), s.k, idx)
-    torch.cuda.synchronize()
-    return idx.cpu().numpy().astype(np.int64)
+def oracle_route(L, s):
+    """The recorded ids: the oracle's predictive route (never the HIP path's)."""
+    return O.route_predict(L["x"], L["W_r"], L["beta"], L["A"], L["B"], s.k)["idx"]
 
 
 def check(L, s, idx, g, z_ref, where):
@@ -77,7 +74,7 @@ def predictive_logits(L):
 def test_diagnostics_tiny_fp32():
     s = W.WORKLOADS["tiny_fp32_T256"]
     L = W.layer_inputs(s, 0, experts=False)
-    idx = gpu_route(L, s)
+    idx = oracle_route(L, s)
     z = predictive_logits(L)
     check(L, s, idx, run(L, s, idx, z), z, "tiny")
 
@@ -92,7 +89,7 @@ def test_diagnostics_shapes(case):
     s = W.LayerShape("case", T=T, d=d, N=N, k=k, m=8, r=r, act=act, skew=skew)
     L = W.layer_inputs(s, 9, experts=False)
     L["A"] = L["A"] * 20.0            # a predictor strong enough to move some routes
-    idx = gpu_route(L, s)
+    idx = oracle_route(L, s)
     z = predictive_logits(L)
     check(L, s, idx, run(L, s, idx, z, idt, pad), z, str(case))
 
@@ -114,6 +111,83 @@ def test_diagnostics_identical_route_and_reference():
 def test_diagnostics_qwen3_30b_full():
     s = W.WORKLOADS["qwen3_30b_T16384"]
     L = W.layer_inputs(s, 0, experts=False)
-    idx = gpu_route(L, s)
+    idx = oracle_route(L, s)
     z = predictive_logits(L)
     check(L, s, idx, run(L, s, idx, z), z, s.name)
+
+
+def run_fused(L, s, idx_np, z_ref, idx_dtype="int32", ldi_pad=0):
+    """pr2_moe_replay_forward_diag and, on the same inputs, pr2_moe_replay_forward
+    and pr2_route_diagnostics."""
+    import torch
+    from paper_2606_00395_amd import binding as B
+    x = to_dev(L["x"], s.act)
+    Wr = to_dev(L["W_r"])
+    br = to_dev(L["beta"]) if L["beta"] is not None else None
+    Wg, Wu, Wd = (to_dev(L[n], s.act) for n in ("W_gate", "W_up", "W_down"))
+    T, k = idx_np.shape
+    dt = torch.int16 if idx_dtype == "int16" else torch.int32
+    buf = torch.full((T, k + ldi_pad), -1, dtype=dt, device="cuda")
+    buf[:, :k] = torch.from_numpy(idx_np.astype(np.int64)).to(dt).to("cuda")
+    idx = buf[:, :k]
+    zr = to_dev(z_ref)
+    cur = torch.full((T, k), -5, dtype=dt, device="cuda")
+    ov = torch.full((T,), -5, dtype=torch.int32, device="cuda")
+    kl = torch.full((T,), float("nan"), device="cuda")
+    hist = torch.full((k + 1,), 12345, dtype=torch.int64, device="cuda")
+    y = torch.empty_like(x)
+    gate = torch.empty((T, k), dtype=torch.float32, device="cuda")
+    B.moe_replay_forward_diag(x, idx, Wr, br, Wg, Wu, Wd, y, gate, zr, cur, ov, kl, hist)
+    y0 = torch.empty_like(x)
+    gate0 = torch.empty_like(gate)
+    B.moe_replay_forward(x, idx, Wr, br, Wg, Wu, Wd, y0, gate0)
+    cur1, ov1, kl1, hist1 = (torch.empty_like(t) for t in (cur, ov, kl, hist))
+    B.route_diagnostics(x, idx, Wr, br, zr, cur1, ov1, kl1, hist1)
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16) if y.dtype == torch.bfloat16 else y,
+                       y0.view(torch.int16) if y0.dtype == torch.bfloat16 else y0), \
+        "fused replay output differs from pr2_moe_replay_forward"
+    assert torch.equal(gate, gate0)
+    for a, b in ((cur, cur1), (ov, ov1), (hist, hist1)):
+        assert torch.equal(a, b), "fused diagnostics differ from pr2_route_diagnostics"
+    assert torch.equal(kl.view(torch.int32), kl1.view(torch.int32))
+    return {"cur": cur.cpu().numpy().astype(np.int64), "overlap": ov.cpu().numpy(),
+            "kl": kl.cpu().numpy(), "hist": hist.cpu().numpy()}
+
+
+@pytest.mark.parametrize("case", [
+    (3000, 256, 64, 6, 8, 128, "bf16", "hot8", "int32", 0),
+    (1000, 512, 128, 8, 16, 256, "bf16", "zipf", "int16", 2),
+    (300, 64, 8, 2, 4, 40, "f32", "none", "int32", 1),
+])
+def test_replay_forward_fused_diagnostics(case):
+    T, d, N, k, r, m, act, skew, idt, pad = case
+    s = W.LayerShape("fused", T=T, d=d, N=N, k=k, m=m, r=r, act=act, skew=skew)
+    L = W.layer_inputs(s, 12)
+    L["A"] = L["A"] * 20.0            # a predictor strong enough to move some routes
+    idx = oracle_route(L, s)
+    z = predictive_logits(L)
+    check(L, s, idx, run_fused(L, s, idx, z, idt, pad), z, "fused " + str(case))
+
+
+def test_replay_forward_fused_diagnostics_qwen3_30b():
+    s = W.WORKLOADS["qwen3_30b_T16384"]
+    L = W.layer_inputs(s, 0)
+    idx = oracle_route(L, s)
+    z = predictive_logits(L)
+    check(L, s, idx, run_fused(L, s, idx, z), z, "fused " + s.name)
+
+
+def test_replay_forward_fused_diagnostics_empty_batch():
+    import torch
+    from paper_2606_00395_amd import binding as B
+    d, N, m, k = 256, 8, 128, 2
+    x = torch.empty((0, d), dtype=torch.bfloat16, device="cuda")
+    idx = torch.empty((0, k), dtype=torch.int32, device="cuda")
+    Wr = torch.zeros((d, N), device="cuda")
+    Wg = torch.zeros((N, m, d), dtype=torch.bfloat16, device="cuda")
+    Wd = torch.zeros((N, d, m), dtype=torch.bfloat16, device="cuda")
+    hist = torch.full((k + 1,), 7, dtype=torch.int64, device="cuda")
+    B.moe_replay_forward_diag(x, idx, Wr, None, Wg, Wg, Wd, torch.empty_like(x), hist_out=hist)
+    torch.cuda.synchronize()
+    assert torch.all(hist == 0)

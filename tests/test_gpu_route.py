@@ -225,3 +225,44 @@ def test_route_reuse_split_matches_fresh_calls(logits, act):
         Ls = dict(L, x=L["x"][a:b])
         ref = oracle_route(Ls, s.k)
         assert compare_route(i0.numpy(), g0.numpy(), ref, s.k, f"reuse step {n}") == 0
+
+
+def test_reuse_checks_the_recorded_split():
+    """pr2_route_predict_reuse reads the split a route call formed in the same
+    workspace and refuses one formed from other weights, in the other layout, or
+    dropped by another call that used the workspace."""
+    torch = torch_mod()
+    from paper_2606_00395_amd import binding as B
+    s = W.LayerShape("reuse", T=300, d=256, N=16, k=4, m=128, r=4, act="bf16", skew="hot8")
+    L = W.layer_inputs(s, 4)
+    x = to_dev(L["x"], "bf16")
+    Wr, br, A, Bm = (to_dev(L[n]) for n in ("W_r", "beta", "A", "B"))
+    rw = B.workspace_bytes(B.make_desc(s.T, s.d, s.N, s.k, s.m, s.r), B.OP_ROUTE)
+    fw = B.workspace_bytes(B.make_desc(s.T, s.d, s.N, s.k, s.m, 0), B.OP_REPLAY_FWD)
+    ws = torch.empty(max(rw, fw), dtype=torch.uint8, device="cuda")
+    idx = torch.empty((s.T, s.k), dtype=torch.int32, device="cuda")
+    idx2 = torch.empty_like(idx)
+    B.route_predict(x, Wr, br, A, Bm, s.k, idx, ws=ws)
+    B.route_predict(x, Wr, br, A, Bm, s.k, idx2, ws=ws, reuse_split=True)
+    torch.cuda.synchronize()
+    assert torch.equal(idx, idx2)
+    ref = oracle_route(L, s.k)
+    compare_route(idx2.cpu().numpy(), None, ref, s.k, "reuse")
+    for kw in (dict(W=Wr.clone()), dict(A=A.clone()), dict(Bm=Bm.clone()),
+               dict(logits=torch.empty((s.T, s.N), device="cuda"))):
+        with pytest.raises(B.Pr2Error) as ei:
+            B.route_predict(x, kw.get("W", Wr), br, kw.get("A", A), kw.get("Bm", Bm), s.k, idx2,
+                            logits_out=kw.get("logits"), ws=ws, reuse_split=True)
+        assert ei.value.status == 5, str(ei.value)
+    # a replay forward writes its own scratch into the workspace: the split is gone
+    y = torch.empty_like(x)
+    B.moe_replay_forward(x, idx, Wr, br, to_dev(L["W_gate"], "bf16"), to_dev(L["W_up"], "bf16"),
+                         to_dev(L["W_down"], "bf16"), y, ws=ws)
+    with pytest.raises(B.Pr2Error) as ei:
+        B.route_predict(x, Wr, br, A, Bm, s.k, idx2, ws=ws, reuse_split=True)
+    assert ei.value.status == 5
+    # forming it again makes the reuse valid again
+    B.route_predict(x, Wr, br, A, Bm, s.k, idx2, ws=ws)
+    B.route_predict(x, Wr, br, A, Bm, s.k, idx2, ws=ws, reuse_split=True)
+    torch.cuda.synchronize()
+    assert torch.equal(idx, idx2)

@@ -479,6 +479,31 @@ def test_workload_generators_are_deterministic_and_row_addressable():
     assert len(fl) == 819 and len(np.unique(fl)) == 819
 
 
+def test_flip_route_recipe_differs_in_exactly_one_slot():
+    """The backward workload's recorded route: the current top-k of the replay
+    router, with the k-th ranked expert swapped for the (k+1)-th on 5 % of the
+    tokens.  Checked with brute force: flipped tokens overlap the current top-k
+    in k-1 ids and hold the (k+1)-th ranked one, the others equal it."""
+    s = W.LayerShape("flip", T=400, d=32, N=12, k=3, m=8, r=0, act="f32", skew="hot8",
+                     flip_frac=0.05)
+    L = W.layer_inputs(s, 3, experts=False)
+    p = O.router_logits(L["x"], L["W_r"], L["beta"])
+    ranked = np.argsort(-p.astype(np.float32), axis=1, kind="stable")[:, :s.k + 1]
+    fl = W.flip_tokens(s, 3)
+    assert len(fl) == 20
+    idx = W.flip_route(ranked, fl, s.k)
+    cur = O.topk_ids(p, s.k)
+    ov = O.route_overlap(idx, cur)
+    flipped = np.zeros(s.T, dtype=bool)
+    flipped[fl] = True
+    assert np.all(ov[flipped] == s.k - 1) and np.all(ov[~flipped] == s.k)
+    np.testing.assert_array_equal(idx[~flipped], cur[~flipped])
+    for t in fl:
+        order = sorted(range(s.N), key=lambda j: (-np.float32(p[t, j]), j))
+        assert order[s.k] in idx[t] and order[s.k - 1] not in idx[t]
+    assert np.all(np.diff(idx, axis=1) > 0)
+
+
 # ------------------------------------------------ route metrics (Sec. 5.4) ---
 
 def test_route_overlap_agreement_and_deviation_brute_force():

@@ -206,6 +206,20 @@ def flip_tokens(shape: LayerShape, seed: int) -> np.ndarray:
     return np.sort(rng.choice(shape.T, n, replace=False))
 
 
+def flip_route(ranked: np.ndarray, tokens: np.ndarray, k: int) -> np.ndarray:
+    """The recorded route of the backward workload from a ranking computed elsewhere.
+
+    ``ranked`` [T, k+1] holds each token's k+1 highest-ranked expert ids, best
+    first.  Every token records its first k ids; each token in ``tokens`` records
+    the (k+1)-th instead of the k-th (a one-slot difference from the current
+    top-k).  Rows are returned sorted ascending, int64 [T, k].  Index work only."""
+    ranked = np.asarray(ranked, dtype=np.int64)
+    assert ranked.ndim == 2 and ranked.shape[1] == k + 1
+    idx = ranked[:, :k].copy()
+    idx[tokens, k - 1] = ranked[tokens, k]
+    return np.sort(idx, axis=1)
+
+
 def layer_inputs(shape: LayerShape, seed: int = 0, experts: bool = True) -> dict:
     """All inputs of one layer as float32 numpy arrays (beta may be None).
 
