@@ -56,6 +56,9 @@ def parse():
     ap.add_argument("--workload", default=None)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="forward mode: skip the other workloads (235B forward, backward, "
+                         "decode, the method's other calls) that follow the headline")
     ap.add_argument("--cpu-sample-tokens", type=int, default=0,
                     help="tokens of the oracle's CPU sample (0: the mode's default)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -296,14 +299,18 @@ def cold_ms_per_step(step, steps, stream):
     return total / steps
 
 
-def graph_ms_per_step(step_on, steps):
+def graph_ms_per_step(step_on, steps, warmup=20):
     """Mean ms per step when the step's launches are captured once into a HIP
-    graph and replayed (no host work or launch gaps between kernels)."""
+    graph and replayed (no host work or launch gaps between kernels).  The
+    first replays after instantiation run slower (measured: 1.565 ms against
+    1.478 ms later on the Qwen3-30B step), so the graph is warmed up like the
+    eager path before it is timed."""
     import torch
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
         step_on(torch.cuda.current_stream())
-    graph.replay()
+    for _ in range(warmup):
+        graph.replay()
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
@@ -376,15 +383,10 @@ def run_forward(args, shape, dev):
 
     ms, kern = timed_steps(step, args.steps, args.warmup, stream, B)
     median = timed_steps.median_ms
-    ms_graph = graph_ms_per_step(step_on, args.steps)
-    ms_cold = cold_ms_per_step(step, args.steps, stream)
-    # the same step with every launch on the caller's stream (no side stream for the
-    # replay gates), for comparison
-    os.environ["PR2_NO_SIDE_STREAM"] = "1"
-    try:
-        ms_inorder, _ = timed_steps(step, args.steps, 2, stream, B)
-    finally:
-        del os.environ["PR2_NO_SIDE_STREAM"]
+    light = getattr(args, "light", False)
+    if not light:
+        ms_graph = graph_ms_per_step(step_on, args.steps)
+        ms_cold = cold_ms_per_step(step, args.steps, stream)
     ab = 2 if shape.act == "bf16" else 4
     ib = 2 if shape.idx_dtype == "int16" else 4
     dominant = "gemm1_gate_up_swiglu"
@@ -405,17 +407,16 @@ def run_forward(args, shape, dev):
                        "unit": "TFLOP/s", "frac": achieved / peak,
                        "traffic": profiled_traffic(f"replay_and_route_kernels_{shape.name}.txt",
                                                   "grouped_gemm_mfma<0>")}
-    out["hip_graph"] = {"ms_per_step": ms_graph, "value": T / (ms_graph * 1e-3),
-                        "note": "the same step captured once and replayed as a HIP graph"}
-    out["cold_cache"] = {"ms_per_step": ms_cold, "value": T / (ms_cold * 1e-3),
-                         "note": "each step after a 512 MiB device write that evicts L2 and "
-                                 "the 256 MB last-level cache"}
+    if not light:
+        out["hip_graph"] = {"ms_per_step": ms_graph, "value": T / (ms_graph * 1e-3),
+                            "note": "the same step captured once and replayed as a HIP graph"}
+        out["cold_cache"] = {"ms_per_step": ms_cold, "value": T / (ms_cold * 1e-3),
+                             "note": "each step after a 512 MiB device write that evicts L2 "
+                                     "and the 256 MB last-level cache"}
     out["ms_per_step_median"] = median
-    out["in_order"] = {"ms_per_step": ms_inorder,
-                       "note": "the replay gates on the caller's stream instead of the side "
-                               "stream (PR2_NO_SIDE_STREAM=1)"}
     out["kernels_ms"] = {n: round(v, 5) for n, v in kern.items()}
-    out["measured_peaks"] = measured_peaks(dev)
+    if not light:
+        out["measured_peaks"] = measured_peaks(dev)
     out["replay_forward"] = {
         "ms": t_replay,
         "mfma_frac_whole_layer": C.expert_flops(T, d, k, m) / (t_replay * 1e-3) / C.PEAK_BF16_FLOPS,
@@ -427,12 +428,50 @@ def run_forward(args, shape, dev):
         "replay_gates": C.replay_gate_bytes(T, d, N, k, ab, ib) / (t_gates * 1e-3) / 1e9,
         "combine": C.combine_bytes(T, d, k, ab, ab) / (t_comb * 1e-3) / 1e9,
         "permute_ms": t_perm,
+        "note": "algorithmic bytes / event-timed duration",
     }
+    # the same kernels' HBM bytes as rocprofv3's FETCH_SIZE + WRITE_SIZE counters read
+    # them (copy-calibrated, from the committed summary of this source), over the
+    # durations measured here
+    prof = f"replay_and_route_kernels_{shape.name}.txt"
+    cg = {}
+    for key, kname, t_ms in (("route_predict", "router_mfma_kernel<2, 0, 0>", t_route),
+                             ("replay_gates", "router_mfma_kernel<2, 1, 0>", t_gates),
+                             ("perm_count", "perm_count_kernel", kern.get("perm_count")),
+                             ("perm_scatter", "perm_scatter_kernel", kern.get("perm_scatter")),
+                             ("combine", "combine_bf16_kernel", t_comb)):
+        b = profiled_traffic(prof, kname)
+        if b is not None and t_ms:
+            cg[key] = {"bytes": b, "gbps": b / (t_ms * 1e-3) / 1e9,
+                       "frac_of_8tbs": b / (t_ms * 1e-3) / C.PEAK_HBM_BYTES}
+    out["hbm_gbps_counters"] = cg or None
     if not args.no_cpu_baseline:
         n_tok = args.cpu_sample_tokens if args.cpu_sample_tokens > 0 else T
         out["cpu_baseline"] = cpu_baseline_forward(shape, L, min(n_tok, T))
         out["cpu_baseline_small_1thread"] = cpu_baseline_small_1thread()
     return out
+
+
+def recorded_flip_route(G, shape, seed, dev):
+    """The backward workload's recorded route: the current router's top-k (this
+    library's router, no predictor) with flip_frac of the tokens recording the
+    (k+1)-th ranked expert in place of the k-th (workloads.flip_route).  The
+    ranking of each token's k+1 ids is read off the router's fp32 logits."""
+    import numpy as np
+    import torch
+    import workloads as W
+    from paper_2606_00395_amd import binding as B
+    T, N, k = shape.T, shape.N, shape.k
+    top = torch.empty((T, k + 1), dtype=torch.int32, device=dev)
+    p = torch.empty((T, N), dtype=torch.float32, device=dev)
+    B.route_predict(G["x"], G["W_r"], G["beta"], None, None, k + 1, top, logits_out=p)
+    top_np = top.cpu().numpy().astype(np.int64)
+    lg = np.take_along_axis(p.cpu().numpy(), top_np, axis=1)
+    # best first; equal logits keep the lower id first (the ids are ascending)
+    order = np.argsort(-lg, axis=1, kind="stable")
+    ranked = np.take_along_axis(top_np, order, axis=1)
+    idx = W.flip_route(ranked, W.flip_tokens(shape, seed), k)
+    return torch.from_numpy(idx.astype(np.int32)).to(dev)
 
 
 def run_backward(args, shape, dev):
@@ -445,9 +484,7 @@ def run_backward(args, shape, dev):
     dy_np = W.upstream_grad(shape, args.seed)
     dy = up(dy_np, True)
     T, d, N, k, m = shape.T, shape.d, shape.N, shape.k, shape.m
-    idx = torch.empty((T, k), dtype=torch.int32, device=dev)
-    # the recorded route: this layer's rollout route (router + predictor)
-    B.route_predict(G["x"], G["W_r"], G["beta"], G["A"], G["B"], k, idx)
+    idx = recorded_flip_route(G, shape, args.seed, dev)
     dx = torch.empty_like(G["x"])
     dWr = torch.empty_like(G["W_r"])
     dbr = torch.empty_like(G["beta"])
@@ -462,11 +499,6 @@ def run_backward(args, shape, dev):
                               G["W_down"], dy, dx, dWr, dbr, dWg, dWu, dWd, ws=ws, stream=stream)
 
     ms, kern = timed_steps(step, args.steps, args.warmup, stream, B)
-    os.environ["PR2_NO_SIDE_STREAM"] = "1"
-    try:
-        ms_inorder, _ = timed_steps(step, args.steps, 2, stream, B)
-    finally:
-        del os.environ["PR2_NO_SIDE_STREAM"]
     flops = {"bwd_preact_gate_up": 4, "bwd_dh_swiglu": 2, "bwd_dx_gemm": 4, "bwd_wgrad_down": 2,
              "bwd_wgrad_gate_up": 4}
     unit = T * k * d * m
@@ -483,9 +515,8 @@ def run_backward(args, shape, dev):
     out["mfma_frac"] = {n: f * unit / (kern[n] * 1e-3) / C.PEAK_BF16_FLOPS
                         for n, f in flops.items() if n in kern}
     out["mfma_frac_whole_backward"] = 16 * unit / (ms * 1e-3) / C.PEAK_BF16_FLOPS
-    out["in_order"] = {"ms_per_step": ms_inorder,
-                       "note": "the router and input-gradient tail on the caller's stream after "
-                               "the weight-gradient GEMMs (PR2_NO_SIDE_STREAM=1)"}
+    out["recorded_route"] = ("the current router's top-k with the k-th ranked expert swapped for "
+                             f"the (k+1)-th on {int(round(shape.flip_frac * T))} tokens")
     if not args.no_cpu_baseline:
         idx_np = idx.cpu().numpy()
         n_tok = args.cpu_sample_tokens if args.cpu_sample_tokens > 0 else 1024
@@ -527,7 +558,8 @@ def run_decode(args, shape, dev):
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
         record_all(torch.cuda.current_stream())      # the capture stream
-    graph.replay()
+    for _ in range(3):
+        graph.replay()
     torch.cuda.synchronize()
     reps = 3
     e0.record(stream)
@@ -544,7 +576,7 @@ def run_decode(args, shape, dev):
     nseq = mb // P
     y = torch.empty((mb, shape.d), dtype=torch.bfloat16, device=dev)
     wsr = B.replay_workspace(Xseq[:mb], buf[:nseq].reshape(mb, k), G["W_r"], G["W_gate"])
-    batches = [0, 15]
+    batches = list(range(S // nseq))          # all 16 micro-batches: the whole record
 
     def step():
         for b in batches:
@@ -688,9 +720,66 @@ def run_next(args, shape, dev):
         "roofline": {"bound": "hbm", "kernel": "route_diagnostics",
                      "achieved": dbytes / (t_diag * 1e-3) / 1e9, "peak": C.PEAK_HBM_BYTES / 1e9,
                      "unit": "GB/s", "frac": dbytes / (t_diag * 1e-3) / C.PEAK_HBM_BYTES}}
+
+    # f3 fused into the replay forward: the same diagnostics from the replay-weight
+    # epilogue (pr2_moe_replay_forward_diag) against the plain replay forward,
+    # interleaved A/B rounds
+    ws_f = B.replay_workspace(x, idx, W_cur, G["W_gate"])
+    yb = torch.empty_like(x)
+    gr = torch.empty((T, k), dtype=torch.float32, device=dev)
+
+    def plain():
+        B.moe_replay_forward(x, idx, W_cur, G["beta"], G["W_gate"], G["W_up"], G["W_down"], yb,
+                             gr, ws=ws_f, stream=stream)
+
+    def fused():
+        B.moe_replay_forward_diag(x, idx, W_cur, G["beta"], G["W_gate"], G["W_up"], G["W_down"],
+                                  yb, gr, z_ref, cur, ov, kl_t, hist, ws=ws_f, stream=stream)
+    ab_ms = {"plain": [], "fused": []}
+    for _ in range(3):
+        for name, fn in (("plain", plain), ("fused", fused)):
+            ab_ms[name].append(timed_steps(fn, args.steps, 3, stream, B)[0])
+    mp = sorted(ab_ms["plain"])[1]
+    mf = sorted(ab_ms["fused"])[1]
+    out["replay_forward_fused_diagnostics"] = {
+        "ms_plain": mp, "ms_with_diagnostics": mf, "ratio": mf / mp,
+        "note": "median of 3 interleaved rounds each; the fused call also writes the current "
+                "top-k, overlap, route KL and deviation histogram"}
     if not args.no_cpu_baseline:
         n_tok = args.cpu_sample_tokens if args.cpu_sample_tokens > 0 else 4096
         out["cpu_baseline"] = cpu_baseline_rollout(shape, L, min(n_tok, T))
+    return out
+
+
+def run_extras(args, dev):
+    """The other workloads, each on its own (GPU timings only, no CPU legs): the
+    Qwen3-235B-A22B-shaped forward, the replay backward, the decode-style record
+    and replay of the whole route record, and the method's other calls."""
+    import copy
+    import torch
+    import workloads as W
+    out = {}
+    a = copy.copy(args)
+    a.no_cpu_baseline = True
+    a.light = True
+    a.steps = min(args.steps, 10)
+    a.warmup = min(args.warmup, 10)
+    legs = (("qwen3_235b_forward", run_forward, "qwen3_235b_T32768"),
+            ("qwen3_30b_backward", run_backward, "qwen3_30b_bwd_T16384"),
+            ("qwen3_30b_decode", run_decode, "qwen3_30b_decode_256x2048"),
+            ("qwen3_30b_next", run_next, "qwen3_30b_T16384"))
+    for name, fn, wl in legs:
+        b = copy.copy(a)
+        if fn is run_decode:
+            b.steps, b.warmup = 3, 1
+        rec = fn(b, W.WORKLOADS[wl], dev)
+        for key in ("n_gpus", "steps", "warmup", "higher_is_better", "scaling", "vs_baseline",
+                    "data"):
+            rec.pop(key, None)
+        out[name] = rec
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        print(f"bench: extra {name} done", file=sys.stderr, flush=True)
     return out
 
 
@@ -715,7 +804,11 @@ def main():
         del a, b
     run = {"forward": run_forward, "backward": run_backward, "decode": run_decode,
            "next": run_next}[args.mode]
-    print(json.dumps(run(args, shape, dev)))
+    rec = run(args, shape, dev)
+    if args.mode == "forward" and not args.no_extras:
+        torch.cuda.empty_cache()
+        rec["extras"] = run_extras(args, dev)
+    print(json.dumps(rec))
 
 
 if __name__ == "__main__":

@@ -18,7 +18,11 @@
  *     caller's workspace `ws` of at least pr2_workspace_bytes(desc, op) bytes (any
  *     alignment; may be NULL when that size is 0).
  *   - Calls are asynchronous on `stream` (NULL = the null stream of the current device) and
- *     run on the current HIP device.  They return once the kernels are enqueued.
+ *     run on the current HIP device.  They return once the kernels are enqueued; every
+ *     launch of a call goes on `stream` (the library owns no stream), so a call can be
+ *     captured into a HIP graph.  Global state: the per-device gfx950 check and the
+ *     workspace split records of pr2_route_predict_reuse, both host-side and guarded by
+ *     mutexes, so calls may come from several threads (each with its own workspace).
  *   - Every argument is checked on the host before any HIP call.  On an error nothing is
  *     enqueued, outputs are untouched, the status says what was wrong and pr2_last_error()
  *     (thread-local) gives a sentence naming the argument.
@@ -166,11 +170,6 @@ pr2_status pr2_route_predict_reuse(const pr2_moe_desc* desc, const void* x, cons
  * bf16 expert GEMMs use MFMA with fp32 accumulation; the SwiGLU activation is rounded to
  * act_dtype before the down projection and the weighted expert outputs are rounded to
  * act_dtype before the combine, which sums each token's k terms in slot order in fp32.
- * Streams: the replay weights are formed on a second stream that the library owns (one per
- * device, created at the first call made outside a HIP graph capture).  That stream is forked
- * from `stream` with an event and joined back before the down projection, so the work stays
- * ordered with respect to `stream` and can be captured into a HIP graph.  With the
- * environment variable PR2_NO_SIDE_STREAM=1, every launch goes on `stream`.
  */
 pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const void* idx,
                                   int64_t ldi, const float* W_r, const float* b_r,
@@ -226,10 +225,13 @@ pr2_status pr2_moe_rollout_forward(const pr2_moe_desc* desc, const void* x, cons
 /*
  * Replay backward (Sec. 4.1 "Replay During Training": the current experts and router are
  * trained through the replayed routes; Alg. 3 in Appendix D, its backward step).  Gradients
- * of L = sum_t <dy_t, y_t> for the replay forward above, with the recorded ids held fixed and
- * the renormalised weights g = softmax over the k recorded logits (renorm must be 1):
+ * of L = sum_t <dy_t, y_t> for the replay forward above, with the recorded ids held fixed:
  *
- *   dg_ts = <dy_t, E_j(x_t)>,  dp_ts = g_ts (dg_ts - sum_s' g_ts' dg_ts')   (j = idx[t, s])
+ *   dg_ts = <dy_t, E_j(x_t)>                                        (j = idx[t, s])
+ *   renorm = 1 (g = softmax over the k recorded logits):
+ *     dp_t,j = g_ts (dg_ts - sum_s' g_ts' dg_ts') at the recorded ids, 0 at the others
+ *   renorm = 0 (g_ts = rho_j of the softmax over all N logits, Eq. pr2_output as printed):
+ *     dp_t,i = rho_ti ([i recorded] dg_ti - sum_s g_ts dg_ts) for every i < N (k <= 64)
  *   dW_r = sum_t x_t^T dp_t,  db_r = sum_t dp_t
  *   dW_gate_j, dW_up_j, dW_down_j = sums over the routes through expert j of the SwiGLU
  *   expert's weight gradients, each route's output scaled by g_ts
@@ -244,15 +246,12 @@ pr2_status pr2_moe_rollout_forward(const pr2_moe_desc* desc, const void* x, cons
  *   ws       >= pr2_workspace_bytes(desc, PR2_OP_REPLAY_BWD)
  * Every gradient is overwritten (not accumulated); an expert no route uses gets zeros, and
  * T = 0 writes zeros to all weight gradients (x, idx, dy, dx, ws may then be NULL).  Results
- * are bitwise deterministic.  renorm = 0 returns PR2_ERR_UNSUPPORTED.  The pre-activations
+ * are bitwise deterministic.  With renorm = 0 the router gradients are dense over N (fp32
+ * FMA passes over x and the [T, N] logit gradient) and k > 64 returns PR2_ERR_UNSUPPORTED.
+ * The pre-activations
  * are recomputed (nothing is saved from the forward call); on the bf16 MFMA path
  * (d % 256 == 0, m % 256 == 0) a, u, their gradients, g H and the per-route input gradients
  * are held in bf16, with fp32 accumulation everywhere.
- * Streams: the replay weights (beside the permutation and the pre-activation GEMM) and, on
- * the MFMA path, the router weight gradient and the combine of the input gradient (beside
- * the expert weight-gradient GEMMs) run on the library's side stream.  The
- * side stream is forked from `stream` and joined back before the call's last launch, the
- * same stream and rules as pr2_moe_replay_forward.
  */
 pr2_status pr2_moe_replay_backward(const pr2_moe_desc* desc, const void* x, const void* idx,
                                    int64_t ldi, const float* W_r, const float* b_r,

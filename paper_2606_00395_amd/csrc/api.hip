@@ -79,50 +79,6 @@ pr2_status device_ready() {
     return PR2_OK;
 }
 
-// ------------------------------------------------------ side stream ----
-// A second stream per device for work that can run beside the caller's: it
-// is forked from the caller's stream and joined back with events, so the
-// caller's ordering (and HIP graph capture, which follows such event edges)
-// is kept.  Created once per device, outside any capture, and kept for the
-// life of the process; g_side_mu is held from a call's fork to its join wait
-// so that calls from several threads cannot interleave the two events.
-struct SideStream {
-    hipStream_t s = nullptr;
-    hipEvent_t fork = nullptr, join = nullptr, mid = nullptr;
-};
-static std::mutex g_side_mu;
-
-static SideStream* side_stream_for(hipStream_t st) {      // caller holds g_side_mu
-    static std::map<int, SideStream> per_dev;
-    const char* off = getenv("PR2_NO_SIDE_STREAM");
-    if (off && off[0] == '1') return nullptr;
-    int dev = -1;
-    if (hipGetDevice(&dev) != hipSuccess) {
-        (void)hipGetLastError();
-        return nullptr;
-    }
-    auto it = per_dev.find(dev);
-    if (it != per_dev.end()) return &it->second;
-    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-    if (hipStreamIsCapturing(st, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) {
-        (void)hipGetLastError();
-        return nullptr;                 // not created during a capture: run in order
-    }
-    SideStream ss;
-    if (hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking) != hipSuccess ||
-        hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&ss.join, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&ss.mid, hipEventDisableTiming) != hipSuccess) {
-        (void)hipGetLastError();
-        if (ss.mid) (void)hipEventDestroy(ss.mid);
-        if (ss.join) (void)hipEventDestroy(ss.join);
-        if (ss.fork) (void)hipEventDestroy(ss.fork);
-        if (ss.s) (void)hipStreamDestroy(ss.s);
-        return nullptr;
-    }
-    return &per_dev.emplace(dev, ss).first->second;
-}
-
 // ------------------------------------------------ weight-split records ----
 // pr2_route_predict_reuse reads the bf16 split of the router (and predictor)
 // weights that an earlier route call left in the same workspace.  Each route
@@ -252,6 +208,14 @@ BwdWs bwd_ws_layout(const pr2_moe_desc& d, void* base) {
     b.order = (int*)take(sizeof(int) * (size_t)d.N);
     b.rwpart = (float*)take(sizeof(float) * (size_t)b.fw.max_tiles * d.d);
     b.rbpart = (float*)take(sizeof(float) * (size_t)b.fw.max_tiles);
+    b.nchunk = 0;
+    if (d.renorm == 0) {
+        b.nchunk = (int)((d.T + 1023) / 1024);
+        b.plog = (float*)take(sizeof(float) * (size_t)d.T * d.N);
+        b.dpf = (float*)take(sizeof(float) * (size_t)d.T * d.N);
+        b.lwpart = (float*)take(sizeof(float) * (size_t)b.nchunk * d.d * d.N);
+        b.lbpart = (float*)take(sizeof(float) * (size_t)b.nchunk * d.N);
+    }
     b.bytes = off + 256;
     return b;
 }
@@ -561,40 +525,12 @@ static pr2_status replay_forward_impl(const pr2_moe_desc* desc, const void* x, c
         if (e != hipSuccess) return hip_fail(e, "error-word reset");
     }
     float* gate = gate_out ? gate_out : w.gate;
-    {
-        // Only the down projection reads the replay gates: they are formed on
-        // the side stream beside the permutation and the gate/up GEMM, and the
-        // caller's stream waits for them before GEMM 2.
-        std::lock_guard<std::mutex> side_lk(g_side_mu);
-        SideStream* side = side_stream_for(st);
-        hipStream_t gst = st;
-        if (side) {
-            e = hipEventRecord(side->fork, st);
-            if (e == hipSuccess) e = hipStreamWaitEvent(side->s, side->fork, 0);
-            if (e != hipSuccess) return hip_fail(e, "side stream fork");
-            gst = side->s;
-        }
-        e = launch_replay_gates(d, x, idx, ldi, W_r, b_r, gate, w.err, w.wsplit, gst, diag);
-        hipEvent_t gates_done = nullptr;
-        if (side) {
-            // joined even when the launch failed, so no forked work is left behind
-            hipError_t ej = hipEventRecord(side->join, side->s);
-            if (ej == hipSuccess) gates_done = side->join;
-            if (e == hipSuccess) e = ej;
-            if (e != hipSuccess && gates_done) (void)hipStreamWaitEvent(st, gates_done, 0);
-        }
-        if (e != hipSuccess) return hip_fail(e, "replay_gates launch");
-        e = launch_permute(d, idx, ldi, w, st);
-        if (e != hipSuccess) {
-            if (gates_done) (void)hipStreamWaitEvent(st, gates_done, 0);
-            return hip_fail(e, "permute launch");
-        }
-        e = launch_expert_gemms(d, x, W_gate, W_up, W_down, gate, w, st, gates_done);
-        if (e != hipSuccess) {
-            if (gates_done) (void)hipStreamWaitEvent(st, gates_done, 0);
-            return hip_fail(e, "expert GEMM launch");
-        }
-    }
+    e = launch_replay_gates(d, x, idx, ldi, W_r, b_r, gate, w.err, w.wsplit, st, diag);
+    if (e != hipSuccess) return hip_fail(e, "replay_gates launch");
+    e = launch_permute(d, idx, ldi, w, st);
+    if (e != hipSuccess) return hip_fail(e, "permute launch");
+    e = launch_expert_gemms(d, x, W_gate, W_up, W_down, gate, w, st);
+    if (e != hipSuccess) return hip_fail(e, "expert GEMM launch");
     e = launch_combine(d, w, y, st);
     if (e != hipSuccess) return hip_fail(e, "combine launch");
     if (validate) {
@@ -630,7 +566,7 @@ pr2_status pr2_moe_replay_forward_diag(const pr2_moe_desc* desc, const void* x, 
     s = check_diag_outputs(*desc, z_ref, cur_idx_out, overlap_out, kl_out, hist_out);
     if (s != PR2_OK) return s;
     const RouteDiag diag{kl_out ? z_ref : nullptr, cur_idx_out, overlap_out, kl_out,
-                         (unsigned long long*)hist_out};
+                         (unsigned long long*)hist_out, nullptr};
     const bool any = cur_idx_out || overlap_out || kl_out || hist_out;
     return replay_forward_impl(desc, x, idx, ldi, W_r, b_r, W_gate, W_up, W_down, y, gate_out,
                                any ? &diag : nullptr, ws, ws_bytes, stream);
@@ -696,8 +632,8 @@ pr2_status pr2_moe_replay_backward(const pr2_moe_desc* desc, const void* x, cons
     pr2_status s = check_desc(desc, true, true);
     if (s != PR2_OK) return s;
     const pr2_moe_desc& d = *desc;
-    if (d.renorm != 1)
-        return fail(PR2_ERR_UNSUPPORTED, "the backward pass needs renorm = 1 (renormalised weights)");
+    if (d.renorm == 0 && d.k > 64)
+        return fail(PR2_ERR_UNSUPPORTED, "the paper-literal backward (renorm = 0) needs k <= 64");
     if (ldi < d.k) return fail(PR2_ERR_SHAPE, "ldi = %lld < k = %d", (long long)ldi, d.k);
     if (!W_r) return fail(PR2_ERR_NULL, "W_r is NULL");
     if (!W_gate || !W_up || !W_down) return fail(PR2_ERR_NULL, "an expert weight pointer is NULL");
@@ -744,37 +680,15 @@ pr2_status pr2_moe_replay_backward(const pr2_moe_desc* desc, const void* x, cons
         e = launch_zero_i32(w.fw.err, ERR_WORDS, st);
         if (e != hipSuccess) return hip_fail(e, "error-word reset");
     }
-    {
-        // On the side stream: the replay weights beside the permutation and the
-        // pre-activation GEMM (the dh kernel waits for them), then the router and
-        // input-gradient tail beside the expert weight-gradient GEMMs (forked and
-        // joined inside the backward launch).
-        std::lock_guard<std::mutex> side_lk(g_side_mu);
-        SideStream* side = side_stream_for(st);
-        hipStream_t gst = st;
-        if (side) {
-            e = hipEventRecord(side->fork, st);
-            if (e == hipSuccess) e = hipStreamWaitEvent(side->s, side->fork, 0);
-            if (e != hipSuccess) return hip_fail(e, "side stream fork");
-            gst = side->s;
-        }
-        e = launch_replay_gates(d, x, idx, ldi, W_r, b_r, w.fw.gate, w.fw.err, w.fw.wsplit, gst);
-        hipEvent_t gates_done = nullptr;
-        if (side) {
-            const hipError_t ej = hipEventRecord(side->mid, side->s);
-            if (ej == hipSuccess) gates_done = side->mid;
-            if (e == hipSuccess) e = ej;
-        }
-        if (e == hipSuccess) e = launch_permute(d, idx, ldi, w.fw, st);
-        if (e != hipSuccess) {
-            if (gates_done) (void)hipStreamWaitEvent(st, gates_done, 0);
-            return hip_fail(e, "replay_gates / permute launch");
-        }
-        e = launch_replay_backward(d, x, idx, ldi, W_r, W_gate, W_up, W_down, dy, w.fw.gate, w,
-                                   out, st, side ? side->s : nullptr, side ? side->fork : nullptr,
-                                   side ? side->join : nullptr, gates_done);
-        if (e != hipSuccess && gates_done) (void)hipStreamWaitEvent(st, gates_done, 0);
-    }
+    // the paper-literal weights also need every token's N logits
+    RouteDiag logits{};
+    logits.p_out = w.plog;
+    e = launch_replay_gates(d, x, idx, ldi, W_r, b_r, w.fw.gate, w.fw.err, w.fw.wsplit, st,
+                            d.renorm == 0 ? &logits : nullptr);
+    if (e == hipSuccess) e = launch_permute(d, idx, ldi, w.fw, st);
+    if (e != hipSuccess) return hip_fail(e, "replay_gates / permute launch");
+    e = launch_replay_backward(d, x, idx, ldi, W_r, W_gate, W_up, W_down, dy, w.fw.gate, w, out,
+                               st);
     if (e != hipSuccess) return hip_fail(e, "backward launch");
     if (validate) {
         int errs[ERR_WORDS];

@@ -2,7 +2,8 @@
 // recorded ids held fixed (Sec. 4.1, replay during training: the experts and
 // the current router receive gradients through the replayed set; the
 // predictor is bypassed and receives none).  Weights are the renormalised
-// replay weights g = softmax of the k recorded logits.
+// replay weights g = softmax of the k recorded logits, or (renorm = 0) the
+// paper-literal rho_j of the softmax over all N logits (Eq. pr2_output).
 //
 // Per route (token t, slot s, expert e, permuted row q), with X = x_t:
 //   a = X W_gate_e^T, u = X W_up_e^T, H = silu(a) * u       (recomputed)
@@ -931,6 +932,180 @@ dx_combine_bf16_kernel(const bf16_t* dxr, const int* inv, const float* dp_route,
     }
 }
 
+// ---------------------------------------------- paper-literal weights ----
+// With the weight of id j equal to rho_j, the softmax of all N current logits
+// (Eq. pr2_output as printed), every logit of a token receives a gradient:
+//   dp_ti = rho_ti ([i in route] dg_ti - sum_{j in route} rho_tj dg_tj),
+// that is g_s (dg_s - inner) at the route's ids and -rho_i inner elsewhere,
+// with inner = sum_s g_s dg_s.  The router gradients become dense over N:
+//   dW_r = x^T dp,  db_r = sum_t dp_t,  and dx_t gains dp_t W_r^T.
+
+// One wavefront per token (k <= 64): dg_s = the sum of its partials, inner in
+// slot order (as the renormalised kernel forms it), rho from the fp32 logits
+// p (max-shifted, fp32, as the forward's weights), the row dpf[t, :] written
+// once.  Out-of-range ids (inv = -1) contribute nothing.
+__global__ void __launch_bounds__(256)
+literal_dp_kernel(const float* dgp, int np, const int* inv, const float* gate, const float* p,
+                  const void* idx, int idx_dtype, int64_t ldi, int64_t T, int k, int N,
+                  float* dpf) {
+    const int lane = threadIdx.x & 63;
+    const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (t >= T) return;                        // uniform across the wavefront
+    float dg = 0.0f, gs = 0.0f;
+    int id = -1;
+    if (lane < k) {
+        const int q = inv[t * k + lane];
+        gs = gate[t * k + lane];
+        if (q >= 0) {
+            for (int pp = 0; pp < np; ++pp) dg += dgp[(int64_t)q * np + pp];
+            id = load_id(idx, idx_dtype, t * ldi + lane);
+        }
+    }
+    float inner = 0.0f;
+    for (int j = 0; j < k; ++j) inner = fmaf(__shfl(gs, j, 64), __shfl(dg, j, 64), inner);
+    const float on_route = gs * (dg - inner);
+    const float* pr = p + t * N;
+    float mx = -INFINITY;
+    for (int i = lane; i < N; i += 64) mx = fmaxf(mx, pr[i]);
+    for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+    float sum = 0.0f;
+    for (int i = lane; i < N; i += 64) sum += expf(pr[i] - mx);
+    for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, 64);
+    for (int i0 = 0; i0 < N; i0 += 64) {
+        const int i = i0 + lane;
+        float v = i < N ? -(expf(pr[i] - mx) / sum) * inner : 0.0f;
+        for (int j = 0; j < k; ++j) {
+            const int idj = __shfl(id, j, 64);
+            const float vj = __shfl(on_route, j, 64);
+            if (idj == i) v = vj;
+        }
+        if (i < N) dpf[t * N + i] = v;
+    }
+}
+
+constexpr int kLitTok = 1024;      // tokens per dW_r partial
+constexpr int kLitTile = 64;       // dW_r partial tile: 64 rows of d x 64 logits
+
+// part[c][i][j] = sum over the tokens of chunk c (in order) of x[t][i] dpf[t][j];
+// dbpart[c][j] the same of dpf[t][j] (workgroups of the first row block).
+template <typename T>
+__global__ void __launch_bounds__(256)
+literal_wgrad_partial_kernel(const T* x, const float* dpf, int64_t Ttot, int d, int N,
+                             float* part, float* dbpart) {
+    __shared__ float xs[32][kLitTile + 1];
+    __shared__ float ps[32][kLitTile + 1];
+    const int i0 = blockIdx.x * kLitTile, j0 = blockIdx.y * kLitTile;
+    const int64_t c = blockIdx.z;
+    const int64_t t0 = c * kLitTok;
+    const int64_t t1 = t0 + kLitTok < Ttot ? t0 + kLitTok : Ttot;
+    const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+    float acc[4][4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[u][v] = 0.0f;
+    float db = 0.0f;
+    for (int64_t tb = t0; tb < t1; tb += 32) {
+        for (int e = threadIdx.x; e < 32 * kLitTile; e += 256) {
+            const int r = e / kLitTile, q = e % kLitTile;
+            const int64_t t = tb + r;
+            xs[r][q] = (t < t1 && i0 + q < d) ? Act<T>::to_f32(x[t * d + i0 + q]) : 0.0f;
+            ps[r][q] = (t < t1 && j0 + q < N) ? dpf[t * N + j0 + q] : 0.0f;
+        }
+        __syncthreads();
+#pragma unroll 4
+        for (int r = 0; r < 32; ++r) {
+            float a[4], b[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                a[u] = xs[r][ty * 4 + u];
+                b[u] = ps[r][tx * 4 + u];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) acc[u][v] = fmaf(a[u], b[v], acc[u][v]);
+        }
+        if (blockIdx.x == 0 && threadIdx.x < kLitTile)
+            for (int r = 0; r < 32; ++r) db += ps[r][threadIdx.x];
+        __syncthreads();
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int i = i0 + ty * 4 + u;
+        if (i >= d) continue;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int j = j0 + tx * 4 + v;
+            if (j < N) part[(c * d + i) * N + j] = acc[u][v];
+        }
+    }
+    if (blockIdx.x == 0 && threadIdx.x < kLitTile && j0 + (int)threadIdx.x < N)
+        dbpart[c * N + j0 + threadIdx.x] = db;
+}
+
+// dW_r[q] and db_r[j]: the chunk partials added in chunk order
+__global__ void __launch_bounds__(256)
+literal_wgrad_reduce_kernel(const float* part, const float* dbpart, int nchunk, int64_t n, int N,
+                            float* dW_r, float* db_r) {
+    for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < n;
+         q += (int64_t)gridDim.x * 256) {
+        float s = 0.0f;
+        for (int c = 0; c < nchunk; ++c) s += part[(int64_t)c * n + q];
+        dW_r[q] = s;
+        if (db_r && q < N) {
+            float b = 0.0f;
+            for (int c = 0; c < nchunk; ++c) b += dbpart[(int64_t)c * N + q];
+            db_r[q] = b;
+        }
+    }
+}
+
+// dx_t = sum_s dxr[route (t, s)] (slot order) + sum_i dpf[t, i] W_r[:, i]
+// (in logit order), fp32: one column per thread, 16 tokens per workgroup.
+constexpr int kLitDxTok = 16;
+template <typename T>
+__global__ void __launch_bounds__(256)
+literal_dx_combine_kernel(const T* dxr, const int* inv, const float* dpf, const float* W_r,
+                          int64_t Ttot, int k, int d, int N, T* dx) {
+    __shared__ float ps[kLitDxTok][64];
+    const int c = blockIdx.x * 256 + threadIdx.x;
+    const int64_t t0 = (int64_t)blockIdx.y * kLitDxTok;
+    float racc[kLitDxTok];
+#pragma unroll
+    for (int r = 0; r < kLitDxTok; ++r) racc[r] = 0.0f;
+    for (int j0 = 0; j0 < N; j0 += 64) {
+        for (int e = threadIdx.x; e < kLitDxTok * 64; e += 256) {
+            const int r = e / 64, q = e % 64;
+            const int64_t t = t0 + r;
+            ps[r][q] = (t < Ttot && j0 + q < N) ? dpf[t * N + j0 + q] : 0.0f;
+        }
+        __syncthreads();
+        if (c < d) {
+            const float* wrow = W_r + (int64_t)c * N + j0;
+            const int jn = N - j0 < 64 ? N - j0 : 64;
+            for (int q = 0; q < jn; ++q) {
+                const float w = wrow[q];
+#pragma unroll
+                for (int r = 0; r < kLitDxTok; ++r) racc[r] = fmaf(ps[r][q], w, racc[r]);
+            }
+        }
+        __syncthreads();
+    }
+    if (c >= d) return;
+#pragma unroll
+    for (int r = 0; r < kLitDxTok; ++r) {
+        const int64_t t = t0 + r;
+        if (t >= Ttot) break;
+        float acc = 0.0f;
+        for (int s = 0; s < k; ++s) {
+            const int q = inv[t * k + s];
+            if (q >= 0) acc += Act<T>::to_f32(dxr[(int64_t)q * d + c]);
+        }
+        dx[t * d + c] = Act<T>::from_f32(acc + racc[r]);
+    }
+}
+
 __global__ void __launch_bounds__(256) fill_zero_kernel(float* p, int64_t n) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
          i += (int64_t)gridDim.x * blockDim.x)
@@ -1002,8 +1177,7 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
                                   int64_t ldi, const float* W_r, const void* W_gate,
                                   const void* W_up, const void* W_down, const void* dy,
                                   const float* gate, const BwdWs& ws, const BwdGrads& out,
-                                  hipStream_t s, hipStream_t side, hipEvent_t fork,
-                                  hipEvent_t join, hipEvent_t gates_ready) {
+                                  hipStream_t s) {
     const ReplayWs& w = ws.fw;
     const bool bf = d.act_dtype == PR2_BF16;
     const bool mfma = bwd_mfma_ok(d);
@@ -1040,9 +1214,6 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
     };
 
     // gate gradient partials and the SwiGLU backward
-    // the dh kernel reads the replay weights: when they come from another
-    // stream, wait for them here
-    if (gates_ready && (e = hipStreamWaitEvent(s, gates_ready, 0)) != hipSuccess) return e;
     if (mfma) {
         g.ntn = d.m / BN;
         LaunchScope scope("bwd_dh_swiglu", s);
@@ -1062,7 +1233,13 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // router-logit gradients (needed by the router weight gradient below)
-    {
+    const bool literal = d.renorm == 0;
+    if (literal) {
+        LaunchScope scope("bwd_gate_grad_literal", s);
+        hipLaunchKernelGGL(literal_dp_kernel, dim3((unsigned)((d.T + 3) / 4)), dim3(256), 0, s,
+                           ws.dgp, ws.np, w.inv, gate, ws.plog, idx, d.idx_dtype, ldi, d.T, d.k,
+                           d.N, ws.dpf);
+    } else {
         LaunchScope scope("bwd_gate_grad", s);
         int kp_log2 = 0;
         while ((1 << kp_log2) < d.k) ++kp_log2;
@@ -1078,11 +1255,43 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
-    // The router weight gradient and the input gradient's combine read neither
-    // the outputs of the expert weight-gradient GEMMs nor write their inputs:
-    // with a side stream they run on it, beside those GEMMs.
+    // the router weight gradient and the combine of the input gradient
     auto tail = [&](hipStream_t ts) -> hipError_t {
         hipError_t e = hipSuccess;
+        if (literal) {
+            // dense over all N logits
+            {
+                LaunchScope scope("bwd_router_wgrad_literal", ts);
+                dim3 grid((unsigned)((d.d + kLitTile - 1) / kLitTile),
+                          (unsigned)((d.N + kLitTile - 1) / kLitTile), (unsigned)ws.nchunk);
+                if (bf)
+                    hipLaunchKernelGGL(literal_wgrad_partial_kernel<bf16_t>, grid, dim3(256), 0, ts,
+                                       (const bf16_t*)x, ws.dpf, d.T, d.d, d.N, ws.lwpart,
+                                       ws.lbpart);
+                else
+                    hipLaunchKernelGGL(literal_wgrad_partial_kernel<float>, grid, dim3(256), 0, ts,
+                                       (const float*)x, ws.dpf, d.T, d.d, d.N, ws.lwpart,
+                                       ws.lbpart);
+                if ((e = hipGetLastError()) != hipSuccess) return e;
+                const int64_t n = (int64_t)d.d * d.N;
+                int64_t blocks = (n + 255) / 256;
+                if (blocks > 4096) blocks = 4096;
+                hipLaunchKernelGGL(literal_wgrad_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0,
+                                   ts, ws.lwpart, ws.lbpart, ws.nchunk, n, d.N, out.dW_r, out.db_r);
+                if ((e = hipGetLastError()) != hipSuccess) return e;
+            }
+            LaunchScope scope("bwd_dx_combine_literal", ts);
+            dim3 grid((unsigned)((d.d + 255) / 256), (unsigned)((d.T + kLitDxTok - 1) / kLitDxTok));
+            if (bf)
+                hipLaunchKernelGGL(literal_dx_combine_kernel<bf16_t>, grid, dim3(256), 0, ts,
+                                   (const bf16_t*)w.O, w.inv, ws.dpf, W_r, d.T, d.k, d.d, d.N,
+                                   (bf16_t*)out.dx);
+            else
+                hipLaunchKernelGGL(literal_dx_combine_kernel<float>, grid, dim3(256), 0, ts,
+                                   (const float*)w.O, w.inv, ws.dpf, W_r, d.T, d.k, d.d, d.N,
+                                   (float*)out.dx);
+            return hipGetLastError();
+        }
         {
             LaunchScope scope("bwd_router_wgrad", ts);
             dim3 grid((unsigned)w.max_tiles, (unsigned)((d.d + 255) / 256));
@@ -1140,18 +1349,6 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
             hipLaunchKernelGGL(bwd_gemm<DX>, grid_for(w.max_tiles * g.ntn), dim3(kThreads), 0, s, g);
         }
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        if (side) {
-            if ((e = hipEventRecord(fork, s)) != hipSuccess) return e;
-            if ((e = hipStreamWaitEvent(side, fork, 0)) != hipSuccess) return e;
-            e = tail(side);
-            const hipError_t ej = hipEventRecord(join, side);
-            if (e == hipSuccess) e = ej;
-            if (e != hipSuccess) {
-                // joined even when a launch failed, so no forked work is left behind
-                if (ej == hipSuccess) (void)hipStreamWaitEvent(s, join, 0);
-                return e;
-            }
-        }
         const int64_t experts_per_xcd = (d.N + kNumXcd - 1) / kNumXcd;
         {
             LaunchScope scope("bwd_wgrad_down", s);
@@ -1159,23 +1356,14 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
                                dim3((unsigned)(kNumXcd * experts_per_xcd * (d.d / BM) * (d.m / BN))),
                                dim3(kThreads), 0, s, g);
         }
-        if ((e = hipGetLastError()) != hipSuccess) {
-            if (side) (void)hipStreamWaitEvent(s, join, 0);
-            return e;
-        }
+        if ((e = hipGetLastError()) != hipSuccess) return e;
         {
             LaunchScope scope("bwd_wgrad_gate_up", s);
             hipLaunchKernelGGL(bwd_gemm<WGU>,
                                dim3((unsigned)(kNumXcd * experts_per_xcd * (2 * d.m / BM) * (d.d / BN))),
                                dim3(kThreads), 0, s, g);
         }
-        e = hipGetLastError();
-        // the caller's stream takes the side stream's work back (also after an error)
-        if (side) {
-            const hipError_t ew = hipStreamWaitEvent(s, join, 0);
-            return e != hipSuccess ? e : ew;
-        }
-        if (e != hipSuccess) return e;
+        if ((e = hipGetLastError()) != hipSuccess) return e;
         return tail(s);
     }
     e = bf ? launch_generic_gemms<bf16_t>(d, x, W_gate, W_up, dy, ws, out, s)

@@ -86,6 +86,12 @@ struct BwdWs {
     int* order;         // [N] experts by decreasing route count
     float* rwpart;      // [max_tiles, d] router weight-gradient partials per 256-row tile
     float* rbpart;      // [max_tiles] router bias-gradient partials
+    // paper-literal weights (renorm = 0) only: the router gradient is dense over N
+    float* plog;        // [T, N] current router logits
+    float* dpf;         // [T, N] router-logit gradient
+    float* lwpart;      // [nchunk, d, N] dW_r partials per chunk of 1024 tokens
+    float* lbpart;      // [nchunk, N] db_r partials
+    int nchunk;
     int np;
     size_t bytes;
 };
@@ -152,6 +158,7 @@ struct RouteDiag {
     int* overlap;               // [T]
     float* kl;                  // [T]
     unsigned long long* hist;   // [k + 1], zeroed by the launch
+    float* p_out;               // [T, N] the current logits p
 };
 hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void* idx, int64_t ldi,
                                const float* W_r, const float* b_r, float* gate_out, int* err,
@@ -172,7 +179,7 @@ hipError_t launch_zero_i32(int* p, int n, hipStream_t s);
 // gemm.hip
 hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void* W_gate,
                                const void* W_up, const void* W_down, const float* gate,
-                               const ReplayWs& ws, hipStream_t s, hipEvent_t before_gemm2 = nullptr);
+                               const ReplayWs& ws, hipStream_t s);
 bool mfma_shape_ok(const pr2_moe_desc& d);
 hipError_t launch_preact(const pr2_moe_desc& d, const void* x, const void* W_gate,
                          const void* W_up, const ReplayWs& ws, void* AU, hipStream_t s);
@@ -212,9 +219,7 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
                                   int64_t ldi, const float* W_r, const void* W_gate,
                                   const void* W_up, const void* W_down, const void* dy,
                                   const float* gate, const BwdWs& ws, const BwdGrads& out,
-                                  hipStream_t s,
-                                  hipStream_t side = nullptr, hipEvent_t fork = nullptr,
-                                  hipEvent_t join = nullptr, hipEvent_t gates_ready = nullptr);
+                                  hipStream_t s);
 hipError_t launch_zero_grads(const pr2_moe_desc& d, const BwdGrads& out, hipStream_t s);
 
 }  // namespace pr2

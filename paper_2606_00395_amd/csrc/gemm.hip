@@ -489,11 +489,7 @@ bool mfma_shape_ok(const pr2_moe_desc& d) {
 
 hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void* W_gate,
                                const void* W_up, const void* W_down, const float* gate,
-                               const ReplayWs& ws, hipStream_t s, hipEvent_t before_gemm2) {
-    // GEMM 2 reads the gates: when they come from another stream, wait here
-    auto wait_gates = [&]() {
-        return before_gemm2 ? hipStreamWaitEvent(s, before_gemm2, 0) : hipSuccess;
-    };
+                               const ReplayWs& ws, hipStream_t s) {
     if (mfma_shape_ok(d)) {
         MfmaArgs g1{};
         g1.A = (const bf16_t*)x;
@@ -531,7 +527,6 @@ hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void*
         g2.group = kGroupGemm2;
         work = ws.max_tiles * g2.ntn;
         grid = ((work + kNumXcd - 1) / kNumXcd) * kNumXcd;
-        if ((e = wait_gates()) != hipSuccess) return e;
         {
             LaunchScope scope("gemm2_down_scale", s);
             hipLaunchKernelGGL(grouped_gemm_mfma<1>, dim3((unsigned)grid), dim3(kGemmThreads), 0,
@@ -551,7 +546,6 @@ hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void*
         }
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        if ((e = wait_gates()) != hipSuccess) return e;
         LaunchScope scope("gemm2_generic", s);
         hipLaunchKernelGGL(gemm2_generic<bf16_t>, grid2, dim3(256), 0, s, (const bf16_t*)ws.H,
                            ws.perm_src, gate, (const bf16_t*)W_down, d.d, d.m, ws.tiles,
@@ -565,7 +559,6 @@ hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void*
         }
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        if ((e = wait_gates()) != hipSuccess) return e;
         LaunchScope scope("gemm2_generic", s);
         hipLaunchKernelGGL(gemm2_generic<float>, grid2, dim3(256), 0, s, (const float*)ws.H,
                            ws.perm_src, gate, (const float*)W_down, d.d, d.m, ws.tiles,

@@ -1326,7 +1326,8 @@ hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void*
     DiagOut g{};
     if (diag) {
         // the diagnostics epilogue runs on the same logits, before the weights
-        g = DiagOut{diag->z_ref, diag->cur_idx, diag->overlap, diag->kl, diag->hist, nullptr};
+        g = DiagOut{diag->z_ref, diag->cur_idx, diag->overlap, diag->kl, diag->hist,
+                    diag->p_out};
         if (diag->hist) {
             LaunchScope scope("replay_diagnostics_zero", s);
             hipLaunchKernelGGL(zero_u64_kernel, dim3(1), dim3(64), 0, s, diag->hist, d.k + 1);

@@ -173,8 +173,15 @@ def test_backward_rejects_bad_arguments():
     assert B.STATUS[backward(d, dWd=FAKE + 4)[0]] == "PR2_ERR_ALIGN"
     assert B.STATUS[backward(d, db=FAKE + 2)[0]] == "PR2_ERR_ALIGN"
     assert B.STATUS[backward(d, ldi=1)[0]] == "PR2_ERR_SHAPE"
+    # the paper-literal weights: accepted for k <= 64 (this host has no GPU), refused above
     st, msg = backward(desc(renorm=False))
-    assert B.STATUS[st] == "PR2_ERR_UNSUPPORTED" and "renorm" in msg
+    assert B.STATUS[st] in ("PR2_ERR_DEVICE", "PR2_OK"), msg
+    dk = desc(renorm=False, N=128, k=65)
+    st, msg = backward(dk)
+    assert B.STATUS[st] == "PR2_ERR_UNSUPPORTED" and "k <= 64" in msg
+    # its workspace holds the dense logits and logit gradients too
+    assert B.workspace_bytes(desc(renorm=False), B.OP_REPLAY_BWD) > \
+        B.workspace_bytes(desc(), B.OP_REPLAY_BWD)
     # T = 0 still has weight gradients to zero: those pointers stay required
     st, _ = backward(desc(T=0), x=0, idx=0, dy=0, dx=0, ws=0, ws_bytes=0, dWg=0)
     assert B.STATUS[st] == "PR2_ERR_NULL"

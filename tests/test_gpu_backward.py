@@ -39,7 +39,7 @@ def recorded_route(L, shape, seed):
     return W.flip_route(ranked, W.flip_tokens(shape, seed), k)
 
 
-def run_bwd(L, idx, dy, act, idx_dtype="int32", ldi_pad=0, ws=None):
+def run_bwd(L, idx, dy, act, idx_dtype="int32", ldi_pad=0, ws=None, renorm=True):
     import torch
     from paper_2606_00395_amd import binding as B
     x = to_dev(L["x"], act)
@@ -59,7 +59,7 @@ def run_bwd(L, idx, dy, act, idx_dtype="int32", ldi_pad=0, ws=None):
     dWu = torch.full(Wu.shape, nan, device="cuda")
     dWd = torch.full(Wd.shape, nan, device="cuda")
     B.moe_replay_backward(x, buf[:, :k], Wr, br, Wg, Wu, Wd, dyd, dx, dWr, dbr, dWg, dWu, dWd,
-                          ws=ws)
+                          ws=ws, renorm=renorm)
     torch.cuda.synchronize()
     out = {"dx": dx.float().cpu().numpy(), "dW_r": dWr.cpu().numpy(), "dbeta": dbr.cpu().numpy(),
            "dW_gate": dWg.cpu().numpy(), "dW_up": dWu.cpu().numpy(), "dW_down": dWd.cpu().numpy()}
@@ -84,9 +84,9 @@ def compare(g, ref, act, where, names=GRADS):
     assert not bad, f"{where}: Frobenius ratios over {TOL[act]}: {bad}"
 
 
-def oracle_bwd(L, idx, dy):
+def oracle_bwd(L, idx, dy, renorm=True):
     return O.replay_backward(L["x"], idx, L["W_r"], L["beta"], L["W_gate"], L["W_up"],
-                             L["W_down"], dy, renorm=True)
+                             L["W_down"], dy, renorm=renorm)
 
 
 def test_backward_tiny_fp32():
@@ -166,20 +166,9 @@ def frob_rows(g, ref):
     return num, den
 
 
-def test_backward_qwen3_30b_full():
-    """The full Qwen3-30B-A3B-shaped backward workload: 16384 tokens, 5 % of them
-    (819) recording the (k+1)-th ranked expert instead of the k-th.  Every
-    expert's dW_gate / dW_up / dW_down slice, every dW_r column and every dx row
-    is held to the 2e-2 relative bar (exact zeros where the oracle has none);
-    a second run is bitwise identical."""
-    s = W.WORKLOADS["qwen3_30b_bwd_T16384"]
-    L = W.layer_inputs(s, 0)
-    idx = recorded_route(L, s, 0)
-    assert (O.route_overlap(idx, O.topk_ids(O.router_logits(L["x"], L["W_r"], L["beta"]), s.k))
-            < s.k).sum() == 819
-    dy = W.upstream_grad(s, 0)
-    g = run_bwd(L, idx, dy, "bf16")
-    ref = oracle_bwd(L, idx, dy)
+def check_full(g, ref, where):
+    """Every expert slice of the expert-weight gradients, every dW_r column and
+    every dx row within the bar; zero exactly where the oracle is zero."""
     tol = TOL["bf16"]
     report = {}
     for n, axis_name in (("dW_gate", "expert"), ("dW_up", "expert"), ("dW_down", "expert"),
@@ -190,19 +179,71 @@ def test_backward_qwen3_30b_full():
         rel = num[~zero] / den[~zero]
         worst = int(np.flatnonzero(~zero)[np.argmax(rel)])
         report[n] = (rel.max(), worst)
-        assert rel.max() <= tol, f"{n}: {axis_name} {worst} rel err {rel.max():.3e} > {tol}"
+        assert rel.max() <= tol, f"{where} {n}: {axis_name} {worst} rel err {rel.max():.3e} > {tol}"
     num, den = frob_rows(g["dW_r"].T, ref["dW_r"].T)           # per expert column
     zero = den == 0
     assert np.all(num[zero] == 0)
     rel = num[~zero] / den[~zero]
     report["dW_r"] = (rel.max(), int(np.flatnonzero(~zero)[np.argmax(rel)]))
-    assert rel.max() <= tol, f"dW_r: column rel err {rel.max():.3e}"
+    assert rel.max() <= tol, f"{where} dW_r: column rel err {rel.max():.3e}"
     e_db = frob(g["dbeta"], ref["dbeta"])
-    assert e_db <= tol, f"dbeta: Frobenius ratio {e_db:.3e}"
-    print(f"\n{s.name}: worst per-slice / per-row / per-column rel err " +
+    assert e_db <= tol, f"{where} dbeta: Frobenius ratio {e_db:.3e}"
+    print(f"\n{where}: worst per-slice / per-row / per-column rel err " +
           ", ".join(f"{n} {v[0]:.2e} (at {v[1]})" for n, v in report.items()) +
           f", dbeta {e_db:.2e}")
+
+
+@pytest.mark.parametrize("renorm", [True, False], ids=["renormalised", "paper_literal"])
+def test_backward_qwen3_30b_full(renorm):
+    """The full Qwen3-30B-A3B-shaped backward workload: 16384 tokens, 5 % of them
+    (819) recording the (k+1)-th ranked expert instead of the k-th.  Every
+    expert's dW_gate / dW_up / dW_down slice, every dW_r column and every dx row
+    is held to the 2e-2 relative bar (exact zeros where the oracle has none);
+    a second run is bitwise identical.  Both weightings: renormalised over the
+    recorded ids, and the printed rho_j of the softmax over all N."""
+    s = W.WORKLOADS["qwen3_30b_bwd_T16384"]
+    L = W.layer_inputs(s, 0)
+    idx = recorded_route(L, s, 0)
+    assert (O.route_overlap(idx, O.topk_ids(O.router_logits(L["x"], L["W_r"], L["beta"]), s.k))
+            < s.k).sum() == 819
+    dy = W.upstream_grad(s, 0)
+    g = run_bwd(L, idx, dy, "bf16", renorm=renorm)
+    ref = oracle_bwd(L, idx, dy, renorm)
+    check_full(g, ref, s.name + ("" if renorm else " (paper-literal)"))
     del ref
-    g2 = run_bwd(L, idx, dy, "bf16")
+    g2 = run_bwd(L, idx, dy, "bf16", renorm=renorm)
     for n in GRADS:
         assert np.array_equal(g[n], g2[n]), f"{n} differs between two runs"
+
+
+LITERAL_CASES = [
+    # (T, d, N, k, m, act, skew, idx_dtype, ldi_pad)
+    (700, 256, 8, 2, 256, "bf16", "hot8", "int32", 0),
+    (1500, 512, 16, 4, 512, "bf16", "zipf", "int16", 3),
+    (2100, 256, 130, 8, 256, "bf16", "hot8", "int32", 0),   # N not a multiple of 64, 3 chunks
+    (520, 256, 12, 3, 256, "bf16", "zipf", "int32", 0),
+    (300, 192, 8, 2, 128, "bf16", "hot8", "int32", 0),      # generic kernels
+    (130, 48, 6, 3, 40, "f32", "none", "int16", 1),         # generic fp32, ragged everything
+    (100, 256, 4, 4, 256, "bf16", "none", "int32", 0),      # k = N: no off-route logits
+]
+
+
+@pytest.mark.parametrize("case", LITERAL_CASES,
+                         ids=[f"T{c[0]}_d{c[1]}_N{c[2]}_k{c[3]}_m{c[4]}_{c[5]}" for c in LITERAL_CASES])
+def test_backward_paper_literal_shapes(case):
+    """renorm = 0: the weights are rho_j of the softmax over all N, so every logit
+    gets a gradient (oracle pinned by central differences on the CPU)."""
+    T, d, N, k, m, act, skew, idt, pad = case
+    s = W.LayerShape("lit", T=T, d=d, N=N, k=k, m=m, r=0, act=act, skew=skew, flip_frac=0.05)
+    L = W.layer_inputs(s, 13)
+    idx = recorded_route(L, s, 13)
+    dy = W.upstream_grad(s, 13)
+    g = run_bwd(L, idx, dy, act, idt, pad, renorm=False)
+    ref = oracle_bwd(L, idx, dy, renorm=False)
+    compare(g, ref, act, "literal " + str(case))
+    # unused experts still get no expert-weight gradient, but their router column does
+    unused = np.setdiff1d(np.arange(N), np.unique(idx))
+    for n in ("dW_gate", "dW_up", "dW_down"):
+        assert np.all(g[n][unused] == 0.0)
+    if len(unused) and k < N:
+        assert np.all(np.abs(g["dW_r"][:, unused]).sum(axis=0) > 0)

@@ -1,16 +1,11 @@
-"""The library's side stream (the replay weights of the forward, the router and
-input-gradient tail of the backward) keeps every call ordered with respect to
-the caller's stream:
+"""Calls on several streams and from several host threads: the library owns no
+stream and keeps no per-call device state outside the caller's workspace, so
 
 * calls made at the same time from two host threads, each on its own stream
   and workspace, give bitwise the outputs of the same calls made one after
-  the other (the fork and join of one call are not interleaved with the
-  other's);
-* a replay backward captured into a HIP graph (fork and join inside the
-  capture) gives, on every replay, bitwise the gradients of the eager call;
-* PR2_NO_SIDE_STREAM=1 (every launch on the caller's stream) gives bitwise
-  the same outputs."""
-import os
+  the other;
+* a replay backward captured into a HIP graph gives, on every replay, bitwise
+  the gradients of the eager call."""
 import threading
 
 import pytest
@@ -117,22 +112,3 @@ def test_backward_graph_replays_match_eager_call():
         assert same(p.outputs()[2:], eager), f"replay {rep}"
         p.forward(st)             # eager work between replays
         torch.cuda.synchronize()
-
-
-def test_in_order_launches_match_side_stream():
-    import torch
-    p = Problem(24)
-    st = torch.cuda.current_stream()
-    p.forward(st)
-    p.backward(st)
-    torch.cuda.synchronize()
-    side = p.outputs()
-    os.environ["PR2_NO_SIDE_STREAM"] = "1"
-    try:
-        p.forward(st)
-        p.backward(st)
-        torch.cuda.synchronize()
-    finally:
-        del os.environ["PR2_NO_SIDE_STREAM"]
-    assert same(p.outputs(), side)
-
