@@ -153,6 +153,24 @@ pr2_status pr2_route_predict_reuse(const pr2_moe_desc* desc, const void* x, cons
                                    void* ws, size_t ws_bytes, pr2_stream_t stream);
 
 /*
+ * Route prediction that allocates nothing, for callers that cannot allocate device memory:
+ * code being captured into a HIP graph, tight serving loops, harnesses that forbid it.
+ * Same arguments (minus the workspace), checks and results as pr2_route_predict: the same
+ * kernels, always the fused (non-split-K) form, whose logits are bitwise those of the split-K
+ * form.  The bf16 split of the weights goes to a file-scope device array of 6 MiB that the
+ * library holds on each GPU it runs on until the process ends; a shape whose split needs more
+ * (3 x 2 bytes x d x the columns N, or N + r when logits_out is given, rounded up to 64)
+ * returns PR2_ERR_UNSUPPORTED with nothing enqueued.  The call allocates and frees nothing;
+ * its first call on a device looks up that device's copy of the array (make it outside a
+ * capture).  Every call on a GPU shares that GPU's array: calls that overlap on one GPU (two
+ * streams, two threads) race and give unspecified routes; order them on one stream.
+ */
+pr2_status pr2_route_predict_noalloc(const pr2_moe_desc* desc, const void* x, const float* W_r,
+                                     const float* b_r, const float* A, const float* B,
+                                     void* idx_out, int64_t ldi, float* gate_out,
+                                     float* logits_out, pr2_stream_t stream);
+
+/*
  * Replay forward during training (Sec. 4.1 "Replay During Training"; Eq. pr2_output;
  * Alg. 3 in Appendix D, its first two steps).  No fresh top-k: the recorded ids are used as
  * given, in any order; the weights come from the current router with the predictor bypassed:

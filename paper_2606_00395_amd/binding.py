@@ -25,6 +25,7 @@ STATUS = ["PR2_OK", "PR2_ERR_NULL", "PR2_ERR_SHAPE", "PR2_ERR_DTYPE", "PR2_ERR_A
 
 # every symbol include/pr2.h declares
 EXPORTS = ["pr2_workspace_bytes", "pr2_route_predict", "pr2_route_predict_reuse",
+           "pr2_route_predict_noalloc",
            "pr2_moe_replay_forward", "pr2_moe_replay_forward_diag",
            "pr2_moe_replay_backward", "pr2_moe_rollout_forward", "pr2_route_diagnostics",
            "pr2_feature_cache_positions", "pr2_route_predict_cached", "pr2_predictor_loss",
@@ -66,6 +67,8 @@ def lib() -> ctypes.CDLL:
     L.pr2_route_predict.restype = c_int
     L.pr2_route_predict_reuse.argtypes = L.pr2_route_predict.argtypes
     L.pr2_route_predict_reuse.restype = c_int
+    L.pr2_route_predict_noalloc.argtypes = [POINTER(MoeDesc), P, P, P, P, P, P, c_int64, P, P, P]
+    L.pr2_route_predict_noalloc.restype = c_int
     L.pr2_moe_replay_forward.argtypes = [POINTER(MoeDesc), P, P, c_int64, P, P, P, P, P, P, P,
                                          P, c_size_t, P]
     L.pr2_moe_replay_forward.restype = c_int
@@ -289,6 +292,23 @@ def route_predict(x, W_r, b_r, A, B, k, idx_out, gate_out=None, logits_out=None,
     fn = lib().pr2_route_predict_reuse if reuse_split else lib().pr2_route_predict
     check(fn(byref(desc), _ptr(x), _ptr(W_r), _ptr(b_r), _ptr(A), _ptr(B), _ptr(idx_out),
              ldi, _ptr(gate_out), _ptr(logits_out), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def route_predict_noalloc(x, W_r, b_r, A, B, k, idx_out, gate_out=None, logits_out=None,
+                          renorm=True, stream=None):
+    """pr2_route_predict_noalloc on torch tensors: pr2_route_predict with the library's
+    own device scratch instead of a workspace (nothing is allocated)."""
+    torch = _torch()
+    T, d, _, dev = _need_act(x)
+    N = _router(W_r, b_r, d, dev)
+    r = _predictor(A, B, d, N, dev)
+    ldi = _need_ids(idx_out, "idx_out", T, k, dev)
+    _need(gate_out, "gate_out", (T, k), torch.float32, dev, optional=True)
+    _need(logits_out, "logits_out", (T, N), torch.float32, dev, optional=True)
+    desc = make_desc(T, d, N, k, 0, r, _act_code(x), _idx_code(idx_out), renorm)
+    check(lib().pr2_route_predict_noalloc(byref(desc), _ptr(x), _ptr(W_r), _ptr(b_r), _ptr(A),
+                                          _ptr(B), _ptr(idx_out), ldi, _ptr(gate_out),
+                                          _ptr(logits_out), _stream(stream)))
 
 
 def replay_workspace(x, idx, W_r, W_gate, renorm=True, stream=None):

@@ -15,7 +15,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libpr2.so")
-SOURCES = ["api.hip", "router.hip", "permute.hip", "gemm.hip", "backward.hip", "predictor.hip"]
+SOURCES = ["api.hip", "router.hip", "permute.hip", "gemm.hip", "backward.hip", "predictor.hip",
+           "noalloc.hip"]
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -348,3 +348,24 @@ def test_reuse_needs_a_recorded_split():
     # the fp64 vector path keeps no split: nothing to check, the call goes on
     st, msg = route_reuse(desc(act=B.PR2_F32))
     assert B.STATUS[st] in ("PR2_ERR_DEVICE", "PR2_OK"), msg
+
+
+def test_noalloc_rejects_a_split_beyond_its_scratch():
+    """pr2_route_predict_noalloc keeps the weight split in a 6 MiB device array: a
+    shape whose split is larger is refused on the host, before any HIP call."""
+    L = B.lib()
+
+    def call(d, logits=None):
+        st = L.pr2_route_predict_noalloc(byref(d), c_void_p(FAKE), c_void_p(FAKE), None,
+                                         c_void_p(FAKE), c_void_p(FAKE), c_void_p(FAKE), d.k,
+                                         None, c_void_p(logits), None)
+        return B.STATUS[st], L.pr2_last_error().decode()
+    # d 8192, N 128 folded: 3 x 2 x 8192 x 128 = 6 MiB fits exactly
+    st, msg = call(desc(d=8192, N=128, k=8, r=16))
+    assert st in ("PR2_ERR_DEVICE", "PR2_OK"), msg
+    # with logits wanted the split is [W_r | A]: 192 columns, 9 MiB
+    st, msg = call(desc(d=8192, N=128, k=8, r=16), logits=FAKE)
+    assert st == "PR2_ERR_UNSUPPORTED" and "scratch" in msg, msg
+    # the usual argument checks still come first
+    st, msg = call(desc(k=0))
+    assert st == "PR2_ERR_SHAPE", msg
