@@ -13,7 +13,9 @@ from ctypes import (POINTER, byref, c_char_p, c_double, c_int, c_int32, c_int64,
                     c_uint64, c_void_p)
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libpr2.so")
+# PR2_LIBRARY names another build of the same library (the host-sanitizer build
+# of build_sanitized.py, for the CPU checks)
+LIB_PATH = os.environ.get("PR2_LIBRARY") or os.path.join(HERE, "libpr2.so")
 
 PR2_F32, PR2_BF16 = 0, 1
 PR2_I32, PR2_I16 = 0, 1

@@ -323,7 +323,11 @@ extern "C" {
 const char* pr2_version(void) { return "pr2-mi355x 0.1"; }
 
 const char* pr2_status_string(pr2_status s) {
-    switch (s) {
+    // a C caller may pass any int: read the raw value (loading an out-of-range
+    // value as the enum type would be undefined behaviour here)
+    int v;
+    memcpy(&v, &s, sizeof v);
+    switch (v) {
         case PR2_OK: return "PR2_OK";
         case PR2_ERR_NULL: return "PR2_ERR_NULL";
         case PR2_ERR_SHAPE: return "PR2_ERR_SHAPE";
