@@ -213,8 +213,10 @@ grouped_gemm_mfma(MfmaArgs g) {
     }
     // A groups of 8 token rows wholly past the end of a partial tile are not
     // copied: no stored output depends on those LDS rows (a wavefront-uniform,
-    // scalar test; the K loop's waits are for all copies in flight, so the count
-    // issued does not matter)
+    // scalar test).  The K loop's waits are for all copies in flight (two
+    // stages: vmcnt 0), so the count issued does not matter; a deeper pipeline
+    // would count copies per stage and must not skip any.
+    static_assert(NSTAGE == 2, "the copy skip below assumes vmcnt(0) waits");
     auto issue = [&](int stage, int k0) {
 #pragma unroll
         for (int i = 0; i < kGroups; ++i) {
