@@ -919,12 +919,12 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
     const int64_t t0 = (int64_t)blockIdx.x * kRTM;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar branches
     const int wr = wave >> 2, wc = wave & 3;
 
     // Copies straight into LDS, 16 bytes per lane: copy slot i of wavefront w
-    // moves 16-row group g = w + 8 i (groups past the end repeat the last
-    // groups: the same bytes to the same place), lane l row 16 g + l/4 at
+    // moves 16-row group g = w + 8 i (a wavefront whose last slot falls past
+    // the end issues one copy fewer per step), lane l row 16 g + l/4 at
     // position l%4.  Rows below kRTM are tokens (past T: the last token, never
     // written out); the rest are the K-tiled split weights of the step.
     const bf16_t* src[GPW];
@@ -932,7 +932,7 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
 #pragma unroll
     for (int i = 0; i < GPW; ++i) {
         int g = wave + 8 * i;
-        if (g >= RT::GROUPS) g = RT::GROUPS - 1 - (g - RT::GROUPS) % 8;
+        if (g >= RT::GROUPS) g = RT::GROUPS - 1;     // never copied (see issue)
         const int row = g * 16 + (lane >> 2);
         const int chunk = (lane & 3) ^ rswz(row);
         if (row < kRTM) {
@@ -943,9 +943,13 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
         }
         dst[i] = g * 1024;
     }
+    // copies per step of this wavefront: GPW, or GPW - 1 when its last slot
+    // is past the last group (the waits below count them)
+    const bool full_slots = wave + 8 * (GPW - 1) < RT::GROUPS;
     auto issue = [&](int stage, int kt) {
 #pragma unroll
         for (int i = 0; i < GPW; ++i) {
+            if (i == GPW - 1 && !full_slots) continue;
             const int64_t step = dst[i] < kRTM * 64 ? (int64_t)kt * kRBK
                                                      : (int64_t)kt * 3 * NCp * kRBK;
             __builtin_amdgcn_global_load_lds((const void*)(src[i] + step),
@@ -993,8 +997,12 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
     for (int kt = kb; kt < ke; ++kt) {
         // step kt landed (later steps may be in flight) and every wavefront is
         // done with step kt-1, whose stage is refilled next
-        if (kt + NSTAGE - 2 < ke) router_wait_vmcnt<(NSTAGE - 2) * GPW>();
-        else router_wait_vmcnt<0>();
+        if (kt + NSTAGE - 2 < ke) {
+            if (full_slots) router_wait_vmcnt<(NSTAGE - 2) * GPW>();
+            else router_wait_vmcnt<(NSTAGE - 2) * (GPW - 1)>();
+        } else {
+            router_wait_vmcnt<0>();
+        }
         // a plain barrier: __syncthreads() would also wait for every copy
         // still in flight (vmcnt(0)) and undo the pipelining
         __builtin_amdgcn_s_waitcnt(0xc07f);      // lgkmcnt(0)
