@@ -93,6 +93,25 @@ def profiled_traffic(profile, kernel):
     return int(m.group(1)) + int(m.group(2)) if m else None
 
 
+def profiled_counters(profile, kernel):
+    """The SQ counter figures (mfma_busy, lds_conflict_per_inst, ...) that the
+    committed summary `profiles/<profile>` holds for `kernel`, or None when the
+    summary is missing or its sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", profile)
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    srcs = re.search(r"kernel_sources: (.+)", text)
+    m = re.search(r"kernel_source_sha256: ([0-9a-f]+)", text)
+    if not srcs or not m or m.group(1) != kernel_source_hash(srcs.group(1).split()):
+        return None
+    m = re.search(r"counters\[" + re.escape(kernel) + r"\]: (.+)", text)
+    if not m:
+        return None
+    vals = m.group(1).split()
+    return {vals[i]: float(vals[i + 1]) for i in range(0, len(vals) - 1, 2)}
+
+
 def blas_threads():
     try:
         from threadpoolctl import threadpool_info
@@ -445,6 +464,13 @@ def run_forward(args, shape, dev):
             cg[key] = {"bytes": b, "gbps": b / (t_ms * 1e-3) / 1e9,
                        "frac_of_8tbs": b / (t_ms * 1e-3) / C.PEAK_HBM_BYTES}
     out["hbm_gbps_counters"] = cg or None
+    out["mfma_busy_counters"] = {
+        key: (profiled_counters(prof, kname) or {}).get("mfma_busy")
+        for key, kname in (("gemm1_gate_up_swiglu", "grouped_gemm_mfma<0>"),
+                           ("gemm2_down_scale", "grouped_gemm_mfma<1>"),
+                           ("route_predict", "router_mfma_kernel<2, 0, 0>"))}
+    out["mfma_busy_counters"]["note"] = ("SQ_VALU_MFMA_BUSY_CYCLES / (4 SIMDs x SQ_BUSY_CU_CYCLES) "
+                                         "from the committed rocprofv3 summary of these sources")
     if not args.no_cpu_baseline:
         n_tok = args.cpu_sample_tokens if args.cpu_sample_tokens > 0 else T
         out["cpu_baseline"] = cpu_baseline_forward(shape, L, min(n_tok, T))

@@ -72,9 +72,15 @@ def drifted(L, s, seed=1):
 
 
 def run_loss(L, s, Tc, kind, identity=False, mini_step=2):
+    """The loss on a feature cache built from the oracle (never from the HIP
+    path): h_old = the cached positions' input rows, p_old = the oracle's router
+    logits there rounded to fp32 (the precision the cache stores)."""
     import torch
     from paper_2606_00395_amd import binding as B
-    pos, _, _, h_cache, p_cache = cache_features(L, s, Tc)
+    pos = O.feature_cache_positions(s.T, Tc, 5)
+    p_old = O.router_logits(L["x"][pos], L["W_r"], L["beta"]).astype(np.float32)
+    h_cache = to_dev(L["x"][pos], s.act)
+    p_cache = to_dev(p_old)
     W_cur, h_cur = drifted(L, s)
     A = L["A"]
     Bm = None if identity else L["B"]
@@ -91,7 +97,7 @@ def run_loss(L, s, Tc, kind, identity=False, mini_step=2):
          "dB": None if identity else dB.cpu().numpy()}
     p_cur = O.router_logits(h_cur[pos], W_cur, L["beta"])
     fn = O.predictive_kl if kind == 0 else O.delta_matching_kl
-    kl_ref, dA_ref, dB_ref = fn(p_cur, L["x"][pos], p_cache.cpu().numpy(), A, Bm)
+    kl_ref, dA_ref, dB_ref = fn(p_cur, L["x"][pos], p_old, A, Bm)
     return g, (kl_ref, dA_ref, dB_ref)
 
 

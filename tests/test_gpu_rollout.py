@@ -101,15 +101,17 @@ def test_rollout_zero_predictor_equals_replay_of_its_route():
     compare_route(g["idx"], g["gate"], ref, s.k, "zero predictor")
 
 
-def test_rollout_qwen3_30b_sampled_rows():
+def test_rollout_qwen3_30b_full():
+    """Every token of the Qwen3-30B-A3B-shaped rollout forward: the predicted
+    route (margin rule), its predictive weights and the layer output (per-row
+    rule, tokens outside the margin)."""
     s = W.WORKLOADS["qwen3_30b_T16384"]
     L = W.layer_inputs(s, 0)
     g = run_rollout(L, s)
-    rows = np.unique(np.concatenate([[0, s.T - 1],
-                                     np.random.default_rng(3).choice(s.T, 254, replace=False)]))
-    y_ref, ref = O.rollout_forward(L["x"][rows], L["W_r"], L["beta"], L["A"], L["B"], s.k,
+    y_ref, ref = O.rollout_forward(L["x"], L["W_r"], L["beta"], L["A"], L["B"], s.k,
                                    L["W_gate"], L["W_up"], L["W_down"])
-    sub = {"idx": g["idx"][rows], "gate": g["gate"][rows], "y": g["y"][rows]}
-    compare_route(sub["idx"], sub["gate"], ref, s.k, s.name)
+    n_excl = compare_route(g["idx"], g["gate"], ref, s.k, s.name)
     keep = ref["margin"] >= MARGIN_EPS
-    compare_rows(sub["y"][keep], y_ref[keep], "bf16", s.name)
+    err = compare_rows(g["y"][keep], y_ref[keep], "bf16", s.name)
+    print(f"\n{s.name}: rollout forward worst row rel err {err:.2e} over {keep.sum()} rows "
+          f"({n_excl} under the margin)")
