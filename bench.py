@@ -543,11 +543,49 @@ def run_backward(args, shape, dev):
     out["mfma_frac_whole_backward"] = 16 * unit / (ms * 1e-3) / C.PEAK_BF16_FLOPS
     out["recorded_route"] = ("the current router's top-k with the k-th ranked expert swapped for "
                              f"the (k+1)-th on {int(round(shape.flip_frac * T))} tokens")
+    out["training_pass"] = training_pass(args, G, idx, dy, (dx, dWr, dbr, dWg, dWu, dWd), ws,
+                                         step, stream)
     if not args.no_cpu_baseline:
         idx_np = idx.cpu().numpy()
         n_tok = args.cpu_sample_tokens if args.cpu_sample_tokens > 0 else 1024
         out["cpu_baseline"] = cpu_baseline_backward(shape, L, idx_np, dy_np, min(n_tok, T))
     return out
+
+
+def training_pass(args, G, idx, dy, grads, bws, backward_step, stream):
+    """The replay forward followed by its backward (one training pass of the MoE
+    layer under the recorded route), two ways: the backward recomputing the
+    experts' gate / up pre-activations, and the forward saving them for the
+    backward (2 m activation values per route held between the passes)."""
+    import torch
+    from paper_2606_00395_amd import binding as B
+    T, k = idx.shape
+    m = G["W_gate"].shape[1]
+    x = G["x"]
+    y = torch.empty_like(x)
+    gate = torch.empty((T, k), dtype=torch.float32, device=x.device)
+    au = torch.empty((T * k, 2 * m), dtype=x.dtype, device=x.device)
+    fws = B.replay_workspace(x, idx, G["W_r"], G["W_gate"])
+    experts = (G["W_gate"], G["W_up"], G["W_down"])
+
+    def recompute():
+        B.moe_replay_forward(x, idx, G["W_r"], G["beta"], *experts, y, gate, ws=fws,
+                             stream=stream)
+        backward_step()
+
+    def saved():
+        B.moe_replay_forward_save(x, idx, G["W_r"], G["beta"], *experts, y, au, gate, ws=fws,
+                                  stream=stream)
+        B.moe_replay_backward_saved(x, idx, G["W_r"], G["beta"], *experts, au, dy, *grads,
+                                    ws=bws, stream=stream)
+
+    ms_r, kern_r = timed_steps(recompute, args.steps, args.warmup, stream, B)
+    ms_s, kern_s = timed_steps(saved, args.steps, args.warmup, stream, B)
+    del au, fws
+    return {"forward_then_backward_ms": ms_r, "with_saved_preactivations_ms": ms_s,
+            "saved_bytes": T * k * 2 * m * x.element_size(),
+            "kernels_ms_recompute": {n: round(v, 5) for n, v in kern_r.items()},
+            "kernels_ms_saved": {n: round(v, 5) for n, v in kern_s.items()}}
 
 
 def run_decode(args, shape, dev):

@@ -196,6 +196,27 @@ pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const
                                   pr2_stream_t stream);
 
 /*
+ * Replay forward that also saves the experts' pre-activations for the backward (Sec. 4.1
+ * "Replay During Training", Alg. 3: the training pass runs the replay forward and then its
+ * backward under the same recorded routes).  Everything pr2_moe_replay_forward does, plus
+ *
+ *   au_out  [T*k, 2m] act_dtype, 16-byte aligned: row q holds a = x W_gate_e^T (first m) and
+ *           u = x W_up_e^T (last m), rounded to act_dtype, for the q-th route in the
+ *           library's expert-sorted order (a stable sort of the routes by expert id, which the
+ *           backward forms again from the same ids).  Opaque to the caller: pass it unchanged
+ *           to pr2_moe_replay_backward_saved with the same desc, x, idx, W_gate and W_up.
+ *
+ * y and gate_out are bitwise those of pr2_moe_replay_forward.  The saved rows are bitwise
+ * what the backward would otherwise recompute, so the saved backward's gradients are bitwise
+ * those of pr2_moe_replay_backward.
+ */
+pr2_status pr2_moe_replay_forward_save(const pr2_moe_desc* desc, const void* x, const void* idx,
+                                       int64_t ldi, const float* W_r, const float* b_r,
+                                       const void* W_gate, const void* W_up, const void* W_down,
+                                       void* y, float* gate_out, void* au_out, void* ws,
+                                       size_t ws_bytes, pr2_stream_t stream);
+
+/*
  * Replay forward with the route-tracking diagnostics of Sec. 5.4 (top-k agreement, routing
  * deviation, route KL) formed in the same pass: the replay-weight epilogue already holds all N
  * current router logits of each token, so it also selects their top-k and compares it with the
@@ -277,6 +298,20 @@ pr2_status pr2_moe_replay_backward(const pr2_moe_desc* desc, const void* x, cons
                                    const void* dy, void* dx, float* dW_r, float* db_r,
                                    float* dW_gate, float* dW_up, float* dW_down, void* ws,
                                    size_t ws_bytes, pr2_stream_t stream);
+
+/*
+ * Replay backward from saved pre-activations: pr2_moe_replay_backward with the gate/up
+ * pre-activations read from au_saved (written by pr2_moe_replay_forward_save with the same
+ * desc, x, idx, W_gate and W_up) instead of recomputed by a grouped GEMM.  au_saved is only
+ * read.  Same arguments otherwise, same workspace, bitwise the same gradients.
+ */
+pr2_status pr2_moe_replay_backward_saved(const pr2_moe_desc* desc, const void* x, const void* idx,
+                                         int64_t ldi, const float* W_r, const float* b_r,
+                                         const void* W_gate, const void* W_up,
+                                         const void* W_down, const void* au_saved,
+                                         const void* dy, void* dx, float* dW_r, float* db_r,
+                                         float* dW_gate, float* dW_up, float* dW_down, void* ws,
+                                         size_t ws_bytes, pr2_stream_t stream);
 
 /*
  * Route-tracking diagnostics (Sec. 5.4: top-k agreement, routing deviation and route KL) of a

@@ -29,6 +29,7 @@ STATUS = ["PR2_OK", "PR2_ERR_NULL", "PR2_ERR_SHAPE", "PR2_ERR_DTYPE", "PR2_ERR_A
 EXPORTS = ["pr2_workspace_bytes", "pr2_route_predict", "pr2_route_predict_reuse",
            "pr2_route_predict_noalloc",
            "pr2_moe_replay_forward", "pr2_moe_replay_forward_diag",
+           "pr2_moe_replay_forward_save", "pr2_moe_replay_backward_saved",
            "pr2_moe_replay_backward", "pr2_moe_rollout_forward", "pr2_route_diagnostics",
            "pr2_feature_cache_positions", "pr2_route_predict_cached", "pr2_predictor_loss",
            "pr2_status_string",
@@ -80,6 +81,12 @@ def lib() -> ctypes.CDLL:
     L.pr2_moe_replay_backward.argtypes = [POINTER(MoeDesc), P, P, c_int64, P, P, P, P, P, P, P,
                                           P, P, P, P, P, P, c_size_t, P]
     L.pr2_moe_replay_backward.restype = c_int
+    L.pr2_moe_replay_forward_save.argtypes = [POINTER(MoeDesc), P, P, c_int64, P, P, P, P, P, P,
+                                              P, P, P, c_size_t, P]
+    L.pr2_moe_replay_forward_save.restype = c_int
+    L.pr2_moe_replay_backward_saved.argtypes = [POINTER(MoeDesc), P, P, c_int64, P, P, P, P, P, P,
+                                                P, P, P, P, P, P, P, P, c_size_t, P]
+    L.pr2_moe_replay_backward_saved.restype = c_int
     L.pr2_moe_rollout_forward.argtypes = [POINTER(MoeDesc), P, P, P, P, P, P, P, P, P, c_int64, P,
                                           P, P, P, c_size_t, P]
     L.pr2_moe_rollout_forward.restype = c_int
@@ -341,6 +348,30 @@ def moe_replay_forward(x, idx, W_r, b_r, W_gate, W_up, W_down, y, gate_out=None,
                                        ws.numel(), _stream(stream)))
 
 
+def moe_replay_forward_save(x, idx, W_r, b_r, W_gate, W_up, W_down, y, au_out, gate_out=None,
+                            ws=None, renorm=True, stream=None):
+    """pr2_moe_replay_forward_save: the replay forward, also writing the experts'
+    pre-activations to ``au_out`` ([T*k, 2m], the activation dtype) for
+    moe_replay_backward_saved."""
+    torch = _torch()
+    T, d, adt, dev = _need_act(x)
+    N = _router(W_r, b_r, d, dev)
+    k = idx.shape[1] if idx.dim() == 2 else -1
+    ldi = _need_ids(idx, "idx", T, k, dev)
+    m = _experts(W_gate, W_up, W_down, N, d, adt, dev)
+    _need(y, "y", (T, d), adt, dev)
+    _need(au_out, "au_out", (T * k, 2 * m), adt, dev)
+    _need(gate_out, "gate_out", (T, k), torch.float32, dev, optional=True)
+    _need_ws(ws, dev)
+    desc = make_desc(T, d, N, k, m, 0, _act_code(x), _idx_code(idx), renorm)
+    if ws is None:
+        ws = replay_workspace(x, idx, W_r, W_gate, renorm, stream)
+    check(lib().pr2_moe_replay_forward_save(byref(desc), _ptr(x), _ptr(idx), ldi, _ptr(W_r),
+                                            _ptr(b_r), _ptr(W_gate), _ptr(W_up), _ptr(W_down),
+                                            _ptr(y), _ptr(gate_out), _ptr(au_out), _ptr(ws),
+                                            ws.numel(), _stream(stream)))
+
+
 def moe_replay_forward_diag(x, idx, W_r, b_r, W_gate, W_up, W_down, y, gate_out=None,
                             z_ref=None, cur_idx_out=None, overlap_out=None, kl_out=None,
                             hist_out=None, ws=None, renorm=True, stream=None):
@@ -530,6 +561,36 @@ def moe_replay_backward(x, idx, W_r, b_r, W_gate, W_up, W_down, dy, dx, dW_r, db
                                         _ptr(W_down), _ptr(dy), _ptr(dx), _ptr(dW_r), _ptr(db_r),
                                         _ptr(dW_gate), _ptr(dW_up), _ptr(dW_down), _ptr(ws),
                                         ws.numel(), _stream(stream)))
+
+
+def moe_replay_backward_saved(x, idx, W_r, b_r, W_gate, W_up, W_down, au_saved, dy, dx, dW_r,
+                              db_r, dW_gate, dW_up, dW_down, ws=None, renorm=True, stream=None):
+    """pr2_moe_replay_backward_saved: the replay backward reading the pre-activations
+    that moe_replay_forward_save wrote (``au_saved`` is only read)."""
+    torch = _torch()
+    T, d, adt, dev = _need_act(x)
+    N = _router(W_r, b_r, d, dev)
+    k = idx.shape[1] if idx.dim() == 2 else -1
+    ldi = _need_ids(idx, "idx", T, k, dev)
+    m = _experts(W_gate, W_up, W_down, N, d, adt, dev)
+    _need(au_saved, "au_saved", (T * k, 2 * m), adt, dev)
+    _need(dy, "dy", (T, d), adt, dev)
+    _need(dx, "dx", (T, d), adt, dev)
+    _need(dW_r, "dW_r", (d, N), torch.float32, dev)
+    _need(db_r, "db_r", (N,), torch.float32, dev, optional=True)
+    _need(dW_gate, "dW_gate", (N, m, d), torch.float32, dev)
+    _need(dW_up, "dW_up", (N, m, d), torch.float32, dev)
+    _need(dW_down, "dW_down", (N, d, m), torch.float32, dev)
+    _need_ws(ws, dev)
+    desc = make_desc(T, d, N, k, m, 0, _act_code(x), _idx_code(idx), renorm)
+    if ws is None:
+        ws = backward_workspace(x, idx, W_r, W_gate, renorm, stream)
+    check(lib().pr2_moe_replay_backward_saved(byref(desc), _ptr(x), _ptr(idx), ldi, _ptr(W_r),
+                                              _ptr(b_r), _ptr(W_gate), _ptr(W_up), _ptr(W_down),
+                                              _ptr(au_saved), _ptr(dy), _ptr(dx), _ptr(dW_r),
+                                              _ptr(db_r), _ptr(dW_gate), _ptr(dW_up),
+                                              _ptr(dW_down), _ptr(ws), ws.numel(),
+                                              _stream(stream)))
 
 
 # ------------------------------------------------------ measurement hooks --

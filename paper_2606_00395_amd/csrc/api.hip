@@ -484,7 +484,8 @@ static pr2_status replay_forward_impl(const pr2_moe_desc* desc, const void* x, c
                                       int64_t ldi, const float* W_r, const float* b_r,
                                       const void* W_gate, const void* W_up, const void* W_down,
                                       void* y, float* gate_out, const RouteDiag* diag, void* ws,
-                                      size_t ws_bytes, pr2_stream_t stream) {
+                                      size_t ws_bytes, pr2_stream_t stream,
+                                      void* au_out = nullptr) {
     pr2_status s = check_desc(desc, true, true);
     if (s != PR2_OK) return s;
     const pr2_moe_desc& d = *desc;
@@ -533,7 +534,7 @@ static pr2_status replay_forward_impl(const pr2_moe_desc* desc, const void* x, c
     if (e != hipSuccess) return hip_fail(e, "replay_gates launch");
     e = launch_permute(d, idx, ldi, w, st);
     if (e != hipSuccess) return hip_fail(e, "permute launch");
-    e = launch_expert_gemms(d, x, W_gate, W_up, W_down, gate, w, st);
+    e = launch_expert_gemms(d, x, W_gate, W_up, W_down, gate, w, st, au_out);
     if (e != hipSuccess) return hip_fail(e, "expert GEMM launch");
     e = launch_combine(d, w, y, st);
     if (e != hipSuccess) return hip_fail(e, "combine launch");
@@ -556,6 +557,19 @@ pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const
                                   pr2_stream_t stream) {
     return replay_forward_impl(desc, x, idx, ldi, W_r, b_r, W_gate, W_up, W_down, y, gate_out,
                                nullptr, ws, ws_bytes, stream);
+}
+
+pr2_status pr2_moe_replay_forward_save(const pr2_moe_desc* desc, const void* x, const void* idx,
+                                       int64_t ldi, const float* W_r, const float* b_r,
+                                       const void* W_gate, const void* W_up, const void* W_down,
+                                       void* y, float* gate_out, void* au_out, void* ws,
+                                       size_t ws_bytes, pr2_stream_t stream) {
+    pr2_status s = check_desc(desc, true, true);
+    if (s != PR2_OK) return s;
+    if (desc->T > 0 && !au_out) return fail(PR2_ERR_NULL, "au_out is NULL");
+    if (!aligned(au_out, 16)) return fail(PR2_ERR_ALIGN, "au_out must be 16-byte aligned");
+    return replay_forward_impl(desc, x, idx, ldi, W_r, b_r, W_gate, W_up, W_down, y, gate_out,
+                               nullptr, ws, ws_bytes, stream, au_out);
 }
 
 pr2_status pr2_moe_replay_forward_diag(const pr2_moe_desc* desc, const void* x, const void* idx,
@@ -627,12 +641,13 @@ pr2_status pr2_moe_rollout_forward(const pr2_moe_desc* desc, const void* x, cons
     return ok();
 }
 
-pr2_status pr2_moe_replay_backward(const pr2_moe_desc* desc, const void* x, const void* idx,
-                                   int64_t ldi, const float* W_r, const float* b_r,
-                                   const void* W_gate, const void* W_up, const void* W_down,
-                                   const void* dy, void* dx, float* dW_r, float* db_r,
-                                   float* dW_gate, float* dW_up, float* dW_down, void* ws,
-                                   size_t ws_bytes, pr2_stream_t stream) {
+static pr2_status replay_backward_impl(const pr2_moe_desc* desc, const void* x, const void* idx,
+                                       int64_t ldi, const float* W_r, const float* b_r,
+                                       const void* W_gate, const void* W_up, const void* W_down,
+                                       const void* au_saved, const void* dy, void* dx,
+                                       float* dW_r, float* db_r, float* dW_gate, float* dW_up,
+                                       float* dW_down, void* ws, size_t ws_bytes,
+                                       pr2_stream_t stream) {
     pr2_status s = check_desc(desc, true, true);
     if (s != PR2_OK) return s;
     const pr2_moe_desc& d = *desc;
@@ -692,7 +707,7 @@ pr2_status pr2_moe_replay_backward(const pr2_moe_desc* desc, const void* x, cons
     if (e == hipSuccess) e = launch_permute(d, idx, ldi, w.fw, st);
     if (e != hipSuccess) return hip_fail(e, "replay_gates / permute launch");
     e = launch_replay_backward(d, x, idx, ldi, W_r, W_gate, W_up, W_down, dy, w.fw.gate, w, out,
-                               st);
+                               st, au_saved);
     if (e != hipSuccess) return hip_fail(e, "backward launch");
     if (validate) {
         int errs[ERR_WORDS];
@@ -704,6 +719,31 @@ pr2_status pr2_moe_replay_backward(const pr2_moe_desc* desc, const void* x, cons
                         errs[ERR_BAD_ID], errs[ERR_DUP_ID]);
     }
     return ok();
+}
+
+pr2_status pr2_moe_replay_backward(const pr2_moe_desc* desc, const void* x, const void* idx,
+                                   int64_t ldi, const float* W_r, const float* b_r,
+                                   const void* W_gate, const void* W_up, const void* W_down,
+                                   const void* dy, void* dx, float* dW_r, float* db_r,
+                                   float* dW_gate, float* dW_up, float* dW_down, void* ws,
+                                   size_t ws_bytes, pr2_stream_t stream) {
+    return replay_backward_impl(desc, x, idx, ldi, W_r, b_r, W_gate, W_up, W_down, nullptr, dy,
+                                dx, dW_r, db_r, dW_gate, dW_up, dW_down, ws, ws_bytes, stream);
+}
+
+pr2_status pr2_moe_replay_backward_saved(const pr2_moe_desc* desc, const void* x, const void* idx,
+                                         int64_t ldi, const float* W_r, const float* b_r,
+                                         const void* W_gate, const void* W_up,
+                                         const void* W_down, const void* au_saved,
+                                         const void* dy, void* dx, float* dW_r, float* db_r,
+                                         float* dW_gate, float* dW_up, float* dW_down, void* ws,
+                                         size_t ws_bytes, pr2_stream_t stream) {
+    pr2_status s = check_desc(desc, true, true);
+    if (s != PR2_OK) return s;
+    if (desc->T > 0 && !au_saved) return fail(PR2_ERR_NULL, "au_saved is NULL");
+    if (!aligned(au_saved, 16)) return fail(PR2_ERR_ALIGN, "au_saved must be 16-byte aligned");
+    return replay_backward_impl(desc, x, idx, ldi, W_r, b_r, W_gate, W_up, W_down, au_saved, dy,
+                                dx, dW_r, db_r, dW_gate, dW_up, dW_down, ws, ws_bytes, stream);
 }
 
 pr2_status pr2_route_diagnostics(const pr2_moe_desc* desc, const void* x, const void* idx,

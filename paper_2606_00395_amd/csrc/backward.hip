@@ -65,7 +65,8 @@ struct BwdArgs {
     const bf16_t* Wu;
     const bf16_t* Wd;
     const float* gate;       // [T*k] replay weights, route order
-    bf16_t* AU;              // [T*k, 2m]: a | u in, da | du out
+    const bf16_t* AUin;      // [T*k, 2m]: a | u (DH reads them here; may be AU itself)
+    bf16_t* AU;              // [T*k, 2m]: da | du out (and what DX, WGU read)
     bf16_t* Hg;              // [T*k, m]: g * H
     float* dgp;              // [T*k, m/128] partial gate gradients
     bf16_t* dxr;             // [T*k, d] per-route input gradients
@@ -478,8 +479,8 @@ bwd_gemm(BwdArgs g) {
         for (int p = 0; p < 8; ++p) {
             const int r = wr * WM + i * 32 + p * 4 + rsub;
             const int64_t q = row0 + (r < rows ? r : 0);
-            av[p] = *(const u32x4*)(g.AU + q * ldau + col);
-            uv[p] = *(const u32x4*)(g.AU + q * ldau + g.m + col);
+            av[p] = *(const u32x4*)(g.AUin + q * ldau + col);
+            uv[p] = *(const u32x4*)(g.AUin + q * ldau + g.m + col);
         }
         {
             const int row = lane & 31;
@@ -561,7 +562,7 @@ __global__ void __launch_bounds__(1024) expert_order_kernel(const int* offsets, 
 template <typename T>
 __global__ void __launch_bounds__(256)
 dh_generic(const T* dy, const int* perm_src, int k, const T* Wd, const float* gate, int d, int m,
-           const int* tiles, const int* tile_count, T* AU, T* Hg, float* dgp) {
+           const int* tiles, const int* tile_count, const T* AUin, T* AU, T* Hg, float* dgp) {
     const int tile = blockIdx.x;
     if (tile >= *tile_count) return;
     const int expert = tiles[3 * tile], row0 = tiles[3 * tile + 1], rows = tiles[3 * tile + 2];
@@ -574,9 +575,10 @@ dh_generic(const T* dy, const int* perm_src, int k, const T* Wd, const float* ga
     const T* w = Wd + (int64_t)expert * d * m + j;
     float G = 0.0f;
     for (int i = 0; i < d; ++i) G = fmaf(Act<T>::to_f32(dyr[i]), Act<T>::to_f32(w[(int64_t)i * m]), G);
+    const T* ain = AUin + q * 2 * m;
     T* au = AU + q * 2 * m;
     float da, du, hg, hG;
-    swiglu_bwd(Act<T>::to_f32(au[j]), Act<T>::to_f32(au[m + j]), G, gate[src],
+    swiglu_bwd(Act<T>::to_f32(ain[j]), Act<T>::to_f32(ain[m + j]), G, gate[src],
                sizeof(T) == 2, da, du, hg, hG);
     au[j] = Act<T>::from_f32(da);
     au[m + j] = Act<T>::from_f32(du);
@@ -1177,12 +1179,13 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
                                   int64_t ldi, const float* W_r, const void* W_gate,
                                   const void* W_up, const void* W_down, const void* dy,
                                   const float* gate, const BwdWs& ws, const BwdGrads& out,
-                                  hipStream_t s) {
+                                  hipStream_t s, const void* au_in) {
     const ReplayWs& w = ws.fw;
     const bool bf = d.act_dtype == PR2_BF16;
     const bool mfma = bwd_mfma_ok(d);
-    hipError_t e = launch_preact(d, x, W_gate, W_up, w, ws.AU, s);
-    if (e != hipSuccess) return e;
+    hipError_t e = hipSuccess;
+    // the pre-activations: recomputed, or read from the forward's saved copy
+    if (!au_in && (e = launch_preact(d, x, W_gate, W_up, w, ws.AU, s)) != hipSuccess) return e;
 
     BwdArgs g{};
     g.perm_src = w.perm_src;
@@ -1203,6 +1206,7 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
     g.Wd = (const bf16_t*)W_down;
     g.gate = gate;
     g.AU = (bf16_t*)ws.AU;
+    g.AUin = au_in ? (const bf16_t*)au_in : g.AU;
     g.Hg = (bf16_t*)w.H;
     g.dgp = ws.dgp;
     g.dxr = (bf16_t*)w.O;
@@ -1224,11 +1228,13 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
             hipLaunchKernelGGL(dh_generic<bf16_t>, dim3((unsigned)w.max_tiles, (unsigned)d.m),
                                dim3(256), 0, s, (const bf16_t*)dy, w.perm_src, d.k,
                                (const bf16_t*)W_down, gate, d.d, d.m, w.tiles, w.tile_count,
+                               au_in ? (const bf16_t*)au_in : (const bf16_t*)ws.AU,
                                (bf16_t*)ws.AU, (bf16_t*)w.H, ws.dgp);
         else
             hipLaunchKernelGGL(dh_generic<float>, dim3((unsigned)w.max_tiles, (unsigned)d.m),
                                dim3(256), 0, s, (const float*)dy, w.perm_src, d.k,
                                (const float*)W_down, gate, d.d, d.m, w.tiles, w.tile_count,
+                               au_in ? (const float*)au_in : (const float*)ws.AU,
                                (float*)ws.AU, (float*)w.H, ws.dgp);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;

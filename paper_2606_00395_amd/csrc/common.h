@@ -177,9 +177,11 @@ hipError_t launch_combine(const pr2_moe_desc& d, const ReplayWs& ws, void* y, hi
 hipError_t launch_zero_i32(int* p, int n, hipStream_t s);
 
 // gemm.hip
+// au_out (or null): also store the pre-activations a | u of every permuted row,
+// [T*k, 2m] act, as the backward's launch_preact forms them
 hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void* W_gate,
                                const void* W_up, const void* W_down, const float* gate,
-                               const ReplayWs& ws, hipStream_t s);
+                               const ReplayWs& ws, hipStream_t s, void* au_out = nullptr);
 bool mfma_shape_ok(const pr2_moe_desc& d);
 hipError_t launch_preact(const pr2_moe_desc& d, const void* x, const void* W_gate,
                          const void* W_up, const ReplayWs& ws, void* AU, hipStream_t s);
@@ -219,7 +221,7 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
                                   int64_t ldi, const float* W_r, const void* W_gate,
                                   const void* W_up, const void* W_down, const void* dy,
                                   const float* gate, const BwdWs& ws, const BwdGrads& out,
-                                  hipStream_t s);
+                                  hipStream_t s, const void* au_in = nullptr);
 hipError_t launch_zero_grads(const pr2_moe_desc& d, const BwdGrads& out, hipStream_t s);
 
 }  // namespace pr2

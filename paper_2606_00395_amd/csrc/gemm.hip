@@ -29,7 +29,8 @@
 // contiguous range of the tile list (same experts, shared L2).
 //
 // A third epilogue serves the backward pass: it stores the pre-activations
-// a = X_e W_gate_e^T and u = X_e W_up_e^T (bf16) instead of H.
+// a = X_e W_gate_e^T and u = X_e W_up_e^T (bf16) instead of H; a fourth stores
+// both (a forward that saves them for the backward).
 //
 // Other shapes and the fp32 path use a plain one-thread-per-output kernel.
 #include "common.h"
@@ -99,6 +100,7 @@ struct MfmaArgs {
     const int* tile_count;
     const float* gate;      // GEMM2
     bf16_t* out;
+    bf16_t* out2;           // GEMM1 that also saves a | u (MODE 3): [T*k, 2m]
     int group;              // work order: groups of this many tiles, panel-major inside
 };
 
@@ -309,11 +311,10 @@ grouped_gemm_mfma(MfmaArgs g) {
     // of token row l%16 of its block (for 32x32 tiles, column
     // 8*(v/4) + 4*(l/32) + v%4 of token row l%32): runs of four consecutive
     // outputs per lane.
-    if (MODE == 0) {
+    if ((MODE == 0 || MODE == 3) && active) {
         // GEMM1: H = silu(gate) * up, stored straight from registers, one
         // 8-byte write per run (gate and up tiles of the same columns sit in
         // the same lanes)
-        if (!active) return;
         const int ncol0 = 4 * (lane / MT);
         constexpr int NA4 = ACCN / 4;           // runs of four per tile
         constexpr int A4STEP = MT == 32 ? 8 : 0;
@@ -339,8 +340,9 @@ grouped_gemm_mfma(MfmaArgs g) {
                 }
             }
         }
-        return;
     }
+    // MODE 3 goes on to save the pre-activations a | u as MODE 2 stores them
+    if (MODE == 0) return;
 
     // GEMM2 (route weight times the output) and the pre-activations (a and u)
     // are staged: the rounded outputs go into this wavefront's LDS region (64
@@ -356,7 +358,8 @@ grouped_gemm_mfma(MfmaArgs g) {
     if (!active) return;
     static_assert(MT == 16, "staged epilogue assumes 16x16 MFMA tiles");
     constexpr int CW = MODE == 1 ? WN : WN / 2;          // columns per output block
-    constexpr int NB = MODE == 2 ? 2 : 1;                 // output blocks per wavefront
+    constexpr bool kPreact = MODE == 2 || MODE == 3;     // stores a | u
+    constexpr int NB = kPreact ? 2 : 1;                   // output blocks per wavefront
     constexpr int RB = CW * 2;                            // bytes per staged row
     constexpr int NCH = RB / 16;                          // 16-byte chunks per row
     unsigned char* stage_w = lds + wave * (NB * WM * RB);
@@ -371,7 +374,7 @@ grouped_gemm_mfma(MfmaArgs g) {
 #pragma unroll
         for (int j = 0; j < (MODE == 1 ? NJ : NJ / 2); ++j) {
             const int col = j * MT + ncol0;
-            if (MODE == 2) {
+            if (kPreact) {
 #pragma unroll
                 for (int half = 0; half < 2; ++half) {
                     const int jj = j + half * (NJ / 2);
@@ -395,18 +398,20 @@ grouped_gemm_mfma(MfmaArgs g) {
     __builtin_amdgcn_wave_barrier();
     constexpr int RPI = 64 / NCH;                         // rows per 64-lane pass
     const int rsub = lane / NCH, ch = lane % NCH;
+    bf16_t* const dst = MODE == 3 ? g.out2 : g.out;
+    const int ldo = MODE == 3 ? 2 * g.n_out : g.n_out;   // MODE 3: H rows are m, a | u rows 2m
 #pragma unroll
     for (int blk = 0; blk < NB; ++blk) {
         int colbase;
         if (MODE == 1) colbase = pn * BP + wc * WN;
-        else colbase = blk * (g.n_out / 2) + pn * 128 + wc * (WN / 2);
+        else colbase = blk * (ldo / 2) + pn * 128 + wc * (WN / 2);
 #pragma unroll
         for (int p = 0; p < WM / RPI; ++p) {
             const int row = p * RPI + rsub;
             const int r = wr * WM + row;
             u32x4 v = *(const u32x4*)(stage_w + blk * WM * RB + row * RB + ((ch ^ (row & (NCH - 1))) << 4));
             if (row & 8) v = u32x4{v[2], v[3], v[0], v[1]};
-            if (r < rows) *(u32x4*)(g.out + ((int64_t)row0 + r) * g.n_out + colbase + ch * 8) = v;
+            if (r < rows) *(u32x4*)(dst + ((int64_t)row0 + r) * ldo + colbase + ch * 8) = v;
         }
     }
 }
@@ -491,7 +496,7 @@ bool mfma_shape_ok(const pr2_moe_desc& d) {
 
 hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void* W_gate,
                                const void* W_up, const void* W_down, const float* gate,
-                               const ReplayWs& ws, hipStream_t s) {
+                               const ReplayWs& ws, hipStream_t s, void* au_out) {
     if (mfma_shape_ok(d)) {
         MfmaArgs g1{};
         g1.A = (const bf16_t*)x;
@@ -511,7 +516,12 @@ hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void*
         g1.group = kGroupGemm1;
         int64_t work = ws.max_tiles * g1.ntn;
         int64_t grid = ((work + kNumXcd - 1) / kNumXcd) * kNumXcd;
-        {
+        if (au_out) {
+            g1.out2 = (bf16_t*)au_out;
+            LaunchScope scope("gemm1_gate_up_swiglu_save", s);
+            hipLaunchKernelGGL(grouped_gemm_mfma<3>, dim3((unsigned)grid), dim3(kGemmThreads), 0,
+                               s, g1);
+        } else {
             LaunchScope scope("gemm1_gate_up_swiglu", s);
             hipLaunchKernelGGL(grouped_gemm_mfma<0>, dim3((unsigned)grid), dim3(kGemmThreads), 0,
                                s, g1);
@@ -537,6 +547,10 @@ hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void*
         return hipGetLastError();
     }
     static_assert(BM == 256, "generic kernels map one thread per tile row");
+    if (au_out) {
+        hipError_t e = launch_preact(d, x, W_gate, W_up, ws, au_out, s);
+        if (e != hipSuccess) return e;
+    }
     dim3 grid1((unsigned)ws.max_tiles, (unsigned)d.m);
     dim3 grid2((unsigned)ws.max_tiles, (unsigned)d.d);
     if (d.act_dtype == PR2_BF16) {

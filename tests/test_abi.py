@@ -188,6 +188,40 @@ def test_backward_rejects_bad_arguments():
     assert B.workspace_bytes(desc(k=0), B.OP_REPLAY_BWD) == 0
 
 
+def test_saved_activation_entry_points_reject_bad_arguments():
+    L = B.lib()
+    d = desc()
+
+    def fwd_save(dd=d, au=FAKE, y=FAKE):
+        ws = B.workspace_bytes(dd, B.OP_REPLAY_FWD)
+        st = L.pr2_moe_replay_forward_save(byref(dd), c_void_p(FAKE), c_void_p(FAKE), dd.k,
+                                           c_void_p(FAKE), None, c_void_p(FAKE), c_void_p(FAKE),
+                                           c_void_p(FAKE), c_void_p(y), None, c_void_p(au),
+                                           c_void_p(FAKE), ws, None)
+        return B.STATUS[st], L.pr2_last_error().decode()
+
+    def bwd_saved(dd=d, au=FAKE, dx=FAKE):
+        ws = B.workspace_bytes(dd, B.OP_REPLAY_BWD)
+        st = L.pr2_moe_replay_backward_saved(byref(dd), c_void_p(FAKE), c_void_p(FAKE), dd.k,
+                                             c_void_p(FAKE), None, c_void_p(FAKE),
+                                             c_void_p(FAKE), c_void_p(FAKE), c_void_p(au),
+                                             c_void_p(FAKE), c_void_p(dx), c_void_p(FAKE), None,
+                                             c_void_p(FAKE), c_void_p(FAKE), c_void_p(FAKE),
+                                             c_void_p(FAKE), ws, None)
+        return B.STATUS[st], L.pr2_last_error().decode()
+
+    assert fwd_save(au=0)[0] == "PR2_ERR_NULL"
+    assert fwd_save(au=FAKE + 8)[0] == "PR2_ERR_ALIGN"
+    assert fwd_save(y=0)[0] == "PR2_ERR_NULL"             # the forward's own checks still run
+    assert bwd_saved(au=0)[0] == "PR2_ERR_NULL"
+    assert bwd_saved(au=FAKE + 8)[0] == "PR2_ERR_ALIGN"
+    assert bwd_saved(dx=0)[0] == "PR2_ERR_NULL"
+    assert bwd_saved(desc(renorm=False, N=128, k=65))[0] == "PR2_ERR_UNSUPPORTED"
+    assert fwd_save(desc(act=7))[0] == "PR2_ERR_DTYPE"
+    for st, msg in (fwd_save(), bwd_saved()):
+        assert st in ("PR2_ERR_DEVICE", "PR2_OK"), msg
+
+
 def test_valid_call_without_gpu_reports_device():
     import torch
     if torch.cuda.is_available():
