@@ -896,12 +896,16 @@ struct RouterTile {
 // and each of them would stream every weight of the projection through one CU.
 // Phase 1 gives workgroup (tile, pair) the two K steps of one K pair and
 // stores their fp32 sum as the fused loop forms it, thread by thread; a
-// reduction kernel adds the pairs of every accumulator in K order in fp64 and
-// rounds once, as the fused loop does; phase 2 takes those logits and runs
-// the epilogue.  The logits are bitwise those of the fused kernel.
+// reduction kernel adds the pairs of every accumulator in K order in fp64,
+// rounds once, as the fused loop does, and stores the logits token-major;
+// phase 2 runs the epilogue over half tiles of kRTM2 tokens, so that twice as
+// many workgroups share the serial top-k rounds.  The logits are bitwise those
+// of the fused kernel.
+constexpr int kRTM2 = kRTM / 2;           // tokens per phase-2 workgroup
+
 struct SplitK {
     float* part;       // [npairs][tiles][kRThreads][8 NTW]: phase 1 output
-    float* logit;      // [tiles][kRThreads][8 NTW]: the reduction's output, phase 2 input
+    float* logit;      // [tiles * kRTM][NCp]: the reduction's output, phase 2 input
 };
 
 template <int NTW, int MODE, int PHASE>   // MODE 0: rollout, 1: replay; PHASE 0: fused, 1, 2: split-K
@@ -916,7 +920,9 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
     static_assert(NSTAGE * RT::STAGEB >= (int)sizeof(float) * (kRTM * NCp + NCp + kRTM * 64 + 257),
                   "logit tile, bias, staged ids and the deviation histogram must fit over the "
                   "copy stages");
-    const int64_t t0 = (int64_t)blockIdx.x * kRTM;
+    // tokens this workgroup's epilogue covers
+    constexpr int TOK = PHASE == 2 ? kRTM2 : kRTM;
+    const int64_t t0 = (int64_t)blockIdx.x * TOK;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar branches
@@ -968,7 +974,7 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
         for (int i = 0; i < kIdsPerThread; ++i) {
             const int e = tid + kRThreads * i;
             const int tok = e / ro.k, slot = e % ro.k;
-            pre_ids[i] = (e < kRTM * ro.k && t0 + tok < T)
+            pre_ids[i] = (e < TOK * ro.k && t0 + tok < T)
                              ? load_id(ro.idx, ro.idx_dtype, (t0 + tok) * ro.ldi + slot) : -1;
         }
     }
@@ -1051,20 +1057,26 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
         return;
     }
     __syncthreads();
-    // logits -> LDS [kRTM][NC]; 16x16 accumulator element v of lane l is C[4*(l/16)+v][l%16]
+    // logits -> LDS [TOK][NC]; 16x16 accumulator element v of lane l is C[4*(l/16)+v][l%16]
     float* lg = (float*)lds;
+    if (PHASE == 2) {
+        // token-major rows of the reduction (rows up to the last tile's end exist)
+        for (int e = tid; e < TOK * NC; e += kRThreads) {
+            const int tok = e / NC;
+            lg[e] = sk.logit[(t0 + tok) * NCp + (e - tok * NC)];
+        }
+    } else {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int t = 0; t < NTW; ++t)
+            for (int t = 0; t < NTW; ++t)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int tok = wr * 32 + i * 16 + 4 * (lane >> 4) + v;
-                const int col = (wc * NTW + t) * 16 + (lane & 15);
-                if (col < NC)
-                    lg[tok * NC + col] = PHASE == 2 ? sk.logit[(my_acc + i * NTW + t) * 4 + v]
-                                                    : (float)acc64[i][t][v];
-            }
+                for (int v = 0; v < 4; ++v) {
+                    const int tok = wr * 32 + i * 16 + 4 * (lane >> 4) + v;
+                    const int col = (wc * NTW + t) * 16 + (lane & 15);
+                    if (col < NC) lg[tok * NC + col] = (float)acc64[i][t][v];
+                }
+    }
     // the router bias and (replay) the staged ids go behind the logit tile
     float* sbias = lg + kRTM * NC;
     int* sids = (int*)(sbias + N);
@@ -1079,7 +1091,7 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
 #pragma unroll
         for (int i = 0; i < kIdsPerThread; ++i) {
             const int e = tid + kRThreads * i;
-            if (e < kRTM * ro.k) sids[e] = pre_ids[i];
+            if (e < TOK * ro.k) sids[e] = pre_ids[i];
         }
     }
     __syncthreads();
@@ -1087,7 +1099,7 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
                                     ro.diag.hist || ro.diag.p_out);
     if (diag) {
         // diagnostics: four tokens per wavefront, one per 16-lane group
-        for (int base = wave * 4; base < kRTM; base += (kRThreads / 64) * 4) {
+        for (int base = wave * 4; base < TOK; base += (kRThreads / 64) * 4) {
             if (t0 + base >= T) break;
             const int tt = base + (lane >> 4);
             const int64_t t = t0 + tt;
@@ -1105,7 +1117,7 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
         return;
     }
     // four tokens per wavefront, one per 16-lane group
-    for (int base = wave * 4; base < kRTM; base += (kRThreads / 64) * 4) {
+    for (int base = wave * 4; base < TOK; base += (kRThreads / 64) * 4) {
         if (t0 + base >= T) break;
         const int tt = base + (lane >> 4);
         const int64_t t = t0 + tt;
@@ -1131,10 +1143,24 @@ size_t router_smem(const ProjArgs& a) {
 
 int ncp_of(int NC) { return ((NC + 63) / 64) * 64; }
 
-// logit[q] = fp32 of the fp64 sum over K pairs p (in order) of part[p][q]
+// The fp32 of the fp64 sum over K pairs p (in order) of part[p][q], stored at
+// the token-major position of accumulator q: q counts, from the fastest, the
+// element v of a 4-vector, the vector (i, t) of a thread, the thread of a
+// workgroup and the tile (the phase-1 layout).
 __global__ void __launch_bounds__(256)
-router_pair_sum_kernel(const float* part, int npairs, int64_t n, float* logit) {
+router_pair_sum_kernel(const float* part, int npairs, int64_t n, int ntw, float* logit) {
+    const int ncp = 64 * ntw;
     for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < n; q += (int64_t)gridDim.x * 256) {
+        const int v = (int)(q & 3);
+        const int64_t vec = q >> 2;
+        const int it = (int)(vec % (2 * ntw));
+        const int64_t thr = vec / (2 * ntw);
+        const int tid = (int)(thr % kRThreads);
+        const int64_t tile = thr / kRThreads;
+        const int wave = tid >> 6, lane = tid & 63;
+        const int i = it / ntw, t = it - i * ntw;
+        const int64_t tok = tile * kRTM + (wave >> 2) * 32 + i * 16 + 4 * (lane >> 4) + v;
+        const int col = ((wave & 3) * ntw + t) * 16 + (lane & 15);
         double acc = 0.0;
         int p = 0;
         for (; p + 8 <= npairs; p += 8) {      // eight loads in flight, added in K order
@@ -1145,7 +1171,7 @@ router_pair_sum_kernel(const float* part, int npairs, int64_t n, float* logit) {
             for (int i = 0; i < 8; ++i) acc += (double)v[i];
         }
         for (; p < npairs; ++p) acc += (double)part[(int64_t)p * n + q];
-        logit[q] = (float)acc;
+        logit[tok * ncp + col] = (float)acc;
     }
 }
 
@@ -1196,10 +1222,11 @@ hipError_t launch_router_mfma(const pr2_moe_desc& d, int NC, int r, const void* 
     int64_t blocks = (n + 255) / 256;
     if (blocks > 2048) blocks = 2048;
     hipLaunchKernelGGL(router_pair_sum_kernel, dim3((unsigned)blocks), dim3(256), 0, s, sk.part,
-                       npairs, n, sk.logit);
+                       npairs, n, NTW, sk.logit);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    const dim3 grid2((unsigned)((d.T + kRTM2 - 1) / kRTM2));
     switch (NTW) {
-#define PR2_CASE(n) case n: hipLaunchKernelGGL((router_mfma_kernel<n, MODE, 2>), grid, dim3(kRThreads), 0, s, xb, Ws, d.T, d.d, d.N, r, NC, po, ro, sk); break;
+#define PR2_CASE(n) case n: hipLaunchKernelGGL((router_mfma_kernel<n, MODE, 2>), grid2, dim3(kRThreads), 0, s, xb, Ws, d.T, d.d, d.N, r, NC, po, ro, sk); break;
         PR2_CASE(1) PR2_CASE(2) PR2_CASE(3)
 #undef PR2_CASE
         default: return hipErrorInvalidValue;
