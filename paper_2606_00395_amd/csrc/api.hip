@@ -530,9 +530,11 @@ static pr2_status replay_forward_impl(const pr2_moe_desc* desc, const void* x, c
         if (e != hipSuccess) return hip_fail(e, "error-word reset");
     }
     float* gate = gate_out ? gate_out : w.gate;
-    e = launch_replay_gates(d, x, idx, ldi, W_r, b_r, gate, w.err, w.wsplit, st, diag);
+    const bool counted = replay_counts_fused(d);
+    e = launch_replay_gates(d, x, idx, ldi, W_r, b_r, gate, w.err, w.wsplit, st, diag,
+                            counted ? w.bcount : nullptr);
     if (e != hipSuccess) return hip_fail(e, "replay_gates launch");
-    e = launch_permute(d, idx, ldi, w, st);
+    e = launch_permute(d, idx, ldi, w, st, counted);
     if (e != hipSuccess) return hip_fail(e, "permute launch");
     e = launch_expert_gemms(d, x, W_gate, W_up, W_down, gate, w, st, au_out);
     if (e != hipSuccess) return hip_fail(e, "expert GEMM launch");
@@ -702,9 +704,10 @@ static pr2_status replay_backward_impl(const pr2_moe_desc* desc, const void* x, 
     // the paper-literal weights also need every token's N logits
     RouteDiag logits{};
     logits.p_out = w.plog;
+    const bool counted = replay_counts_fused(d);
     e = launch_replay_gates(d, x, idx, ldi, W_r, b_r, w.fw.gate, w.fw.err, w.fw.wsplit, st,
-                            d.renorm == 0 ? &logits : nullptr);
-    if (e == hipSuccess) e = launch_permute(d, idx, ldi, w.fw, st);
+                            d.renorm == 0 ? &logits : nullptr, counted ? w.fw.bcount : nullptr);
+    if (e == hipSuccess) e = launch_permute(d, idx, ldi, w.fw, st, counted);
     if (e != hipSuccess) return hip_fail(e, "replay_gates / permute launch");
     e = launch_replay_backward(d, x, idx, ldi, W_r, W_gate, W_up, W_down, dy, w.fw.gate, w, out,
                                st, au_saved);

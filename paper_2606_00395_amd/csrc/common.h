@@ -160,9 +160,18 @@ struct RouteDiag {
     unsigned long long* hist;   // [k + 1], zeroed by the launch
     float* p_out;               // [T, N] the current logits p
 };
+// counts (or null): also write the permutation's per-block expert counts
+// ([N][nblk], blocks of perm_tokens_per_block(k) tokens) and count the
+// out-of-range ids, as the permutation's count pass does; only where
+// replay_counts_fused(d) holds
 hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void* idx, int64_t ldi,
                                const float* W_r, const float* b_r, float* gate_out, int* err,
-                               void* split_ws, hipStream_t s, const RouteDiag* diag = nullptr);
+                               void* split_ws, hipStream_t s, const RouteDiag* diag = nullptr,
+                               int* counts = nullptr);
+// whether the replay-weight pass can form the permutation's counts: the fused
+// MFMA router (not its split-K form) with k in {8, 16, 32, 64}, whose count
+// blocks (512 / k tokens) tile its 64-token workgroups
+bool replay_counts_fused(const pr2_moe_desc& d);
 
 hipError_t launch_route_diagnostics(const pr2_moe_desc& d, const void* x, const void* idx,
                                     int64_t ldi, const float* W_r, const float* b_r,
@@ -170,8 +179,10 @@ hipError_t launch_route_diagnostics(const pr2_moe_desc& d, const void* x, const 
                                     unsigned long long* hist, void* split_ws, hipStream_t s);
 
 // permute.hip
+// counted: the per-block counts and the out-of-range count are already in the
+// workspace (written by the replay-weight pass)
 hipError_t launch_permute(const pr2_moe_desc& d, const void* idx, int64_t ldi, const ReplayWs& ws,
-                          hipStream_t s);
+                          hipStream_t s, bool counted = false);
 hipError_t launch_combine(const pr2_moe_desc& d, const ReplayWs& ws, void* y, hipStream_t s);
 // p[0..n) = 0 (one workgroup; for the few error words)
 hipError_t launch_zero_i32(int* p, int n, hipStream_t s);

@@ -13,7 +13,9 @@
 //           each entry's position is its block base + the entries of the same
 //           expert before it.  perm_src[pos] = t*k + s, inv[t*k + s] = pos.
 // Out-of-range ids are not dispatched (inv = -1); the count pass is the one
-// place that counts them (in the workspace's error words).
+// place that counts them (in the workspace's error words).  The replay forward
+// and backward form the counts in their replay-weight pass instead, where that
+// pass's workgroups cover whole count blocks (it also counts those ids then).
 //
 // Combine: y_t = sum over slots s (in slot order) of the weighted expert output
 // row O[inv[t*k + s]], accumulated in fp32 (Eq. pr2_output).
@@ -364,10 +366,10 @@ combine_kernel(const T* O, const int* inv, int64_t ntok, int k, int d, T* y) {
 }  // namespace
 
 hipError_t launch_permute(const pr2_moe_desc& d, const void* idx, int64_t ldi, const ReplayWs& ws,
-                          hipStream_t s) {
+                          hipStream_t s, bool counted) {
     const int tb = perm_tokens_per_block(d.k);
     const size_t sm = sizeof(int) * (size_t)d.N;
-    {
+    if (!counted) {
         LaunchScope scope("perm_count", s);
         hipLaunchKernelGGL(perm_count_kernel, dim3((unsigned)ws.nblk), dim3(64), sm, s, idx,
                            d.idx_dtype, ldi, d.T, d.k, d.N, tb, ws.nblk, ws.bcount, ws.err);

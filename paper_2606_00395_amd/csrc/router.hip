@@ -292,6 +292,9 @@ struct ReplayOut {
     int* err;
     int validate;
     DiagOut diag;
+    int* counts;          // the permutation's counts [N][nblk], or null
+    int64_t nblk;
+    int tb;               // tokens per count block (divides kRTM)
 };
 
 __device__ __forceinline__ double wave_sum_f64(double v) {
@@ -917,9 +920,10 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
     constexpr int NSTAGE = RT::NSTAGE;
     constexpr int GPW = RT::GPW;
     __shared__ __attribute__((aligned(1024))) unsigned char lds[NSTAGE * RT::STAGEB];
-    static_assert(NSTAGE * RT::STAGEB >= (int)sizeof(float) * (kRTM * NCp + NCp + kRTM * 64 + 257),
-                  "logit tile, bias, staged ids and the deviation histogram must fit over the "
-                  "copy stages");
+    static_assert(NSTAGE * RT::STAGEB >=
+                      (int)sizeof(float) * (kRTM * NCp + NCp + kRTM * 64 + 257 + 8 * NCp),
+                  "logit tile, bias, staged ids, the deviation histogram and the count "
+                  "blocks' histograms must fit over the copy stages");
     // tokens this workgroup's epilogue covers
     constexpr int TOK = PHASE == 2 ? kRTM2 : kRTM;
     const int64_t t0 = (int64_t)blockIdx.x * TOK;
@@ -1087,6 +1091,12 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
     const bool lds_hist = MODE == 1 && ro.diag.hist != nullptr;
     if (lds_hist)
         for (int i = tid; i <= ro.k; i += kRThreads) shist[i] = 0u;
+    // the permutation's expert counts of the count blocks inside this tile
+    // (kRTM / tb <= 8 of them), after the deviation histogram
+    const bool fcount = MODE == 1 && PHASE == 0 && ro.counts != nullptr && stage_ids;
+    int* chist = (int*)(shist + 257);
+    const int nsub = fcount ? kRTM / ro.tb : 0;
+    for (int i = tid; i < nsub * N; i += kRThreads) chist[i] = 0;
     if (stage_ids) {
 #pragma unroll
         for (int i = 0; i < kIdsPerThread; ++i) {
@@ -1095,6 +1105,24 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
         }
     }
     __syncthreads();
+    if (fcount) {
+        int bad = 0;
+        for (int e = tid; e < kRTM * ro.k; e += kRThreads) {
+            const int tok = e / ro.k;
+            if (t0 + tok >= T) break;
+            const int id = sids[e];
+            if (id >= 0 && id < N) atomicAdd(&chist[(tok / ro.tb) * N + id], 1);
+            else ++bad;
+        }
+        bad = wave_sum_i32(bad);
+        if (lane == 0 && bad) atomicAdd(ro.err + ERR_BAD_ID, bad);
+        __syncthreads();
+        const int64_t b0 = (int64_t)blockIdx.x * nsub;
+        for (int i = tid; i < nsub * N; i += kRThreads) {
+            const int sub = i / N;
+            if (b0 + sub < ro.nblk) ro.counts[(int64_t)(i - sub * N) * ro.nblk + b0 + sub] = chist[i];
+        }
+    }
     const bool diag = MODE == 1 && (ro.diag.cur_idx || ro.diag.overlap || ro.diag.kl ||
                                     ro.diag.hist || ro.diag.p_out);
     if (diag) {
@@ -1354,9 +1382,15 @@ hipError_t launch_router_replay(const pr2_moe_desc& d, const void* x, const floa
 
 }  // namespace
 
+bool replay_counts_fused(const pr2_moe_desc& d) {
+    return router_mfma_ok(d, d.N) && !use_splitk(d) &&
+           (d.k == 8 || d.k == 16 || d.k == 32 || d.k == 64);
+}
+
 hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void* idx, int64_t ldi,
                                const float* W_r, const float* b_r, float* gate_out, int* err,
-                               void* split_ws, hipStream_t s, const RouteDiag* diag) {
+                               void* split_ws, hipStream_t s, const RouteDiag* diag,
+                               int* counts) {
     const char* v = getenv("PR2_VALIDATE");
     DiagOut g{};
     if (diag) {
@@ -1372,6 +1406,12 @@ hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void*
     }
     ReplayOut o{b_r, d.k, d.renorm, idx, d.idx_dtype, ldi, gate_out, err,
                 (v && v[0] == '1') ? 1 : 0, g};
+    if (counts) {
+        if (!replay_counts_fused(d)) return hipErrorInvalidValue;
+        o.counts = counts;
+        o.tb = perm_tokens_per_block(d.k);
+        o.nblk = (d.T + o.tb - 1) / o.tb;
+    }
     return launch_router_replay(d, x, W_r, o, split_ws, "replay_gates", s);
 }
 

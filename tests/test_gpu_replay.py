@@ -72,6 +72,11 @@ CASES = [
     (70, 256, 128, 8, 128, "bf16", "hot8", True, "int32", 0, "few_tokens_many_experts"),
     (40, 256, 512, 256, 128, "bf16", "none", True, "int32", 0, "k256_N512_max_route"),
     (33, 64, 1024, 96, 32, "f32", "zipf", False, "int16", 1, "N1024_literal_generic"),
+    # more than 32 tiles of 64 tokens: the replay-weight pass forms the
+    # permutation's counts (k = 8, 16, 32, 64), ragged last tile
+    (4100, 256, 64, 16, 128, "bf16", "zipf", True, "int16", 3, "fused_counts_k16"),
+    (2113, 256, 64, 32, 128, "bf16", "hot8", False, "int32", 0, "fused_counts_k32"),
+    (2177, 128, 128, 64, 128, "bf16", "none", True, "int32", 1, "fused_counts_k64"),
 ]
 
 
@@ -146,10 +151,22 @@ def test_replay_validate_flags_bad_routes(qwen30b):
     os.environ["PR2_VALIDATE"] = "1"
     try:
         run_replay(D, idx[:n], x=x)     # valid route passes
-        for r in (bad, dup):
+        for r, what in ((bad, "2 out-of-range and 0 repeated"),
+                        (dup, "0 out-of-range and 1 repeated")):
             with pytest.raises(B.Pr2Error) as ei:
                 run_replay(D, r, x=x)
-            assert ei.value.status == 7
+            assert ei.value.status == 7 and what in str(ei.value), str(ei.value)
+        # 4096 tokens: the counts (and the out-of-range count) come from the
+        # replay-weight pass, which must count each bad id once
+        n = 4096
+        bad = idx[:n].copy()
+        bad[3, 2] = s.N + 5
+        bad[3000, 1] = -1
+        bad[4095, 7] = 1 << 20
+        with pytest.raises(B.Pr2Error) as ei:
+            run_replay(D, bad, x=D["x"][:n])
+        assert ei.value.status == 7 and "3 out-of-range and 0 repeated" in str(ei.value), \
+            str(ei.value)
     finally:
         del os.environ["PR2_VALIDATE"]
 
