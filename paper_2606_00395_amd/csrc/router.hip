@@ -1064,11 +1064,11 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
     // logits -> LDS [TOK][NC]; 16x16 accumulator element v of lane l is C[4*(l/16)+v][l%16]
     float* lg = (float*)lds;
     if (PHASE == 2) {
-        // token-major rows of the reduction (rows up to the last tile's end exist)
-        for (int e = tid; e < TOK * NC; e += kRThreads) {
-            const int tok = e / NC;
-            lg[e] = sk.logit[(t0 + tok) * NCp + (e - tok * NC)];
-        }
+        // token-major rows of the reduction (rows up to the last tile's end
+        // exist), a wavefront per row
+        for (int tok = wave; tok < TOK; tok += kRThreads / 64)
+            for (int col = lane; col < NC; col += 64)
+                lg[tok * NC + col] = sk.logit[(t0 + tok) * NCp + col];
     } else {
 #pragma unroll
         for (int i = 0; i < 2; ++i)
