@@ -631,10 +631,12 @@ pr2_status pr2_moe_rollout_forward(const pr2_moe_desc* desc, const void* x, cons
     ReplayWs w = rollout_ws_layout(d, ws);
     drop_split_records(ws, ws_bytes);
     float* gate = gate_out ? gate_out : w.gate;
+    bool counted = false;
     hipError_t e = launch_route_predict(d, x, W_r, b_r, A, B, idx_out, ldi, gate, logits_out,
-                                        w.wsplit, st);
+                                        w.wsplit, st, FeatureCache{}, false, true, w.bcount,
+                                        &counted);
     if (e != hipSuccess) return hip_fail(e, "route_predict launch");
-    e = launch_permute(d, idx_out, ldi, w, st);
+    e = launch_permute(d, idx_out, ldi, w, st, counted);
     if (e != hipSuccess) return hip_fail(e, "permute launch");
     e = launch_expert_gemms(d, x, W_gate, W_up, W_down, gate, w, st);
     if (e != hipSuccess) return hip_fail(e, "expert GEMM launch");

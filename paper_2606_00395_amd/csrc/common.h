@@ -145,7 +145,10 @@ hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const floa
                                 const float* b_r, const float* A, const float* B, void* idx_out,
                                 int64_t ldi, float* gate_out, float* logits_out, void* split_ws,
                                 hipStream_t s, const FeatureCache& cache = FeatureCache{},
-                                bool reuse_split = false, bool splitk_ok = true);
+                                bool reuse_split = false, bool splitk_ok = true,
+                                int* counts = nullptr, bool* counted = nullptr);
+// (counts, counted: as launch_replay_gates' counts, for the ids this call
+// selects; *counted says whether the kernel path taken wrote them)
 // current router logits p = x W_r + b_r of every token into p_out [T, N]
 hipError_t launch_router_logits(const pr2_moe_desc& d, const void* x, const float* W_r,
                                 const float* b_r, float* p_out, void* split_ws, hipStream_t s);

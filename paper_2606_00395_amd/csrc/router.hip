@@ -144,6 +144,9 @@ struct PredictOut {
     const void* x;        // the layer input, for the hidden-feature copy
     int d;
     int act_dtype;
+    int* counts;          // the permutation's counts [N][nblk], or null
+    int64_t nblk;
+    int tb;               // tokens per count block (divides kRTM)
 };
 
 // k rounds of a wavefront arg-max over orderable keys (lane l holds ids
@@ -533,7 +536,7 @@ __device__ __forceinline__ int gsum_i32(int v) {
 // Rollout epilogue of token t (valid: t < T) by one 16-lane group.
 template <int MAXV16>
 __device__ void predict_group(const float* row, int64_t t, bool valid, int N, int r,
-                              const PredictOut& o, const float* bias) {
+                              const PredictOut& o, const float* bias, int* lids = nullptr) {
     const int lane = threadIdx.x & 63;
     const int l16 = lane & 15, grp = lane >> 4;
     float* lrow = (valid && o.logits_out) ? o.logits_out + t * N : nullptr;
@@ -621,6 +624,7 @@ __device__ void predict_group(const float* row, int64_t t, bool valid, int N, in
             if (o.idx_dtype == PR2_I16) ((int16_t*)o.idx_out)[pos] = (int16_t)j;
             else ((int32_t*)o.idx_out)[pos] = j;
             if (o.gate_out) o.gate_out[t * o.k + rank] = e[v] / denom;
+            if (lids) lids[rank] = j;
         }
         before += __popc(gbits);
     }
@@ -1092,11 +1096,36 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
     if (lds_hist)
         for (int i = tid; i <= ro.k; i += kRThreads) shist[i] = 0u;
     // the permutation's expert counts of the count blocks inside this tile
-    // (kRTM / tb <= 8 of them), after the deviation histogram
-    const bool fcount = MODE == 1 && PHASE == 0 && ro.counts != nullptr && stage_ids;
+    // (kRTM / tb <= 8 of them), after the deviation histogram: from the staged
+    // recorded ids (replay), or from the ids the epilogue selects (rollout)
+    const bool fcount = PHASE == 0 && (MODE == 1 ? ro.counts != nullptr && stage_ids
+                                                 : po.counts != nullptr);
     int* chist = (int*)(shist + 257);
-    const int nsub = fcount ? kRTM / ro.tb : 0;
+    const int ctb = MODE == 1 ? ro.tb : po.tb;
+    const int nsub = fcount ? kRTM / ctb : 0;
     for (int i = tid; i < nsub * N; i += kRThreads) chist[i] = 0;
+    // histogram of ids[tok * k + s] over this tile's tokens, then its global
+    // store; every thread calls it (two barriers)
+    auto count_blocks = [&](int k, int* counts, int64_t nblk, int* err) {
+        int bad = 0;
+        for (int e = tid; e < kRTM * k; e += kRThreads) {
+            const int tok = e / k;
+            if (t0 + tok >= T) break;
+            const int id = sids[e];
+            if (id >= 0 && id < N) atomicAdd(&chist[(tok / ctb) * N + id], 1);
+            else ++bad;
+        }
+        if (err) {
+            bad = wave_sum_i32(bad);
+            if (lane == 0 && bad) atomicAdd(err + ERR_BAD_ID, bad);
+        }
+        __syncthreads();
+        const int64_t b0 = (int64_t)blockIdx.x * nsub;
+        for (int i = tid; i < nsub * N; i += kRThreads) {
+            const int sub = i / N;
+            if (b0 + sub < nblk) counts[(int64_t)(i - sub * N) * nblk + b0 + sub] = chist[i];
+        }
+    };
     if (stage_ids) {
 #pragma unroll
         for (int i = 0; i < kIdsPerThread; ++i) {
@@ -1105,24 +1134,7 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
         }
     }
     __syncthreads();
-    if (fcount) {
-        int bad = 0;
-        for (int e = tid; e < kRTM * ro.k; e += kRThreads) {
-            const int tok = e / ro.k;
-            if (t0 + tok >= T) break;
-            const int id = sids[e];
-            if (id >= 0 && id < N) atomicAdd(&chist[(tok / ro.tb) * N + id], 1);
-            else ++bad;
-        }
-        bad = wave_sum_i32(bad);
-        if (lane == 0 && bad) atomicAdd(ro.err + ERR_BAD_ID, bad);
-        __syncthreads();
-        const int64_t b0 = (int64_t)blockIdx.x * nsub;
-        for (int i = tid; i < nsub * N; i += kRThreads) {
-            const int sub = i / N;
-            if (b0 + sub < ro.nblk) ro.counts[(int64_t)(i - sub * N) * ro.nblk + b0 + sub] = chist[i];
-        }
-    }
+    if (MODE == 1 && fcount) count_blocks(ro.k, ro.counts, ro.nblk, ro.err);
     const bool diag = MODE == 1 && (ro.diag.cur_idx || ro.diag.overlap || ro.diag.kl ||
                                     ro.diag.hist || ro.diag.p_out);
     if (diag) {
@@ -1150,9 +1162,14 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
         const int tt = base + (lane >> 4);
         const int64_t t = t0 + tt;
         const bool valid = t < T;
-        if (MODE == 0) predict_group<4 * NTW>(lg + tt * NC, t, valid, N, r, po, sbias);
+        if (MODE == 0) predict_group<4 * NTW>(lg + tt * NC, t, valid, N, r, po, sbias,
+                                              fcount ? sids + tt * po.k : nullptr);
         else replay_group<4 * NTW>(lg + tt * NC, t, valid, N, ro, sbias,
                                    stage_ids ? sids + tt * ro.k : nullptr);
+    }
+    if (MODE == 0 && fcount) {
+        __syncthreads();
+        count_blocks(po.k, po.counts, po.nblk, nullptr);
     }
 }
 
@@ -1298,13 +1315,26 @@ hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const floa
                                 const float* b_r, const float* A, const float* B, void* idx_out,
                                 int64_t ldi, float* gate_out, float* logits_out, void* split_ws,
                                 hipStream_t s, const FeatureCache& cache, bool reuse_split,
-                                bool splitk_ok) {
+                                bool splitk_ok, int* counts, bool* counted) {
     // reuse_split: split_ws already holds this call's split (same weights, same layout)
     const float* Bn = d.r > 0 ? B : nullptr;
+    if (counted) *counted = false;
+    // the fused MFMA kernel (not its split-K form) also forms the permutation's
+    // counts when its 64-token tiles hold whole count blocks
+    auto add_counts = [&](PredictOut& o) {
+        if (!counts || (splitk_ok && use_splitk(d)) ||
+            !(d.k == 8 || d.k == 16 || d.k == 32 || d.k == 64))
+            return;
+        o.counts = counts;
+        o.tb = perm_tokens_per_block(d.k);
+        o.nblk = (d.T + o.tb - 1) / o.tb;
+        if (counted) *counted = true;
+    };
     if (logits_out == nullptr && cache.row == nullptr && router_mfma_ok(d, d.N)) {
         // the router logits are not wanted: fold the predictor into the weights
         PredictOut o{b_r, Bn, d.k, d.renorm, 1, idx_out, d.idx_dtype, ldi, gate_out, nullptr,
                      FeatureCache{}, x, d.d, d.act_dtype};
+        add_counts(o);
         if (!reuse_split) {
             hipError_t e = launch_split(W_r, A, Bn, d, d.r, 1, (bf16_t*)split_ws, s);
             if (e != hipSuccess) return e;
@@ -1317,6 +1347,7 @@ hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const floa
                  x, d.d, d.act_dtype};
     const int NC = d.N + d.r;
     if (router_mfma_ok(d, NC)) {
+        add_counts(o);
         if (!reuse_split) {
             hipError_t e = launch_split(W_r, A, Bn, d, d.r, 0, (bf16_t*)split_ws, s);
             if (e != hipSuccess) return e;

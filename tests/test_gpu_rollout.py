@@ -67,6 +67,10 @@ CASES = [
     (777, 512, 64, 6, 128, 5, "bf16", "zipf", "int16", 2, False, True),
     (300, 192, 8, 2, 96, 3, "bf16", "none", "int32", 0, True, True),      # generic GEMMs
     (129, 64, 32, 8, 48, 4, "f32", "hot8", "int32", 0, False, False),
+    # more than 32 tiles of 64 tokens: the route kernel forms the permutation's
+    # counts (folded and unfolded predictor), ragged last tile
+    (4100, 256, 64, 16, 128, 8, "bf16", "zipf", "int16", 3, True, False),
+    (2177, 128, 128, 32, 128, 4, "bf16", "hot8", "int32", 0, False, True),
 ]
 
 
