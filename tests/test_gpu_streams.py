@@ -5,7 +5,8 @@ stream and keeps no per-call device state outside the caller's workspace, so
   and workspace, give bitwise the outputs of the same calls made one after
   the other;
 * a replay backward captured into a HIP graph gives, on every replay, bitwise
-  the gradients of the eager call."""
+  the gradients of the eager call, and so does the training pass that saves
+  the pre-activations in its forward."""
 import threading
 
 import pytest
@@ -110,5 +111,44 @@ def test_backward_graph_replays_match_eager_call():
         graph.replay()
         torch.cuda.synchronize()
         assert same(p.outputs()[2:], eager), f"replay {rep}"
+        p.forward(st)             # eager work between replays
+        torch.cuda.synchronize()
+
+
+def test_training_pass_with_saved_preactivations_graph_replays_match_eager():
+    """pr2_moe_replay_forward_save then pr2_moe_replay_backward_saved, captured
+    into one HIP graph: every replay gives bitwise the eager outputs and
+    gradients (with other eager work between the replays)."""
+    import torch
+    from paper_2606_00395_amd import binding as B
+    p = Problem(24)
+    s = SHAPE
+    au = torch.empty((s.T * s.k, 2 * s.m), dtype=torch.bfloat16, device="cuda")
+
+    def step(st):
+        B.moe_replay_forward_save(p.x, p.idx, p.Wr, p.br, p.Wg, p.Wu, p.Wd, p.y, au, p.gate,
+                                  ws=p.ws_f, stream=st)
+        B.moe_replay_backward_saved(p.x, p.idx, p.Wr, p.br, p.Wg, p.Wu, p.Wd, au, p.dy, *p.grads,
+                                    ws=p.ws_b, stream=st)
+
+    st = torch.cuda.current_stream()
+    step(st)
+    torch.cuda.synchronize()
+    eager = p.outputs()
+    # the recomputing calls give the same outputs and gradients
+    p.forward(st)
+    p.backward(st)
+    torch.cuda.synchronize()
+    assert same(p.outputs(), eager), "saved and recomputing passes differ"
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step(torch.cuda.current_stream())
+    for rep in range(3):
+        for t in [p.y, p.gate] + p.grads:
+            t.fill_(float("nan"))
+        au.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        assert same(p.outputs(), eager), f"replay {rep}"
         p.forward(st)             # eager work between replays
         torch.cuda.synchronize()
