@@ -902,17 +902,17 @@ struct RouterTile {
 // Split-K for small token counts: a few 64-token tiles cannot fill the GPU,
 // and each of them would stream every weight of the projection through one CU.
 // Phase 1 gives workgroup (tile, pair) the two K steps of one K pair and
-// stores their fp32 sum as the fused loop forms it, thread by thread; a
-// reduction kernel adds the pairs of every accumulator in K order in fp64,
-// rounds once, as the fused loop does, and stores the logits token-major;
-// phase 2 runs the epilogue over half tiles of kRTM2 tokens, so that twice as
-// many workgroups share the serial top-k rounds.  The logits are bitwise those
-// of the fused kernel.
-constexpr int kRTM2 = kRTM / 2;           // tokens per phase-2 workgroup
+// stores their fp32 sum as the fused loop forms it, token-major; phase 2 adds
+// the pairs of each logit in K order in fp64 and rounds once, as the fused
+// loop does, then runs the epilogue, over workgroups of kRTM2 tokens (more
+// workgroups share the serial top-k rounds and the pair sums).  The logits
+// are bitwise those of the fused kernel.
+constexpr int kRTM2 = 16;                 // tokens per phase-2 workgroup
 
 struct SplitK {
-    float* part;       // [npairs][tiles][kRThreads][8 NTW]: phase 1 output
-    float* logit;      // [tiles * kRTM][NCp]: the reduction's output, phase 2 input
+    float* part;       // [npairs][rows][NCp]: phase 1 output, token-major
+    int64_t rows;      // tiles * kRTM
+    int npairs;
 };
 
 template <int NTW, int MODE, int PHASE>   // MODE 0: rollout, 1: replay; PHASE 0: fused, 1, 2: split-K
@@ -1003,8 +1003,6 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
     // K steps of this workgroup: all (fused), one pair (phase 1), none (phase 2)
     const int kb = PHASE == 1 ? (int)blockIdx.y * 2 : 0;
     const int ke = PHASE == 1 ? min(nk, kb + 2) : (PHASE == 2 ? 0 : nk);
-    // this thread's accumulators in the split-K buffers: 2 NTW vectors of 4
-    const int64_t my_acc = ((int64_t)blockIdx.x * kRThreads + tid) * (2 * NTW);
 #pragma unroll
     for (int st = 0; st < NSTAGE - 1; ++st)
         if (kb + st < ke) issue(st, kb + st);
@@ -1055,24 +1053,67 @@ router_mfma_kernel(const bf16_t* x, const bf16_t* Ws, int64_t T, int d, int N, i
         }
     }
     if (PHASE == 1) {
-        // the pair's sum (no global store inside the loop: the compiler would
-        // then wait for every copy in flight before each LDS read)
-        f32x4* pp = (f32x4*)sk.part + (int64_t)blockIdx.y * gridDim.x * kRThreads * (2 * NTW) + my_acc;
+        // the pair's sums, token-major (no global store inside the loop: the
+        // compiler would then wait for every copy in flight before each LDS read)
+        float* pp = sk.part + ((int64_t)blockIdx.y * sk.rows + (int64_t)blockIdx.x * kRTM) * NCp;
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
-            for (int t = 0; t < NTW; ++t) pp[i * NTW + t] = acc[i][t];
+            for (int t = 0; t < NTW; ++t)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int tok = wr * 32 + i * 16 + 4 * (lane >> 4) + v;
+                    const int col = (wc * NTW + t) * 16 + (lane & 15);
+                    pp[tok * NCp + col] = acc[i][t][v];
+                }
         return;
     }
     __syncthreads();
     // logits -> LDS [TOK][NC]; 16x16 accumulator element v of lane l is C[4*(l/16)+v][l%16]
     float* lg = (float*)lds;
     if (PHASE == 2) {
-        // token-major rows of the reduction (rows up to the last tile's end
-        // exist), a wavefront per row
-        for (int tok = wave; tok < TOK; tok += kRThreads / 64)
-            for (int col = lane; col < NC; col += 64)
-                lg[tok * NC + col] = sk.logit[(t0 + tok) * NCp + col];
+        // logit (row wave + 8 a, column lane + 64 b): the fp64 sum over the K
+        // pairs, in order, of phase 1's partial sums, rounded once; eight
+        // pairs of every element are loaded before any is added (rows up to
+        // the last tile's end exist)
+        static_assert(TOK % (kRThreads / 64) == 0, "rows per wavefront");
+        constexpr int RPW = TOK / (kRThreads / 64);
+        const int64_t pstride = sk.rows * NCp;
+        const float* src = sk.part + (t0 + wave) * NCp + lane;
+        double s[RPW][NTW];
+#pragma unroll
+        for (int a = 0; a < RPW; ++a)
+#pragma unroll
+            for (int b = 0; b < NTW; ++b) s[a][b] = 0.0;
+        int p0 = 0;
+        for (; p0 + 8 <= sk.npairs; p0 += 8) {
+            float v[8][RPW][NTW];
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+#pragma unroll
+                for (int a = 0; a < RPW; ++a)
+#pragma unroll
+                    for (int b = 0; b < NTW; ++b)
+                        v[q][a][b] = src[(int64_t)(p0 + q) * pstride + a * (kRThreads / 64) * NCp + b * 64];
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+#pragma unroll
+                for (int a = 0; a < RPW; ++a)
+#pragma unroll
+                    for (int b = 0; b < NTW; ++b) s[a][b] += (double)v[q][a][b];
+        }
+        for (; p0 < sk.npairs; ++p0)
+#pragma unroll
+            for (int a = 0; a < RPW; ++a)
+#pragma unroll
+                for (int b = 0; b < NTW; ++b)
+                    s[a][b] += (double)src[(int64_t)p0 * pstride + a * (kRThreads / 64) * NCp + b * 64];
+#pragma unroll
+        for (int a = 0; a < RPW; ++a)
+#pragma unroll
+            for (int b = 0; b < NTW; ++b)
+                if (lane + 64 * b < NC)
+                    lg[(wave + a * (kRThreads / 64)) * NC + lane + 64 * b] = (float)s[a][b];
     } else {
 #pragma unroll
         for (int i = 0; i < 2; ++i)
@@ -1188,37 +1229,6 @@ size_t router_smem(const ProjArgs& a) {
 
 int ncp_of(int NC) { return ((NC + 63) / 64) * 64; }
 
-// The fp32 of the fp64 sum over K pairs p (in order) of part[p][q], stored at
-// the token-major position of accumulator q: q counts, from the fastest, the
-// element v of a 4-vector, the vector (i, t) of a thread, the thread of a
-// workgroup and the tile (the phase-1 layout).
-__global__ void __launch_bounds__(256)
-router_pair_sum_kernel(const float* part, int npairs, int64_t n, int ntw, float* logit) {
-    const int ncp = 64 * ntw;
-    for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < n; q += (int64_t)gridDim.x * 256) {
-        const int v = (int)(q & 3);
-        const int64_t vec = q >> 2;
-        const int it = (int)(vec % (2 * ntw));
-        const int64_t thr = vec / (2 * ntw);
-        const int tid = (int)(thr % kRThreads);
-        const int64_t tile = thr / kRThreads;
-        const int wave = tid >> 6, lane = tid & 63;
-        const int i = it / ntw, t = it - i * ntw;
-        const int64_t tok = tile * kRTM + (wave >> 2) * 32 + i * 16 + 4 * (lane >> 4) + v;
-        const int col = ((wave & 3) * ntw + t) * 16 + (lane & 15);
-        double acc = 0.0;
-        int p = 0;
-        for (; p + 8 <= npairs; p += 8) {      // eight loads in flight, added in K order
-            float v[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) v[i] = part[(int64_t)(p + i) * n + q];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) acc += (double)v[i];
-        }
-        for (; p < npairs; ++p) acc += (double)part[(int64_t)p * n + q];
-        logit[tok * ncp + col] = (float)acc;
-    }
-}
 
 // split-K below this many 64-token tiles, for K loops of at least kSplitMinSteps
 constexpr int kSplitMaxTiles = 32;
@@ -1241,7 +1251,7 @@ hipError_t launch_router_mfma(const pr2_moe_desc& d, int NC, int r, const void* 
     const int64_t tiles = (d.T + kRTM - 1) / kRTM;
     dim3 grid((unsigned)tiles);
     const bf16_t* xb = (const bf16_t*)x;
-    SplitK sk{nullptr, nullptr};
+    SplitK sk{nullptr, 0, 0};
     if (!splitk_ok || !use_splitk(d)) {
         switch (NTW) {
 #define PR2_CASE(n) case n: hipLaunchKernelGGL((router_mfma_kernel<n, MODE, 0>), grid, dim3(kRThreads), 0, s, xb, Ws, d.T, d.d, d.N, r, NC, po, ro, sk); break;
@@ -1252,9 +1262,9 @@ hipError_t launch_router_mfma(const pr2_moe_desc& d, int NC, int r, const void* 
         return hipGetLastError();
     }
     const int npairs = (d.d / kRBK + 1) / 2;
-    const int64_t n = tiles * kRTM * ncp_of(NC);     // accumulators of all tiles
     sk.part = (float*)((char*)Ws + split_weight_bytes(NC, d.d));
-    sk.logit = sk.part + (int64_t)npairs * n;
+    sk.rows = tiles * kRTM;
+    sk.npairs = npairs;
     dim3 pgrid((unsigned)tiles, (unsigned)npairs);
     switch (NTW) {
 #define PR2_CASE(n) case n: hipLaunchKernelGGL((router_mfma_kernel<n, 0, 1>), pgrid, dim3(kRThreads), 0, s, xb, Ws, d.T, d.d, d.N, r, NC, po, ro, sk); break;
@@ -1264,11 +1274,6 @@ hipError_t launch_router_mfma(const pr2_moe_desc& d, int NC, int r, const void* 
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    int64_t blocks = (n + 255) / 256;
-    if (blocks > 2048) blocks = 2048;
-    hipLaunchKernelGGL(router_pair_sum_kernel, dim3((unsigned)blocks), dim3(256), 0, s, sk.part,
-                       npairs, n, NTW, sk.logit);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
     const dim3 grid2((unsigned)((d.T + kRTM2 - 1) / kRTM2));
     switch (NTW) {
 #define PR2_CASE(n) case n: hipLaunchKernelGGL((router_mfma_kernel<n, MODE, 2>), grid2, dim3(kRThreads), 0, s, xb, Ws, d.T, d.d, d.N, r, NC, po, ro, sk); break;
@@ -1302,7 +1307,7 @@ size_t router_split_bytes(int NC, const pr2_moe_desc& d) {
     if (d.T > 0 && d.d / kRBK >= kSplitMinSteps) {
         const int64_t tiles = min((d.T + kRTM - 1) / kRTM, (int64_t)kSplitMaxTiles);
         const int64_t n = tiles * kRTM * ncp_of(NC);
-        b += ((d.d / kRBK + 1) / 2 + 1) * (size_t)n * sizeof(float);   // pair sums, logits
+        b += ((d.d / kRBK + 1) / 2) * (size_t)n * sizeof(float);       // pair sums
     }
     return b;
 }
