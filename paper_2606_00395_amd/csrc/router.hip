@@ -907,7 +907,7 @@ struct RouterTile {
 // loop does, then runs the epilogue, over workgroups of kRTM2 tokens (more
 // workgroups share the serial top-k rounds and the pair sums).  The logits
 // are bitwise those of the fused kernel.
-constexpr int kRTM2 = 16;                 // tokens per phase-2 workgroup
+constexpr int kRTM2 = 8;                  // tokens per phase-2 workgroup
 
 struct SplitK {
     float* part;       // [npairs][rows][NCp]: phase 1 output, token-major
