@@ -118,6 +118,8 @@ CASES = [
     (300, 192, 8, 2, 128, "bf16", "hot8", "int32", 0, False),
     (130, 48, 6, 3, 40, "f32", "none", "int16", 1, True),        # generic fp32, ragged
     (100, 256, 4, 4, 256, "bf16", "none", "int32", 0, True),     # k = N
+    (300, 256, 512, 64, 128, "bf16", "zipf", "int16", 1, True),  # k = 64 of 512 experts
+    (150, 256, 256, 64, 128, "bf16", "none", "int32", 0, False),
 ]
 
 
