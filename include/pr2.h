@@ -208,7 +208,9 @@ pr2_status pr2_moe_replay_forward(const pr2_moe_desc* desc, const void* x, const
  *
  * y and gate_out are bitwise those of pr2_moe_replay_forward.  The saved rows are bitwise
  * what the backward would otherwise recompute, so the saved backward's gradients are bitwise
- * those of pr2_moe_replay_backward.
+ * those of pr2_moe_replay_backward.  Same workspace and checks as pr2_moe_replay_forward, and
+ * au_out NULL with T > 0 returns PR2_ERR_NULL, a misaligned au_out PR2_ERR_ALIGN (nothing
+ * enqueued).
  */
 pr2_status pr2_moe_replay_forward_save(const pr2_moe_desc* desc, const void* x, const void* idx,
                                        int64_t ldi, const float* W_r, const float* b_r,
@@ -303,7 +305,10 @@ pr2_status pr2_moe_replay_backward(const pr2_moe_desc* desc, const void* x, cons
  * Replay backward from saved pre-activations: pr2_moe_replay_backward with the gate/up
  * pre-activations read from au_saved (written by pr2_moe_replay_forward_save with the same
  * desc, x, idx, W_gate and W_up) instead of recomputed by a grouped GEMM.  au_saved is only
- * read.  Same arguments otherwise, same workspace, bitwise the same gradients.
+ * read.  Same arguments otherwise, same workspace, bitwise the same gradients; au_saved NULL
+ * with T > 0 returns PR2_ERR_NULL, a misaligned one PR2_ERR_ALIGN (nothing enqueued).  A
+ * buffer not written by pr2_moe_replay_forward_save for these inputs gives wrong gradients
+ * (nothing detects it).
  */
 pr2_status pr2_moe_replay_backward_saved(const pr2_moe_desc* desc, const void* x, const void* idx,
                                          int64_t ldi, const float* W_r, const float* b_r,
