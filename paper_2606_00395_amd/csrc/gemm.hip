@@ -32,6 +32,15 @@
 // a = X_e W_gate_e^T and u = X_e W_up_e^T (bf16) instead of H; a fourth stores
 // both (a forward that saves them for the backward).
 //
+// When m is a multiple of 192, the forward GEMM1 runs a second kernel with a
+// 384-row panel (192 gate + 192 up rows; 80 KiB per LDS stage, all 160 KiB of
+// LDS in two stages), 17 % fewer copied bytes per flop: each of the eight
+// wavefronts owns 64 token rows x 192 panel rows (192 accumulators per lane),
+// reads its A fragments once per K=32 step and its B fragments two tiles at a
+// time, double-buffered.  Per output the sums run in the same K order as the
+// 256-row panel, so H is bitwise the same; measured 2 % faster on both layer
+// shapes.
+//
 // Other shapes and the fp32 path use a plain one-thread-per-output kernel.
 #include "common.h"
 
@@ -483,6 +492,170 @@ gemm2_generic(const T* H, const int* perm_src, const float* gate, const T* Wd, i
     O[(int64_t)(row0 + r) * d + col] = Act<T>::from_f32(gate[perm_src[row0 + r]] * a);
 }
 
+// ------------------------------------------- GEMM1 with a 384-row panel --
+constexpr int BPW = 384;                          // panel rows
+constexpr int WNW = 192;                          // panel rows per wavefront (96 gate + 96 up)
+constexpr int NJW = WNW / MT;                     // 12
+constexpr int STAGEBW = (BM + BPW) * ROWB;        // 80 KiB
+constexpr int LDSBW = NSTAGE * STAGEBW;           // 160 KiB
+constexpr int kAGroupsW = BM / kRowsPerDma / NWAVE;          // 4 token-row groups per wavefront
+constexpr int kWGroupsW = (BPW / 2) / kRowsPerDma / NWAVE;   // 3 gate (and 3 up) groups per wavefront
+static_assert(kAGroupsW * kRowsPerDma * NWAVE == BM && kWGroupsW * kRowsPerDma * NWAVE * 2 == BPW,
+              "row groups divide evenly");
+
+__global__ void __launch_bounds__(kGemmThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+gemm1_wide(MfmaArgs g) {
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[LDSBW];
+    const int ntile = *g.tile_count;
+    const int64_t L = (int64_t)ntile * g.ntn;
+    const int64_t per_xcd = (L + kNumXcd - 1) / kNumXcd;
+    const int64_t local = blockIdx.x / kNumXcd;
+    if (local >= per_xcd) return;
+    const int64_t logical = (int64_t)(blockIdx.x % kNumXcd) * per_xcd + local;
+    if (logical >= L) return;
+    const int tile = (int)(logical / g.ntn);
+    const int pn = (int)(logical % g.ntn);
+    const int expert = g.tiles[3 * tile + 0];
+    const int row0 = g.tiles[3 * tile + 1];
+    const int rows = g.tiles[3 * tile + 2];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wr = wave / (BPW / WNW);
+    const int wc = wave % (BPW / WNW);
+    const bool active = wr * WM < rows;
+
+    // copies: wavefront w moves token-row groups 4w..4w+3, gate groups
+    // 3w..3w+2 and up groups 3w..3w+2 (8 rows of 128 bytes each)
+    const bf16_t* wg = g.W0 + (int64_t)expert * g.w_stride;
+    const bf16_t* wu = g.W1 + (int64_t)expert * g.w_stride;
+    uint32_t soa[kAGroupsW], sog[kWGroupsW], sou[kWGroupsW];
+    {
+        int rsrc[kAGroupsW];
+#pragma unroll
+        for (int i = 0; i < kAGroupsW; ++i) {
+            const int r = (wave * kAGroupsW + i) * kRowsPerDma + lane / CHUNKS;
+            rsrc[i] = g.perm_src[row0 + (r < rows ? r : 0)];
+        }
+#pragma unroll
+        for (int i = 0; i < kAGroupsW; ++i) {
+            const int r = (wave * kAGroupsW + i) * kRowsPerDma + lane / CHUNKS;
+            const int64_t row = (int64_t)(min(max(rsrc[i], 0), g.Tk - 1) / g.k);
+            soa[i] = (uint32_t)(row * g.K + ((lane % CHUNKS) ^ swz(r)) * 8);
+        }
+#pragma unroll
+        for (int i = 0; i < kWGroupsW; ++i) {
+            const int pr = (wave * kWGroupsW + i) * kRowsPerDma + lane / CHUNKS;   // 0..191
+            const uint32_t off = (uint32_t)((int64_t)(pn * (BPW / 2) + pr) * g.K);
+            sog[i] = off + ((lane % CHUNKS) ^ swz(BM + pr)) * 8;
+            sou[i] = off + ((lane % CHUNKS) ^ swz(BM + BPW / 2 + pr)) * 8;
+        }
+    }
+    static_assert(NSTAGE == 2, "the copy skip below assumes vmcnt(0) waits");
+    auto issue = [&](int stage, int k0) {
+        unsigned char* sb = lds + stage * STAGEBW;
+#pragma unroll
+        for (int i = 0; i < kAGroupsW; ++i) {
+            const int grp = wave * kAGroupsW + i;
+            if (grp * kRowsPerDma >= rows) continue;
+            __builtin_amdgcn_global_load_lds((const void*)(g.A + (soa[i] + (uint32_t)k0)),
+                                             (lds_void*)(sb + grp * 1024), 16, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < kWGroupsW; ++i) {
+            const int grp = BM / kRowsPerDma + wave * kWGroupsW + i;
+            __builtin_amdgcn_global_load_lds((const void*)(wg + (sog[i] + (uint32_t)k0)),
+                                             (lds_void*)(sb + grp * 1024), 16, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < kWGroupsW; ++i) {
+            const int grp = (BM + BPW / 2) / kRowsPerDma + wave * kWGroupsW + i;
+            __builtin_amdgcn_global_load_lds((const void*)(wu + (sou[i] + (uint32_t)k0)),
+                                             (lds_void*)(sb + grp * 1024), 16, 0, 0);
+        }
+    };
+
+    accv acc[MI][NJW];
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NJW; ++j)
+#pragma unroll
+            for (int v = 0; v < ACCN; ++v) acc[i][j][v] = 0.0f;
+
+    const int lrow = lane % MT;
+    const int sw = swz(lrow);
+    const int grp = lane / MT;
+    const int cperm = MT == 16 ? (((grp & 1) << 1) | (grp >> 1)) : grp;
+    int kpos[NKS];
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks)
+        kpos[ks] = lrow * ROWB + ((((MK / 8) * ks + cperm) ^ sw) << 4);
+    const int a0 = (wr * WM) * ROWB;
+    // panel row of fragment j: gate rows for j < NJW/2, the matching up rows after
+    const int b0 = (BM + wc * (WNW / 2)) * ROWB;
+
+    const int nk = g.K / BK;
+    issue(0, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+        wait_vmcnt<0>();
+        __syncthreads();
+        if (kt + 1 < nk) issue((kt + 1) % NSTAGE, (kt + 1) * BK);
+        if (active) {
+            const unsigned char* base = lds + (kt % NSTAGE) * STAGEBW;
+#pragma unroll
+            for (int ks = 0; ks < NKS; ++ks) {
+                bf16x8 fa[MI], fb[2][2];
+                auto read_pair = [&](int buf, int jp) {
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const int j = 2 * jp + h;
+                        const int prow = (j < NJW / 2 ? 0 : BPW / 2) + (j % (NJW / 2)) * MT;
+                        fb[buf][h] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + b0 + prow * ROWB + kpos[ks]));
+                    }
+                };
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+                    fa[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + a0 + i * MT * ROWB + kpos[ks]));
+                read_pair(0, 0);
+#pragma unroll
+                for (int jp = 0; jp < NJW / 2; ++jp) {
+                    if (jp + 1 < NJW / 2) read_pair((jp + 1) & 1, jp + 1);
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int h = 0; h < 2; ++h)
+#pragma unroll
+                        for (int i = 0; i < MI; ++i)
+                            acc[i][2 * jp + h] = mfma_bf16(fb[jp & 1][h], fa[i], acc[i][2 * jp + h]);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            }
+        }
+    }
+    if (!active) return;
+    // H = silu(gate) * up straight from registers (8-byte runs)
+    const int ncol0 = 4 * (lane / MT);
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+        const int r = wr * WM + i * MT + (lane % MT);
+        if (r >= rows) continue;
+        bf16_t* orow = g.out + ((int64_t)row0 + r) * g.n_out;
+#pragma unroll
+        for (int j = 0; j < NJW / 2; ++j) {
+            const int col = pn * (BPW / 2) + wc * (WNW / 2) + j * MT + ncol0;
+            uint32_t w[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const float h0 = silu_f(acc[i][j][2 * h]) * acc[i][j + NJW / 2][2 * h];
+                const float h1 = silu_f(acc[i][j][2 * h + 1]) * acc[i][j + NJW / 2][2 * h + 1];
+                w[h] = (uint32_t)f32_to_bf16(h0) | ((uint32_t)f32_to_bf16(h1) << 16);
+            }
+            *(uint2*)(orow + col) = make_uint2(w[0], w[1]);
+        }
+    }
+}
+
 }  // namespace
 
 bool mfma_shape_ok(const pr2_moe_desc& d) {
@@ -516,7 +689,15 @@ hipError_t launch_expert_gemms(const pr2_moe_desc& d, const void* x, const void*
         g1.group = kGroupGemm1;
         int64_t work = ws.max_tiles * g1.ntn;
         int64_t grid = ((work + kNumXcd - 1) / kNumXcd) * kNumXcd;
-        if (au_out) {
+        if (!au_out && d.m % (BPW / 2) == 0) {
+            // the 384-row panel: m / 192 panels per tile
+            g1.ntn = d.m / (BPW / 2);
+            const int64_t wide = ws.max_tiles * g1.ntn;
+            const int64_t wgrid = ((wide + kNumXcd - 1) / kNumXcd) * kNumXcd;
+            LaunchScope scope("gemm1_gate_up_swiglu", s);
+            hipLaunchKernelGGL(gemm1_wide, dim3((unsigned)wgrid), dim3(kGemmThreads), 0, s, g1);
+            g1.ntn = d.m / 128;
+        } else if (au_out) {
             g1.out2 = (bf16_t*)au_out;
             LaunchScope scope("gemm1_gate_up_swiglu_save", s);
             hipLaunchKernelGGL(grouped_gemm_mfma<3>, dim3((unsigned)grid), dim3(kGemmThreads), 0,

@@ -72,6 +72,10 @@ CASES = [
     (70, 256, 128, 8, 128, "bf16", "hot8", True, "int32", 0, "few_tokens_many_experts"),
     (40, 256, 512, 256, 128, "bf16", "none", True, "int32", 0, "k256_N512_max_route"),
     (33, 64, 1024, 96, 32, "f32", "zipf", False, "int16", 1, "N1024_literal_generic"),
+    # m a multiple of 192: the gate/up GEMM with 384-row panels (one and two
+    # panels per tile, ragged tiles)
+    (1300, 256, 16, 4, 192, "bf16", "hot8", True, "int32", 0, "wide_panel_m192"),
+    (900, 512, 8, 2, 384, "bf16", "zipf", False, "int16", 2, "wide_panel_m384"),
     # more than 32 tiles of 64 tokens: the replay-weight pass forms the
     # permutation's counts (k = 8, 16, 32, 64), ragged last tile
     (4100, 256, 64, 16, 128, "bf16", "zipf", True, "int16", 3, "fused_counts_k16"),
