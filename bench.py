@@ -93,6 +93,12 @@ def profiled_traffic(profile, kernel):
     return int(m.group(1)) + int(m.group(2)) if m else None
 
 
+def gemm1_kernel(m):
+    """The gate/up GEMM kernel the library launches for expert width m (its
+    name in the rocprofv3 summaries)."""
+    return "gemm1_wide" if m % 192 == 0 else "grouped_gemm_mfma<0>"
+
+
 def profiled_counters(profile, kernel):
     """The SQ counter figures (mfma_busy, lds_conflict_per_inst, ...) that the
     committed summary `profiles/<profile>` holds for `kernel`, or None when the
@@ -425,7 +431,7 @@ def run_forward(args, shape, dev):
     out["roofline"] = {"bound": "mfma", "kernel": dominant, "achieved": achieved, "peak": peak,
                        "unit": "TFLOP/s", "frac": achieved / peak,
                        "traffic": profiled_traffic(f"replay_and_route_kernels_{shape.name}.txt",
-                                                  "grouped_gemm_mfma<0>")}
+                                                  gemm1_kernel(shape.m))}
     if not light:
         out["hip_graph"] = {"ms_per_step": ms_graph, "value": T / (ms_graph * 1e-3),
                             "note": "the same step captured once and replayed as a HIP graph"}
@@ -466,7 +472,7 @@ def run_forward(args, shape, dev):
     out["hbm_gbps_counters"] = cg or None
     out["mfma_busy_counters"] = {
         key: (profiled_counters(prof, kname) or {}).get("mfma_busy")
-        for key, kname in (("gemm1_gate_up_swiglu", "grouped_gemm_mfma<0>"),
+        for key, kname in (("gemm1_gate_up_swiglu", gemm1_kernel(shape.m)),
                            ("gemm2_down_scale", "grouped_gemm_mfma<1>"),
                            ("route_predict", "router_mfma_kernel<2, 0, 0>"))}
     out["mfma_busy_counters"]["note"] = ("SQ_VALU_MFMA_BUSY_CYCLES / (4 SIMDs x SQ_BUSY_CU_CYCLES) "
@@ -710,7 +716,7 @@ def run_next(args, shape, dev):
     out["roofline"] = {"bound": "mfma", "kernel": dominant, "achieved": achieved, "peak": peak,
                        "unit": "TFLOP/s", "frac": achieved / peak,
                        "traffic": profiled_traffic(f"replay_and_route_kernels_{shape.name}.txt",
-                                                  "grouped_gemm_mfma<0>")}
+                                                  gemm1_kernel(shape.m))}
     out["kernels_ms"] = kern
     out["rollout_paper_literal_gates"] = {"ms": ms_lit, "value": T / (ms_lit * 1e-3),
                                           "kernels_ms": kern_lit}
