@@ -441,7 +441,9 @@ def run_forward(args, shape, dev):
     out["ms_per_step_median"] = median
     out["kernels_ms"] = {n: round(v, 5) for n, v in kern.items()}
     if not light:
-        out["measured_peaks"] = measured_peaks(dev)
+        out["measured_peaks"] = mp = measured_peaks(dev)
+        # the gate/up GEMM's rate over the library's dense square GEMM, same GPU, same run
+        mp["gemm1_over_library_gemm"] = (f_g1 / (t_g1 * 1e-3) / 1e12) / mp["library_gemm_bf16_tflops"]
     out["replay_forward"] = {
         "ms": t_replay,
         "mfma_frac_whole_layer": C.expert_flops(T, d, k, m) / (t_replay * 1e-3) / C.PEAK_BF16_FLOPS,
