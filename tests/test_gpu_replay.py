@@ -76,6 +76,7 @@ CASES = [
     # panels per tile, ragged tiles)
     (1300, 256, 16, 4, 192, "bf16", "hot8", True, "int32", 0, "wide_panel_m192"),
     (900, 512, 8, 2, 384, "bf16", "zipf", False, "int16", 2, "wide_panel_m384"),
+    (70, 256, 128, 8, 576, "bf16", "hot8", True, "int32", 0, "wide_panel_few_rows_per_expert"),
     # more than 32 tiles of 64 tokens: the replay-weight pass forms the
     # permutation's counts (k = 8, 16, 32, 64), ragged last tile
     (4100, 256, 64, 16, 128, "bf16", "zipf", True, "int16", 3, "fused_counts_k16"),
