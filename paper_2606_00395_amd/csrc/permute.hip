@@ -247,6 +247,15 @@ perm_scatter_kernel(const void* idx, int idx_dtype, int64_t ldi, int64_t T, int 
     const int64_t tend = t0 + tb < T ? t0 + tb : T;
     const int entries = (int)((tend - t0) * k);
     const uint64_t lt = lane ? ((~0ull) >> (64 - lane)) : 0ull;
+    // the ids of up to kPrefetch passes are loaded before the first pass, so
+    // the passes (each ending in a barrier) do not wait on global loads
+    constexpr int kPrefetch = kEntriesPerPermBlock / 64;
+    int pre[kPrefetch];
+#pragma unroll
+    for (int i = 0; i < kPrefetch; ++i) {
+        const int q = i * 64 + lane;
+        pre[i] = q < entries ? load_id(idx, idx_dtype, (t0 + q / k) * ldi + q % k) : -1;
+    }
     for (int q0 = 0; q0 < entries; q0 += 64) {
         const int q = q0 + lane;
         int e = -1;
@@ -255,7 +264,11 @@ perm_scatter_kernel(const void* idx, int idx_dtype, int64_t ldi, int64_t T, int 
             int64_t t = t0 + q / k;
             int s = q % k;
             src = t * k + s;
-            e = load_id(idx, idx_dtype, t * ldi + s);
+            int pe = pre[0];
+#pragma unroll
+            for (int i = 1; i < kPrefetch; ++i)
+                if (q0 == i * 64) pe = pre[i];
+            e = q0 < kPrefetch * 64 ? pe : load_id(idx, idx_dtype, t * ldi + s);
             if (e < 0 || e >= N) {
                 inv[src] = -1;
                 e = -1;
