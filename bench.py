@@ -465,6 +465,7 @@ def run_forward(args, shape, dev):
     for key, kname, t_ms in (("route_predict", "router_mfma_kernel<2, 0, 0>", t_route),
                              ("replay_gates", "router_mfma_kernel<2, 1, 0>", t_gates),
                              ("perm_count", "perm_count_kernel", kern.get("perm_count")),
+                             ("perm_scan", "perm_scan_kernel", kern.get("perm_scan")),
                              ("perm_scatter", "perm_scatter_kernel", kern.get("perm_scatter")),
                              ("combine", "combine_bf16_kernel", t_comb)):
         b = profiled_traffic(prof, kname)
