@@ -552,6 +552,20 @@ def run_backward(args, shape, dev):
     out["mfma_frac_whole_backward"] = 16 * unit / (ms * 1e-3) / C.PEAK_BF16_FLOPS
     out["recorded_route"] = ("the current router's top-k with the k-th ranked expert swapped for "
                              f"the (k+1)-th on {int(round(shape.flip_frac * T))} tokens")
+    # the printed weights (rho_j of the softmax over all N): the logit gradient
+    # is dense over N, so the router gradient and the router term of dx cover
+    # every expert
+    ws_lit = B.backward_workspace(G["x"], idx, G["W_r"], G["W_gate"], renorm=False)
+
+    def literal_step():
+        B.moe_replay_backward(G["x"], idx, G["W_r"], G["beta"], G["W_gate"], G["W_up"],
+                              G["W_down"], dy, dx, dWr, dbr, dWg, dWu, dWd, ws=ws_lit,
+                              renorm=False, stream=stream)
+
+    ms_lit, kern_lit = timed_steps(literal_step, args.steps, args.warmup, stream, B)
+    del ws_lit
+    out["paper_literal_weights"] = {"ms": ms_lit, "value": T / (ms_lit * 1e-3),
+                                    "kernels_ms": {n: round(v, 5) for n, v in kern_lit.items()}}
     out["training_pass"] = training_pass(args, G, idx, dy, (dx, dWr, dbr, dWg, dWu, dWd), ws,
                                          step, stream)
     if not args.no_cpu_baseline:

@@ -1068,9 +1068,9 @@ literal_wgrad_reduce_kernel(const float* part, const float* dbpart, int nchunk, 
 constexpr int kLitDxTok = 16;
 template <typename T>
 __global__ void __launch_bounds__(256)
-literal_dx_combine_kernel(const T* dxr, const int* inv, const float* dpf, const float* W_r,
+literal_dx_combine_kernel(const T* dxr, const int* inv, const float* dpf, const float* wrt,
                           int64_t Ttot, int k, int d, int N, T* dx) {
-    __shared__ float ps[kLitDxTok][64];
+    __shared__ __attribute__((aligned(16))) float ps[kLitDxTok][64];
     const int c = blockIdx.x * 256 + threadIdx.x;
     const int64_t t0 = (int64_t)blockIdx.y * kLitDxTok;
     float racc[kLitDxTok];
@@ -1084,10 +1084,26 @@ literal_dx_combine_kernel(const T* dxr, const int* inv, const float* dpf, const 
         }
         __syncthreads();
         if (c < d) {
-            const float* wrow = W_r + (int64_t)c * N + j0;
+            // W_r transposed ([N, d]): a wavefront reads 64 consecutive columns
+            const float* wcol = wrt + (int64_t)j0 * d + c;
             const int jn = N - j0 < 64 ? N - j0 : 64;
-            for (int q = 0; q < jn; ++q) {
-                const float w = wrow[q];
+            // four logits per step: one 16-byte (broadcast) LDS read per token
+            // for four FMAs, added in the same order as one at a time
+            int q = 0;
+            for (; q + 4 <= jn; q += 4) {
+                const float w0 = wcol[(int64_t)q * d], w1 = wcol[(int64_t)(q + 1) * d],
+                            w2 = wcol[(int64_t)(q + 2) * d], w3 = wcol[(int64_t)(q + 3) * d];
+#pragma unroll
+                for (int r = 0; r < kLitDxTok; ++r) {
+                    const f32x4 p = *(const f32x4*)&ps[r][q];
+                    racc[r] = fmaf(p[0], w0, racc[r]);
+                    racc[r] = fmaf(p[1], w1, racc[r]);
+                    racc[r] = fmaf(p[2], w2, racc[r]);
+                    racc[r] = fmaf(p[3], w3, racc[r]);
+                }
+            }
+            for (; q < jn; ++q) {
+                const float w = wcol[(int64_t)q * d];
 #pragma unroll
                 for (int r = 0; r < kLitDxTok; ++r) racc[r] = fmaf(ps[r][q], w, racc[r]);
             }
@@ -1105,6 +1121,74 @@ literal_dx_combine_kernel(const T* dxr, const int* inv, const float* dpf, const 
             if (q >= 0) acc += Act<T>::to_f32(dxr[(int64_t)q * d + c]);
         }
         dx[t * d + c] = Act<T>::from_f32(acc + racc[r]);
+    }
+}
+
+// The same with four consecutive columns per thread (d % 4 == 0): each
+// broadcast LDS read of four logits feeds 64 FMAs; every output's sums run in
+// the same order as above, so the result is bitwise the same.
+template <typename T>
+__global__ void __launch_bounds__(256)
+literal_dx_combine4_kernel(const T* dxr, const int* inv, const float* dpf, const float* wrt,
+                           int64_t Ttot, int k, int d, int N, T* dx) {
+    __shared__ __attribute__((aligned(16))) float ps[kLitDxTok][64];
+    const int c = (blockIdx.x * 256 + threadIdx.x) * 4;
+    const int64_t t0 = (int64_t)blockIdx.y * kLitDxTok;
+    float racc[kLitDxTok][4];
+#pragma unroll
+    for (int r = 0; r < kLitDxTok; ++r)
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) racc[r][cc] = 0.0f;
+    for (int j0 = 0; j0 < N; j0 += 64) {
+        for (int e = threadIdx.x; e < kLitDxTok * 64; e += 256) {
+            const int r = e / 64, q = e % 64;
+            const int64_t t = t0 + r;
+            ps[r][q] = (t < Ttot && j0 + q < N) ? dpf[t * N + j0 + q] : 0.0f;
+        }
+        __syncthreads();
+        if (c < d) {
+            const float* wcol = wrt + (int64_t)j0 * d + c;
+            const int jn = N - j0 < 64 ? N - j0 : 64;
+            int q = 0;
+            for (; q + 4 <= jn; q += 4) {
+                f32x4 w[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) w[u] = *(const f32x4*)(wcol + (int64_t)(q + u) * d);
+#pragma unroll
+                for (int r = 0; r < kLitDxTok; ++r) {
+                    const f32x4 p = *(const f32x4*)&ps[r][q];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u)
+#pragma unroll
+                        for (int cc = 0; cc < 4; ++cc)
+                            racc[r][cc] = fmaf(p[u], w[u][cc], racc[r][cc]);
+                }
+            }
+            for (; q < jn; ++q) {
+                const f32x4 w = *(const f32x4*)(wcol + (int64_t)q * d);
+#pragma unroll
+                for (int r = 0; r < kLitDxTok; ++r)
+#pragma unroll
+                    for (int cc = 0; cc < 4; ++cc) racc[r][cc] = fmaf(ps[r][q], w[cc], racc[r][cc]);
+            }
+        }
+        __syncthreads();
+    }
+    if (c >= d) return;
+#pragma unroll
+    for (int r = 0; r < kLitDxTok; ++r) {
+        const int64_t t = t0 + r;
+        if (t >= Ttot) break;
+        float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        for (int s = 0; s < k; ++s) {
+            const int q = inv[t * k + s];
+            if (q < 0) continue;
+            const T* row = dxr + (int64_t)q * d + c;
+#pragma unroll
+            for (int cc = 0; cc < 4; ++cc) acc[cc] += Act<T>::to_f32(row[cc]);
+        }
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) dx[t * d + c + cc] = Act<T>::from_f32(acc[cc] + racc[r][cc]);
     }
 }
 
@@ -1261,6 +1345,14 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
+    // W_r transposed, [N, d]: rows of the router term
+    auto launch_transpose_wr = [&](hipStream_t ts) -> hipError_t {
+        LaunchScope scope("bwd_transpose_wr", ts);
+        hipLaunchKernelGGL(transpose_wr_kernel,
+                           dim3((unsigned)((d.d + 31) / 32), (unsigned)((d.N + 31) / 32)), dim3(256),
+                           0, ts, W_r, d.d, d.N, ws.wrt);
+        return hipGetLastError();
+    };
     // the router weight gradient and the combine of the input gradient
     auto tail = [&](hipStream_t ts) -> hipError_t {
         hipError_t e = hipSuccess;
@@ -1286,15 +1378,29 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
                                    ts, ws.lwpart, ws.lbpart, ws.nchunk, n, d.N, out.dW_r, out.db_r);
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
+            if ((e = launch_transpose_wr(ts)) != hipSuccess) return e;
             LaunchScope scope("bwd_dx_combine_literal", ts);
+            if (d.d % 4 == 0) {
+                dim3 grid4((unsigned)((d.d + 1023) / 1024),
+                           (unsigned)((d.T + kLitDxTok - 1) / kLitDxTok));
+                if (bf)
+                    hipLaunchKernelGGL(literal_dx_combine4_kernel<bf16_t>, grid4, dim3(256), 0, ts,
+                                       (const bf16_t*)w.O, w.inv, ws.dpf, ws.wrt, d.T, d.k, d.d, d.N,
+                                       (bf16_t*)out.dx);
+                else
+                    hipLaunchKernelGGL(literal_dx_combine4_kernel<float>, grid4, dim3(256), 0, ts,
+                                       (const float*)w.O, w.inv, ws.dpf, ws.wrt, d.T, d.k, d.d, d.N,
+                                       (float*)out.dx);
+                return hipGetLastError();
+            }
             dim3 grid((unsigned)((d.d + 255) / 256), (unsigned)((d.T + kLitDxTok - 1) / kLitDxTok));
             if (bf)
                 hipLaunchKernelGGL(literal_dx_combine_kernel<bf16_t>, grid, dim3(256), 0, ts,
-                                   (const bf16_t*)w.O, w.inv, ws.dpf, W_r, d.T, d.k, d.d, d.N,
+                                   (const bf16_t*)w.O, w.inv, ws.dpf, ws.wrt, d.T, d.k, d.d, d.N,
                                    (bf16_t*)out.dx);
             else
                 hipLaunchKernelGGL(literal_dx_combine_kernel<float>, grid, dim3(256), 0, ts,
-                                   (const float*)w.O, w.inv, ws.dpf, W_r, d.T, d.k, d.d, d.N,
+                                   (const float*)w.O, w.inv, ws.dpf, ws.wrt, d.T, d.k, d.d, d.N,
                                    (float*)out.dx);
             return hipGetLastError();
         }
@@ -1317,13 +1423,7 @@ hipError_t launch_replay_backward(const pr2_moe_desc& d, const void* x, const vo
         }
 
         // input gradient: per-route rows plus the router term dp W_r^T
-        {
-            LaunchScope scope("bwd_transpose_wr", ts);
-            hipLaunchKernelGGL(transpose_wr_kernel,
-                               dim3((unsigned)((d.d + 31) / 32), (unsigned)((d.N + 31) / 32)), dim3(256),
-                               0, ts, W_r, d.d, d.N, ws.wrt);
-        }
-        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = launch_transpose_wr(ts)) != hipSuccess) return e;
         LaunchScope scope("bwd_dx_combine", ts);
         if (bf && d.d % 8 == 0) {
             const int64_t want = (d.T + kDxTok - 1) / kDxTok;
