@@ -994,8 +994,8 @@ template <typename T>
 __global__ void __launch_bounds__(256)
 literal_wgrad_partial_kernel(const T* x, const float* dpf, int64_t Ttot, int d, int N,
                              float* part, float* dbpart) {
-    __shared__ float xs[32][kLitTile + 1];
-    __shared__ float ps[32][kLitTile + 1];
+    __shared__ __attribute__((aligned(16))) float xs[32][kLitTile];
+    __shared__ __attribute__((aligned(16))) float ps[32][kLitTile];
     const int i0 = blockIdx.x * kLitTile, j0 = blockIdx.y * kLitTile;
     const int64_t c = blockIdx.z;
     const int64_t t0 = c * kLitTok;
@@ -1017,12 +1017,9 @@ literal_wgrad_partial_kernel(const T* x, const float* dpf, int64_t Ttot, int d, 
         __syncthreads();
 #pragma unroll 4
         for (int r = 0; r < 32; ++r) {
-            float a[4], b[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                a[u] = xs[r][ty * 4 + u];
-                b[u] = ps[r][tx * 4 + u];
-            }
+            // 16-byte reads: four rows of x (a 16-lane broadcast) and four logits
+            const f32x4 a = *(const f32x4*)&xs[r][ty * 4];
+            const f32x4 b = *(const f32x4*)&ps[r][tx * 4];
 #pragma unroll
             for (int u = 0; u < 4; ++u)
 #pragma unroll
