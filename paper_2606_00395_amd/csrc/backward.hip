@@ -187,7 +187,6 @@ bwd_gemm(BwdArgs g) {
     const int wc = wave & 1;             // 128-column block
     const int half = wave >> 2;          // operand this wavefront loads: 0 rows, 1 columns
     const bool active = wr * WM < rows;
-    const bool dma = kRowTiles && half == 0;
 
     // ---- operand loading.  Both operands are copied global -> LDS with
     // 16-byte direct-to-LDS loads; wavefronts 0-3 copy the row operand (C

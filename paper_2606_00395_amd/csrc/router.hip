@@ -819,8 +819,8 @@ typedef __attribute__((address_space(3))) void lds_void;
 // and each part's 32 x 32 block (2 KiB, contiguous in Ws) is stored 8 bytes
 // per thread.
 __global__ void __launch_bounds__(256)
-router_split_kernel(const float* W_r, const float* A, const float* B, int d, int N, int r,
-                    int folded, int NCp, bf16_t* Ws) {
+router_split_kernel(const float* W_r, const float* A, const float* B, int N, int r, int folded,
+                    int NCp, bf16_t* Ws) {
     __shared__ bf16_t tile[3][32][kRBK + 1];
     // the predictor factors this workgroup folds in: A rows kt*32.. and B columns c0..
     constexpr int kStageR = 64;
@@ -1290,7 +1290,7 @@ hipError_t launch_split(const float* W_r, const float* A, const float* B, const 
     const int NCp = ncp_of(NC);
     LaunchScope scope("router_split", s);
     hipLaunchKernelGGL(router_split_kernel, dim3((unsigned)(NCp / 32), (unsigned)(d.d / kRBK)),
-                       dim3(256), 0, s, W_r, A, B, d.d, d.N, r, folded, NCp, Ws);
+                       dim3(256), 0, s, W_r, A, B, d.N, r, folded, NCp, Ws);
     return hipGetLastError();
 }
 
@@ -1338,7 +1338,7 @@ hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const floa
     if (logits_out == nullptr && cache.row == nullptr && router_mfma_ok(d, d.N)) {
         // the router logits are not wanted: fold the predictor into the weights
         PredictOut o{b_r, Bn, d.k, d.renorm, 1, idx_out, d.idx_dtype, ldi, gate_out, nullptr,
-                     FeatureCache{}, x, d.d, d.act_dtype};
+                     FeatureCache{}, x, d.d, d.act_dtype, nullptr, 0, 0};
         add_counts(o);
         if (!reuse_split) {
             hipError_t e = launch_split(W_r, A, Bn, d, d.r, 1, (bf16_t*)split_ws, s);
@@ -1349,7 +1349,7 @@ hipError_t launch_route_predict(const pr2_moe_desc& d, const void* x, const floa
                                      splitk_ok);
     }
     PredictOut o{b_r, Bn, d.k, d.renorm, 0, idx_out, d.idx_dtype, ldi, gate_out, logits_out, cache,
-                 x, d.d, d.act_dtype};
+                 x, d.d, d.act_dtype, nullptr, 0, 0};
     const int NC = d.N + d.r;
     if (router_mfma_ok(d, NC)) {
         add_counts(o);
@@ -1441,7 +1441,7 @@ hipError_t launch_replay_gates(const pr2_moe_desc& d, const void* x, const void*
         }
     }
     ReplayOut o{b_r, d.k, d.renorm, idx, d.idx_dtype, ldi, gate_out, err,
-                (v && v[0] == '1') ? 1 : 0, g};
+                (v && v[0] == '1') ? 1 : 0, g, nullptr, 0, 0};
     if (counts) {
         if (!replay_counts_fused(d)) return hipErrorInvalidValue;
         o.counts = counts;
@@ -1455,7 +1455,7 @@ hipError_t launch_router_logits(const pr2_moe_desc& d, const void* x, const floa
                                 const float* b_r, float* p_out, void* split_ws, hipStream_t s) {
     DiagOut g{};
     g.p_out = p_out;
-    ReplayOut o{b_r, d.k, 1, nullptr, d.idx_dtype, d.k, nullptr, nullptr, 0, g};
+    ReplayOut o{b_r, d.k, 1, nullptr, d.idx_dtype, d.k, nullptr, nullptr, 0, g, nullptr, 0, 0};
     return launch_router_replay(d, x, W_r, o, split_ws, "router_logits", s);
 }
 
@@ -1471,7 +1471,7 @@ hipError_t launch_route_diagnostics(const pr2_moe_desc& d, const void* x, const 
     }
     if (d.T == 0) return hipSuccess;
     ReplayOut o{b_r, d.k, 1, idx, d.idx_dtype, ldi, nullptr, nullptr, 0,
-                DiagOut{z_ref, cur_idx, overlap, kl, hist, nullptr}};
+                DiagOut{z_ref, cur_idx, overlap, kl, hist, nullptr}, nullptr, 0, 0};
     return launch_router_replay(d, x, W_r, o, split_ws, "route_diagnostics", s);
 }
 
